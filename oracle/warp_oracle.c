@@ -1,0 +1,265 @@
+/*
+ * Plain CPU oracle of the WARP search path. TEST INFRASTRUCTURE ONLY: only the
+ * tests, the smoke check and the benchmark's CPU-baseline leg may load it.
+ *
+ * Each function follows one passage of the paper (WARP, SIGIR '25):
+ *   oracle_centroid_scores  Section 4.3, S_{c,q} = C q^T
+ *   oracle_select           Section 4.3, top-n_probe centroids and WARP_SELECT's
+ *                           missing-similarity estimate from cumulative cluster sizes
+ *   lut / token score       Section 4.4, Eq. warp_selective_sum and the table
+ *                           upsilon = q_hat x omega_hat
+ *   search                  Section 4.5, token-level max (r_tok) and document-level
+ *                           sum with imputation (r_doc, Eq. doc_level_reduce), then
+ *                           top-k; scores follow Eq. 1 without the 1/Z factor.
+ *
+ * Written to be read, not to be fast: full sorts, dense per-query arrays, one
+ * embedding at a time. Parallel over queries only.
+ */
+#include "warp_oracle.h"
+
+#include <math.h>
+#include <omp.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ABSENT INT64_MIN
+
+/* R(x): x in fixed point with ORACLE_FRAC_BITS fraction bits, round half to even. */
+static int64_t fixed(double x) { return (int64_t)nearbyint(ldexp(x, ORACLE_FRAC_BITS)); }
+
+/* Packed b-bit code of dimension d of one embedding's code row, most significant bits first. */
+static int code_at(const uint8_t* row, int32_t nbits, int32_t d) {
+    int per_byte = 8 / nbits;
+    int byte = row[d / per_byte];
+    int shift = 8 - nbits * (d % per_byte + 1);
+    return (byte >> shift) & ((1 << nbits) - 1);
+}
+
+void oracle_centroid_scores(const float* centroids, int32_t n_c, int32_t dim, const float* q,
+                            double* out) {
+    for (int32_t c = 0; c < n_c; ++c) {
+        double s = 0.0;
+        for (int32_t d = 0; d < dim; ++d) s += (double)centroids[(int64_t)c * dim + d] * (double)q[d];
+        out[c] = s;
+    }
+}
+
+typedef struct {
+    double s;
+    int32_t id;
+} scored_centroid;
+
+/* centroid order: higher score first, lower id first among equal scores */
+static int by_score_desc(const void* a, const void* b) {
+    const scored_centroid* x = (const scored_centroid*)a;
+    const scored_centroid* y = (const scored_centroid*)b;
+    if (x->s > y->s) return -1;
+    if (x->s < y->s) return 1;
+    return (x->id > y->id) - (x->id < y->id);
+}
+
+void oracle_select(const double* scores, const int64_t* offsets, int32_t n_c, int32_t nprobe,
+                   int64_t t_prime, int32_t* sel, double* m) {
+    scored_centroid* order = (scored_centroid*)malloc(sizeof(scored_centroid) * (size_t)n_c);
+    for (int32_t c = 0; c < n_c; ++c) {
+        order[c].s = scores[c];
+        order[c].id = c;
+    }
+    qsort(order, (size_t)n_c, sizeof(scored_centroid), by_score_desc);
+    for (int32_t j = 0; j < nprobe; ++j) sel[j] = order[j].id;
+    /* first position whose inclusive cumulative size exceeds t'; the last one if none does */
+    int32_t p_star = n_c - 1;
+    int64_t cum = 0;
+    for (int32_t p = 0; p < n_c; ++p) {
+        int32_t c = order[p].id;
+        cum += offsets[c + 1] - offsets[c];
+        if (cum > t_prime) {
+            p_star = p;
+            break;
+        }
+    }
+    *m = order[p_star].s;
+    free(order);
+}
+
+/* upsilon[d][beta] = R(q_d * omega_beta): the per-token bucket-weight table */
+static void build_lut(const float* q, int32_t dim, const float* w, int32_t nbits, int64_t* lut) {
+    int nb = 1 << nbits;
+    for (int32_t d = 0; d < dim; ++d)
+        for (int b = 0; b < nb; ++b) lut[d * nb + b] = fixed((double)q[d] * (double)w[b]);
+}
+
+/* selective sum: centroid term plus one table entry per dimension */
+static int64_t token_score(const int64_t* lut, int32_t dim, int32_t nbits, int64_t centroid_term,
+                           const uint8_t* row) {
+    int nb = 1 << nbits;
+    int64_t t = centroid_term;
+    for (int32_t d = 0; d < dim; ++d) t += lut[d * nb + code_at(row, nbits, d)];
+    return t;
+}
+
+void oracle_token_scores(const float* q, int32_t dim, double centroid_score, const uint8_t* codes,
+                         int32_t nbits, const float* bucket_weights, int64_t e0, int64_t e1,
+                         int32_t* out) {
+    int64_t* lut = (int64_t*)malloc(sizeof(int64_t) * (size_t)dim << nbits);
+    build_lut(q, dim, bucket_weights, nbits, lut);
+    int64_t row_bytes = (int64_t)dim * nbits / 8;
+    for (int64_t e = e0; e < e1; ++e)
+        out[e - e0] = (int32_t)token_score(lut, dim, nbits, fixed(centroid_score), codes + e * row_bytes);
+    free(lut);
+}
+
+typedef struct {
+    int64_t score;
+    int32_t doc;
+} scored_doc;
+
+/* result order: higher score first, lower document id first among equal scores */
+static int by_doc_score_desc(const void* a, const void* b) {
+    const scored_doc* x = (const scored_doc*)a;
+    const scored_doc* y = (const scored_doc*)b;
+    if (x->score > y->score) return -1;
+    if (x->score < y->score) return 1;
+    return (x->doc > y->doc) - (x->doc < y->doc);
+}
+
+typedef struct {
+    const float* centroids;
+    int32_t n_c, dim;
+    const int64_t* offsets;
+    const int32_t* doc_ids;
+    const uint8_t* codes;
+    int32_t nbits;
+    const float* w;
+    int32_t n_docs;
+    int32_t n_qtok, nprobe, k, flags;
+    int64_t t_prime;
+    const int32_t* doc_len; /* only with ORACLE_EQ1_LITERAL */
+} search_args;
+
+static void search_one(const search_args* a, const float* query, int32_t* out_ids, int64_t* out_fixed,
+                       float* out_scores, int32_t* out_count, int32_t* sel, int64_t* m_fixed,
+                       uint32_t* cand_bitmap, int64_t* n_scored, int64_t* doc_fixed) {
+    const int32_t T = a->n_qtok, D = a->dim, P = a->nprobe, n_docs = a->n_docs;
+    const int64_t row_bytes = (int64_t)D * a->nbits / 8;
+    double* S = (double*)malloc(sizeof(double) * (size_t)a->n_c);
+    int32_t* my_sel = (int32_t*)malloc(sizeof(int32_t) * (size_t)T * P);
+    int64_t* M = (int64_t*)malloc(sizeof(int64_t) * (size_t)T);
+    int64_t* lut = (int64_t*)malloc(sizeof(int64_t) * (size_t)D << a->nbits);
+    /* best[i][doc]: token-level max over every retrieved embedding of doc for token i */
+    int64_t* best = (int64_t*)malloc(sizeof(int64_t) * (size_t)T * n_docs);
+    int32_t* seen = NULL; /* retrieved embeddings per (token, doc), Eq.-1-literal reading only */
+    if (a->flags & ORACLE_EQ1_LITERAL) seen = (int32_t*)calloc((size_t)T * n_docs, sizeof(int32_t));
+    for (int64_t x = 0; x < (int64_t)T * n_docs; ++x) best[x] = ABSENT;
+    int64_t scored = 0;
+
+    for (int32_t i = 0; i < T; ++i) {
+        const float* q = query + (int64_t)i * D;
+        /* candidate generation: centroid scores, n_probe best, missing similarity */
+        double m;
+        oracle_centroid_scores(a->centroids, a->n_c, D, q, S);
+        oracle_select(S, a->offsets, a->n_c, P, a->t_prime, my_sel + (int64_t)i * P, &m);
+        M[i] = fixed(m);
+        /* decompression: selective sum over every embedding of every probed cluster */
+        build_lut(q, D, a->w, a->nbits, lut);
+        int64_t min_retrieved = INT64_MAX;
+        for (int32_t j = 0; j < P; ++j) {
+            int32_t c = my_sel[(int64_t)i * P + j];
+            int64_t centroid_term = fixed(S[c]);
+            for (int64_t e = a->offsets[c]; e < a->offsets[c + 1]; ++e) {
+                int64_t t = token_score(lut, D, a->nbits, centroid_term, a->codes + e * row_bytes);
+                int32_t doc = a->doc_ids[e];
+                int64_t* cell = &best[(int64_t)i * n_docs + doc];
+                if (*cell == ABSENT || t > *cell) *cell = t; /* r_tok */
+                if (seen) seen[(int64_t)i * n_docs + doc] += 1;
+                if (t < min_retrieved) min_retrieved = t;
+                ++scored;
+            }
+        }
+        if (a->flags & ORACLE_M_MIN_RETRIEVED) M[i] = (min_retrieved == INT64_MAX) ? 0 : min_retrieved;
+    }
+
+    /* document-level reduction over the candidate set (docs with any retrieved token) */
+    scored_doc* cand = (scored_doc*)malloc(sizeof(scored_doc) * (size_t)(n_docs > 0 ? n_docs : 1));
+    int32_t n_cand = 0;
+    for (int32_t doc = 0; doc < n_docs; ++doc) {
+        int any = 0;
+        for (int32_t i = 0; i < T; ++i) any |= best[(int64_t)i * n_docs + doc] != ABSENT;
+        if (doc_fixed) doc_fixed[doc] = ABSENT;
+        if (!any) continue;
+        int64_t score = 0;
+        for (int32_t i = 0; i < T; ++i) {
+            int64_t v = best[(int64_t)i * n_docs + doc];
+            if (v == ABSENT) {
+                score += M[i]; /* r_doc: a missing entry takes the token's estimate */
+            } else if (seen && seen[(int64_t)i * n_docs + doc] < a->doc_len[doc]) {
+                score += v > M[i] ? v : M[i]; /* Eq. 1 literal: an unretrieved doc token contributes m_i */
+            } else {
+                score += v;
+            }
+        }
+        if (doc_fixed) doc_fixed[doc] = score;
+        if (cand_bitmap) cand_bitmap[doc >> 5] |= 1u << (doc & 31);
+        cand[n_cand].score = score;
+        cand[n_cand].doc = doc;
+        ++n_cand;
+    }
+    qsort(cand, (size_t)n_cand, sizeof(scored_doc), by_doc_score_desc);
+    int32_t n_out = n_cand < a->k ? n_cand : a->k;
+    for (int32_t r = 0; r < a->k; ++r) {
+        if (r < n_out) {
+            out_ids[r] = cand[r].doc;
+            out_fixed[r] = cand[r].score;
+            out_scores[r] = (float)ldexp((double)cand[r].score, -ORACLE_FRAC_BITS);
+        } else {
+            out_ids[r] = -1;
+            out_fixed[r] = INT64_MIN;
+            out_scores[r] = -INFINITY;
+        }
+    }
+    *out_count = n_out;
+    if (sel) memcpy(sel, my_sel, sizeof(int32_t) * (size_t)T * P);
+    if (m_fixed) memcpy(m_fixed, M, sizeof(int64_t) * (size_t)T);
+    if (n_scored) *n_scored = scored;
+    free(cand);
+    free(seen);
+    free(best);
+    free(lut);
+    free(M);
+    free(my_sel);
+    free(S);
+}
+
+int oracle_search(const float* centroids, int32_t n_c, int32_t dim, const int64_t* offsets,
+                  const int32_t* doc_ids, const uint8_t* codes, int32_t nbits,
+                  const float* bucket_weights, int32_t n_docs, const float* queries,
+                  int32_t n_queries, int32_t n_qtok, int32_t nprobe, int64_t t_prime, int32_t k,
+                  int32_t flags, int32_t* out_ids, int64_t* out_fixed, float* out_scores,
+                  int32_t* out_counts, int32_t* sel, int64_t* m_fixed, uint32_t* cand_bitmap,
+                  int64_t* n_scored, int64_t* doc_fixed, int32_t n_threads) {
+    if (n_c < 1 || dim < 1 || n_docs < 0 || n_queries < 0 || n_qtok < 1 || nprobe < 1 ||
+        nprobe > n_c || k < 1 || t_prime < 0)
+        return -1;
+    if (!(nbits == 1 || nbits == 2 || nbits == 4 || nbits == 8) || (dim * nbits) % 8 != 0) return -1;
+    int32_t* doc_len = NULL;
+    if (flags & ORACLE_EQ1_LITERAL) {
+        doc_len = (int32_t*)calloc((size_t)(n_docs > 0 ? n_docs : 1), sizeof(int32_t));
+        for (int64_t e = 0; e < offsets[n_c]; ++e) doc_len[doc_ids[e]] += 1;
+    }
+    search_args a = {centroids, n_c,   dim,     offsets, doc_ids, codes, nbits, bucket_weights,
+                     n_docs,    n_qtok, nprobe, k,       flags,   t_prime, doc_len};
+    int64_t words = ((int64_t)n_docs + 31) / 32;
+    if (cand_bitmap) memset(cand_bitmap, 0, sizeof(uint32_t) * (size_t)(words * n_queries));
+    if (n_threads <= 0) n_threads = omp_get_num_procs();
+#pragma omp parallel for schedule(dynamic, 1) num_threads(n_threads)
+    for (int32_t qi = 0; qi < n_queries; ++qi) {
+        search_one(&a, queries + (int64_t)qi * n_qtok * dim, out_ids + (int64_t)qi * k,
+                   out_fixed + (int64_t)qi * k, out_scores + (int64_t)qi * k, out_counts + qi,
+                   sel ? sel + (int64_t)qi * n_qtok * nprobe : NULL,
+                   m_fixed ? m_fixed + (int64_t)qi * n_qtok : NULL,
+                   cand_bitmap ? cand_bitmap + qi * words : NULL, n_scored ? n_scored + qi : NULL,
+                   doc_fixed ? doc_fixed + (int64_t)qi * n_docs : NULL);
+    }
+    free(doc_len);
+    return 0;
+}
