@@ -1,0 +1,196 @@
+"""Benchmark of the WARP search path on one MI355X.
+
+A step is one batched search (centroid filter GEMM, selection, plan, residual
+scan, document fold, top-k) of the workload's whole query batch, with the
+index and the queries already resident in HBM. Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import subprocess
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+METRIC = "queries/s, p50 query latency, scored embeddings/s (% of HBM peak BW)"
+HBM_PEAK_GBS = 8000.0
+FP32_MFMA_PEAK_TFLOPS = 157.3
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_model() -> str:
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor()
+
+
+def host_threads() -> int:
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:
+        return os.cpu_count() or 1
+
+
+def describe(wl) -> str:
+    lens = (f"U[{int(wl.len_a)},{int(wl.len_b)}]" if wl.len_kind == "uniform"
+            else f"lognormal mean {wl.len_a:g} cap {int(wl.len_b)}")
+    return (f"{wl.name}: {wl.n_docs} docs ({lens} tokens), {wl.n_centroids} centroids, Zipf {wl.zipf_s}, "
+            f"b={wl.nbits}, {wl.n_queries} queries x {wl.n_qtok} tokens, nprobe={wl.nprobe}, "
+            f"t'={wl.t_prime}, k={wl.k}")
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="small")
+    ap.add_argument("--latency-runs", type=int, default=100)
+    ap.add_argument("--cpu-queries", type=int, default=48)
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the search path has no multi-GPU mode (--gpus {args.gpus} "
+              f"requested). Run with --gpus 1.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import synth
+    from paper_2501_17788_amd import Index
+
+    wl = synth.WORKLOADS[args.workload]
+    log(f"bench: generating {describe(wl)}")
+    t0 = time.time()
+    data = synth.make_index(wl, workers=min(16, host_threads()))
+    log(f"bench: {data.n_embeddings} embeddings in {time.time() - t0:.1f} s")
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    ix = Index.from_synthetic(data)
+    q = torch.from_numpy(data.queries).to(dev)
+    nq = wl.n_queries
+
+    # scored embeddings per query (exact, from the engine's own counters)
+    dbg = ix.search_debug(data.queries, wl.nprobe, wl.t_prime, wl.k)
+    scored = dbg["n_scored"].astype(np.int64)
+    row_bytes = 128 * wl.nbits // 8 + 4
+
+    stream = torch.cuda.current_stream(dev)
+    out = None
+    for _ in range(args.warmup):
+        out = ix.search_async(q, wl.nprobe, wl.t_prime, wl.k, out=out)
+    ix.sync()
+    log(f"bench: warmup done ({args.warmup} steps)")
+
+    ix.set_timing(True)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        out = ix.search_async(q, wl.nprobe, wl.t_prime, wl.k, out=out)
+    torch.cuda.synchronize()
+    t_end = time.perf_counter()
+    ix.sync()  # settles the per-stage event timings
+    stages = ix.stage_timings()
+    ix.set_timing(False)
+    elapsed = t_end - t_start
+    ms_step = elapsed * 1e3 / args.steps
+    qps = nq * args.steps / elapsed
+    log(f"bench: {args.steps} steps in {elapsed:.3f} s -> {qps:.1f} queries/s")
+    # the timed batch agrees with the debug run
+    ids = out[0].cpu().numpy()
+    same_as_debug = bool(np.array_equal(ids, dbg["ids"]))
+
+    # batch-1 latency
+    lat = []
+    q1 = [q[i:i + 1].contiguous() for i in range(min(nq, 16))]
+    out1 = None
+    for i in range(5):
+        out1 = ix.search_async(q1[i % len(q1)], wl.nprobe, wl.t_prime, wl.k, out=out1)
+    torch.cuda.synchronize()
+    for i in range(args.latency_runs):
+        a = time.perf_counter()
+        out1 = ix.search_async(q1[i % len(q1)], wl.nprobe, wl.t_prime, wl.k, out=out1)
+        torch.cuda.synchronize()
+        lat.append((time.perf_counter() - a) * 1e3)
+    p50, p99 = float(np.percentile(lat, 50)), float(np.percentile(lat, 99))
+    log(f"bench: batch-1 latency p50 {p50:.3f} ms p99 {p99:.3f} ms")
+
+    # roofline of the dominant kernel: the residual scan
+    scan_ms, scan_n = stages["scan"]
+    scan_avg_s = scan_ms / 1e3 / max(scan_n, 1)
+    launches_per_step = max(scan_n, 1) / args.steps
+    scan_bytes = float(scored.sum()) * row_bytes / launches_per_step  # algorithmic bytes per launch
+    achieved = scan_bytes / scan_avg_s / 1e9
+    gemm_ms, gemm_n = stages["filter_gemm"]
+    gemm_flops = 2.0 * nq * wl.n_qtok * wl.n_centroids * 128 / (max(gemm_n, 1) / args.steps)
+    gemm_tflops = gemm_flops / (gemm_ms / 1e3 / max(gemm_n, 1)) / 1e12 if gemm_n else None
+
+    cpu = None
+    if not args.no_cpu:
+        import oracle
+
+        nc = min(args.cpu_queries, nq)
+        threads = host_threads()
+        log(f"bench: oracle on {nc} queries with {threads} threads")
+        a = time.perf_counter()
+        ref = oracle.search_index(data, queries=data.queries[:nc], threads=threads, debug=False)
+        cpu_s = time.perf_counter() - a
+        cpu = {"value": nc / cpu_s, "unit": "queries/s", "cores": threads, "kind": "oracle",
+               "sample": f"first {nc} of the {nq} queries of the same workload "
+                         f"({int(scored[:nc].sum())} scored embeddings), {cpu_s:.1f} s wall",
+               "cpu_model": cpu_model()}
+        cpu["parity_ids"] = bool(np.array_equal(ref["ids"], dbg["ids"][:nc]))
+        cpu["parity_fixed_scores"] = bool(np.array_equal(ref["fixed"], dbg["fixed"][:nc]))
+
+    rec = {
+        "metric": METRIC,
+        "value": qps,
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "i32",
+        "data": "synthetic",
+        "config": {"workload": describe(wl), "n_embeddings": data.n_embeddings,
+                   "scored_embeddings_per_query": float(scored.mean()), "batch": nq},
+        "p50_ms_batch1": p50,
+        "p99_ms_batch1": p99,
+        "scored_emb_per_s": float(scored.sum()) * args.steps / elapsed,
+        "hbm_frac_effective": float(scored.sum()) * args.steps * row_bytes / elapsed / (HBM_PEAK_GBS * 1e9),
+        "stage_ms_per_step": {k: v[0] / args.steps for k, v in stages.items()},
+        "roofline": {"bound": "hbm", "kernel": "k_scan", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "algorithmic_bytes_per_launch": scan_bytes,
+                     "avg_launch_ms": scan_avg_s * 1e3},
+        "filter_gemm": {"tflops": gemm_tflops, "peak": FP32_MFMA_PEAK_TFLOPS,
+                        "frac": (gemm_tflops / FP32_MFMA_PEAK_TFLOPS) if gemm_tflops else None},
+        "cpu_baseline": cpu,
+        "timed_batch_matches_debug_run": same_as_debug,
+    }
+    print(json.dumps(rec), flush=True)
+    ix.close()
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,176 @@
+/*
+ * warp.h - C ABI of the WARP multi-vector search engine for AMD Instinct MI355X
+ * (gfx950).
+ *
+ * The engine implements the search path of WARP (Scheerer et al., SIGIR '25):
+ *   1. WARP_SELECT (Section 4.3): query-token x centroid scores S = C q^T, the
+ *      n_probe best centroids of every query token, and the missing-similarity
+ *      estimate m_i = score of the first centroid, in score order, at which the
+ *      cumulative cluster size exceeds t'.
+ *   2. Implicit decompression (Section 4.4, Eq. warp_selective_sum): every
+ *      embedding of every probed cluster is scored from its packed b-bit residual
+ *      codes as S_{c,q_i} + sum_d upsilon_{i,d}[code_d], with the per-token table
+ *      upsilon = q_hat x omega_hat.
+ *   3. Two-stage reduction (Section 4.5): token-level max per (document, query
+ *      token) (r_tok), then a document-level sum in which a missing entry takes
+ *      m_i (r_doc, Eq. doc_level_reduce), then the top-k documents.
+ *
+ * Arithmetic. Centroid scores are computed in fp64 in dimension order; every
+ * token score and document score is held in fixed point with
+ * warp_fixed_point_bits() fraction bits (R(x) = round-half-even(x * 2^F)):
+ *   token score  t = R(S_{c,q_i}) + sum_d R(q_{i,d} * omega[code_d])   (int32)
+ *   doc score    s = sum_i (max retrieved t, or R(m_i) if none)        (int64)
+ * so every max and sum is exact and independent of the order of evaluation.
+ * The reported float score is (float)(s * 2^-F). Ties between documents are
+ * broken by the lower document id; ties between centroids by the lower id.
+ *
+ * Index layout. Embeddings are grouped by cluster: cluster c owns embeddings
+ * [cluster_offsets[c], cluster_offsets[c+1]). Each embedding has a document id
+ * and dim * nbits / 8 code bytes; code bytes hold 8 / nbits dimensions each,
+ * the first dimension in the most significant bits (for nbits = 4, dimension
+ * 2j is bits 7..4 of byte j). Inside a cluster, embeddings should be ordered by
+ * document id (results do not depend on it; throughput does).
+ *
+ * Errors. Every call returns WARP_OK or a negative code and never aborts. On an
+ * error the outputs are unspecified and warp_last_error() describes the cause.
+ *
+ * Threads. Calls on one index are serialised by a lock inside the index.
+ */
+#ifndef WARP_H
+#define WARP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    WARP_OK = 0,
+    WARP_EINVAL = -1,  /* an argument is out of range or inconsistent            */
+    WARP_ENOMEM = -2,  /* device memory could not be allocated                   */
+    WARP_EDEVICE = -3, /* no usable gfx950 device, or a HIP runtime call failed  */
+    WARP_ENOTSUP = -4  /* a valid request this engine does not implement         */
+};
+
+typedef struct warp_index warp_index; /* opaque; owns all of its device memory */
+
+/* Number of fraction bits F of the fixed-point token and document scores (26). */
+int warp_fixed_point_bits(void);
+
+/* Thread-local description of the last non-OK return on this thread. */
+const char* warp_last_error(void);
+
+/*
+ * Build a device-resident index (Section 4.1's index: centroids, per-cluster
+ * document ids and packed residual codes, bucket weights).
+ *
+ *   centroids        [n_centroids][dim] fp32, each row of unit norm (within 1e-3)
+ *   n_centroids      >= 1
+ *   dim              must be 128 (else WARP_ENOTSUP)
+ *   cluster_offsets  [n_centroids + 1] int64: offsets[0] = 0, non-decreasing;
+ *                    N = offsets[n_centroids] embeddings, N < 2^40
+ *   doc_ids          [N] int32, 0 <= id < n_docs, grouped by cluster
+ *   codes            [N][dim * nbits / 8] uint8, grouped by cluster
+ *   nbits            2 or 4 (1 and 8: WARP_ENOTSUP)
+ *   bucket_weights   [2^nbits] fp32, finite, |w| <= 2
+ *   n_docs           1 <= n_docs <= 2^24
+ *   out              receives the index on WARP_OK; untouched otherwise
+ *
+ * warp_index_load reads host pointers; warp_index_load_device reads device
+ * pointers (on the current device). Both copy: the caller keeps ownership of
+ * its arrays and may free them once the call returns. Validation reads every
+ * element (offsets, ids, weights, centroid norms) before anything is kept.
+ */
+int warp_index_load(const float* centroids, int32_t n_centroids, int32_t dim,
+                    const int64_t* cluster_offsets, const int32_t* doc_ids, const uint8_t* codes,
+                    int32_t nbits, const float* bucket_weights, int32_t n_docs, warp_index** out);
+int warp_index_load_device(const float* centroids, int32_t n_centroids, int32_t dim,
+                           const int64_t* cluster_offsets, const int32_t* doc_ids,
+                           const uint8_t* codes, int32_t nbits, const float* bucket_weights,
+                           int32_t n_docs, warp_index** out);
+
+/* Free an index and all of its device memory. NULL is ignored. */
+void warp_index_free(warp_index* idx);
+
+/* Sizes of an index: any pointer may be NULL. */
+int warp_index_info(const warp_index* idx, int32_t* n_centroids, int64_t* n_embeddings,
+                    int32_t* n_docs, int32_t* nbits);
+
+/*
+ * Search a batch of queries (Section 4, the four retrieval steps after query
+ * encoding).
+ *
+ *   queries      [n_queries][n_qtok][dim] fp32 host, each token of norm <= 1 + 1e-3
+ *   n_queries    >= 1
+ *   n_qtok       1..32 (query_maxlen = 32); every token takes part in the sum
+ *   nprobe       1..n_centroids; above 256: WARP_ENOTSUP
+ *   t_prime      >= 0, in embeddings
+ *   k            1..4096
+ *   out_doc_ids  [n_queries][k] caller-owned host; -1 past the result count
+ *   out_scores   [n_queries][k] caller-owned host; -inf past the result count
+ *   out_counts   [n_queries] host or NULL: min(k, number of candidate documents)
+ *
+ * Only candidate documents (those with at least one retrieved embedding) are
+ * ranked. Blocks until the results are in host memory.
+ */
+int warp_search(warp_index* idx, const float* queries, int32_t n_queries, int32_t n_qtok,
+                int32_t nprobe, int64_t t_prime, int32_t k, int32_t* out_doc_ids,
+                float* out_scores, int32_t* out_counts);
+
+/*
+ * As warp_search, with every pointer in device memory, enqueued on `hip_stream`
+ * (a hipStream_t, NULL for the default stream); returns once the work is
+ * enqueued. out_fixed_scores [n_queries][k] (int64, INT64_MIN padding) and
+ * out_counts may be NULL. Query norms are checked on the device: that error,
+ * and a centroid-selection overflow (more than 1024 centroids whose scores fall
+ * within about 3e-3 of a selection boundary, only possible with degenerate
+ * centroid sets), are reported by warp_index_sync. The index's scratch memory
+ * is shared by its searches: enqueue the searches of one index on one stream.
+ */
+int warp_search_async(warp_index* idx, const float* queries, int32_t n_queries, int32_t n_qtok,
+                      int32_t nprobe, int64_t t_prime, int32_t k, int32_t* out_doc_ids,
+                      float* out_scores, int32_t* out_counts, int64_t* out_fixed_scores,
+                      void* hip_stream);
+
+/* Wait for the index's outstanding work on `hip_stream` and report any deferred
+ * device-side error. */
+int warp_index_sync(warp_index* idx, void* hip_stream);
+
+/*
+ * warp_search plus intermediate results, all host memory (any may be NULL):
+ *   out_fixed_scores [n_queries][k]                 int64 document scores (INT64_MIN padding)
+ *   sel              [n_queries][n_qtok][nprobe]    probed centroids, in (score desc, id asc) order
+ *   m_fixed          [n_queries][n_qtok]            R(m_i)
+ *   cand_bitmap      [n_queries][ceil(n_docs/32)]   bit d%32 of word d/32: doc d is a candidate
+ *   n_scored         [n_queries]                    embeddings scored (sum of probed cluster sizes)
+ */
+int warp_search_debug(warp_index* idx, const float* queries, int32_t n_queries, int32_t n_qtok,
+                      int32_t nprobe, int64_t t_prime, int32_t k, int32_t* out_doc_ids,
+                      float* out_scores, int32_t* out_counts, int64_t* out_fixed_scores,
+                      int32_t* sel, int64_t* m_fixed, uint32_t* cand_bitmap, int64_t* n_scored);
+
+/*
+ * The fp32 matrix-core centroid scores that drive centroid selection, for
+ * checking their error bound: out [n_tok][n_centroids] fp32 host, for host
+ * queries [n_tok][dim]. Selection treats them as within 2^-13 of the fp64
+ * scores and recomputes every centroid near a selection boundary in fp64.
+ */
+int warp_centroid_filter_scores(warp_index* idx, const float* queries, int32_t n_tok, float* out);
+
+/*
+ * Per-stage device time, measured with HIP events on the stream each search
+ * runs on. warp_set_timing(idx, 1) starts recording and clears the totals;
+ * warp_stage_timings returns, per stage, the summed milliseconds and the number
+ * of launches since then, counting the searches completed by a synchronising
+ * call (warp_search, warp_search_debug, warp_index_sync). Stages: [0] centroid
+ * filter GEMM, [1] selection, [2] plan, [3] residual scan, [4] document fold,
+ * [5] top-k.
+ */
+int warp_set_timing(warp_index* idx, int32_t enable);
+int warp_stage_timings(const warp_index* idx, double* total_ms, int64_t* launches, int32_t n);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

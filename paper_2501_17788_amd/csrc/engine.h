@@ -1,0 +1,85 @@
+// Internal declarations shared by the engine's translation units: constants of
+// the fixed-point contract, device-side layouts, and the host-side launchers
+// each kernel file exports. Nothing here is part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace warp {
+
+constexpr int kDim = 128;          // token embedding dimension
+constexpr int kFrac = 26;          // fixed-point fraction bits of token and doc scores
+constexpr int kMaxQtok = 32;       // query_maxlen
+constexpr int kMaxProbe = 256;     // largest n_probe the selection and scan kernels hold
+constexpr int kMaxK = 4096;        // largest k the device top-k sorts
+constexpr int kMaxDocs = 1 << 24;  // document ids packed into the low 24 bits of a sort key
+constexpr int32_t kAbsent = INT32_MIN;  // "no retrieved embedding" in the token-max table
+
+// Centroid selection: the fp32 matrix-core scores are within kFilterEps of the
+// fp64 scores; bins of the score histogram are wider than 2 * kFilterEps.
+constexpr float kFilterEps = 1.0f / 8192.0f;
+constexpr int kSelBins = 4096;
+constexpr float kSelLim = 1.0625f;  // |score| <= (1 + 1e-3)^2 < kSelLim
+constexpr int kSelCap = 1024;       // centroids near one selection boundary held in LDS
+
+// Residual scan work split: a tile is kScanIters iterations of one embedding per thread.
+constexpr int kScanBlock = 512;
+constexpr int kScanIters = 8;
+constexpr int kScanTile = kScanBlock * kScanIters;
+
+// Error bits the device reports through the index's flag word.
+constexpr int kErrSelOverflow = 1;
+constexpr int kErrSelNoCrossing = 2;
+constexpr int kErrDocRange = 1 << 8;
+constexpr int kErrQueryNorm = 1 << 9;
+
+struct WaveArgs {
+    // index
+    const float* centroids;     // [n_c][128]
+    const int64_t* offsets;     // [n_c + 1]
+    const int32_t* sizes;       // [n_c]
+    const int32_t* doc_ids;     // [N]
+    const uint8_t* codes;       // [N][16 * nbits]
+    const float* weights;       // [2^nbits]
+    int32_t n_c, n_docs, nbits;
+    // wave of queries
+    const float* queries;       // [n_tok][128], n_tok = n_q * n_qtok
+    int32_t n_q, n_qtok, nprobe, k;
+    int64_t t_prime;
+    // scratch
+    float* filter;              // [n_tok][n_c]
+    int32_t* sel;               // [n_tok][nprobe]
+    int32_t* base;              // [n_tok][nprobe]  R(S64) of the probed centroids
+    int64_t* seg_start;         // [n_tok][nprobe]  first embedding of each probed cluster
+    int64_t* seg_pref;          // [n_tok][nprobe + 1] cumulative probed sizes
+    int64_t* m_fixed;           // [n_tok]
+    int64_t* tile_start;        // [n_tok + 1]
+    int32_t* tokmax;            // [n_tok][n_docs], kAbsent when not retrieved
+    uint64_t* keys;             // [n_q][n_docs]
+    int32_t* err;               // device flag word
+    // outputs (device; the debug ones may be null)
+    int32_t* out_ids;           // [n_q][k]
+    float* out_scores;          // [n_q][k]
+    int64_t* out_fixed;         // [n_q][k] or null
+    int32_t* out_counts;        // [n_q] or null
+    int32_t* dbg_sel;           // [n_q][n_qtok][nprobe] or null
+    int64_t* dbg_m;             // [n_q][n_qtok] or null
+    uint32_t* dbg_bitmap;       // [n_q][ceil(n_docs / 32)] or null
+    int64_t* dbg_scored;        // [n_q] or null
+    int32_t scan_grid;          // persistent workgroups of the residual scan
+};
+
+void launch_filter_gemm(const float* q, int32_t n_tok, const float* c, int32_t n_c, float* out,
+                        hipStream_t s);
+void launch_select(const WaveArgs& a, hipStream_t s);
+void launch_plan(const WaveArgs& a, hipStream_t s);
+void launch_scan(const WaveArgs& a, hipStream_t s);
+void launch_fold(const WaveArgs& a, hipStream_t s);
+void launch_topk(const WaveArgs& a, hipStream_t s);
+void launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
+void launch_check_docs(const int32_t* ids, int64_t n, int32_t n_docs, int32_t* err, hipStream_t s);
+void launch_check_queries(const float* q, int64_t n_tok, int32_t* err, hipStream_t s);
+int scan_blocks_per_cu(int nbits);
+
+}  // namespace warp

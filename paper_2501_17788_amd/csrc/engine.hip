@@ -1,0 +1,616 @@
+// Host side of the engine: the C ABI of include/warp.h, argument validation,
+// device memory of the index and of the per-search scratch, and the launch
+// sequence of one search (Section 4: candidate generation, decompression,
+// scoring). Queries are processed in waves; a wave holds one token-max table
+// row per query token and one sort key per document for each of its queries.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "engine.h"
+#include "warp.h"
+
+using namespace warp;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+#define HIP_TRY(expr)                                                                         \
+    do {                                                                                      \
+        hipError_t e_ = (expr);                                                               \
+        if (e_ != hipSuccess) return fail(WARP_EDEVICE, "%s failed: %s", #expr, hipGetErrorString(e_)); \
+    } while (0)
+
+constexpr uint64_t kMagic = 0x5741525049445831ull;  // "WARPIDX1"
+constexpr int kStages = 6;
+
+struct DevBuf {
+    void* p = nullptr;
+    size_t bytes = 0;
+};
+
+}  // namespace
+
+struct warp_index {
+    uint64_t magic = kMagic;
+    int device = 0;
+    int32_t n_c = 0, n_docs = 0, nbits = 0;
+    int64_t n_emb = 0;
+    float* centroids = nullptr;
+    int64_t* offsets = nullptr;
+    int32_t* sizes = nullptr;
+    int32_t* doc_ids = nullptr;
+    uint8_t* codes = nullptr;
+    float* weights = nullptr;
+    int32_t* err = nullptr;
+    hipStream_t stream = nullptr;
+    int scan_grid = 0;
+    // per-search scratch, grown on demand
+    DevBuf filter, sel, base, seg_start, seg_pref, m_fixed, tile_start, tokmax, keys;
+    int64_t tokmax_ready = 0;  // leading elements of tokmax holding kAbsent
+    // staging of the host-pointer calls
+    DevBuf st_q, st_ids, st_scores, st_fixed, st_counts, st_sel, st_m, st_bitmap, st_scored;
+    std::mutex lock;
+    // stage timing
+    bool timing = false;
+    std::vector<hipEvent_t> ev_pool;
+    std::vector<hipEvent_t> ev_pending;  // groups of kStages + 1
+    double stage_ms[kStages] = {0};
+    int64_t stage_launches[kStages] = {0};
+};
+
+namespace {
+
+int grow(DevBuf& b, size_t bytes) {
+    if (bytes == 0) bytes = 16;
+    if (b.bytes >= bytes) return WARP_OK;
+    if (b.p) (void)hipFree(b.p);
+    b.p = nullptr;
+    b.bytes = 0;
+    if (hipMalloc(&b.p, bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(WARP_ENOMEM, "hipMalloc of %zu bytes failed", bytes);
+    }
+    b.bytes = bytes;
+    return WARP_OK;
+}
+
+void release(DevBuf& b) {
+    if (b.p) (void)hipFree(b.p);
+    b.p = nullptr;
+    b.bytes = 0;
+}
+
+int check_device() {
+    int n = 0;
+    if (hipGetDeviceCount(&n) != hipSuccess || n < 1) {
+        (void)hipGetLastError();
+        return fail(WARP_EDEVICE, "no HIP device is available");
+    }
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    hipDeviceProp_t prop;
+    HIP_TRY(hipGetDeviceProperties(&prop, dev));
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return fail(WARP_EDEVICE, "device %d is %s; this library is built for gfx950 only", dev,
+                    prop.gcnArchName);
+    return WARP_OK;
+}
+
+bool is_index(const warp_index* idx) { return idx && idx->magic == kMagic; }
+
+// Host-side checks of the small index arrays.
+int validate_index_host(const float* C, int32_t n_c, int32_t dim, const int64_t* off, int32_t nbits,
+                        const float* w, int32_t n_docs) {
+    if (n_c < 1) return fail(WARP_EINVAL, "n_centroids must be >= 1 (got %d)", n_c);
+    if (dim != kDim) return fail(WARP_ENOTSUP, "dim must be 128 (got %d)", dim);
+    if (nbits == 1 || nbits == 8) return fail(WARP_ENOTSUP, "nbits = %d is not implemented (2 or 4)", nbits);
+    if (nbits != 2 && nbits != 4) return fail(WARP_EINVAL, "nbits must be 2 or 4 (got %d)", nbits);
+    if (n_docs < 1 || n_docs > kMaxDocs) return fail(WARP_EINVAL, "n_docs must be in [1, 2^24] (got %d)", n_docs);
+    if (!C || !off || !w) return fail(WARP_EINVAL, "null index array");
+    if (off[0] != 0) return fail(WARP_EINVAL, "cluster_offsets[0] must be 0");
+    for (int32_t c = 0; c < n_c; ++c) {
+        const int64_t sz = off[c + 1] - off[c];
+        if (sz < 0) return fail(WARP_EINVAL, "cluster_offsets decrease at cluster %d", c);
+        if (sz > INT32_MAX) return fail(WARP_ENOTSUP, "cluster %d has more than 2^31-1 embeddings", c);
+    }
+    if (off[n_c] >= (1ll << 40)) return fail(WARP_EINVAL, "more than 2^40 embeddings");
+    for (int b = 0; b < (1 << nbits); ++b)
+        if (!std::isfinite(w[b]) || std::fabs(w[b]) > 2.0f)
+            return fail(WARP_EINVAL, "bucket weight %d is not finite or exceeds 2 in magnitude", b);
+    for (int32_t c = 0; c < n_c; ++c) {
+        double s = 0;
+        for (int d = 0; d < kDim; ++d) {
+            const float v = C[(int64_t)c * kDim + d];
+            if (!std::isfinite(v)) return fail(WARP_EINVAL, "centroid %d is not finite", c);
+            s += (double)v * v;
+        }
+        if (std::fabs(std::sqrt(s) - 1.0) > 1e-3) return fail(WARP_EINVAL, "centroid %d is not of unit norm", c);
+    }
+    return WARP_OK;
+}
+
+int validate_queries_host(const float* q, int64_t n_tok) {
+    for (int64_t t = 0; t < n_tok; ++t) {
+        double s = 0;
+        for (int d = 0; d < kDim; ++d) {
+            const float v = q[t * kDim + d];
+            if (!std::isfinite(v)) return fail(WARP_EINVAL, "query token %lld is not finite", (long long)t);
+            s += (double)v * v;
+        }
+        if (std::sqrt(s) > 1.0 + 1e-3) return fail(WARP_EINVAL, "query token %lld has norm > 1 + 1e-3", (long long)t);
+    }
+    return WARP_OK;
+}
+
+int validate_search(const warp_index* idx, const void* queries, int32_t n_queries, int32_t n_qtok,
+                    int32_t nprobe, int64_t t_prime, int32_t k, const void* ids, const void* scores) {
+    if (!is_index(idx)) return fail(WARP_EINVAL, "invalid or freed index handle");
+    if (!queries || !ids || !scores) return fail(WARP_EINVAL, "null query or output pointer");
+    if (n_queries < 1) return fail(WARP_EINVAL, "n_queries must be >= 1 (got %d)", n_queries);
+    if (n_qtok < 1 || n_qtok > kMaxQtok) return fail(WARP_EINVAL, "n_qtok must be in [1, 32] (got %d)", n_qtok);
+    if (nprobe < 1 || nprobe > idx->n_c)
+        return fail(WARP_EINVAL, "nprobe must be in [1, n_centroids] (got %d)", nprobe);
+    if (nprobe > kMaxProbe) return fail(WARP_ENOTSUP, "nprobe above %d is not implemented", kMaxProbe);
+    if (t_prime < 0) return fail(WARP_EINVAL, "t_prime must be >= 0");
+    if (k < 1) return fail(WARP_EINVAL, "k must be >= 1 (got %d)", k);
+    if (k > kMaxK) return fail(WARP_ENOTSUP, "k above %d is not implemented", kMaxK);
+    return WARP_OK;
+}
+
+int finish_load(warp_index* idx, const int64_t* off_host) {
+    std::vector<int32_t> sz(idx->n_c);
+    for (int32_t c = 0; c < idx->n_c; ++c) sz[c] = (int32_t)(off_host[c + 1] - off_host[c]);
+    HIP_TRY(hipMemcpy(idx->sizes, sz.data(), sizeof(int32_t) * idx->n_c, hipMemcpyHostToDevice));
+    launch_fill_i32(idx->err, 1, 0, idx->stream);
+    launch_check_docs(idx->doc_ids, idx->n_emb, idx->n_docs, idx->err, idx->stream);
+    int32_t err = 0;
+    HIP_TRY(hipMemcpyAsync(&err, idx->err, sizeof err, hipMemcpyDeviceToHost, idx->stream));
+    HIP_TRY(hipStreamSynchronize(idx->stream));
+    if (err & kErrDocRange) return fail(WARP_EINVAL, "a document id is outside [0, n_docs)");
+    int cus = 0;
+    HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, idx->device));
+    idx->scan_grid = cus * scan_blocks_per_cu(idx->nbits);
+    return WARP_OK;
+}
+
+int load_common(const float* C, int32_t n_c, int32_t dim, const int64_t* off, const int32_t* doc_ids,
+                const uint8_t* codes, int32_t nbits, const float* w, int32_t n_docs, warp_index** out,
+                bool device_ptrs) {
+    if (!out) return fail(WARP_EINVAL, "out is null");
+    if (!C || !off || !w || !doc_ids || !codes) return fail(WARP_EINVAL, "null index array");
+    if (n_c < 1) return fail(WARP_EINVAL, "n_centroids must be >= 1 (got %d)", n_c);
+    if (dim != kDim) return fail(WARP_ENOTSUP, "dim must be 128 (got %d)", dim);
+    int rc = WARP_OK;
+    if (!device_ptrs) {  // host arrays are checked before any device call
+        rc = validate_index_host(C, n_c, dim, off, nbits, w, n_docs);
+        if (rc) return rc;
+    }
+    rc = check_device();
+    if (rc) return rc;
+    // host copies of the small arrays for validation
+    std::vector<float> hC, hw;
+    std::vector<int64_t> hoff;
+    const float* vC = C;
+    const int64_t* voff = off;
+    const float* vw = w;
+    if (device_ptrs) {
+        if (nbits != 2 && nbits != 4) return validate_index_host(C, n_c, dim, off, nbits, w, n_docs);
+        hC.resize((size_t)n_c * kDim);
+        hoff.resize((size_t)n_c + 1);
+        hw.resize((size_t)1 << nbits);
+        HIP_TRY(hipMemcpy(hC.data(), C, hC.size() * 4, hipMemcpyDeviceToHost));
+        HIP_TRY(hipMemcpy(hoff.data(), off, hoff.size() * 8, hipMemcpyDeviceToHost));
+        HIP_TRY(hipMemcpy(hw.data(), w, hw.size() * 4, hipMemcpyDeviceToHost));
+        vC = hC.data();
+        voff = hoff.data();
+        vw = hw.data();
+    }
+    if (device_ptrs) {
+        rc = validate_index_host(vC, n_c, dim, voff, nbits, vw, n_docs);
+        if (rc) return rc;
+    }
+
+    warp_index* idx = new warp_index();
+    HIP_TRY(hipGetDevice(&idx->device));
+    idx->n_c = n_c;
+    idx->n_docs = n_docs;
+    idx->nbits = nbits;
+    idx->n_emb = voff[n_c];
+    const size_t row = (size_t)kDim * nbits / 8;
+    const hipMemcpyKind kind = device_ptrs ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
+    auto alloc = [&](void** p, size_t bytes) -> int {
+        if (hipMalloc(p, bytes ? bytes : 16) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(WARP_ENOMEM, "hipMalloc of %zu bytes for the index failed", bytes);
+        }
+        return WARP_OK;
+    };
+    rc = alloc((void**)&idx->centroids, (size_t)n_c * kDim * 4);
+    if (!rc) rc = alloc((void**)&idx->offsets, ((size_t)n_c + 1) * 8);
+    if (!rc) rc = alloc((void**)&idx->sizes, (size_t)n_c * 4);
+    if (!rc) rc = alloc((void**)&idx->doc_ids, (size_t)idx->n_emb * 4);
+    if (!rc) rc = alloc((void**)&idx->codes, (size_t)idx->n_emb * row + 16);
+    if (!rc) rc = alloc((void**)&idx->weights, (size_t)4 << nbits);
+    if (!rc) rc = alloc((void**)&idx->err, 64);
+    if (!rc && hipStreamCreateWithFlags(&idx->stream, hipStreamNonBlocking) != hipSuccess)
+        rc = fail(WARP_EDEVICE, "hipStreamCreate failed");
+    if (!rc && (hipMemcpy(idx->centroids, C, (size_t)n_c * kDim * 4, kind) != hipSuccess ||
+                hipMemcpy(idx->offsets, off, ((size_t)n_c + 1) * 8, kind) != hipSuccess ||
+                hipMemcpy(idx->doc_ids, doc_ids, (size_t)idx->n_emb * 4, kind) != hipSuccess ||
+                hipMemcpy(idx->codes, codes, (size_t)idx->n_emb * row, kind) != hipSuccess ||
+                hipMemcpy(idx->weights, w, (size_t)4 << nbits, kind) != hipSuccess))
+        rc = fail(WARP_EDEVICE, "copying the index to the device failed");
+    if (!rc) rc = finish_load(idx, voff);
+    if (rc) {
+        std::string msg = g_err;
+        warp_index_free(idx);
+        g_err = msg;
+        return rc;
+    }
+    *out = idx;
+    return WARP_OK;
+}
+
+// Device scratch for a wave of `qw` queries of `T` tokens.
+int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P) {
+    const int64_t n_tok = (int64_t)qw * T;
+    int rc = WARP_OK;
+    if (!rc) rc = grow(idx->filter, (size_t)n_tok * idx->n_c * 4);
+    if (!rc) rc = grow(idx->sel, (size_t)n_tok * P * 4);
+    if (!rc) rc = grow(idx->base, (size_t)n_tok * P * 4);
+    if (!rc) rc = grow(idx->seg_start, (size_t)n_tok * P * 8);
+    if (!rc) rc = grow(idx->seg_pref, (size_t)n_tok * (P + 1) * 8);
+    if (!rc) rc = grow(idx->m_fixed, (size_t)n_tok * 8);
+    if (!rc) rc = grow(idx->tile_start, (size_t)(n_tok + 1) * 8);
+    if (!rc) rc = grow(idx->keys, (size_t)qw * idx->n_docs * 8);
+    if (rc) return rc;
+    const int64_t need = n_tok * idx->n_docs;
+    if ((int64_t)(idx->tokmax.bytes / 4) < need) {
+        rc = grow(idx->tokmax, (size_t)need * 4);
+        if (rc) return rc;
+        idx->tokmax_ready = 0;
+    }
+    if (idx->tokmax_ready < need) {
+        launch_fill_i32((int32_t*)idx->tokmax.p, need, kAbsent, idx->stream);
+        HIP_TRY(hipStreamSynchronize(idx->stream));
+        idx->tokmax_ready = need;
+    }
+    return WARP_OK;
+}
+
+int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T) {
+    size_t budget = (size_t)32 << 30;
+    if (const char* s = std::getenv("WARP_SCRATCH_MB")) budget = (size_t)std::atoll(s) << 20;
+    size_t free_b = 0, total_b = 0;
+    if (hipMemGetInfo(&free_b, &total_b) == hipSuccess) {
+        const size_t cap = free_b / 2 + idx->tokmax.bytes + idx->filter.bytes + idx->keys.bytes;
+        if (cap < budget) budget = cap;
+    }
+    const size_t per = (size_t)T * idx->n_docs * 4 + (size_t)idx->n_docs * 8 + (size_t)T * idx->n_c * 4 +
+                       (size_t)T * 1024;
+    int64_t qw = (int64_t)(budget / per);
+    if (qw < 1) qw = 1;
+    if (qw > n_queries) qw = n_queries;
+    if (qw > 65535) qw = 65535;
+    return (int32_t)qw;
+}
+
+hipEvent_t take_event(warp_index* idx) {
+    if (!idx->ev_pool.empty()) {
+        hipEvent_t e = idx->ev_pool.back();
+        idx->ev_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    (void)hipEventCreate(&e);
+    return e;
+}
+
+void settle_timings(warp_index* idx) {
+    const size_t g = kStages + 1;
+    for (size_t i = 0; i + g <= idx->ev_pending.size(); i += g) {
+        for (int s = 0; s < kStages; ++s) {
+            float ms = 0.f;
+            if (hipEventElapsedTime(&ms, idx->ev_pending[i + s], idx->ev_pending[i + s + 1]) == hipSuccess) {
+                idx->stage_ms[s] += ms;
+                idx->stage_launches[s] += 1;
+            }
+        }
+    }
+    for (hipEvent_t e : idx->ev_pending) idx->ev_pool.push_back(e);
+    idx->ev_pending.clear();
+}
+
+struct SearchOut {
+    int32_t* ids;
+    float* scores;
+    int64_t* fixed;
+    int32_t* counts;
+    int32_t* sel;
+    int64_t* m;
+    uint32_t* bitmap;
+    int64_t* scored;
+};
+
+// Enqueue a whole search on `s`; every pointer is device memory.
+int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t T, int32_t P,
+                   int64_t t_prime, int32_t k, const SearchOut& o, hipStream_t s) {
+    const int32_t qw = wave_queries(idx, n_queries, T);
+    int rc = reserve(idx, qw, T, P);
+    if (rc) return rc;
+    launch_check_queries(dq, (int64_t)n_queries * T, idx->err, s);
+    const int64_t words = ((int64_t)idx->n_docs + 31) / 32;
+    for (int32_t q0 = 0; q0 < n_queries; q0 += qw) {
+        const int32_t nq = n_queries - q0 < qw ? n_queries - q0 : qw;
+        WaveArgs a{};
+        a.centroids = idx->centroids;
+        a.offsets = idx->offsets;
+        a.sizes = idx->sizes;
+        a.doc_ids = idx->doc_ids;
+        a.codes = idx->codes;
+        a.weights = idx->weights;
+        a.n_c = idx->n_c;
+        a.n_docs = idx->n_docs;
+        a.nbits = idx->nbits;
+        a.queries = dq + (int64_t)q0 * T * kDim;
+        a.n_q = nq;
+        a.n_qtok = T;
+        a.nprobe = P;
+        a.k = k;
+        a.t_prime = t_prime;
+        a.filter = (float*)idx->filter.p;
+        a.sel = (int32_t*)idx->sel.p;
+        a.base = (int32_t*)idx->base.p;
+        a.seg_start = (int64_t*)idx->seg_start.p;
+        a.seg_pref = (int64_t*)idx->seg_pref.p;
+        a.m_fixed = (int64_t*)idx->m_fixed.p;
+        a.tile_start = (int64_t*)idx->tile_start.p;
+        a.tokmax = (int32_t*)idx->tokmax.p;
+        a.keys = (uint64_t*)idx->keys.p;
+        a.err = idx->err;
+        a.out_ids = o.ids + (int64_t)q0 * k;
+        a.out_scores = o.scores + (int64_t)q0 * k;
+        a.out_fixed = o.fixed ? o.fixed + (int64_t)q0 * k : nullptr;
+        a.out_counts = o.counts ? o.counts + q0 : nullptr;
+        a.dbg_sel = o.sel ? o.sel + (int64_t)q0 * T * P : nullptr;
+        a.dbg_m = o.m ? o.m + (int64_t)q0 * T : nullptr;
+        a.dbg_bitmap = o.bitmap ? o.bitmap + (int64_t)q0 * words : nullptr;
+        a.dbg_scored = o.scored ? o.scored + q0 : nullptr;
+        a.scan_grid = idx->scan_grid;
+
+        hipEvent_t ev[kStages + 1] = {};
+        if (idx->timing)
+            for (int e = 0; e <= kStages; ++e) ev[e] = take_event(idx);
+        auto mark = [&](int e) {
+            if (idx->timing) (void)hipEventRecord(ev[e], s);
+        };
+        mark(0);
+        launch_filter_gemm(a.queries, nq * T, idx->centroids, idx->n_c, a.filter, s);
+        mark(1);
+        launch_select(a, s);
+        mark(2);
+        launch_plan(a, s);
+        mark(3);
+        launch_scan(a, s);
+        mark(4);
+        launch_fold(a, s);
+        mark(5);
+        launch_topk(a, s);
+        mark(6);
+        if (idx->timing)
+            for (int e = 0; e <= kStages; ++e) idx->ev_pending.push_back(ev[e]);
+        hipError_t le = hipGetLastError();
+        if (le != hipSuccess) return fail(WARP_EDEVICE, "kernel launch failed: %s", hipGetErrorString(le));
+    }
+    return WARP_OK;
+}
+
+int read_device_errors(warp_index* idx, hipStream_t s) {
+    int32_t err = 0;
+    HIP_TRY(hipMemcpyAsync(&err, idx->err, sizeof err, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (idx->timing) settle_timings(idx);
+    if (err) launch_fill_i32(idx->err, 1, 0, s);
+    if (err & kErrQueryNorm)
+        return fail(WARP_EINVAL, "a query token is not finite or has norm > 1 + 1e-3");
+    if (err & kErrSelOverflow)
+        return fail(WARP_ENOTSUP,
+                    "centroid selection overflow: more than %d centroids fall in one selection band "
+                    "(degenerate centroid scores)", kSelCap);
+    if (err & kErrSelNoCrossing) return fail(WARP_EDEVICE, "centroid selection found no t' crossing");
+    return WARP_OK;
+}
+
+int search_host(warp_index* idx, const float* queries, int32_t n_queries, int32_t n_qtok, int32_t nprobe,
+                int64_t t_prime, int32_t k, int32_t* ids, float* scores, int32_t* counts, int64_t* fixed,
+                int32_t* sel, int64_t* m, uint32_t* bitmap, int64_t* scored) {
+    int rc = validate_search(idx, queries, n_queries, n_qtok, nprobe, t_prime, k, ids, scores);
+    if (rc) return rc;
+    std::lock_guard<std::mutex> g(idx->lock);
+    HIP_TRY(hipSetDevice(idx->device));
+    const int64_t n_tok = (int64_t)n_queries * n_qtok;
+    rc = validate_queries_host(queries, n_tok);
+    if (rc) return rc;
+    const int64_t words = ((int64_t)idx->n_docs + 31) / 32;
+    const size_t nk = (size_t)n_queries * k;
+    if (!rc) rc = grow(idx->st_q, (size_t)n_tok * kDim * 4);
+    if (!rc) rc = grow(idx->st_ids, nk * 4);
+    if (!rc) rc = grow(idx->st_scores, nk * 4);
+    if (!rc) rc = grow(idx->st_fixed, nk * 8);
+    if (!rc) rc = grow(idx->st_counts, (size_t)n_queries * 4);
+    if (!rc && sel) rc = grow(idx->st_sel, (size_t)n_tok * nprobe * 4);
+    if (!rc && m) rc = grow(idx->st_m, (size_t)n_tok * 8);
+    if (!rc && bitmap) rc = grow(idx->st_bitmap, (size_t)n_queries * words * 4);
+    if (!rc && scored) rc = grow(idx->st_scored, (size_t)n_queries * 8);
+    if (rc) return rc;
+    hipStream_t s = idx->stream;
+    HIP_TRY(hipMemcpyAsync(idx->st_q.p, queries, (size_t)n_tok * kDim * 4, hipMemcpyHostToDevice, s));
+    SearchOut o{(int32_t*)idx->st_ids.p, (float*)idx->st_scores.p, (int64_t*)idx->st_fixed.p,
+                (int32_t*)idx->st_counts.p,  sel ? (int32_t*)idx->st_sel.p : nullptr,
+                m ? (int64_t*)idx->st_m.p : nullptr, bitmap ? (uint32_t*)idx->st_bitmap.p : nullptr,
+                scored ? (int64_t*)idx->st_scored.p : nullptr};
+    rc = enqueue_search(idx, (const float*)idx->st_q.p, n_queries, n_qtok, nprobe, t_prime, k, o, s);
+    if (rc) return rc;
+    HIP_TRY(hipMemcpyAsync(ids, o.ids, nk * 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(scores, o.scores, nk * 4, hipMemcpyDeviceToHost, s));
+    if (fixed) HIP_TRY(hipMemcpyAsync(fixed, o.fixed, nk * 8, hipMemcpyDeviceToHost, s));
+    if (counts) HIP_TRY(hipMemcpyAsync(counts, o.counts, (size_t)n_queries * 4, hipMemcpyDeviceToHost, s));
+    if (sel) HIP_TRY(hipMemcpyAsync(sel, o.sel, (size_t)n_tok * nprobe * 4, hipMemcpyDeviceToHost, s));
+    if (m) HIP_TRY(hipMemcpyAsync(m, o.m, (size_t)n_tok * 8, hipMemcpyDeviceToHost, s));
+    if (bitmap)
+        HIP_TRY(hipMemcpyAsync(bitmap, o.bitmap, (size_t)n_queries * words * 4, hipMemcpyDeviceToHost, s));
+    if (scored) HIP_TRY(hipMemcpyAsync(scored, o.scored, (size_t)n_queries * 8, hipMemcpyDeviceToHost, s));
+    return read_device_errors(idx, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+int warp_fixed_point_bits(void) { return kFrac; }
+
+const char* warp_last_error(void) { return g_err.c_str(); }
+
+int warp_index_load(const float* centroids, int32_t n_centroids, int32_t dim, const int64_t* cluster_offsets,
+                    const int32_t* doc_ids, const uint8_t* codes, int32_t nbits, const float* bucket_weights,
+                    int32_t n_docs, warp_index** out) {
+    return load_common(centroids, n_centroids, dim, cluster_offsets, doc_ids, codes, nbits, bucket_weights,
+                       n_docs, out, false);
+}
+
+int warp_index_load_device(const float* centroids, int32_t n_centroids, int32_t dim,
+                           const int64_t* cluster_offsets, const int32_t* doc_ids, const uint8_t* codes,
+                           int32_t nbits, const float* bucket_weights, int32_t n_docs, warp_index** out) {
+    return load_common(centroids, n_centroids, dim, cluster_offsets, doc_ids, codes, nbits, bucket_weights,
+                       n_docs, out, true);
+}
+
+void warp_index_free(warp_index* idx) {
+    if (!is_index(idx)) return;
+    {
+        std::lock_guard<std::mutex> g(idx->lock);
+        (void)hipSetDevice(idx->device);
+        if (idx->stream) (void)hipStreamSynchronize(idx->stream);
+        for (void* p : {(void*)idx->centroids, (void*)idx->offsets, (void*)idx->sizes, (void*)idx->doc_ids,
+                        (void*)idx->codes, (void*)idx->weights, (void*)idx->err})
+            if (p) (void)hipFree(p);
+        for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_start, &idx->seg_pref, &idx->m_fixed,
+                          &idx->tile_start, &idx->tokmax, &idx->keys, &idx->st_q, &idx->st_ids, &idx->st_scores,
+                          &idx->st_fixed, &idx->st_counts, &idx->st_sel, &idx->st_m, &idx->st_bitmap,
+                          &idx->st_scored})
+            release(*b);
+        for (hipEvent_t e : idx->ev_pool) (void)hipEventDestroy(e);
+        for (hipEvent_t e : idx->ev_pending) (void)hipEventDestroy(e);
+        if (idx->stream) (void)hipStreamDestroy(idx->stream);
+        idx->magic = 0;
+    }
+    delete idx;
+}
+
+int warp_index_info(const warp_index* idx, int32_t* n_centroids, int64_t* n_embeddings, int32_t* n_docs,
+                    int32_t* nbits) {
+    if (!is_index(idx)) return fail(WARP_EINVAL, "invalid or freed index handle");
+    if (n_centroids) *n_centroids = idx->n_c;
+    if (n_embeddings) *n_embeddings = idx->n_emb;
+    if (n_docs) *n_docs = idx->n_docs;
+    if (nbits) *nbits = idx->nbits;
+    return WARP_OK;
+}
+
+int warp_search(warp_index* idx, const float* queries, int32_t n_queries, int32_t n_qtok, int32_t nprobe,
+                int64_t t_prime, int32_t k, int32_t* out_doc_ids, float* out_scores, int32_t* out_counts) {
+    return search_host(idx, queries, n_queries, n_qtok, nprobe, t_prime, k, out_doc_ids, out_scores, out_counts,
+                       nullptr, nullptr, nullptr, nullptr, nullptr);
+}
+
+int warp_search_debug(warp_index* idx, const float* queries, int32_t n_queries, int32_t n_qtok, int32_t nprobe,
+                      int64_t t_prime, int32_t k, int32_t* out_doc_ids, float* out_scores, int32_t* out_counts,
+                      int64_t* out_fixed_scores, int32_t* sel, int64_t* m_fixed, uint32_t* cand_bitmap,
+                      int64_t* n_scored) {
+    return search_host(idx, queries, n_queries, n_qtok, nprobe, t_prime, k, out_doc_ids, out_scores, out_counts,
+                       out_fixed_scores, sel, m_fixed, cand_bitmap, n_scored);
+}
+
+int warp_search_async(warp_index* idx, const float* queries, int32_t n_queries, int32_t n_qtok, int32_t nprobe,
+                      int64_t t_prime, int32_t k, int32_t* out_doc_ids, float* out_scores, int32_t* out_counts,
+                      int64_t* out_fixed_scores, void* hip_stream) {
+    int rc = validate_search(idx, queries, n_queries, n_qtok, nprobe, t_prime, k, out_doc_ids, out_scores);
+    if (rc) return rc;
+    std::lock_guard<std::mutex> g(idx->lock);
+    HIP_TRY(hipSetDevice(idx->device));
+    hipStream_t s = (hipStream_t)hip_stream;
+    SearchOut o{out_doc_ids, out_scores, out_fixed_scores, out_counts, nullptr, nullptr, nullptr, nullptr};
+    return enqueue_search(idx, queries, n_queries, n_qtok, nprobe, t_prime, k, o, s);
+}
+
+int warp_index_sync(warp_index* idx, void* hip_stream) {
+    if (!is_index(idx)) return fail(WARP_EINVAL, "invalid or freed index handle");
+    std::lock_guard<std::mutex> g(idx->lock);
+    HIP_TRY(hipSetDevice(idx->device));
+    return read_device_errors(idx, (hipStream_t)hip_stream);
+}
+
+int warp_centroid_filter_scores(warp_index* idx, const float* queries, int32_t n_tok, float* out) {
+    if (!is_index(idx)) return fail(WARP_EINVAL, "invalid or freed index handle");
+    if (!queries || !out || n_tok < 1) return fail(WARP_EINVAL, "bad arguments");
+    std::lock_guard<std::mutex> g(idx->lock);
+    HIP_TRY(hipSetDevice(idx->device));
+    DevBuf q, f;
+    int rc = grow(q, (size_t)n_tok * kDim * 4);
+    if (!rc) rc = grow(f, (size_t)n_tok * idx->n_c * 4);
+    if (!rc) {
+        hipStream_t s = idx->stream;
+        if (hipMemcpyAsync(q.p, queries, (size_t)n_tok * kDim * 4, hipMemcpyHostToDevice, s) != hipSuccess)
+            rc = fail(WARP_EDEVICE, "copy failed");
+        if (!rc) launch_filter_gemm((const float*)q.p, n_tok, idx->centroids, idx->n_c, (float*)f.p, s);
+        if (!rc && (hipMemcpyAsync(out, f.p, (size_t)n_tok * idx->n_c * 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
+                    hipStreamSynchronize(s) != hipSuccess))
+            rc = fail(WARP_EDEVICE, "filter scores failed");
+    }
+    release(q);
+    release(f);
+    return rc;
+}
+
+int warp_set_timing(warp_index* idx, int32_t enable) {
+    if (!is_index(idx)) return fail(WARP_EINVAL, "invalid or freed index handle");
+    std::lock_guard<std::mutex> g(idx->lock);
+    idx->timing = enable != 0;
+    for (int s = 0; s < kStages; ++s) {
+        idx->stage_ms[s] = 0;
+        idx->stage_launches[s] = 0;
+    }
+    for (hipEvent_t e : idx->ev_pending) idx->ev_pool.push_back(e);
+    idx->ev_pending.clear();
+    return WARP_OK;
+}
+
+int warp_stage_timings(const warp_index* idx, double* total_ms, int64_t* launches, int32_t n) {
+    if (!is_index(idx)) return fail(WARP_EINVAL, "invalid or freed index handle");
+    for (int s = 0; s < n && s < kStages; ++s) {
+        if (total_ms) total_ms[s] = idx->stage_ms[s];
+        if (launches) launches[s] = idx->stage_launches[s];
+    }
+    return WARP_OK;
+}
+
+}  // extern "C"

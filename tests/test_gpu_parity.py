@@ -1,0 +1,281 @@
+"""Parity of the HIP engine with the CPU oracle (run on an MI355X).
+
+Bit-exact: probed centroids and their order, the missing-similarity estimates,
+candidate sets, embeddings scored, top-k ids and fixed-point document scores.
+Float scores: the float of the same fixed-point value (identical), and within
+1e-4 relative of the fp64 real-valued score.
+"""
+from __future__ import annotations
+
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from helpers import FRAC, explicit_decompress, load_dyadic
+
+pytestmark = pytest.mark.gpu
+
+EXACT = ("ids", "fixed", "counts", "sel", "m_fixed", "cand_bitmap", "n_scored")
+
+
+def _engine():
+    import paper_2501_17788_amd as w
+    return w
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def compare(got: dict, want: dict, rows=None, label=""):
+    for key in EXACT:
+        g = got[key] if rows is None else got[key][rows]
+        if not np.array_equal(g, want[key]):
+            bad = np.argwhere(g != want[key]) if g.shape == want[key].shape else "shape"
+            raise AssertionError(f"{label}: {key} differs at {bad[:5] if not isinstance(bad, str) else bad}")
+    g = got["scores"] if rows is None else got["scores"][rows]
+    np.testing.assert_array_equal(g, want["scores"])
+
+
+def run_both(data, queries=None, nprobe=None, t_prime=None, k=None, label=""):
+    w = _engine()
+    wl = data.workload
+    Q = data.queries if queries is None else queries
+    nprobe = wl.nprobe if nprobe is None else nprobe
+    t_prime = wl.t_prime if t_prime is None else t_prime
+    k = wl.k if k is None else k
+    say(f"[{label}] n_emb={data.n_embeddings} n_c={len(data.offsets) - 1} nbits={data.nbits} "
+        f"queries={Q.shape} nprobe={nprobe} t'={t_prime} k={k}")
+    with w.Index.from_synthetic(data) as ix:
+        got = ix.search_debug(Q, nprobe, t_prime, k)
+    want = oracle.search_index(data, queries=Q, nprobe=nprobe, t_prime=t_prime, k=k)
+    compare(got, want, label=label)
+    return got
+
+
+def real_valued_scores(data, Q, sel, m_fixed, docs):
+    """fp64 scores of `docs` for one query: explicit decompression of every probed
+    embedding (Eq. decompress), token max per doc, missing entries take m_i."""
+    X = explicit_decompress(data.centroids, data.offsets, data.codes, data.nbits, data.bucket_weights)
+    out = np.zeros(len(docs))
+    pos = {d: j for j, d in enumerate(docs)}
+    for i, q in enumerate(Q):
+        best = {}
+        for c in sel[i]:
+            e0, e1 = int(data.offsets[c]), int(data.offsets[c + 1])
+            s = X[e0:e1] @ q.astype(np.float64)
+            for d, v in zip(data.doc_ids[e0:e1].tolist(), s.tolist()):
+                if d in pos:
+                    best[d] = max(best.get(d, -np.inf), v)
+        # m_i as a real value: the estimate is an fp64 centroid score, R() of it is stored
+        for d, j in pos.items():
+            out[j] += best[d] if d in best else m_fixed[i] / FRAC
+    return out
+
+
+# ----------------------------------------------------------------------------- hand-built
+
+@pytest.mark.parametrize("case", range(8))
+def test_dyadic_example(case):
+    w = _engine()
+    g, ix_arrays, Q = load_dyadic()
+    c = g["cases"][case]
+    say(f"[dyadic {c['name']}] nprobe={c['nprobe']} t'={c['t_prime']} k={c['k']}")
+    with w.Index(**ix_arrays) as ix:
+        got = ix.search_debug(Q, c["nprobe"], c["t_prime"], c["k"])
+    assert got["ids"].tolist() == c["ids"]
+    assert got["sel"].tolist() == c["sel"]
+    assert (got["m_fixed"] / FRAC).tolist() == c["m"]
+    assert got["n_scored"].tolist() == c["n_scored"]
+    assert got["counts"].tolist() == c["counts"]
+    want = oracle.search(queries=Q, nprobe=c["nprobe"], t_prime=c["t_prime"], k=c["k"], **ix_arrays)
+    compare(got, want, label=f"dyadic {c['name']}")
+
+
+# ----------------------------------------------------------------------------- random small
+
+CASES = [
+    # seed, n_centroids, n_docs, max_len, nbits, n_queries, n_qtok, nprobe, t_prime, k
+    (0, 16, 40, 8, 4, 3, 4, 4, 10, 5),
+    (1, 16, 40, 8, 2, 3, 4, 4, 10, 5),
+    (2, 1, 10, 3, 4, 2, 32, 1, 0, 20),          # one centroid
+    (3, 50, 300, 12, 4, 5, 32, 7, 0, 50),       # t' = 0
+    (4, 50, 300, 12, 2, 5, 17, 7, 10 ** 9, 50),  # t' above N: lowest score
+    (5, 64, 200, 10, 4, 4, 32, 64, 100, 300),   # nprobe = all clusters, k above candidates
+    (6, 200, 1000, 20, 4, 7, 32, 32, 500, 100),
+    (7, 200, 1000, 20, 2, 7, 1, 3, 50, 1),      # one query token, k = 1
+    (8, 300, 5000, 30, 4, 3, 32, 256, 2000, 4096),  # largest nprobe and k
+    (9, 40, 100000, 1, 4, 2, 8, 5, 7, 10),      # most documents have no embedding at all
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"seed{c[0]}" for c in CASES])
+def test_random_small(case):
+    seed, n_c, n_docs, max_len, nbits, nq, nt, nprobe, tp, k = case
+    if seed == 9:
+        wl = synth.random_small_workload(seed, n_centroids=n_c, n_docs=300, max_len=max_len, nbits=nbits,
+                                         n_queries=nq, n_qtok=nt, nprobe=nprobe, t_prime=tp, k=k)
+        data = synth.make_index(wl, workers=1)
+        data.workload = synth.with_overrides(wl, n_docs=n_docs)  # ids < 300 of 100000 docs
+    else:
+        wl = synth.random_small_workload(seed, n_centroids=n_c, n_docs=n_docs, max_len=max_len, nbits=nbits,
+                                         n_queries=nq, n_qtok=nt, nprobe=nprobe, t_prime=tp, k=k)
+        data = synth.make_index(wl, workers=1)
+    run_both(data, label=f"random seed {seed}")
+
+
+def test_empty_clusters_and_ragged_tiles():
+    # many centroids, few embeddings: most clusters are empty; tails of every tile are ragged
+    wl = synth.random_small_workload(11, n_centroids=1024, n_docs=700, max_len=9, nbits=4, n_queries=6,
+                                     n_qtok=32, nprobe=40, t_prime=30, k=25, zipf_s=0.3)
+    data = synth.make_index(wl, workers=1)
+    assert (np.diff(data.offsets) == 0).sum() > 20
+    run_both(data, label="empty clusters")
+
+
+# ----------------------------------------------------------------------------- workloads
+
+def test_tiny_workload_exact_and_real_valued():
+    data = synth.make_index(synth.with_overrides(synth.WORKLOADS["tiny"], n_queries=4), workers=1)
+    got = run_both(data, label="tiny")
+    for qi in range(len(data.queries)):
+        n = int(got["counts"][qi])
+        docs = got["ids"][qi, :n]
+        ref = real_valued_scores(data, data.queries[qi], got["sel"][qi], got["m_fixed"][qi], docs)
+        rel = np.abs(got["scores"][qi, :n].astype(np.float64) - ref) / np.maximum(1.0, np.abs(ref))
+        assert rel.max() <= 1e-4, rel.max()
+    assert got["ids"][0, 0] == data.query_targets[0]
+
+
+@pytest.mark.parametrize("nbits", [2, 4])
+def test_tiny_workload_both_code_widths(nbits):
+    wl = synth.with_overrides(synth.WORKLOADS["tiny"], nbits=nbits, n_queries=3, nprobe=32, k=100)
+    run_both(synth.make_index(wl, workers=1), label=f"tiny nbits={nbits}")
+
+
+def test_many_waves_match_one_wave(monkeypatch):
+    w = _engine()
+    data = synth.make_index(synth.with_overrides(synth.WORKLOADS["tiny"], n_queries=9), workers=1)
+    wl = data.workload
+    say("[waves] one wave")
+    with w.Index.from_synthetic(data) as ix:
+        one = ix.search_debug(data.queries, wl.nprobe, wl.t_prime, wl.k)
+        monkeypatch.setenv("WARP_SCRATCH_MB", "1")  # forces one query per wave
+        say("[waves] one query per wave")
+        many = ix.search_debug(data.queries, wl.nprobe, wl.t_prime, wl.k)
+    for key in EXACT + ("scores",):
+        np.testing.assert_array_equal(one[key], many[key])
+
+
+def test_deterministic_and_async_matches_sync():
+    import torch
+
+    w = _engine()
+    data = synth.make_index(synth.with_overrides(synth.WORKLOADS["tiny"], n_queries=5), workers=1)
+    wl = data.workload
+    with w.Index.from_synthetic(data) as ix:
+        say("[async] sync twice")
+        a = ix.search_debug(data.queries, wl.nprobe, wl.t_prime, wl.k)
+        b = ix.search_debug(data.queries, wl.nprobe, wl.t_prime, wl.k)
+        for key in EXACT + ("scores",):
+            np.testing.assert_array_equal(a[key], b[key])
+        say("[async] device tensors")
+        q = torch.from_numpy(data.queries).cuda()
+        ids, scores, counts, fixed = ix.search_async(q, wl.nprobe, wl.t_prime, wl.k)
+        ix.sync()
+        np.testing.assert_array_equal(ids.cpu().numpy(), a["ids"])
+        np.testing.assert_array_equal(scores.cpu().numpy(), a["scores"])
+        np.testing.assert_array_equal(counts.cpu().numpy(), a["counts"])
+        np.testing.assert_array_equal(fixed.cpu().numpy(), a["fixed"])
+
+
+def test_index_from_device_tensors():
+    import torch
+
+    w = _engine()
+    data = synth.make_index(synth.with_overrides(synth.WORKLOADS["tiny"], n_queries=2), workers=1)
+    wl = data.workload
+    t = {k: torch.from_numpy(np.ascontiguousarray(getattr(data, k))).cuda()
+         for k in ("centroids", "offsets", "doc_ids", "codes", "bucket_weights")}
+    say("[device load]")
+    with w.Index.from_device(t["centroids"], t["offsets"], t["doc_ids"], t["codes"], data.nbits,
+                             t["bucket_weights"], data.n_docs) as ix:
+        got = ix.search_debug(data.queries, wl.nprobe, wl.t_prime, wl.k)
+    compare(got, oracle.search_index(data), label="device load")
+
+
+def test_filter_scores_within_selection_margin():
+    w = _engine()
+    data = synth.make_index(synth.with_overrides(synth.WORKLOADS["tiny"], n_queries=8), workers=1)
+    toks = data.queries.reshape(-1, 128)
+    say("[filter] tiny, 256 tokens")
+    with w.Index.from_synthetic(data) as ix:
+        F = ix.filter_scores(toks)
+    S = toks.astype(np.float64) @ data.centroids.astype(np.float64).T
+    err = np.abs(F - S).max()
+    say(f"[filter] max |f - S64| = {err:.3g}")
+    assert err <= 2.0 ** -16  # the selection assumes 2^-13
+
+
+def test_gpu_argument_errors():
+    w = _engine()
+    data = synth.make_index(synth.random_small_workload(1), workers=1)
+    with w.Index.from_synthetic(data) as ix:
+        Q = data.queries
+        say("[errors]")
+        for args, code in [((Q, 0, 1, 1), w.EINVAL), ((Q, 17, 1, 1), w.EINVAL), ((Q, 4, -1, 1), w.EINVAL),
+                           ((Q, 4, 1, 0), w.EINVAL), ((Q, 4, 1, 4097), w.ENOTSUP),
+                           ((Q * 1.01, 4, 1, 3), w.EINVAL), ((np.zeros((1, 33, 128)), 4, 1, 3), w.EINVAL)]:
+            with pytest.raises(w.WarpError) as e:
+                ix.search(*args)
+            assert e.value.code == code, (e.value, args[1:])
+        # the index still works after rejected calls
+        compare(ix.search_debug(Q, 4, 10, 5), oracle.search_index(data), label="after errors")
+    bad = data.doc_ids.copy()
+    bad[0] = data.n_docs
+    with pytest.raises(w.WarpError) as e:
+        w.Index(data.centroids, data.offsets, bad, data.codes, data.nbits, data.bucket_weights, data.n_docs)
+    assert e.value.code == w.EINVAL and "document id" in e.value.msg
+
+
+def test_async_query_norm_error_reported_by_sync():
+    import torch
+
+    w = _engine()
+    data = synth.make_index(synth.random_small_workload(2), workers=1)
+    with w.Index.from_synthetic(data) as ix:
+        q = torch.from_numpy(data.queries * 1.1).cuda()
+        ix.search_async(q, 4, 10, 5)
+        with pytest.raises(w.WarpError) as e:
+            ix.sync()
+        assert e.value.code == w.EINVAL and "norm" in e.value.msg
+        ix.search_async(torch.from_numpy(data.queries).cuda(), 4, 10, 5)
+        ix.sync()  # cleared
+
+
+# ----------------------------------------------------------------------------- the 256-query workload
+
+@pytest.fixture(scope="module")
+def small_data():
+    return synth.make_index(synth.WORKLOADS["small"], workers=min(16, os.cpu_count() or 1))
+
+
+def test_small_workload_sampled_queries(small_data):
+    """All 256 queries in one launch (the benchmark's configuration); a sample of
+    them checked against the oracle element by element."""
+    w = _engine()
+    data = small_data
+    wl = data.workload
+    say(f"[small] {data.n_embeddings} embeddings, 256 queries, nprobe={wl.nprobe} t'={wl.t_prime} k={wl.k}")
+    with w.Index.from_synthetic(data) as ix:
+        got = ix.search_debug(data.queries, wl.nprobe, wl.t_prime, wl.k)
+    rows = np.array([0, 1, 37, 100, 128, 200, 254, 255])
+    say(f"[small] oracle on queries {rows.tolist()}")
+    want = oracle.search_index(data, queries=data.queries[rows])
+    compare(got, want, rows=rows, label="small")
+    hit = (got["ids"][:, 0] == data.query_targets).mean()
+    say(f"[small] target doc ranked first for {hit:.1%} of queries; mean scored/query "
+        f"{got['n_scored'].mean():.3g}")
