@@ -64,6 +64,9 @@ def main() -> int:
     ap.add_argument("--latency-runs", type=int, default=100)
     ap.add_argument("--cpu-queries", type=int, default=48)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="after the run, copy a buffer of this size 3 times on the device (a kernel of "
+                         "known traffic to scale HBM counters against)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the search path has no multi-GPU mode (--gpus {args.gpus} "
@@ -189,6 +192,14 @@ def main() -> int:
     }
     print(json.dumps(rec), flush=True)
     ix.close()
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib << 18  # float32 elements
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"bench: copied {args.copy_calibration_mib} MiB 3 times")
     return 0
 
 
