@@ -28,6 +28,14 @@ constexpr int kScanBlock = 512;
 constexpr int kScanIters = 8;
 constexpr int kScanTile = kScanBlock * kScanIters;
 
+// Cluster-major residual scan: a work item is (cluster, chunk of kCmChunk embeddings
+// held in registers, group of kCmGroup probing tokens scored kCmPack at a time).
+constexpr int kCmBlock = 512;
+constexpr int kCmRows = 2;  // embeddings per thread (the chunk is kCmBlock * rows)
+constexpr int kCmGroup = 16;
+constexpr int kCmPack = 4;
+constexpr int kPlanBlock = 1024;  // clusters per block of the pairing prefix sums
+
 // Error bits the device reports through the index's flag word.
 constexpr int kErrSelOverflow = 1;
 constexpr int kErrSelNoCrossing = 2;
@@ -58,6 +66,13 @@ struct WaveArgs {
     int32_t* tokmax;            // [n_tok][n_docs], kAbsent when not retrieved
     uint64_t* keys;             // [n_q][n_docs]
     int32_t* err;               // device flag word
+    // cluster-major pairing
+    int32_t* ccount;            // [n_c] probing tokens per cluster
+    int32_t* cursor;            // [n_c] scatter cursors
+    int64_t* item_start;        // [n_c + 1] exclusive prefix of work items
+    int32_t* pair_start;        // [n_c + 1] exclusive prefix of pairs
+    int32_t* plist;             // [n_tok * nprobe][2]: (wave token, R(S64)) grouped by cluster
+    int64_t* blk;               // [2 * ceil(n_c / kPlanBlock)] block sums of items and pairs
     // outputs (device; the debug ones may be null)
     int32_t* out_ids;           // [n_q][k]
     float* out_scores;          // [n_q][k]
@@ -68,6 +83,7 @@ struct WaveArgs {
     uint32_t* dbg_bitmap;       // [n_q][ceil(n_docs / 32)] or null
     int64_t* dbg_scored;        // [n_q] or null
     int32_t scan_grid;          // persistent workgroups of the residual scan
+    int32_t cm_rows;            // embeddings per thread of the cluster-major scan (1 or 2)
 };
 
 void launch_filter_gemm(const float* q, int32_t n_tok, const float* c, int32_t n_c, float* out,
@@ -75,6 +91,9 @@ void launch_filter_gemm(const float* q, int32_t n_tok, const float* c, int32_t n
 void launch_select(const WaveArgs& a, hipStream_t s);
 void launch_plan(const WaveArgs& a, hipStream_t s);
 void launch_scan(const WaveArgs& a, hipStream_t s);
+void launch_pairing(const WaveArgs& a, hipStream_t s);
+void launch_scan_cm(const WaveArgs& a, hipStream_t s);
+int scan_cm_blocks_per_cu(int nbits, int rows);
 void launch_fold(const WaveArgs& a, hipStream_t s);
 void launch_topk(const WaveArgs& a, hipStream_t s);
 void launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);

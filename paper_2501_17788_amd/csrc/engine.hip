@@ -62,9 +62,11 @@ struct warp_index {
     float* weights = nullptr;
     int32_t* err = nullptr;
     hipStream_t stream = nullptr;
-    int scan_grid = 0;
+    int scan_grid = 0;     // persistent workgroups of the token-major scan
+    int scan_cm_grid[2] = {0, 0};  // persistent workgroups of the cluster-major scan, rows 1 and 2
     // per-search scratch, grown on demand
     DevBuf filter, sel, base, seg_start, seg_pref, m_fixed, tile_start, tokmax, keys;
+    DevBuf ccount, cursor, item_start, pair_start, plist, blk;
     int64_t tokmax_ready = 0;  // leading elements of tokmax holding kAbsent
     // staging of the host-pointer calls
     DevBuf st_q, st_ids, st_scores, st_fixed, st_counts, st_sel, st_m, st_bitmap, st_scored;
@@ -189,6 +191,8 @@ int finish_load(warp_index* idx, const int64_t* off_host) {
     int cus = 0;
     HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, idx->device));
     idx->scan_grid = cus * scan_blocks_per_cu(idx->nbits);
+    idx->scan_cm_grid[0] = cus * scan_cm_blocks_per_cu(idx->nbits, 1);
+    idx->scan_cm_grid[1] = cus * scan_cm_blocks_per_cu(idx->nbits, 2);
     return WARP_OK;
 }
 
@@ -282,6 +286,13 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P) {
     if (!rc) rc = grow(idx->m_fixed, (size_t)n_tok * 8);
     if (!rc) rc = grow(idx->tile_start, (size_t)(n_tok + 1) * 8);
     if (!rc) rc = grow(idx->keys, (size_t)qw * idx->n_docs * 8);
+    const int64_t nblk = ((int64_t)idx->n_c + kPlanBlock - 1) / kPlanBlock;
+    if (!rc) rc = grow(idx->ccount, (size_t)idx->n_c * 4);
+    if (!rc) rc = grow(idx->cursor, (size_t)idx->n_c * 4);
+    if (!rc) rc = grow(idx->item_start, ((size_t)idx->n_c + 1) * 8);
+    if (!rc) rc = grow(idx->pair_start, ((size_t)idx->n_c + 1) * 4);
+    if (!rc) rc = grow(idx->plist, (size_t)n_tok * P * 8);
+    if (!rc) rc = grow(idx->blk, (size_t)nblk * 16);
     if (rc) return rc;
     const int64_t need = n_tok * idx->n_docs;
     if ((int64_t)(idx->tokmax.bytes / 4) < need) {
@@ -306,7 +317,7 @@ int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T) {
         if (cap < budget) budget = cap;
     }
     const size_t per = (size_t)T * idx->n_docs * 4 + (size_t)idx->n_docs * 8 + (size_t)T * idx->n_c * 4 +
-                       (size_t)T * 1024;
+                       (size_t)T * kMaxProbe * 32 + (size_t)T * 1024;
     int64_t qw = (int64_t)(budget / per);
     if (qw < 1) qw = 1;
     if (qw > n_queries) qw = n_queries;
@@ -358,6 +369,10 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
     int rc = reserve(idx, qw, T, P);
     if (rc) return rc;
     launch_check_queries(dq, (int64_t)n_queries * T, idx->err, s);
+    const char* scan_env = std::getenv("WARP_SCAN");
+    const bool cluster_major = !(scan_env && std::strcmp(scan_env, "token") == 0);
+    const char* rows_env = std::getenv("WARP_CM_ROWS");
+    const int cm_rows = (rows_env && std::atoi(rows_env) == 1) ? 1 : kCmRows;
     const int64_t words = ((int64_t)idx->n_docs + 31) / 32;
     for (int32_t q0 = 0; q0 < n_queries; q0 += qw) {
         const int32_t nq = n_queries - q0 < qw ? n_queries - q0 : qw;
@@ -395,7 +410,14 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         a.dbg_m = o.m ? o.m + (int64_t)q0 * T : nullptr;
         a.dbg_bitmap = o.bitmap ? o.bitmap + (int64_t)q0 * words : nullptr;
         a.dbg_scored = o.scored ? o.scored + q0 : nullptr;
-        a.scan_grid = idx->scan_grid;
+        a.ccount = (int32_t*)idx->ccount.p;
+        a.cursor = (int32_t*)idx->cursor.p;
+        a.item_start = (int64_t*)idx->item_start.p;
+        a.pair_start = (int32_t*)idx->pair_start.p;
+        a.plist = (int32_t*)idx->plist.p;
+        a.blk = (int64_t*)idx->blk.p;
+        a.cm_rows = cm_rows;
+        a.scan_grid = cluster_major ? idx->scan_cm_grid[cm_rows - 1] : idx->scan_grid;
 
         hipEvent_t ev[kStages + 1] = {};
         if (idx->timing)
@@ -409,8 +431,10 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         launch_select(a, s);
         mark(2);
         launch_plan(a, s);
+        if (cluster_major) launch_pairing(a, s);
         mark(3);
-        launch_scan(a, s);
+        if (cluster_major) launch_scan_cm(a, s);
+        else launch_scan(a, s);
         mark(4);
         launch_fold(a, s);
         mark(5);
@@ -514,7 +538,8 @@ void warp_index_free(warp_index* idx) {
                         (void*)idx->codes, (void*)idx->weights, (void*)idx->err})
             if (p) (void)hipFree(p);
         for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_start, &idx->seg_pref, &idx->m_fixed,
-                          &idx->tile_start, &idx->tokmax, &idx->keys, &idx->st_q, &idx->st_ids, &idx->st_scores,
+                          &idx->tile_start, &idx->tokmax, &idx->keys, &idx->ccount, &idx->cursor, &idx->item_start,
+                          &idx->pair_start, &idx->plist, &idx->blk, &idx->st_q, &idx->st_ids, &idx->st_scores,
                           &idx->st_fixed, &idx->st_counts, &idx->st_sel, &idx->st_m, &idx->st_bitmap,
                           &idx->st_scored})
             release(*b);

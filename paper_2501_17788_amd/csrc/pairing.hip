@@ -1,0 +1,113 @@
+// Cluster-major work plan of one wave of queries: every (query token, probed
+// cluster) pair is bucketed by cluster (a counting sort), and each probed
+// cluster is cut into work items of (kCmChunk embeddings) x (kCmGroup tokens),
+// so that the residual scan reads a cluster chunk once for all the tokens that
+// probe it. Pair order inside a bucket follows atomic arrival and does not
+// affect results: the token-level max is exact and commutative.
+#include "engine.h"
+
+namespace warp {
+
+// pairs of tokens whose selection overflowed carry cluster -1 and are skipped
+__global__ __launch_bounds__(256) void k_pair_count(WaveArgs a) {
+    const int64_t n = (int64_t)a.n_q * a.n_qtok * a.nprobe;
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    const int c = a.sel[i];
+    if (c >= 0) atomicAdd(&a.ccount[c], 1);
+}
+
+__device__ __forceinline__ int64_t cluster_items(int32_t n_tok, int32_t size, int32_t chunk) {
+    if (n_tok <= 0 || size <= 0) return 0;
+    return (int64_t)((size + chunk - 1) / chunk) * ((n_tok + kCmGroup - 1) / kCmGroup);
+}
+
+// exclusive scans of items and pairs inside each block of kPlanBlock clusters
+__global__ __launch_bounds__(kPlanBlock) void k_cplan_local(WaveArgs a) {
+    __shared__ int64_t si[kPlanBlock];
+    __shared__ int64_t sp[kPlanBlock];
+    const int tid = threadIdx.x;
+    const int64_t c = (int64_t)blockIdx.x * kPlanBlock + tid;
+    const bool in = c < a.n_c;
+    const int32_t nt = in ? a.ccount[c] : 0;
+    const int64_t items = in ? cluster_items(nt, a.sizes[c], kCmBlock * a.cm_rows) : 0;
+    si[tid] = items;
+    sp[tid] = nt;
+    __syncthreads();
+    for (int off = 1; off < kPlanBlock; off <<= 1) {
+        const int64_t vi = tid >= off ? si[tid - off] : 0;
+        const int64_t vp = tid >= off ? sp[tid - off] : 0;
+        __syncthreads();
+        si[tid] += vi;
+        sp[tid] += vp;
+        __syncthreads();
+    }
+    if (in) {
+        a.item_start[c] = si[tid] - items;
+        a.pair_start[c] = (int32_t)(sp[tid] - nt);
+        a.cursor[c] = 0;
+    }
+    if (tid == kPlanBlock - 1) {
+        a.blk[2 * blockIdx.x] = si[tid];
+        a.blk[2 * blockIdx.x + 1] = sp[tid];
+    }
+}
+
+// add the sums of all earlier blocks; the last block also writes the totals
+__global__ __launch_bounds__(kPlanBlock) void k_cplan_add(WaveArgs a) {
+    __shared__ int64_t ri[kPlanBlock];
+    __shared__ int64_t rp[kPlanBlock];
+    const int tid = threadIdx.x;
+    const int b = blockIdx.x;
+    const int nblk = gridDim.x;
+    int64_t vi = 0, vp = 0;
+    for (int j = tid; j < b; j += kPlanBlock) {
+        vi += a.blk[2 * j];
+        vp += a.blk[2 * j + 1];
+    }
+    ri[tid] = vi;
+    rp[tid] = vp;
+    __syncthreads();
+    for (int off = kPlanBlock / 2; off > 0; off >>= 1) {
+        if (tid < off) {
+            ri[tid] += ri[tid + off];
+            rp[tid] += rp[tid + off];
+        }
+        __syncthreads();
+    }
+    const int64_t oi = ri[0], op = rp[0];
+    const int64_t c = (int64_t)b * kPlanBlock + tid;
+    if (c < a.n_c) {
+        a.item_start[c] += oi;
+        a.pair_start[c] += (int32_t)op;
+    }
+    if (b == nblk - 1 && tid == 0) {
+        a.item_start[a.n_c] = oi + a.blk[2 * b];
+        a.pair_start[a.n_c] = (int32_t)(op + a.blk[2 * b + 1]);
+    }
+}
+
+__global__ __launch_bounds__(256) void k_pair_scatter(WaveArgs a) {
+    const int64_t n = (int64_t)a.n_q * a.n_qtok * a.nprobe;
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    const int c = a.sel[i];
+    if (c < 0) return;
+    const int slot = atomicAdd(&a.cursor[c], 1);
+    const int64_t p = (int64_t)a.pair_start[c] + slot;
+    a.plist[2 * p] = (int32_t)(i / a.nprobe);  // wave token
+    a.plist[2 * p + 1] = a.base[i];           // R(S64) of (token, cluster)
+}
+
+void launch_pairing(const WaveArgs& a, hipStream_t s) {
+    const int64_t n = (int64_t)a.n_q * a.n_qtok * a.nprobe;
+    const unsigned pb = (unsigned)((n + 255) / 256);
+    const unsigned nblk = (unsigned)((a.n_c + kPlanBlock - 1) / kPlanBlock);
+    launch_fill_i32(a.ccount, a.n_c, 0, s);
+    hipLaunchKernelGGL(k_pair_count, dim3(pb), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_cplan_local, dim3(nblk), dim3(kPlanBlock), 0, s, a);
+    hipLaunchKernelGGL(k_cplan_add, dim3(nblk), dim3(kPlanBlock), 0, s, a);
+    hipLaunchKernelGGL(k_pair_scatter, dim3(pb), dim3(256), 0, s, a);
+}
+
+}  // namespace warp

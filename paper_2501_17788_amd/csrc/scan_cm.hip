@@ -1,0 +1,236 @@
+// Cluster-major implicit decompression and token-level max (Sections 4.4, 4.5).
+//
+// Same arithmetic as the token-major scan: for a probing token i of cluster c and
+// every embedding e of c,
+//     t = R(S64[i][c]) + sum_d R(q_{i,d} * omega[code_{e,d}])          (int32, exact)
+// then tokmax[i][doc(e)] = max(...) through a wave segmented max and one
+// atomicMax per run of equal documents.
+//
+// Order of work: a work item is (cluster, chunk of kCmChunk embeddings, group of
+// kCmGroup probing tokens); items of one chunk are consecutive, so a persistent
+// workgroup walking a contiguous item range loads a chunk's codes into registers
+// once and scores them against every token of its items. The HBM traffic of the
+// scan is then about one read of every probed cluster per wave of queries,
+// instead of one read per probing token.
+//
+// Table: the per-token table upsilon = q_hat x omega_hat (Section 4.4) is held
+// per code nibble: entry [n][v] is the sum of the per-dimension entries of the
+// dimensions packed in nibble n when it holds v (one dimension for b = 4, two for
+// b = 2), so the integer sums are those of the per-dimension table. Each entry
+// packs kCmPack = 4 tokens (an int4), so one 16-byte LDS read serves four tokens;
+// all lanes of a wave read the same nibble row of 16 entries at a time, which
+// the LDS serves without bank conflicts. The table is built in LDS directly from
+// the fp32 query tokens: R(q_d * omega_v) in fp64, as in the definition.
+#include "engine.h"
+
+namespace warp {
+
+__device__ __forceinline__ int fixed_prod(double q, double w) {
+    return (int)__builtin_rint(q * w * (double)(1 << kFrac));
+}
+
+template <int NBITS, int ROWS>
+__global__ __launch_bounds__(kCmBlock) void k_scan_cm(WaveArgs a) {
+    constexpr int CHUNK = kCmBlock * ROWS;  // embeddings held in registers per workgroup
+    constexpr int BYTES = kDim * NBITS / 8;  // code bytes per embedding
+    constexpr int VEC = BYTES / 16;          // 16-byte loads per embedding
+    constexpr int NN = 2 * BYTES;            // nibbles per embedding
+    constexpr int ENT = NN * 16;             // table entries per token
+    constexpr int PER = ENT / kCmBlock;      // entries built per thread
+    static_assert(PER * kCmBlock == ENT, "table must split evenly");
+    __shared__ int4 lut[ENT];
+    __shared__ double qd[kCmPack][kDim];
+    __shared__ int s_pair[kCmPack][2];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int n_c = a.n_c;
+    const int64_t* item_start = a.item_start;
+    const int64_t total = item_start[n_c];
+    const int64_t G = gridDim.x;
+    int64_t item = total * blockIdx.x / G;
+    const int64_t last = total * (blockIdx.x + 1) / G;
+    if (item >= last) return;
+
+    // cluster of the first item: item_start[c] <= item < item_start[c + 1]
+    int lo = 0, hi = n_c;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (item_start[mid] <= item) lo = mid;
+        else hi = mid;
+    }
+    int c = lo;
+
+    // every table entry this thread builds has nibble value v = tid % 16
+    const int v = tid & 15;
+    const double w_a = (double)a.weights[NBITS == 4 ? v : (v >> 2)];
+    const double w_b = (double)a.weights[NBITS == 4 ? 0 : (v & 3)];
+
+    int cur_c = -1;
+    int64_t cur_chunk = -1;
+    uint4 code[ROWS][VEC];
+    int doc[ROWS];
+    bool act[ROWS];
+    bool wave_act[ROWS];
+    const uint8_t* __restrict__ codes = a.codes;
+
+    while (item < last) {
+        while (item_start[c + 1] <= item) ++c;
+        const int nt = a.ccount[c];
+        const int groups = (nt + kCmGroup - 1) / kCmGroup;
+        const int64_t l = item - item_start[c];
+        const int64_t chunk = l / groups;
+        const int grp = (int)(l - chunk * groups);
+        if (c != cur_c || chunk != cur_chunk) {
+            const int64_t e0 = a.offsets[c] + chunk * CHUNK;
+            const int64_t e_end = a.offsets[c + 1];
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r) {
+                const int64_t e = e0 + r * kCmBlock + tid;
+                act[r] = e < e_end;
+                doc[r] = -1 - lane;  // inactive lanes never match a neighbour
+                if (act[r]) {
+                    const uint4* row = reinterpret_cast<const uint4*>(codes + e * BYTES);
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) code[r][i] = row[i];
+                    doc[r] = a.doc_ids[e];
+                }
+                wave_act[r] = __any(act[r]);
+            }
+            cur_c = c;
+            cur_chunk = chunk;
+        }
+        const int p_first = a.pair_start[c] + grp * kCmGroup;
+        const int p_end = min(p_first + kCmGroup, a.pair_start[c] + nt);
+        for (int p = p_first; p < p_end; p += kCmPack) {
+            const int ng = min(kCmPack, p_end - p);
+            __syncthreads();  // the previous table and query rows are no longer read
+            if (tid < kCmPack) {
+                s_pair[tid][0] = tid < ng ? a.plist[2 * (int64_t)(p + tid)] : -1;
+                s_pair[tid][1] = tid < ng ? a.plist[2 * (int64_t)(p + tid) + 1] : 0;
+            }
+            {
+                const int g = tid >> 7, d = tid & 127;  // kCmPack x 128 = kCmBlock values
+                float qv = 0.f;
+                if (g < ng) {
+                    const int t = a.plist[2 * (int64_t)(p + g)];
+                    qv = a.queries[(int64_t)t * kDim + d];
+                }
+                qd[g][d] = (double)qv;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < PER; ++i) {
+                const int x = tid + kCmBlock * i;
+                const int n = x >> 4;                 // nibble n of dword n / 8, nibble n % 8
+                const int m = n & 7;
+                const int j = 4 * (n >> 3) + (m >> 1);  // code byte holding the nibble
+                int val[kCmPack];
+                if (NBITS == 4) {
+                    const int d = 2 * j + ((m & 1) ? 0 : 1);  // high nibble: dimension 2j
+#pragma unroll
+                    for (int g = 0; g < kCmPack; ++g) val[g] = fixed_prod(qd[g][d], w_a);
+                } else {
+                    const int d = (m & 1) ? 4 * j : 4 * j + 2;  // high nibble: dimensions 4j, 4j+1
+#pragma unroll
+                    for (int g = 0; g < kCmPack; ++g)
+                        val[g] = fixed_prod(qd[g][d], w_a) + fixed_prod(qd[g][d + 1], w_b);
+                }
+                lut[x] = make_int4(val[0], val[1], val[2], val[3]);
+            }
+            __syncthreads();
+            int tok[kCmPack], base[kCmPack];
+#pragma unroll
+            for (int g = 0; g < kCmPack; ++g) {
+                tok[g] = s_pair[g][0];
+                base[g] = s_pair[g][1];
+            }
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r) {
+                if (!wave_act[r]) continue;  // wave-uniform
+                int acc[kCmPack];
+#pragma unroll
+                for (int g = 0; g < kCmPack; ++g) acc[g] = base[g];
+                const char* lbase = reinterpret_cast<const char*>(lut);
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) {
+                    uint4 cw = code[r][i];
+                    // keep the nibble extraction inside the token loop: hoisting all
+                    // 128 table addresses out of it costs more registers than it saves
+                    asm volatile("" : "+v"(cw.x), "+v"(cw.y), "+v"(cw.z), "+v"(cw.w));
+                    const unsigned wv[4] = {cw.x, cw.y, cw.z, cw.w};
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        // byte b of `even` is 16 x nibble 2b of the dword (the byte offset of
+                        // entry v in its 16-entry row of 16-byte entries); `odd` holds nibble 2b+1
+                        const unsigned even = (wv[k] << 4) & 0xF0F0F0F0u;
+                        const unsigned odd = wv[k] & 0xF0F0F0F0u;
+                        const int row = (4 * i + k) * 8;  // first nibble row of the dword
+                        int4 e[8];
+#pragma unroll
+                        for (int b = 0; b < 4; ++b) {
+                            e[2 * b] = *reinterpret_cast<const int4*>(lbase + (row + 2 * b) * 256 +
+                                                                       ((even >> (8 * b)) & 0xFFu));
+                            e[2 * b + 1] = *reinterpret_cast<const int4*>(lbase + (row + 2 * b + 1) * 256 +
+                                                                           ((odd >> (8 * b)) & 0xFFu));
+                        }
+#pragma unroll
+                        for (int b = 0; b < 8; b += 2) {
+                            acc[0] += e[b].x + e[b + 1].x;
+                            acc[1] += e[b].y + e[b + 1].y;
+                            acc[2] += e[b].z + e[b + 1].z;
+                            acc[3] += e[b].w + e[b + 1].w;
+                        }
+                    }
+                }
+                // segmented max over runs of equal doc ids in adjacent lanes, per token
+                const int dcur = doc[r];
+#pragma unroll
+                for (int off = 1; off < 64; off <<= 1) {
+                    const int d2 = __shfl_up(dcur, off, 64);
+                    const bool same = lane >= off && d2 == dcur;
+#pragma unroll
+                    for (int g = 0; g < kCmPack; ++g) {
+                        const int s2 = __shfl_up(acc[g], off, 64);
+                        if (same && s2 > acc[g]) acc[g] = s2;
+                    }
+                }
+                const int dn = __shfl_down(dcur, 1, 64);
+                if (act[r] && (lane == 63 || dn != dcur)) {
+#pragma unroll
+                    for (int g = 0; g < kCmPack; ++g)
+                        if (g < ng) atomicMax(&a.tokmax[(int64_t)tok[g] * a.n_docs + dcur], acc[g]);
+                }
+            }
+        }
+        ++item;
+    }
+}
+
+template <int NBITS, int ROWS>
+static void launch_cm(const WaveArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL((k_scan_cm<NBITS, ROWS>), dim3(a.scan_grid), dim3(kCmBlock), 0, s, a);
+}
+
+void launch_scan_cm(const WaveArgs& a, hipStream_t s) {
+    if (a.nbits == 4) {
+        if (a.cm_rows == 1) launch_cm<4, 1>(a, s);
+        else launch_cm<4, 2>(a, s);
+    } else {
+        if (a.cm_rows == 1) launch_cm<2, 1>(a, s);
+        else launch_cm<2, 2>(a, s);
+    }
+}
+
+int scan_cm_blocks_per_cu(int nbits, int rows) {
+    int n = 0;
+    if (nbits == 4)
+        (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &n, rows == 1 ? k_scan_cm<4, 1> : k_scan_cm<4, 2>, kCmBlock, 0);
+    else
+        (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &n, rows == 1 ? k_scan_cm<2, 1> : k_scan_cm<2, 2>, kCmBlock, 0);
+    return n > 0 ? n : 1;
+}
+
+}  // namespace warp

@@ -198,7 +198,7 @@ __global__ __launch_bounds__(256) void k_select(WaveArgs a) {
     if (nA > kSelCap || nB > kSelCap || nA < P || nB < 1) {
         // degenerate score distribution: leave a token that scans nothing
         for (int j = tid; j < P; j += NT) {
-            sel[j] = 0;
+            sel[j] = -1;  // probes nothing
             base[j] = 0;
             seg_start[j] = 0;
         }

@@ -21,6 +21,16 @@ pytestmark = pytest.mark.gpu
 EXACT = ("ids", "fixed", "counts", "sel", "m_fixed", "cand_bitmap", "n_scored")
 
 
+@pytest.fixture(autouse=True, params=["cluster", "cluster1", "token"])
+def scan_variant(request, monkeypatch):
+    """Every parity test runs with each residual scan: cluster-major with two and
+    with one embedding per thread, and token-major."""
+    monkeypatch.setenv("WARP_SCAN", "token" if request.param == "token" else "cluster")
+    monkeypatch.setenv("WARP_CM_ROWS", "1" if request.param == "cluster1" else "2")
+    print(f"[scan={request.param}]", flush=True)
+    return request.param
+
+
 def _engine():
     import paper_2501_17788_amd as w
     return w
