@@ -19,9 +19,18 @@ constexpr int32_t kAbsent = INT32_MIN;  // "no retrieved embedding" in the token
 // Centroid selection: the fp32 matrix-core scores are within kFilterEps of the
 // fp64 scores; bins of the score histogram are wider than 2 * kFilterEps.
 constexpr float kFilterEps = 1.0f / 8192.0f;
-constexpr int kSelBins = 4096;
+constexpr int kSelBins = 2048;
 constexpr float kSelLim = 1.0625f;  // |score| <= (1 + 1e-3)^2 < kSelLim
 constexpr int kSelCap = 1024;       // centroids near one selection boundary held in LDS
+static_assert(2.0f * kSelLim / kSelBins > 2.0f * kFilterEps, "a bin must be wider than 2 eps");
+
+// Histogram bin of a filter score: floor((f + kSelLim) * kSelBins / (2 kSelLim)),
+// clamped. Monotone non-decreasing in f.
+__device__ __forceinline__ int score_bin(float f) {
+    const float scale = (float)kSelBins / (2.0f * kSelLim);
+    int b = (int)floorf((f + kSelLim) * scale);
+    return b < 0 ? 0 : (b >= kSelBins ? kSelBins - 1 : b);
+}
 
 // Residual scan work split: a tile is kScanIters iterations of one embedding per thread.
 constexpr int kScanBlock = 512;
@@ -31,7 +40,7 @@ constexpr int kScanTile = kScanBlock * kScanIters;
 // Cluster-major residual scan: a work item is (cluster, chunk of kCmChunk embeddings
 // held in registers, group of kCmGroup probing tokens scored kCmPack at a time).
 constexpr int kCmBlock = 512;
-constexpr int kCmRows = 2;  // embeddings per thread (the chunk is kCmBlock * rows)
+constexpr int kCmRows = 1;  // embeddings per thread (the chunk is kCmBlock * rows)
 constexpr int kCmGroup = 16;
 constexpr int kCmPack = 4;
 constexpr int kPlanBlock = 1024;  // clusters per block of the pairing prefix sums
@@ -56,7 +65,7 @@ struct WaveArgs {
     int32_t n_q, n_qtok, nprobe, k;
     int64_t t_prime;
     // scratch
-    float* filter;              // [n_tok][n_c]
+    uint16_t* filter_bins;      // [n_tok][n_c] histogram bin of each filter score
     int32_t* sel;               // [n_tok][nprobe]
     int32_t* base;              // [n_tok][nprobe]  R(S64) of the probed centroids
     int64_t* seg_start;         // [n_tok][nprobe]  first embedding of each probed cluster
@@ -86,8 +95,9 @@ struct WaveArgs {
     int32_t cm_rows;            // embeddings per thread of the cluster-major scan (1 or 2)
 };
 
-void launch_filter_gemm(const float* q, int32_t n_tok, const float* c, int32_t n_c, float* out,
-                        hipStream_t s);
+// out_bins [n_tok][n_c] u16 bins (the search path) or, if null, out_scores fp32
+void launch_filter_gemm(const float* q, int32_t n_tok, const float* c, int32_t n_c, uint16_t* out_bins,
+                        float* out_scores, hipStream_t s);
 void launch_select(const WaveArgs& a, hipStream_t s);
 void launch_plan(const WaveArgs& a, hipStream_t s);
 void launch_scan(const WaveArgs& a, hipStream_t s);

@@ -278,7 +278,7 @@ int load_common(const float* C, int32_t n_c, int32_t dim, const int64_t* off, co
 int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P) {
     const int64_t n_tok = (int64_t)qw * T;
     int rc = WARP_OK;
-    if (!rc) rc = grow(idx->filter, (size_t)n_tok * idx->n_c * 4);
+    if (!rc) rc = grow(idx->filter, (size_t)n_tok * idx->n_c * 2);
     if (!rc) rc = grow(idx->sel, (size_t)n_tok * P * 4);
     if (!rc) rc = grow(idx->base, (size_t)n_tok * P * 4);
     if (!rc) rc = grow(idx->seg_start, (size_t)n_tok * P * 8);
@@ -316,7 +316,7 @@ int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T) {
         const size_t cap = free_b / 2 + idx->tokmax.bytes + idx->filter.bytes + idx->keys.bytes;
         if (cap < budget) budget = cap;
     }
-    const size_t per = (size_t)T * idx->n_docs * 4 + (size_t)idx->n_docs * 8 + (size_t)T * idx->n_c * 4 +
+    const size_t per = (size_t)T * idx->n_docs * 4 + (size_t)idx->n_docs * 8 + (size_t)T * idx->n_c * 2 +
                        (size_t)T * kMaxProbe * 32 + (size_t)T * 1024;
     int64_t qw = (int64_t)(budget / per);
     if (qw < 1) qw = 1;
@@ -372,7 +372,7 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
     const char* scan_env = std::getenv("WARP_SCAN");
     const bool cluster_major = !(scan_env && std::strcmp(scan_env, "token") == 0);
     const char* rows_env = std::getenv("WARP_CM_ROWS");
-    const int cm_rows = (rows_env && std::atoi(rows_env) == 1) ? 1 : kCmRows;
+    const int cm_rows = rows_env ? (std::atoi(rows_env) == 2 ? 2 : 1) : kCmRows;
     const int64_t words = ((int64_t)idx->n_docs + 31) / 32;
     for (int32_t q0 = 0; q0 < n_queries; q0 += qw) {
         const int32_t nq = n_queries - q0 < qw ? n_queries - q0 : qw;
@@ -392,7 +392,7 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         a.nprobe = P;
         a.k = k;
         a.t_prime = t_prime;
-        a.filter = (float*)idx->filter.p;
+        a.filter_bins = (uint16_t*)idx->filter.p;
         a.sel = (int32_t*)idx->sel.p;
         a.base = (int32_t*)idx->base.p;
         a.seg_start = (int64_t*)idx->seg_start.p;
@@ -426,7 +426,7 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
             if (idx->timing) (void)hipEventRecord(ev[e], s);
         };
         mark(0);
-        launch_filter_gemm(a.queries, nq * T, idx->centroids, idx->n_c, a.filter, s);
+        launch_filter_gemm(a.queries, nq * T, idx->centroids, idx->n_c, a.filter_bins, nullptr, s);
         mark(1);
         launch_select(a, s);
         mark(2);
@@ -606,7 +606,7 @@ int warp_centroid_filter_scores(warp_index* idx, const float* queries, int32_t n
         hipStream_t s = idx->stream;
         if (hipMemcpyAsync(q.p, queries, (size_t)n_tok * kDim * 4, hipMemcpyHostToDevice, s) != hipSuccess)
             rc = fail(WARP_EDEVICE, "copy failed");
-        if (!rc) launch_filter_gemm((const float*)q.p, n_tok, idx->centroids, idx->n_c, (float*)f.p, s);
+        if (!rc) launch_filter_gemm((const float*)q.p, n_tok, idx->centroids, idx->n_c, nullptr, (float*)f.p, s);
         if (!rc && (hipMemcpyAsync(out, f.p, (size_t)n_tok * idx->n_c * 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
                     hipStreamSynchronize(s) != hipSuccess))
             rc = fail(WARP_EDEVICE, "filter scores failed");

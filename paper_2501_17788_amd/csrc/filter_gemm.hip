@@ -6,76 +6,109 @@
 // selection boundary is rescored in fp64 by the selection kernel, so the result
 // of the search does not depend on the accumulation order used here.
 //
-// Work split: a workgroup of 4 waves owns a 64-token x 64-centroid tile, each
-// wave a 32 x 32 block (2 x 2 MFMA blocks). Lane group g = lane / 16 supplies the
-// K index k = 32 g + s of MFMA step s, so every lane streams one contiguous
-// 128-byte half-row of its token and of its centroid with 16-byte loads; the
-// sum over all 128 dimensions is the same whatever K order the steps take.
+// Tiling: a workgroup of 4 waves owns a 128-token x 128-centroid tile; K = 128
+// is staged through LDS in two halves of 64 with coalesced 16-byte loads, rows
+// padded to 68 floats so that the 16 lanes of each ds_read_b128 pass hit 16
+// distinct 4-bank groups. Each wave computes a 64 x 64 block as 4 x 4 MFMA
+// blocks of 16 x 16. Lane group g = lane / 16 reads 4 consecutive k with one
+// 16-byte LDS read and feeds them to 4 successive MFMA steps: step s of a
+// 16-wide k slice uses k = 4 g + s on both operands, so every k is summed once.
 #include "engine.h"
 
 namespace warp {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
+constexpr int kGT = 128;       // tile rows (tokens) and columns (centroids)
+constexpr int kGK = 64;        // k staged per half
+constexpr int kGPad = kGK + 4;  // padded LDS row (floats)
+
+// BINS: write the selection histogram bin of each score (u16); else the fp32 score.
+template <bool BINS>
 __global__ __launch_bounds__(256) void k_filter_gemm(const float* __restrict__ q, int32_t n_tok,
                                                      const float* __restrict__ cen, int32_t n_c,
-                                                     float* __restrict__ out) {
-    const int wave = threadIdx.x >> 6;
-    const int lane = threadIdx.x & 63;
+                                                     void* __restrict__ out) {
+    __shared__ float As[kGT * kGPad];
+    __shared__ float Bs[kGT * kGPad];
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6;
+    const int lane = tid & 63;
     const int li = lane & 15;
     const int g = lane >> 4;
-    const int64_t t0 = (int64_t)blockIdx.y * 64 + (wave >> 1) * 32;
-    const int64_t c0 = (int64_t)blockIdx.x * 64 + (wave & 1) * 32;
+    const int64_t t_base = (int64_t)blockIdx.y * kGT;
+    const int64_t c_base = (int64_t)blockIdx.x * kGT;
+    const int wr = (wave >> 1) * 64;  // this wave's rows within the tile
+    const int wc = (wave & 1) * 64;   // and columns
 
-    const int64_t ta = t0 + li, tb = t0 + 16 + li;
-    const int64_t ca = c0 + li, cb = c0 + 16 + li;
-    const bool va = ta < n_tok, vb = tb < n_tok, vc = ca < n_c, vd = cb < n_c;
-    const float4* pa = reinterpret_cast<const float4*>(q + (va ? ta : 0) * kDim + 32 * g);
-    const float4* pb = reinterpret_cast<const float4*>(q + (vb ? tb : 0) * kDim + 32 * g);
-    const float4* pc = reinterpret_cast<const float4*>(cen + (vc ? ca : 0) * kDim + 32 * g);
-    const float4* pd = reinterpret_cast<const float4*>(cen + (vd ? cb : 0) * kDim + 32 * g);
+    floatx4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = (floatx4){0.f, 0.f, 0.f, 0.f};
 
-    floatx4 acc00 = {0.f, 0.f, 0.f, 0.f}, acc01 = acc00, acc10 = acc00, acc11 = acc00;
-    const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-    for (int kc = 0; kc < 8; ++kc) {
-        const float4 a0 = va ? pa[kc] : zero;
-        const float4 a1 = vb ? pb[kc] : zero;
-        const float4 b0 = vc ? pc[kc] : zero;
-        const float4 b1 = vd ? pd[kc] : zero;
-        const float av0[4] = {a0.x, a0.y, a0.z, a0.w};
-        const float av1[4] = {a1.x, a1.y, a1.z, a1.w};
-        const float bv0[4] = {b0.x, b0.y, b0.z, b0.w};
-        const float bv1[4] = {b1.x, b1.y, b1.z, b1.w};
+    for (int half = 0; half < 2; ++half) {
+        if (half) __syncthreads();
+        // stage: 128 rows x 64 floats per operand = 2048 float4, 8 per thread
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            acc00 = __builtin_amdgcn_mfma_f32_16x16x4f32(av0[s], bv0[s], acc00, 0, 0, 0);
-            acc01 = __builtin_amdgcn_mfma_f32_16x16x4f32(av0[s], bv1[s], acc01, 0, 0, 0);
-            acc10 = __builtin_amdgcn_mfma_f32_16x16x4f32(av1[s], bv0[s], acc10, 0, 0, 0);
-            acc11 = __builtin_amdgcn_mfma_f32_16x16x4f32(av1[s], bv1[s], acc11, 0, 0, 0);
+        for (int it = 0; it < 8; ++it) {
+            const int f = tid + 256 * it;
+            const int row = f >> 4, c4 = f & 15;
+            const int64_t tr = t_base + row, cr = c_base + row;
+            float4 va = make_float4(0.f, 0.f, 0.f, 0.f), vb = va;
+            if (tr < n_tok) va = *reinterpret_cast<const float4*>(q + tr * kDim + half * kGK + 4 * c4);
+            if (cr < n_c) vb = *reinterpret_cast<const float4*>(cen + cr * kDim + half * kGK + 4 * c4);
+            *reinterpret_cast<float4*>(&As[row * kGPad + 4 * c4]) = va;
+            *reinterpret_cast<float4*>(&Bs[row * kGPad + 4 * c4]) = vb;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int ks = 0; ks < kGK; ks += 16) {
+            float4 a[4], b[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                a[i] = *reinterpret_cast<const float4*>(&As[(wr + 16 * i + li) * kGPad + ks + 4 * g]);
+                b[i] = *reinterpret_cast<const float4*>(&Bs[(wc + 16 * i + li) * kGPad + ks + 4 * g]);
+            }
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float av = s == 0 ? a[i].x : s == 1 ? a[i].y : s == 2 ? a[i].z : a[i].w;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const float bv = s == 0 ? b[j].x : s == 1 ? b[j].y : s == 2 ? b[j].z : b[j].w;
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[i][j], 0, 0, 0);
+                    }
+                }
+            }
         }
     }
-    // D[i][j] of a 16 x 16 block sits in lane j + 16 * (i / 4), element i % 4.
-    const floatx4 accs[2][2] = {{acc00, acc01}, {acc10, acc11}};
+    // D[r][cidx] of a 16 x 16 block sits in lane cidx + 16 * (r / 4), element r % 4.
 #pragma unroll
-    for (int bi = 0; bi < 2; ++bi) {
+    for (int i = 0; i < 4; ++i) {
 #pragma unroll
-        for (int bj = 0; bj < 2; ++bj) {
-            const int64_t c = c0 + 16 * bj + li;
+        for (int j = 0; j < 4; ++j) {
+            const int64_t c = c_base + wc + 16 * j + li;
             if (c >= n_c) continue;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int64_t t = t0 + 16 * bi + 4 * g + r;
-                if (t < n_tok) out[t * n_c + c] = accs[bi][bj][r];
+                const int64_t t = t_base + wr + 16 * i + 4 * g + r;
+                if (t >= n_tok) continue;
+                if (BINS) static_cast<uint16_t*>(out)[t * n_c + c] = (uint16_t)score_bin(acc[i][j][r]);
+                else static_cast<float*>(out)[t * n_c + c] = acc[i][j][r];
             }
         }
     }
 }
 
-void launch_filter_gemm(const float* q, int32_t n_tok, const float* c, int32_t n_c, float* out,
-                        hipStream_t s) {
-    dim3 grid((n_c + 63) / 64, (n_tok + 63) / 64);
-    hipLaunchKernelGGL(k_filter_gemm, grid, dim3(256), 0, s, q, n_tok, c, n_c, out);
+void launch_filter_gemm(const float* q, int32_t n_tok, const float* c, int32_t n_c, uint16_t* out_bins,
+                        float* out_scores, hipStream_t s) {
+    dim3 grid((n_c + kGT - 1) / kGT, (n_tok + kGT - 1) / kGT);
+    if (out_bins)
+        hipLaunchKernelGGL(k_filter_gemm<true>, grid, dim3(256), 0, s, q, n_tok, c, n_c, (void*)out_bins);
+    else
+        hipLaunchKernelGGL(k_filter_gemm<false>, grid, dim3(256), 0, s, q, n_tok, c, n_c, (void*)out_scores);
 }
 
 }  // namespace warp

@@ -4,26 +4,24 @@
 // cumulative cluster size exceeds t' (the last centroid when none does).
 //
 // The exact order is defined on fp64 scores S64 = sum_d (double)c_d (double)q_d
-// taken in dimension order. One workgroup per token:
-//   1. a histogram of the fp32 matrix-core scores f over kSelBins equal bins of
-//      [-kSelLim, kSelLim), counting centroids and summing their sizes;
+// taken in dimension order. The filter GEMM gives, for every (token, centroid),
+// the histogram bin of its fp32 matrix-core score f (score_bin). One workgroup
+// per token:
+//   1. a histogram over the bins, counting centroids and summing their sizes;
 //   2. from the top bin down: the bin b_P where the centroid count reaches
 //      n_probe and the bin b_t where the size sum first exceeds t';
-//   3. every centroid whose bin is within 2 of those boundaries, or above b_P,
-//      is rescored in fp64 and sorted by (S64 desc, id asc).
+//   3. every centroid whose bin is within 2 of b_t, or at least b_P - 2, is
+//      rescored in fp64 and sorted by (S64 desc, id asc).
 // Since |f - S64| <= kFilterEps and a bin is wider than 2 kFilterEps, a centroid
-// three or more bins above (below) the t' bin scores strictly above (below) m_i,
-// and no centroid outside the collected set can be among the n_probe best. So
-// the rescored set decides sel and m_i exactly, as the full fp64 sort would.
+// three or more bins above (below) b_t scores strictly above (below) m_i, and no
+// centroid below bin b_P - 2 can be among the n_probe best. Walking the rescored
+// band in exact order, starting from the size of every bin above it, the first
+// entry whose cumulative size exceeds t' gives m_i: entries of the band that lie
+// above the true boundary reach at most the size of all bins above b_t, which
+// does not exceed t'. So sel and m_i are those of the full fp64 sort.
 #include "engine.h"
 
 namespace warp {
-
-__device__ __forceinline__ int score_bin(float f) {
-    const float scale = (float)kSelBins / (2.0f * kSelLim);
-    int b = (int)floorf((f + kSelLim) * scale);
-    return b < 0 ? 0 : (b >= kSelBins ? kSelBins - 1 : b);
-}
 
 __device__ __forceinline__ int64_t to_fixed(double x) {
     return (int64_t)__builtin_rint(x * (double)(1 << kFrac));
@@ -60,16 +58,23 @@ __device__ void sort_desc(double* s, int* id, int n) {
 }
 
 // fp64 centroid score, accumulated in dimension order (each product is exact).
-__device__ __forceinline__ double score64(const float* __restrict__ cen, int c, const float* qs) {
+// The row is loaded in four slices of eight 16-byte loads, all in flight at once.
+__device__ __noinline__ double score64(const float* __restrict__ cen, int c, const float* qs) {
     const float4* row = reinterpret_cast<const float4*>(cen + (int64_t)c * kDim);
     double s = 0.0;
-#pragma unroll 4
-    for (int k = 0; k < kDim / 4; ++k) {
-        const float4 v = row[k];
-        s = __builtin_fma((double)v.x, (double)qs[4 * k + 0], s);
-        s = __builtin_fma((double)v.y, (double)qs[4 * k + 1], s);
-        s = __builtin_fma((double)v.z, (double)qs[4 * k + 2], s);
-        s = __builtin_fma((double)v.w, (double)qs[4 * k + 3], s);
+#pragma unroll
+    for (int sl = 0; sl < 4; ++sl) {
+        float4 v[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = row[8 * sl + k];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int d = 32 * sl + 4 * k;
+            s = __builtin_fma((double)v[k].x, (double)qs[d + 0], s);
+            s = __builtin_fma((double)v[k].y, (double)qs[d + 1], s);
+            s = __builtin_fma((double)v[k].z, (double)qs[d + 2], s);
+            s = __builtin_fma((double)v[k].w, (double)qs[d + 3], s);
+        }
     }
     return s;
 }
@@ -80,27 +85,87 @@ __device__ __forceinline__ int pow2_at_least(int n) {
     return p;
 }
 
-__global__ __launch_bounds__(256) void k_select(WaveArgs a) {
-    constexpr int NT = 256;
+constexpr int kSelThreads = 512;
+
+// Inclusive prefix sum of n <= kSelCap int64 values in LDS.
+__device__ void block_inclusive_scan(int64_t* v, int n, int64_t* tmp) {
+    constexpr int NT = kSelThreads;
+    const int tid = threadIdx.x;
+    const int per = (n + NT - 1) / NT;
+    const int lo = tid * per < n ? tid * per : n;
+    const int hi = lo + per < n ? lo + per : n;
+    int64_t run = 0;
+    for (int i = lo; i < hi; ++i) run += v[i];
+    tmp[tid] = run;
+    __syncthreads();
+    for (int off = 1; off < NT; off <<= 1) {
+        const int64_t x = tid >= off ? tmp[tid - off] : 0;
+        __syncthreads();
+        tmp[tid] += x;
+        __syncthreads();
+    }
+    run = tmp[tid] - run;
+    for (int i = lo; i < hi; ++i) {
+        run += v[i];
+        v[i] = run;
+    }
+    __syncthreads();
+}
+
+constexpr unsigned long long kCntOne = 1ull << 40;  // histogram word: (count << 40) | size sum
+constexpr unsigned long long kSizeMask = kCntOne - 1;
+
+// Calls f(c, bin) for every centroid of the token's row of bins: 16-byte loads of
+// eight bins when the row is 16-byte aligned, four loads in flight per thread.
+template <typename F>
+__device__ __forceinline__ void for_each_bin(const uint16_t* bins, int n_c, F f) {
+    constexpr int NT = kSelThreads;
+    const int tid = threadIdx.x;
+    if ((n_c & 7) == 0 && ((uintptr_t)bins & 15) == 0) {
+        const uint4* b4 = reinterpret_cast<const uint4*>(bins);
+        const int n8 = n_c >> 3;
+        for (int j0 = 0; j0 < n8; j0 += 4 * NT) {
+            uint4 v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int j = j0 + u * NT + tid;
+                v[u] = j < n8 ? b4[j] : make_uint4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int j = j0 + u * NT + tid;
+                if (j >= n8) continue;
+                const unsigned w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    f(8 * j + 2 * h, (int)(w[h] & 0xFFFFu));
+                    f(8 * j + 2 * h + 1, (int)(w[h] >> 16));
+                }
+            }
+        }
+    } else {
+        for (int c = tid; c < n_c; c += NT) f(c, (int)bins[c]);
+    }
+}
+
+__global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
+    constexpr int NT = kSelThreads;
     constexpr int PER = kSelBins / NT;
-    __shared__ uint32_t hcnt[kSelBins];
-    __shared__ unsigned long long hw[kSelBins];
-    __shared__ uint32_t scnt[NT];
-    __shared__ unsigned long long sw[NT];
+    __shared__ unsigned long long hist[kSelBins];
+    __shared__ unsigned long long sfx[NT];
     __shared__ float qs[kDim];
     __shared__ double sA[kSelCap], sB[kSelCap];
     __shared__ int idA[kSelCap], idB[kSelCap];
-    __shared__ int s_bP, s_bt, s_blo, s_nA, s_nB;
+    __shared__ int64_t cum[kSelCap];
+    __shared__ int s_bP, s_bt, s_blo, s_nA, s_nB, s_cross;
     __shared__ unsigned long long s_wabove;
+    int64_t* scan_tmp = reinterpret_cast<int64_t*>(sfx);  // free once the bin suffix sums are used
 
     const int t = blockIdx.x;
     const int tid = threadIdx.x;
     const int n_c = a.n_c, P = a.nprobe;
     const unsigned long long tp = (unsigned long long)a.t_prime;
-    for (int i = tid; i < kSelBins; i += NT) {
-        hcnt[i] = 0;
-        hw[i] = 0;
-    }
+    for (int i = tid; i < kSelBins; i += NT) hist[i] = 0;
     if (tid < kDim) qs[tid] = a.queries[(int64_t)t * kDim + tid];
     if (tid == 0) {
         s_bP = -1;
@@ -109,43 +174,37 @@ __global__ __launch_bounds__(256) void k_select(WaveArgs a) {
         s_nA = 0;
         s_nB = 0;
         s_wabove = 0;
+        s_cross = kSelCap;
     }
     __syncthreads();
 
-    // 1. histogram of filter scores: counts and size sums
-    const float* f = a.filter + (int64_t)t * n_c;
-    for (int c = tid; c < n_c; c += NT) {
-        const int b = score_bin(f[c]);
-        atomicAdd(&hcnt[b], 1u);
-        const int32_t sz = a.sizes[c];
-        if (sz) atomicAdd(&hw[b], (unsigned long long)sz);
-    }
+    // 1. histogram: one packed (count, size) word per bin
+    const uint16_t* bins = a.filter_bins + (int64_t)t * n_c;
+    const int32_t* sizes = a.sizes;
+    for_each_bin(bins, n_c, [&](int c, int b) {
+        atomicAdd(&hist[b], kCntOne | (unsigned long long)sizes[c]);
+    });
     __syncthreads();
 
-    // 2. suffix sums over bins; thread tid owns bins [PER * tid, PER * tid + PER)
-    uint32_t own_c = 0;
-    unsigned long long own_w = 0;
-    for (int j = 0; j < PER; ++j) {
-        own_c += hcnt[PER * tid + j];
-        own_w += hw[PER * tid + j];
-    }
-    scnt[tid] = own_c;
-    sw[tid] = own_w;
+    // 2. suffix sums over bins; thread tid owns bins [PER * tid, PER * tid + PER).
+    //    Packed words add field by field: sizes total < 2^40, counts < 2^24.
+    unsigned long long own = 0;
+    for (int j = 0; j < PER; ++j) own += hist[PER * tid + j];
+    sfx[tid] = own;
     __syncthreads();
-    for (int off = 1; off < NT; off <<= 1) {  // inclusive suffix scan over threads
-        const uint32_t vc = tid + off < NT ? scnt[tid + off] : 0;
-        const unsigned long long vw = tid + off < NT ? sw[tid + off] : 0;
+    for (int off = 1; off < NT; off <<= 1) {
+        const unsigned long long x = tid + off < NT ? sfx[tid + off] : 0;
         __syncthreads();
-        scnt[tid] += vc;
-        sw[tid] += vw;
+        sfx[tid] += x;
         __syncthreads();
     }
-    const uint32_t above_c = scnt[tid] - own_c;
-    const unsigned long long above_w = sw[tid] - own_w;
+    const unsigned long long above = sfx[tid] - own;
+    const uint32_t above_c = (uint32_t)(above >> 40), own_c = (uint32_t)(own >> 40);
+    const unsigned long long above_w = above & kSizeMask, own_w = own & kSizeMask;
     if (above_c < (uint32_t)P && above_c + own_c >= (uint32_t)P) {
         uint32_t run = above_c;
         for (int j = PER - 1; j >= 0; --j) {
-            run += hcnt[PER * tid + j];
+            run += (uint32_t)(hist[PER * tid + j] >> 40);
             if (run >= (uint32_t)P) {
                 s_bP = PER * tid + j;
                 break;
@@ -156,16 +215,17 @@ __global__ __launch_bounds__(256) void k_select(WaveArgs a) {
         unsigned long long run = above_w;
         for (int j = PER - 1; j >= 0; --j) {
             const int b = PER * tid + j;
-            if (run + hw[b] > tp) {
+            const unsigned long long w = hist[b] & kSizeMask;
+            if (run + w > tp) {
                 s_bt = b;
                 s_wabove = run;  // size of every bin above b
                 break;
             }
-            run += hw[b];
+            run += w;
         }
     }
     for (int j = 0; j < PER; ++j) {
-        if (hcnt[PER * tid + j]) {
+        if (hist[PER * tid + j] >> 40) {
             atomicMin(&s_blo, PER * tid + j);
             break;
         }
@@ -178,8 +238,7 @@ __global__ __launch_bounds__(256) void k_select(WaveArgs a) {
     const int bt_lo = clamp ? s_blo : (s_bt - 2 < 0 ? 0 : s_bt - 2);
     const int bt_hi = clamp ? (s_blo + 2 < kSelBins ? s_blo + 2 : kSelBins - 1)
                             : (s_bt + 2 < kSelBins ? s_bt + 2 : kSelBins - 1);
-    for (int c = tid; c < n_c; c += NT) {
-        const int b = score_bin(f[c]);
+    for_each_bin(bins, n_c, [&](int c, int b) {
         if (b >= bA) {
             const int p = atomicAdd(&s_nA, 1);
             if (p < kSelCap) idA[p] = c;
@@ -188,7 +247,7 @@ __global__ __launch_bounds__(256) void k_select(WaveArgs a) {
             const int p = atomicAdd(&s_nB, 1);
             if (p < kSelCap) idB[p] = c;
         }
-    }
+    });
     __syncthreads();
     const int nA = s_nA, nB = s_nB;
     int32_t* sel = a.sel + (int64_t)t * P;
@@ -196,9 +255,9 @@ __global__ __launch_bounds__(256) void k_select(WaveArgs a) {
     int64_t* seg_start = a.seg_start + (int64_t)t * P;
     int64_t* seg_pref = a.seg_pref + (int64_t)t * (P + 1);
     if (nA > kSelCap || nB > kSelCap || nA < P || nB < 1) {
-        // degenerate score distribution: leave a token that scans nothing
+        // degenerate score distribution: leave a token that probes and scans nothing
         for (int j = tid; j < P; j += NT) {
-            sel[j] = -1;  // probes nothing
+            sel[j] = -1;
             base[j] = 0;
             seg_start[j] = 0;
         }
@@ -210,57 +269,55 @@ __global__ __launch_bounds__(256) void k_select(WaveArgs a) {
         return;
     }
 
-    // 4. fp64 rescoring and exact order
+    // 4. fp64 rescoring (both lists in one pass) and exact order
     const int pA = pow2_at_least(nA), pB = pow2_at_least(nB);
-    for (int p = tid; p < pA; p += NT) {
-        if (p < nA) {
-            sA[p] = score64(a.centroids, idA[p], qs);
+    for (int p = tid; p < pA + pB; p += NT) {
+        const bool in_a = p < pA;
+        const int q = in_a ? p : p - pA;
+        int* ids = in_a ? idA : idB;
+        double* ss = in_a ? sA : sB;
+        if (q < (in_a ? nA : nB)) {
+            ss[q] = score64(a.centroids, ids[q], qs);
         } else {
-            sA[p] = -__builtin_inf();
-            idA[p] = 0x7fffffff;
-        }
-    }
-    for (int p = tid; p < pB; p += NT) {
-        if (p < nB) {
-            sB[p] = score64(a.centroids, idB[p], qs);
-        } else {
-            sB[p] = -__builtin_inf();
-            idB[p] = 0x7fffffff;
+            ss[q] = -__builtin_inf();
+            ids[q] = 0x7fffffff;
         }
     }
     __syncthreads();
     sort_desc(sA, idA, pA);
     sort_desc(sB, idB, pB);
 
+    // 5. the n_probe best, their fixed-point scores and the prefix of their sizes
     for (int j = tid; j < P; j += NT) {
         const int c = idA[j];
         sel[j] = c;
         base[j] = (int32_t)to_fixed(sA[j]);
         seg_start[j] = a.offsets[c];
+        cum[j] = sizes[c];
         if (a.dbg_sel) a.dbg_sel[(int64_t)t * P + j] = c;
     }
+    __syncthreads();
+    block_inclusive_scan(cum, P, scan_tmp);
+    for (int j = tid; j <= P; j += NT) seg_pref[j] = j == 0 ? 0 : cum[j - 1];
+    __syncthreads();
+
+    // 6. m_i: the first band entry, in exact order, whose cumulative size (from the
+    //    size of everything above the band) exceeds t'
+    for (int p = tid; p < nB; p += NT) cum[p] = sizes[idB[p]];
+    __syncthreads();
+    block_inclusive_scan(cum, nB, scan_tmp);
+    if (!clamp) {
+        unsigned long long band_above = s_wabove;
+        for (int b = s_bt + 1; b <= bt_hi; ++b) band_above -= hist[b] & kSizeMask;
+        for (int p = tid; p < nB; p += NT)
+            if (band_above + (unsigned long long)cum[p] > tp) atomicMin(&s_cross, p);
+    }
+    __syncthreads();
     if (tid == 0) {
-        int64_t run = 0;
-        seg_pref[0] = 0;
-        for (int j = 0; j < P; ++j) {
-            run += a.sizes[idA[j]];
-            seg_pref[j + 1] = run;
-        }
-        // m_i: walk the boundary band in exact order from the size of everything above it
-        double m = sB[nB - 1];
+        double m = sB[nB - 1];  // clamp: the lowest score
         if (!clamp) {
-            unsigned long long cum = s_wabove;
-            for (int b = s_bt + 1; b <= bt_hi; ++b) cum -= hw[b];
-            bool found = false;
-            for (int p = 0; p < nB; ++p) {
-                cum += (unsigned long long)a.sizes[idB[p]];
-                if (cum > tp) {
-                    m = sB[p];
-                    found = true;
-                    break;
-                }
-            }
-            if (!found) atomicOr(a.err, kErrSelNoCrossing);
+            if (s_cross < nB) m = sB[s_cross];
+            else atomicOr(a.err, kErrSelNoCrossing);
         }
         a.m_fixed[t] = to_fixed(m);
         if (a.dbg_m) a.dbg_m[t] = to_fixed(m);
@@ -269,7 +326,7 @@ __global__ __launch_bounds__(256) void k_select(WaveArgs a) {
 
 void launch_select(const WaveArgs& a, hipStream_t s) {
     const int n_tok = a.n_q * a.n_qtok;
-    hipLaunchKernelGGL(k_select, dim3(n_tok), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_select, dim3(n_tok), dim3(kSelThreads), 0, s, a);
 }
 
 }  // namespace warp
