@@ -29,6 +29,43 @@ __device__ __forceinline__ int fixed_prod(double q, double w) {
     return (int)__builtin_rint(q * w * (double)(1 << kFrac));
 }
 
+// Wave-level segmented max-scan over runs of equal document ids, the gfx9 DPP
+// pattern of a wave64 inclusive scan: row_shr 1, 2, 4, 8 inside rows of 16 lanes,
+// then row_bcast 15 (rows 1, 3) and row_bcast 31 (rows 2, 3). A step merges the
+// source lane only when it holds the same document; merging values of one
+// document is always correct, and every lane of a contiguous run is covered by
+// the run's last lane as in the plain scan.
+constexpr int kDppCtrl[6] = {0x111, 0x112, 0x114, 0x118, 0x142, 0x143};
+constexpr int kDppRows[6] = {0xf, 0xf, 0xf, 0xf, 0xa, 0xc};
+
+template <int K>
+__device__ __forceinline__ int dpp_src(int v) {
+    return __builtin_amdgcn_update_dpp(INT32_MIN, v, kDppCtrl[K], kDppRows[K], 0xf, false);
+}
+
+// Bit k: the step-k source lane holds the same document as this lane.
+__device__ __forceinline__ unsigned same_doc_steps(int doc) {
+    unsigned m = 0;
+    m |= (dpp_src<0>(doc) == doc) ? 1u : 0u;
+    m |= (dpp_src<1>(doc) == doc) ? 2u : 0u;
+    m |= (dpp_src<2>(doc) == doc) ? 4u : 0u;
+    m |= (dpp_src<3>(doc) == doc) ? 8u : 0u;
+    m |= (dpp_src<4>(doc) == doc) ? 16u : 0u;
+    m |= (dpp_src<5>(doc) == doc) ? 32u : 0u;
+    return m;
+}
+
+__device__ __forceinline__ int seg_max(int v, unsigned same) {
+    int s;
+    s = dpp_src<0>(v); v = (same & 1u) && s > v ? s : v;
+    s = dpp_src<1>(v); v = (same & 2u) && s > v ? s : v;
+    s = dpp_src<2>(v); v = (same & 4u) && s > v ? s : v;
+    s = dpp_src<3>(v); v = (same & 8u) && s > v ? s : v;
+    s = dpp_src<4>(v); v = (same & 16u) && s > v ? s : v;
+    s = dpp_src<5>(v); v = (same & 32u) && s > v ? s : v;
+    return v;
+}
+
 template <int NBITS, int ROWS>
 __global__ __launch_bounds__(kCmBlock) void k_scan_cm(WaveArgs a) {
     constexpr int CHUNK = kCmBlock * ROWS;  // embeddings held in registers per workgroup
@@ -72,6 +109,8 @@ __global__ __launch_bounds__(kCmBlock) void k_scan_cm(WaveArgs a) {
     int doc[ROWS];
     bool act[ROWS];
     bool wave_act[ROWS];
+    unsigned same[ROWS];   // DPP steps that merge the same document
+    bool run_end[ROWS];    // last lane of its run of equal documents
     const uint8_t* __restrict__ codes = a.codes;
 
     while (item < last) {
@@ -96,6 +135,9 @@ __global__ __launch_bounds__(kCmBlock) void k_scan_cm(WaveArgs a) {
                     doc[r] = a.doc_ids[e];
                 }
                 wave_act[r] = __any(act[r]);
+                same[r] = same_doc_steps(doc[r]);
+                const int dn = __shfl_down(doc[r], 1, 64);
+                run_end[r] = act[r] && (lane == 63 || dn != doc[r]);
             }
             cur_c = c;
             cur_chunk = chunk;
@@ -141,9 +183,9 @@ __global__ __launch_bounds__(kCmBlock) void k_scan_cm(WaveArgs a) {
             __syncthreads();
             int tok[kCmPack], base[kCmPack];
 #pragma unroll
-            for (int g = 0; g < kCmPack; ++g) {
-                tok[g] = s_pair[g][0];
-                base[g] = s_pair[g][1];
+            for (int g = 0; g < kCmPack; ++g) {  // uniform across the workgroup: scalar registers
+                tok[g] = __builtin_amdgcn_readfirstlane(s_pair[g][0]);
+                base[g] = __builtin_amdgcn_readfirstlane(s_pair[g][1]);
             }
 #pragma unroll
             for (int r = 0; r < ROWS; ++r) {
@@ -166,40 +208,34 @@ __global__ __launch_bounds__(kCmBlock) void k_scan_cm(WaveArgs a) {
                         const unsigned even = (wv[k] << 4) & 0xF0F0F0F0u;
                         const unsigned odd = wv[k] & 0xF0F0F0F0u;
                         const int row = (4 * i + k) * 8;  // first nibble row of the dword
-                        int4 e[8];
 #pragma unroll
-                        for (int b = 0; b < 4; ++b) {
-                            e[2 * b] = *reinterpret_cast<const int4*>(lbase + (row + 2 * b) * 256 +
-                                                                       ((even >> (8 * b)) & 0xFFu));
-                            e[2 * b + 1] = *reinterpret_cast<const int4*>(lbase + (row + 2 * b + 1) * 256 +
-                                                                           ((odd >> (8 * b)) & 0xFFu));
-                        }
+                        for (int h = 0; h < 2; ++h) {  // four lookups in flight at a time
+                            int4 e[4];
 #pragma unroll
-                        for (int b = 0; b < 8; b += 2) {
-                            acc[0] += e[b].x + e[b + 1].x;
-                            acc[1] += e[b].y + e[b + 1].y;
-                            acc[2] += e[b].z + e[b + 1].z;
-                            acc[3] += e[b].w + e[b + 1].w;
+                            for (int b = 2 * h; b < 2 * h + 2; ++b) {
+                                e[2 * (b - 2 * h)] = *reinterpret_cast<const int4*>(
+                                    lbase + (row + 2 * b) * 256 + ((even >> (8 * b)) & 0xFFu));
+                                e[2 * (b - 2 * h) + 1] = *reinterpret_cast<const int4*>(
+                                    lbase + (row + 2 * b + 1) * 256 + ((odd >> (8 * b)) & 0xFFu));
+                            }
+#pragma unroll
+                            for (int b = 0; b < 4; b += 2) {
+                                acc[0] += e[b].x + e[b + 1].x;
+                                acc[1] += e[b].y + e[b + 1].y;
+                                acc[2] += e[b].z + e[b + 1].z;
+                                acc[3] += e[b].w + e[b + 1].w;
+                            }
                         }
                     }
                 }
-                // segmented max over runs of equal doc ids in adjacent lanes, per token
-                const int dcur = doc[r];
+                // inner-cluster max: segmented max over runs of equal documents, then one
+                // atomicMax per run and token
 #pragma unroll
-                for (int off = 1; off < 64; off <<= 1) {
-                    const int d2 = __shfl_up(dcur, off, 64);
-                    const bool same = lane >= off && d2 == dcur;
-#pragma unroll
-                    for (int g = 0; g < kCmPack; ++g) {
-                        const int s2 = __shfl_up(acc[g], off, 64);
-                        if (same && s2 > acc[g]) acc[g] = s2;
-                    }
-                }
-                const int dn = __shfl_down(dcur, 1, 64);
-                if (act[r] && (lane == 63 || dn != dcur)) {
+                for (int g = 0; g < kCmPack; ++g) acc[g] = seg_max(acc[g], same[r]);
+                if (run_end[r]) {
 #pragma unroll
                     for (int g = 0; g < kCmPack; ++g)
-                        if (g < ng) atomicMax(&a.tokmax[(int64_t)tok[g] * a.n_docs + dcur], acc[g]);
+                        if (g < ng) atomicMax(&a.tokmax[(int64_t)tok[g] * a.n_docs + doc[r]], acc[g]);
                 }
             }
         }
