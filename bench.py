@@ -23,6 +23,39 @@ import numpy as np  # noqa: E402
 METRIC = "queries/s, p50 query latency, scored embeddings/s (% of HBM peak BW)"
 HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
+# LDS read peak: 256 CUs x 256 B/clk (one 64-lane ds_read_b128 every 4 cycles) x 2.4 GHz
+LDS_PEAK_GBS = 256 * 256 * 2.4
+CSRC = os.path.join(ROOT, "paper_2501_17788_amd", "csrc")
+TRAFFIC_TABLE = os.path.join(ROOT, "profiles", "traffic.md")
+
+
+def csrc_hash() -> str:
+    """Hash of the engine sources: counter figures are used only for the code they measured."""
+    import hashlib
+
+    h = hashlib.sha1()
+    for name in sorted(os.listdir(CSRC)):
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch (FETCH_SIZE x 2 + WRITE_SIZE x 1, calibrated on a copy kernel)
+    recorded in profiles/traffic.md for these exact sources, else None."""
+    try:
+        rows = open(TRAFFIC_TABLE).read().splitlines()
+    except OSError:
+        return None
+    h = csrc_hash()
+    for line in rows:
+        cells = [c.strip() for c in line.strip().strip("|").split("|")]
+        if len(cells) >= 5 and cells[0] == kernel and cells[1] == workload and cells[2] == h:
+            try:
+                return float(cells[3]) + float(cells[4])
+            except ValueError:
+                return None
+    return None
 
 
 def log(*a):
@@ -138,8 +171,23 @@ def main() -> int:
     scan_ms, scan_n = stages["scan"]
     scan_avg_s = scan_ms / 1e3 / max(scan_n, 1)
     launches_per_step = max(scan_n, 1) / args.steps
-    scan_bytes = float(scored.sum()) * row_bytes / launches_per_step  # algorithmic bytes per launch
-    achieved = scan_bytes / scan_avg_s / 1e9
+    pairs_per_launch = float(scored.sum()) / launches_per_step  # scored (token, embedding) pairs
+    hbm_equiv = pairs_per_launch * row_bytes / scan_avg_s / 1e9  # 16b + 4 bytes per scored pair
+    cluster_major = os.environ.get("WARP_SCAN", "cluster") != "token"
+    if cluster_major:
+        # one 16-byte table entry (four tokens) per code nibble: 4 * 32 * b bytes of LDS per pair
+        lds_bytes = pairs_per_launch * 4.0 * 32 * wl.nbits
+        roofline = {"bound": "alu", "kernel": "k_scan_cm", "resource": "LDS table reads",
+                    "achieved": lds_bytes / scan_avg_s / 1e9, "peak": LDS_PEAK_GBS, "unit": "GB/s",
+                    "frac": lds_bytes / scan_avg_s / 1e9 / LDS_PEAK_GBS,
+                    "traffic": measured_traffic("k_scan_cm", wl.name),
+                    "algorithmic_bytes_per_launch": lds_bytes, "avg_launch_ms": scan_avg_s * 1e3}
+    else:
+        roofline = {"bound": "hbm", "kernel": "k_scan", "achieved": hbm_equiv, "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": hbm_equiv / HBM_PEAK_GBS,
+                    "traffic": measured_traffic("k_scan", wl.name),
+                    "algorithmic_bytes_per_launch": pairs_per_launch * row_bytes,
+                    "avg_launch_ms": scan_avg_s * 1e3}
     gemm_ms, gemm_n = stages["filter_gemm"]
     gemm_flops = 2.0 * nq * wl.n_qtok * wl.n_centroids * 128 / (max(gemm_n, 1) / args.steps)
     gemm_tflops = gemm_flops / (gemm_ms / 1e3 / max(gemm_n, 1)) / 1e12 if gemm_n else None
@@ -181,10 +229,9 @@ def main() -> int:
         "scored_emb_per_s": float(scored.sum()) * args.steps / elapsed,
         "hbm_frac_effective": float(scored.sum()) * args.steps * row_bytes / elapsed / (HBM_PEAK_GBS * 1e9),
         "stage_ms_per_step": {k: v[0] / args.steps for k, v in stages.items()},
-        "roofline": {"bound": "hbm", "kernel": "k_scan", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "algorithmic_bytes_per_launch": scan_bytes,
-                     "avg_launch_ms": scan_avg_s * 1e3},
+        "roofline": roofline,
+        "scan_hbm_equivalent": {"bytes_per_scored_embedding": row_bytes, "GBps": hbm_equiv,
+                                "frac_of_hbm_peak": hbm_equiv / HBM_PEAK_GBS},
         "filter_gemm": {"tflops": gemm_tflops, "peak": FP32_MFMA_PEAK_TFLOPS,
                         "frac": (gemm_tflops / FP32_MFMA_PEAK_TFLOPS) if gemm_tflops else None},
         "cpu_baseline": cpu,

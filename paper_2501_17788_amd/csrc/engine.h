@@ -39,10 +39,9 @@ constexpr int kScanTile = kScanBlock * kScanIters;
 
 // Cluster-major residual scan: a work item is (cluster, chunk of kCmChunk embeddings
 // held in registers, group of kCmGroup probing tokens scored kCmPack at a time).
-constexpr int kCmBlock = 512;
-constexpr int kCmRows = 1;  // embeddings per thread (the chunk is kCmBlock * rows)
+constexpr int kCmBlock = 512;  // also the chunk: one embedding per thread
 constexpr int kCmGroup = 16;
-constexpr int kCmPack = 4;
+constexpr int kCmPack = 4;     // tokens scored per table pass (4 or 8)
 constexpr int kPlanBlock = 1024;  // clusters per block of the pairing prefix sums
 
 // Error bits the device reports through the index's flag word.
@@ -92,7 +91,7 @@ struct WaveArgs {
     uint32_t* dbg_bitmap;       // [n_q][ceil(n_docs / 32)] or null
     int64_t* dbg_scored;        // [n_q] or null
     int32_t scan_grid;          // persistent workgroups of the residual scan
-    int32_t cm_rows;            // embeddings per thread of the cluster-major scan (1 or 2)
+    int32_t cm_pack;            // tokens per table pass of the cluster-major scan (4 or 8)
 };
 
 // out_bins [n_tok][n_c] u16 bins (the search path) or, if null, out_scores fp32
@@ -103,7 +102,7 @@ void launch_plan(const WaveArgs& a, hipStream_t s);
 void launch_scan(const WaveArgs& a, hipStream_t s);
 void launch_pairing(const WaveArgs& a, hipStream_t s);
 void launch_scan_cm(const WaveArgs& a, hipStream_t s);
-int scan_cm_blocks_per_cu(int nbits, int rows);
+int scan_cm_blocks_per_cu(int nbits, int pack);
 void launch_fold(const WaveArgs& a, hipStream_t s);
 void launch_topk(const WaveArgs& a, hipStream_t s);
 void launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);

@@ -63,7 +63,7 @@ struct warp_index {
     int32_t* err = nullptr;
     hipStream_t stream = nullptr;
     int scan_grid = 0;     // persistent workgroups of the token-major scan
-    int scan_cm_grid[2] = {0, 0};  // persistent workgroups of the cluster-major scan, rows 1 and 2
+    int scan_cm_grid[2] = {0, 0};  // persistent workgroups of the cluster-major scan, pack 4 and 8
     // per-search scratch, grown on demand
     DevBuf filter, sel, base, seg_start, seg_pref, m_fixed, tile_start, tokmax, keys;
     DevBuf ccount, cursor, item_start, pair_start, plist, blk;
@@ -191,8 +191,8 @@ int finish_load(warp_index* idx, const int64_t* off_host) {
     int cus = 0;
     HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, idx->device));
     idx->scan_grid = cus * scan_blocks_per_cu(idx->nbits);
-    idx->scan_cm_grid[0] = cus * scan_cm_blocks_per_cu(idx->nbits, 1);
-    idx->scan_cm_grid[1] = cus * scan_cm_blocks_per_cu(idx->nbits, 2);
+    idx->scan_cm_grid[0] = cus * scan_cm_blocks_per_cu(idx->nbits, 4);
+    idx->scan_cm_grid[1] = cus * scan_cm_blocks_per_cu(idx->nbits, 8);
     return WARP_OK;
 }
 
@@ -371,8 +371,8 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
     launch_check_queries(dq, (int64_t)n_queries * T, idx->err, s);
     const char* scan_env = std::getenv("WARP_SCAN");
     const bool cluster_major = !(scan_env && std::strcmp(scan_env, "token") == 0);
-    const char* rows_env = std::getenv("WARP_CM_ROWS");
-    const int cm_rows = rows_env ? (std::atoi(rows_env) == 2 ? 2 : 1) : kCmRows;
+    const char* pack_env = std::getenv("WARP_CM_PACK");
+    const int cm_pack = pack_env ? (std::atoi(pack_env) == 8 ? 8 : 4) : kCmPack;
     const int64_t words = ((int64_t)idx->n_docs + 31) / 32;
     for (int32_t q0 = 0; q0 < n_queries; q0 += qw) {
         const int32_t nq = n_queries - q0 < qw ? n_queries - q0 : qw;
@@ -416,8 +416,8 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         a.pair_start = (int32_t*)idx->pair_start.p;
         a.plist = (int32_t*)idx->plist.p;
         a.blk = (int64_t*)idx->blk.p;
-        a.cm_rows = cm_rows;
-        a.scan_grid = cluster_major ? idx->scan_cm_grid[cm_rows - 1] : idx->scan_grid;
+        a.cm_pack = cm_pack;
+        a.scan_grid = cluster_major ? idx->scan_cm_grid[cm_pack == 8 ? 1 : 0] : idx->scan_grid;
 
         hipEvent_t ev[kStages + 1] = {};
         if (idx->timing)

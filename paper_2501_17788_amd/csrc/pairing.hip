@@ -1,6 +1,6 @@
 // Cluster-major work plan of one wave of queries: every (query token, probed
 // cluster) pair is bucketed by cluster (a counting sort), and each probed
-// cluster is cut into work items of (kCmChunk embeddings) x (kCmGroup tokens),
+// cluster is cut into work items of (kCmBlock embeddings) x (kCmGroup tokens),
 // so that the residual scan reads a cluster chunk once for all the tokens that
 // probe it. Pair order inside a bucket follows atomic arrival and does not
 // affect results: the token-level max is exact and commutative.
@@ -17,9 +17,9 @@ __global__ __launch_bounds__(256) void k_pair_count(WaveArgs a) {
     if (c >= 0) atomicAdd(&a.ccount[c], 1);
 }
 
-__device__ __forceinline__ int64_t cluster_items(int32_t n_tok, int32_t size, int32_t chunk) {
+__device__ __forceinline__ int64_t cluster_items(int32_t n_tok, int32_t size) {
     if (n_tok <= 0 || size <= 0) return 0;
-    return (int64_t)((size + chunk - 1) / chunk) * ((n_tok + kCmGroup - 1) / kCmGroup);
+    return (int64_t)((size + kCmBlock - 1) / kCmBlock) * ((n_tok + kCmGroup - 1) / kCmGroup);
 }
 
 // exclusive scans of items and pairs inside each block of kPlanBlock clusters
@@ -30,7 +30,7 @@ __global__ __launch_bounds__(kPlanBlock) void k_cplan_local(WaveArgs a) {
     const int64_t c = (int64_t)blockIdx.x * kPlanBlock + tid;
     const bool in = c < a.n_c;
     const int32_t nt = in ? a.ccount[c] : 0;
-    const int64_t items = in ? cluster_items(nt, a.sizes[c], kCmBlock * a.cm_rows) : 0;
+    const int64_t items = in ? cluster_items(nt, a.sizes[c]) : 0;
     si[tid] = items;
     sp[tid] = nt;
     __syncthreads();

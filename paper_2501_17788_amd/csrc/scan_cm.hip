@@ -6,7 +6,7 @@
 // then tokmax[i][doc(e)] = max(...) through a wave segmented max and one
 // atomicMax per run of equal documents.
 //
-// Order of work: a work item is (cluster, chunk of kCmChunk embeddings, group of
+// Order of work: a work item is (cluster, chunk of kCmBlock embeddings, group of
 // kCmGroup probing tokens); items of one chunk are consecutive, so a persistent
 // workgroup walking a contiguous item range loads a chunk's codes into registers
 // once and scores them against every token of its items. The HBM traffic of the
@@ -16,11 +16,12 @@
 // Table: the per-token table upsilon = q_hat x omega_hat (Section 4.4) is held
 // per code nibble: entry [n][v] is the sum of the per-dimension entries of the
 // dimensions packed in nibble n when it holds v (one dimension for b = 4, two for
-// b = 2), so the integer sums are those of the per-dimension table. Each entry
-// packs kCmPack = 4 tokens (an int4), so one 16-byte LDS read serves four tokens;
-// all lanes of a wave read the same nibble row of 16 entries at a time, which
-// the LDS serves without bank conflicts. The table is built in LDS directly from
-// the fp32 query tokens: R(q_d * omega_v) in fp64, as in the definition.
+// b = 2), so the integer sums are those of the per-dimension table. One 16-byte
+// entry holds four tokens; with PACK = 8 a second table of the next four tokens
+// sits at a fixed offset, read with the same address register. All lanes of a
+// wave read the same nibble row of 16 entries at a time, which the LDS serves
+// without bank conflicts. The table is built in LDS directly from the fp32 query
+// tokens: R(q_d * omega_v) in fp64, as in the definition.
 #include "engine.h"
 
 namespace warp {
@@ -66,18 +67,20 @@ __device__ __forceinline__ int seg_max(int v, unsigned same) {
     return v;
 }
 
-template <int NBITS, int ROWS>
+template <int NBITS, int PACK>
 __global__ __launch_bounds__(kCmBlock) void k_scan_cm(WaveArgs a) {
-    constexpr int CHUNK = kCmBlock * ROWS;  // embeddings held in registers per workgroup
     constexpr int BYTES = kDim * NBITS / 8;  // code bytes per embedding
     constexpr int VEC = BYTES / 16;          // 16-byte loads per embedding
     constexpr int NN = 2 * BYTES;            // nibbles per embedding
     constexpr int ENT = NN * 16;             // table entries per token
     constexpr int PER = ENT / kCmBlock;      // entries built per thread
+    constexpr int TABLES = PACK / 4;         // 16-byte tables of four tokens
     static_assert(PER * kCmBlock == ENT, "table must split evenly");
-    __shared__ int4 lut[ENT];
-    __shared__ double qd[kCmPack][kDim];
-    __shared__ int s_pair[kCmPack][2];
+    static_assert((PACK * kDim) % kCmBlock == 0, "query staging");
+    static_assert((TABLES - 1) * ENT * 16 + NN * 256 <= 65536, "second table within the LDS offset field");
+    __shared__ int4 lut[TABLES * ENT];
+    __shared__ double qd[PACK][kDim];
+    __shared__ int s_pair[PACK][2];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -105,12 +108,10 @@ __global__ __launch_bounds__(kCmBlock) void k_scan_cm(WaveArgs a) {
 
     int cur_c = -1;
     int64_t cur_chunk = -1;
-    uint4 code[ROWS][VEC];
-    int doc[ROWS];
-    bool act[ROWS];
-    bool wave_act[ROWS];
-    unsigned same[ROWS];   // DPP steps that merge the same document
-    bool run_end[ROWS];    // last lane of its run of equal documents
+    uint4 code[VEC];
+    int doc = 0;
+    bool act = false, wave_act = false, run_end = false;
+    unsigned same = 0;  // DPP steps that merge the same document
     const uint8_t* __restrict__ codes = a.codes;
 
     while (item < last) {
@@ -121,38 +122,35 @@ __global__ __launch_bounds__(kCmBlock) void k_scan_cm(WaveArgs a) {
         const int64_t chunk = l / groups;
         const int grp = (int)(l - chunk * groups);
         if (c != cur_c || chunk != cur_chunk) {
-            const int64_t e0 = a.offsets[c] + chunk * CHUNK;
-            const int64_t e_end = a.offsets[c + 1];
+            const int64_t e = a.offsets[c] + chunk * kCmBlock + tid;
+            act = e < a.offsets[c + 1];
+            doc = -1 - lane;  // inactive lanes never match a neighbour
+            if (act) {
+                const uint4* row = reinterpret_cast<const uint4*>(codes + e * BYTES);
 #pragma unroll
-            for (int r = 0; r < ROWS; ++r) {
-                const int64_t e = e0 + r * kCmBlock + tid;
-                act[r] = e < e_end;
-                doc[r] = -1 - lane;  // inactive lanes never match a neighbour
-                if (act[r]) {
-                    const uint4* row = reinterpret_cast<const uint4*>(codes + e * BYTES);
-#pragma unroll
-                    for (int i = 0; i < VEC; ++i) code[r][i] = row[i];
-                    doc[r] = a.doc_ids[e];
-                }
-                wave_act[r] = __any(act[r]);
-                same[r] = same_doc_steps(doc[r]);
-                const int dn = __shfl_down(doc[r], 1, 64);
-                run_end[r] = act[r] && (lane == 63 || dn != doc[r]);
+                for (int i = 0; i < VEC; ++i) code[i] = row[i];
+                doc = a.doc_ids[e];
             }
+            wave_act = __any(act);
+            same = same_doc_steps(doc);
+            const int dn = __shfl_down(doc, 1, 64);
+            run_end = act && (lane == 63 || dn != doc);
             cur_c = c;
             cur_chunk = chunk;
         }
         const int p_first = a.pair_start[c] + grp * kCmGroup;
         const int p_end = min(p_first + kCmGroup, a.pair_start[c] + nt);
-        for (int p = p_first; p < p_end; p += kCmPack) {
-            const int ng = min(kCmPack, p_end - p);
+        for (int p = p_first; p < p_end; p += PACK) {
+            const int ng = min(PACK, p_end - p);
             __syncthreads();  // the previous table and query rows are no longer read
-            if (tid < kCmPack) {
+            if (tid < PACK) {
                 s_pair[tid][0] = tid < ng ? a.plist[2 * (int64_t)(p + tid)] : -1;
                 s_pair[tid][1] = tid < ng ? a.plist[2 * (int64_t)(p + tid) + 1] : 0;
             }
-            {
-                const int g = tid >> 7, d = tid & 127;  // kCmPack x 128 = kCmBlock values
+#pragma unroll
+            for (int h = 0; h < (PACK * kDim) / kCmBlock; ++h) {
+                const int x = tid + kCmBlock * h;
+                const int g = x >> 7, d = x & 127;
                 float qv = 0.f;
                 if (g < ng) {
                     const int t = a.plist[2 * (int64_t)(p + g)];
@@ -164,108 +162,111 @@ __global__ __launch_bounds__(kCmBlock) void k_scan_cm(WaveArgs a) {
 #pragma unroll
             for (int i = 0; i < PER; ++i) {
                 const int x = tid + kCmBlock * i;
-                const int n = x >> 4;                 // nibble n of dword n / 8, nibble n % 8
+                const int n = x >> 4;                   // nibble n of dword n / 8, nibble n % 8
                 const int m = n & 7;
                 const int j = 4 * (n >> 3) + (m >> 1);  // code byte holding the nibble
-                int val[kCmPack];
-                if (NBITS == 4) {
-                    const int d = 2 * j + ((m & 1) ? 0 : 1);  // high nibble: dimension 2j
 #pragma unroll
-                    for (int g = 0; g < kCmPack; ++g) val[g] = fixed_prod(qd[g][d], w_a);
-                } else {
-                    const int d = (m & 1) ? 4 * j : 4 * j + 2;  // high nibble: dimensions 4j, 4j+1
+                for (int tb = 0; tb < TABLES; ++tb) {
+                    int val[4];
+                    if (NBITS == 4) {
+                        const int d = 2 * j + ((m & 1) ? 0 : 1);  // high nibble: dimension 2j
 #pragma unroll
-                    for (int g = 0; g < kCmPack; ++g)
-                        val[g] = fixed_prod(qd[g][d], w_a) + fixed_prod(qd[g][d + 1], w_b);
+                        for (int g = 0; g < 4; ++g) val[g] = fixed_prod(qd[4 * tb + g][d], w_a);
+                    } else {
+                        const int d = (m & 1) ? 4 * j : 4 * j + 2;  // high nibble: dimensions 4j, 4j+1
+#pragma unroll
+                        for (int g = 0; g < 4; ++g)
+                            val[g] = fixed_prod(qd[4 * tb + g][d], w_a) + fixed_prod(qd[4 * tb + g][d + 1], w_b);
+                    }
+                    lut[tb * ENT + x] = make_int4(val[0], val[1], val[2], val[3]);
                 }
-                lut[x] = make_int4(val[0], val[1], val[2], val[3]);
             }
             __syncthreads();
-            int tok[kCmPack], base[kCmPack];
+            if (!wave_act) continue;  // wave-uniform
+            int tok[PACK], acc[PACK];
 #pragma unroll
-            for (int g = 0; g < kCmPack; ++g) {  // uniform across the workgroup: scalar registers
+            for (int g = 0; g < PACK; ++g) {  // uniform across the workgroup: scalar registers
                 tok[g] = __builtin_amdgcn_readfirstlane(s_pair[g][0]);
-                base[g] = __builtin_amdgcn_readfirstlane(s_pair[g][1]);
+                acc[g] = __builtin_amdgcn_readfirstlane(s_pair[g][1]);
             }
+            const char* lbase = reinterpret_cast<const char*>(lut);
 #pragma unroll
-            for (int r = 0; r < ROWS; ++r) {
-                if (!wave_act[r]) continue;  // wave-uniform
-                int acc[kCmPack];
+            for (int i = 0; i < VEC; ++i) {
+                uint4 cw = code[i];
+                // keep the nibble extraction inside the token loop: hoisting all
+                // table addresses out of it costs more registers than it saves
+                asm volatile("" : "+v"(cw.x), "+v"(cw.y), "+v"(cw.z), "+v"(cw.w));
+                const unsigned wv[4] = {cw.x, cw.y, cw.z, cw.w};
 #pragma unroll
-                for (int g = 0; g < kCmPack; ++g) acc[g] = base[g];
-                const char* lbase = reinterpret_cast<const char*>(lut);
+                for (int k = 0; k < 4; ++k) {
+                    // byte b of `even` is 16 x nibble 2b of the dword (the byte offset of
+                    // entry v in its 16-entry row of 16-byte entries); `odd` holds nibble 2b+1
+                    const unsigned even = (wv[k] << 4) & 0xF0F0F0F0u;
+                    const unsigned odd = wv[k] & 0xF0F0F0F0u;
+                    const int row = (4 * i + k) * 8;  // first nibble row of the dword
 #pragma unroll
-                for (int i = 0; i < VEC; ++i) {
-                    uint4 cw = code[r][i];
-                    // keep the nibble extraction inside the token loop: hoisting all
-                    // 128 table addresses out of it costs more registers than it saves
-                    asm volatile("" : "+v"(cw.x), "+v"(cw.y), "+v"(cw.z), "+v"(cw.w));
-                    const unsigned wv[4] = {cw.x, cw.y, cw.z, cw.w};
+                    for (int h = 0; h < 2; ++h) {  // four lookups per table in flight
+                        int4 e[TABLES][4];
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        // byte b of `even` is 16 x nibble 2b of the dword (the byte offset of
-                        // entry v in its 16-entry row of 16-byte entries); `odd` holds nibble 2b+1
-                        const unsigned even = (wv[k] << 4) & 0xF0F0F0F0u;
-                        const unsigned odd = wv[k] & 0xF0F0F0F0u;
-                        const int row = (4 * i + k) * 8;  // first nibble row of the dword
+                        for (int b = 2 * h; b < 2 * h + 2; ++b) {
+                            const char* pe = lbase + (row + 2 * b) * 256 + ((even >> (8 * b)) & 0xFFu);
+                            const char* po = lbase + (row + 2 * b + 1) * 256 + ((odd >> (8 * b)) & 0xFFu);
 #pragma unroll
-                        for (int h = 0; h < 2; ++h) {  // four lookups in flight at a time
-                            int4 e[4];
-#pragma unroll
-                            for (int b = 2 * h; b < 2 * h + 2; ++b) {
-                                e[2 * (b - 2 * h)] = *reinterpret_cast<const int4*>(
-                                    lbase + (row + 2 * b) * 256 + ((even >> (8 * b)) & 0xFFu));
-                                e[2 * (b - 2 * h) + 1] = *reinterpret_cast<const int4*>(
-                                    lbase + (row + 2 * b + 1) * 256 + ((odd >> (8 * b)) & 0xFFu));
+                            for (int tb = 0; tb < TABLES; ++tb) {
+                                e[tb][2 * (b - 2 * h)] = *reinterpret_cast<const int4*>(pe + tb * ENT * 16);
+                                e[tb][2 * (b - 2 * h) + 1] = *reinterpret_cast<const int4*>(po + tb * ENT * 16);
                             }
+                        }
+#pragma unroll
+                        for (int tb = 0; tb < TABLES; ++tb) {
 #pragma unroll
                             for (int b = 0; b < 4; b += 2) {
-                                acc[0] += e[b].x + e[b + 1].x;
-                                acc[1] += e[b].y + e[b + 1].y;
-                                acc[2] += e[b].z + e[b + 1].z;
-                                acc[3] += e[b].w + e[b + 1].w;
+                                acc[4 * tb + 0] += e[tb][b].x + e[tb][b + 1].x;
+                                acc[4 * tb + 1] += e[tb][b].y + e[tb][b + 1].y;
+                                acc[4 * tb + 2] += e[tb][b].z + e[tb][b + 1].z;
+                                acc[4 * tb + 3] += e[tb][b].w + e[tb][b + 1].w;
                             }
                         }
                     }
                 }
-                // inner-cluster max: segmented max over runs of equal documents, then one
-                // atomicMax per run and token
+            }
+            // inner-cluster max: segmented max over runs of equal documents, then one
+            // atomicMax per run and token
 #pragma unroll
-                for (int g = 0; g < kCmPack; ++g) acc[g] = seg_max(acc[g], same[r]);
-                if (run_end[r]) {
+            for (int g = 0; g < PACK; ++g) acc[g] = seg_max(acc[g], same);
+            if (run_end) {
 #pragma unroll
-                    for (int g = 0; g < kCmPack; ++g)
-                        if (g < ng) atomicMax(&a.tokmax[(int64_t)tok[g] * a.n_docs + doc[r]], acc[g]);
-                }
+                for (int g = 0; g < PACK; ++g)
+                    if (g < ng) atomicMax(&a.tokmax[(int64_t)tok[g] * a.n_docs + doc], acc[g]);
             }
         }
         ++item;
     }
 }
 
-template <int NBITS, int ROWS>
+template <int NBITS, int PACK>
 static void launch_cm(const WaveArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL((k_scan_cm<NBITS, ROWS>), dim3(a.scan_grid), dim3(kCmBlock), 0, s, a);
+    hipLaunchKernelGGL((k_scan_cm<NBITS, PACK>), dim3(a.scan_grid), dim3(kCmBlock), 0, s, a);
 }
 
 void launch_scan_cm(const WaveArgs& a, hipStream_t s) {
     if (a.nbits == 4) {
-        if (a.cm_rows == 1) launch_cm<4, 1>(a, s);
-        else launch_cm<4, 2>(a, s);
+        if (a.cm_pack == 8) launch_cm<4, 8>(a, s);
+        else launch_cm<4, 4>(a, s);
     } else {
-        if (a.cm_rows == 1) launch_cm<2, 1>(a, s);
-        else launch_cm<2, 2>(a, s);
+        if (a.cm_pack == 8) launch_cm<2, 8>(a, s);
+        else launch_cm<2, 4>(a, s);
     }
 }
 
-int scan_cm_blocks_per_cu(int nbits, int rows) {
+int scan_cm_blocks_per_cu(int nbits, int pack) {
     int n = 0;
     if (nbits == 4)
         (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &n, rows == 1 ? k_scan_cm<4, 1> : k_scan_cm<4, 2>, kCmBlock, 0);
+            &n, pack == 8 ? k_scan_cm<4, 8> : k_scan_cm<4, 4>, kCmBlock, 0);
     else
         (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &n, rows == 1 ? k_scan_cm<2, 1> : k_scan_cm<2, 2>, kCmBlock, 0);
+            &n, pack == 8 ? k_scan_cm<2, 8> : k_scan_cm<2, 4>, kCmBlock, 0);
     return n > 0 ? n : 1;
 }
 

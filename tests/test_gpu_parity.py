@@ -21,12 +21,12 @@ pytestmark = pytest.mark.gpu
 EXACT = ("ids", "fixed", "counts", "sel", "m_fixed", "cand_bitmap", "n_scored")
 
 
-@pytest.fixture(autouse=True, params=["cluster", "cluster1", "token"])
+@pytest.fixture(autouse=True, params=["cluster", "cluster8", "token"])
 def scan_variant(request, monkeypatch):
-    """Every parity test runs with each residual scan: cluster-major with two and
-    with one embedding per thread, and token-major."""
+    """Every parity test runs with each residual scan: cluster-major scoring four
+    or eight tokens per table pass, and token-major."""
     monkeypatch.setenv("WARP_SCAN", "token" if request.param == "token" else "cluster")
-    monkeypatch.setenv("WARP_CM_ROWS", "1" if request.param == "cluster1" else "2")
+    monkeypatch.setenv("WARP_CM_PACK", "8" if request.param == "cluster8" else "4")
     print(f"[scan={request.param}]", flush=True)
     return request.param
 
