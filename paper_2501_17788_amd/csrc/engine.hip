@@ -308,13 +308,22 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P) {
     return WARP_OK;
 }
 
+// Queries per wave: as many as the scratch budget holds. The budget is
+// WARP_SCRATCH_MB if set, else 60% of the device memory that is free or already
+// held as scratch by this index. A larger wave lets the cluster-major scan read
+// each probed cluster once for more queries.
 int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T) {
-    size_t budget = (size_t)32 << 30;
-    if (const char* s = std::getenv("WARP_SCRATCH_MB")) budget = (size_t)std::atoll(s) << 20;
-    size_t free_b = 0, total_b = 0;
-    if (hipMemGetInfo(&free_b, &total_b) == hipSuccess) {
-        const size_t cap = free_b / 2 + idx->tokmax.bytes + idx->filter.bytes + idx->keys.bytes;
-        if (cap < budget) budget = cap;
+    const size_t held = idx->tokmax.bytes + idx->filter.bytes + idx->keys.bytes + idx->plist.bytes;
+    size_t budget = 0;
+    if (const char* s = std::getenv("WARP_SCRATCH_MB")) {
+        budget = (size_t)std::atoll(s) << 20;
+    } else {
+        size_t free_b = 0, total_b = 0;
+        if (hipMemGetInfo(&free_b, &total_b) != hipSuccess) {
+            (void)hipGetLastError();
+            free_b = (size_t)8 << 30;
+        }
+        budget = (size_t)(0.6 * (double)(free_b + held));
     }
     const size_t per = (size_t)T * idx->n_docs * 4 + (size_t)idx->n_docs * 8 + (size_t)T * idx->n_c * 2 +
                        (size_t)T * kMaxProbe * 32 + (size_t)T * 1024;

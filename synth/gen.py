@@ -157,45 +157,107 @@ def pack_codes(codes: np.ndarray, nbits: int) -> np.ndarray:
 
 
 # ----------------------------------------------------------------------------
-# chunked token generation (process-pool friendly)
+# chunked token generation (fork-based process pool; outputs in shared memory)
 
 _G: dict = {}
 
 
-def _init_worker(state: dict) -> None:
-    _G.clear()
-    _G.update(state)
+def _draw_clusters(chunk: int, n: int) -> np.ndarray:
+    """Cluster ids of the n tokens of chunk `chunk` (Zipf rank -> permuted centroid)."""
+    w: Workload = _G["w"]
+    u = _rng(w.seed, S_DRAWS, chunk).random(n)
+    z = np.minimum(np.searchsorted(_G["cdf"], u, side="right"), w.n_centroids - 1)
+    return _G["perm"][z].astype(np.int32)
 
 
 def _tokens(chunk: int, e0: int, e1: int):
     """Tokens [e0, e1) of chunk `chunk`: (cluster ids, fp32 unit vectors)."""
     w: Workload = _G["w"]
     n = e1 - e0
-    u = _rng(w.seed, S_DRAWS, chunk).random(n)
-    z = np.minimum(np.searchsorted(_G["cdf"], u, side="right"), w.n_centroids - 1)
-    cl = _G["perm"][z].astype(np.int32)
-    noise = _rng(w.seed, S_NOISE, chunk).standard_normal((n, DIM))
-    x = _normalize_rows(_G["C"][cl].astype(np.float64) + w.token_noise * noise).astype(np.float32)
+    cl = _draw_clusters(chunk, n)
+    noise = _rng(w.seed, S_NOISE, chunk).standard_normal((n, DIM), dtype=np.float32)
+    x = _G["C"][cl]
+    x += np.float32(w.token_noise) * noise
+    x /= np.sqrt(np.einsum("ij,ij->i", x, x))[:, None]
     return cl, x
 
 
-def _chunk_job(chunk: int):
-    n_total = _G["n_total"]
-    e0 = chunk * CHUNK
-    e1 = min(n_total, e0 + CHUNK)
-    cl, x = _tokens(chunk, e0, e1)
-    r = x - _G["C"][cl]
-    codes = np.searchsorted(_G["cutoffs"], r.ravel(), side="right").reshape(r.shape)
-    packed = pack_codes(codes, _G["w"].nbits)
+def _codes(r: np.ndarray, nbits: int) -> np.ndarray:
+    """Per-dimension code = number of cutoffs <= r, packed MSB-first. The cutoffs are
+    compared as the smallest float32 at or above each fp64 cutoff, which gives the same
+    decision for float32 residuals as the fp64 comparison."""
+    cut32 = _G["cut32"]
+    code = np.zeros(r.shape, np.uint8)
+    for c in cut32:
+        code += r >= c
+    return pack_codes(code, nbits)
+
+
+def _chunk_range(s: int):
+    """Chunks of super-range s (contiguous, so each worker walks docs in order)."""
+    n_chunks, n_super = _G["n_chunks"], _G["n_super"]
+    return range(s * n_chunks // n_super, (s + 1) * n_chunks // n_super)
+
+
+def _count_job(s: int) -> np.ndarray:
+    w: Workload = _G["w"]
+    counts = np.zeros(w.n_centroids, np.int64)
+    for chunk in _chunk_range(s):
+        e0 = chunk * CHUNK
+        e1 = min(_G["n_total"], e0 + CHUNK)
+        counts += np.bincount(_draw_clusters(chunk, e1 - e0), minlength=w.n_centroids)
+    return counts
+
+
+def _write_job(s: int):
+    """Generate the chunks of super-range s and write codes and doc ids into their
+    final (cluster-grouped, doc-ascending) positions; return the query tokens."""
+    w: Workload = _G["w"]
+    cursor = _G["start"][s].copy()
+    codes_out, docs_out, doc_of = _G["codes_out"], _G["docs_out"], _G["doc_of"]
     want = _G["want"]
-    lo, hi = np.searchsorted(want, [e0, e1])
-    picked = x[want[lo:hi] - e0] if hi > lo else np.zeros((0, DIM), np.float32)
-    return chunk, cl, packed, picked
+    picked = []
+    for chunk in _chunk_range(s):
+        e0 = chunk * CHUNK
+        e1 = min(_G["n_total"], e0 + CHUNK)
+        cl, x = _tokens(chunk, e0, e1)
+        packed = _codes(x - _G["C"][cl], w.nbits)
+        order = np.argsort(cl, kind="stable")
+        scl = cl[order]
+        first = np.r_[True, scl[1:] != scl[:-1]]
+        starts = np.flatnonzero(first)
+        rank = np.arange(len(scl)) - np.repeat(starts, np.diff(np.r_[starts, len(scl)]))
+        pos = cursor[scl] + rank
+        codes_out[pos] = packed[order]
+        docs_out[pos] = doc_of(e0 + order)
+        u, cnt = scl[starts], np.diff(np.r_[starts, len(scl)])
+        cursor[u] += cnt
+        lo, hi = np.searchsorted(want, [e0, e1])
+        if hi > lo:
+            picked.append((want[lo:hi], x[want[lo:hi] - e0]))
+    return picked
 
 
-def _state(w: Workload, C, perm, cdf, cutoffs, n_total, want) -> dict:
-    return {"w": w, "C": C, "perm": perm, "cdf": cdf, "cutoffs": cutoffs, "n_total": n_total,
-            "want": want}
+def _state(w: Workload, C, perm, cdf, n_total) -> dict:
+    return {"w": w, "C": C, "perm": perm, "cdf": cdf, "n_total": n_total}
+
+
+def _shared(shape, dtype) -> np.ndarray:
+    """An array in anonymous shared memory, inherited by forked workers."""
+    import mmap
+
+    nbytes = int(np.prod(shape)) * np.dtype(dtype).itemsize
+    buf = mmap.mmap(-1, max(nbytes, 1))
+    return np.frombuffer(buf, dtype=dtype, count=int(np.prod(shape))).reshape(shape)
+
+
+def _run(jobs, fn, workers):
+    if workers > 1 and len(jobs) > 1:
+        import multiprocessing as mp
+
+        with ProcessPoolExecutor(min(workers, len(jobs)), mp_context=mp.get_context("fork")) as ex:
+            return list(ex.map(fn, jobs))
+    return [fn(j) for j in jobs]
 
 
 def token_vectors(w: Workload, emb_ids: np.ndarray) -> np.ndarray:
@@ -203,7 +265,8 @@ def token_vectors(w: Workload, emb_ids: np.ndarray) -> np.ndarray:
     C = make_centroids(w)
     perm = _rng(w.seed, S_PERM).permutation(w.n_centroids)
     cdf = zipf_cdf(w.n_centroids, w.zipf_s)
-    _init_worker(_state(w, C, perm, cdf, None, None, None))
+    _G.clear()
+    _G.update(_state(w, C, perm, cdf, None))
     out = np.zeros((len(emb_ids), DIM), np.float32)
     ids = np.asarray(emb_ids, dtype=np.int64)
     for chunk in np.unique(ids // CHUNK):
@@ -214,10 +277,13 @@ def token_vectors(w: Workload, emb_ids: np.ndarray) -> np.ndarray:
     return out
 
 
-def make_index(w: Workload, with_queries: bool = True, workers: int | None = None) -> SyntheticIndex:
-    """Generate the whole index (and, optionally, the query batch) of workload `w`."""
+def make_index(w: Workload, with_queries: bool = True, workers: int | None = None,
+               progress=None) -> SyntheticIndex:
+    """Generate the whole index (and, optionally, the query batch) of workload `w`.
+    `progress(msg)` is called between the phases of a large generation."""
     if DIM % (8 // w.nbits) != 0 or w.nbits not in (1, 2, 4, 8):
         raise ValueError("nbits must be 1, 2, 4 or 8")
+    say = progress or (lambda msg: None)
     C = make_centroids(w)
     perm = _rng(w.seed, S_PERM).permutation(w.n_centroids).astype(np.int64)
     cdf = zipf_cdf(w.n_centroids, w.zipf_s)
@@ -225,18 +291,22 @@ def make_index(w: Workload, with_queries: bool = True, workers: int | None = Non
     doc_start = np.zeros(w.n_docs + 1, np.int64)
     np.cumsum(lens, out=doc_start[1:])
     n_total = int(doc_start[-1])
+    _G.clear()
+    _G.update(_state(w, C, perm, cdf, n_total))
 
-    # Quantile cutoffs and bucket weights from the residuals of the first tokens.
-    _init_worker(_state(w, C, perm, cdf, None, n_total, None))
+    # quantile cutoffs and bucket weights from the residuals of the first tokens
     ns = min(n_total, QUANTILE_SAMPLE)
     cl_s, x_s = _tokens(0, 0, ns)
     sample = (x_s - C[cl_s]).astype(np.float64).ravel()
     nb = 1 << w.nbits
     cutoffs = np.quantile(sample, np.arange(1, nb) / nb)
     weights = np.quantile(sample, (np.arange(nb) + 0.5) / nb).astype(np.float32)
+    cut32 = cutoffs.astype(np.float32)
+    cut32 = np.where(cut32.astype(np.float64) < cutoffs, np.nextafter(cut32, np.float32(np.inf)), cut32)
+    _G["cut32"] = cut32.astype(np.float32)
 
-    # Query targets: documents and token positions (drawn before the token pass so the
-    # pass can keep exactly the tokens the queries need).
+    # query targets: documents and token positions, drawn before the token pass so that
+    # the pass keeps exactly the tokens the queries need
     want = np.zeros(0, np.int64)
     if with_queries:
         qr = _rng(w.seed, S_QUERIES)
@@ -245,50 +315,42 @@ def make_index(w: Workload, with_queries: bool = True, workers: int | None = Non
         q_emb = doc_start[targets][:, None] + pos
         q_noise = qr.standard_normal((w.n_queries, w.n_qtok, DIM))
         want = np.unique(q_emb.ravel())
+    _G["want"] = want
 
-    n_chunks = (n_total + CHUNK - 1) // CHUNK
-    state = _state(w, C, perm, cdf, cutoffs, n_total, want)
-    cluster = np.empty(n_total, np.int32)
-    codes = np.empty((n_total, DIM * w.nbits // 8), np.uint8)
-    picked = [None] * n_chunks
     if workers is None:
         workers = min(16, os.cpu_count() or 1)
-    if workers > 1 and n_chunks > 2:
-        import multiprocessing as mp
-        ctx = mp.get_context("fork")
-        with ProcessPoolExecutor(workers, mp_context=ctx, initializer=_init_worker,
-                                 initargs=(state,)) as ex:
-            results = ex.map(_chunk_job, range(n_chunks), chunksize=1)
-            for chunk, cl, packed, pk in results:
-                e0 = chunk * CHUNK
-                cluster[e0:e0 + len(cl)] = cl
-                codes[e0:e0 + len(cl)] = packed
-                picked[chunk] = pk
-    else:
-        _init_worker(state)
-        for chunk in range(n_chunks):
-            _, cl, packed, pk = _chunk_job(chunk)
-            e0 = chunk * CHUNK
-            cluster[e0:e0 + len(cl)] = cl
-            codes[e0:e0 + len(cl)] = packed
-            picked[chunk] = pk
+    n_chunks = (n_total + CHUNK - 1) // CHUNK
+    n_super = max(1, min(n_chunks, 4 * workers))
+    _G["n_chunks"], _G["n_super"] = n_chunks, n_super
 
-    doc_of = np.repeat(np.arange(w.n_docs, dtype=np.int32), lens)
-    order = np.argsort(cluster, kind="stable")
-    counts = np.bincount(cluster, minlength=w.n_centroids)
+    # pass 1: cluster sizes per super-range -> cluster offsets and write cursors
+    counts = np.stack(_run(list(range(n_super)), _count_job, workers))
+    sizes = counts.sum(axis=0)
     offsets = np.zeros(w.n_centroids + 1, np.int64)
-    np.cumsum(counts, out=offsets[1:])
+    np.cumsum(sizes, out=offsets[1:])
+    start = offsets[:-1][None, :] + np.cumsum(counts, axis=0) - counts
+    _G["start"] = start
+    say(f"cluster sizes done ({n_total} embeddings, {n_chunks} chunks)")
+
+    # pass 2: tokens, codes, and their scatter into cluster order
+    codes = _shared((n_total, DIM * w.nbits // 8), np.uint8)
+    doc_ids = _shared((n_total,), np.int32)
+    _G["codes_out"], _G["docs_out"] = codes, doc_ids
+    _G["doc_of"] = lambda e: (np.searchsorted(doc_start, e, side="right") - 1).astype(np.int32)
+    picked = [p for part in _run(list(range(n_super)), _write_job, workers) for p in part]
+    say("codes done")
+
     idx = SyntheticIndex(
-        workload=w, centroids=C, offsets=offsets, doc_ids=doc_of[order],
-        codes=codes[order], bucket_weights=weights, bucket_cutoffs=cutoffs, doc_lengths=lens)
-    del codes, cluster
+        workload=w, centroids=C, offsets=offsets, doc_ids=doc_ids, codes=codes,
+        bucket_weights=weights, bucket_cutoffs=cutoffs, doc_lengths=lens)
     if with_queries:
-        xs = np.concatenate([p for p in picked if p is not None and len(p)]) if len(want) else \
-            np.zeros((0, DIM), np.float32)
-        row = np.searchsorted(want, q_emb)
+        ids = np.concatenate([p[0] for p in picked]) if picked else np.zeros(0, np.int64)
+        xs = np.concatenate([p[1] for p in picked]) if picked else np.zeros((0, DIM), np.float32)
+        row = np.searchsorted(ids, q_emb)
         x = xs[row].astype(np.float64)
         idx.queries = _normalize_rows(x + w.query_noise * q_noise).astype(np.float32)
         idx.query_targets = targets.astype(np.int32)
+    _G.clear()
     return idx
 
 
