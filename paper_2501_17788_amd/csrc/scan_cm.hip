@@ -26,8 +26,30 @@
 
 namespace warp {
 
-__device__ __forceinline__ int fixed_prod(double q, double w) {
-    return (int)__builtin_rint(q * w * (double)(1 << kFrac));
+// R(q * w) for a query value already scaled by 2^kFrac (exact: a power of two).
+__device__ __forceinline__ int fixed_prod(double q_scaled, double w) {
+    return (int)__builtin_rint(q_scaled * w);
+}
+
+// 16 x (high nibble of byte B of w): one SDWA AND, the byte offset of table entry
+// v in its row of 16-byte entries. The low nibble of byte B is the same operation
+// on w << 4.
+template <int B>
+__device__ __forceinline__ unsigned nib16(unsigned w, unsigned mask_f0) {
+    unsigned r;
+    if (B == 0) {
+        r = w & 0xF0u;
+    } else if (B == 1) {
+        asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_1 src1_sel:DWORD"
+            : "=v"(r) : "v"(w), "v"(mask_f0));
+    } else if (B == 2) {
+        asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_2 src1_sel:DWORD"
+            : "=v"(r) : "v"(w), "v"(mask_f0));
+    } else {
+        asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_3 src1_sel:DWORD"
+            : "=v"(r) : "v"(w), "v"(mask_f0));
+    }
+    return r;
 }
 
 // Wave-level segmented max-scan over runs of equal document ids, the gfx9 DPP
@@ -156,7 +178,7 @@ __global__ __launch_bounds__(kCmBlock) void k_scan_cm(WaveArgs a) {
                     const int t = a.plist[2 * (int64_t)(p + g)];
                     qv = a.queries[(int64_t)t * kDim + d];
                 }
-                qd[g][d] = (double)qv;
+                qd[g][d] = (double)qv * (double)(1 << kFrac);
             }
             __syncthreads();
 #pragma unroll
@@ -190,6 +212,7 @@ __global__ __launch_bounds__(kCmBlock) void k_scan_cm(WaveArgs a) {
                 acc[g] = __builtin_amdgcn_readfirstlane(s_pair[g][1]);
             }
             const char* lbase = reinterpret_cast<const char*>(lut);
+            const unsigned mask_f0 = 0xF0u;
 #pragma unroll
             for (int i = 0; i < VEC; ++i) {
                 uint4 cw = code[i];
@@ -199,18 +222,21 @@ __global__ __launch_bounds__(kCmBlock) void k_scan_cm(WaveArgs a) {
                 const unsigned wv[4] = {cw.x, cw.y, cw.z, cw.w};
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
-                    // byte b of `even` is 16 x nibble 2b of the dword (the byte offset of
-                    // entry v in its 16-entry row of 16-byte entries); `odd` holds nibble 2b+1
-                    const unsigned even = (wv[k] << 4) & 0xF0F0F0F0u;
-                    const unsigned odd = wv[k] & 0xF0F0F0F0u;
+                    // entry offsets: nibble 2b of the dword is the low nibble of byte b
+                    // (read from w << 4), nibble 2b + 1 its high nibble
+                    const unsigned w = wv[k], w4 = w << 4;
+                    const unsigned off_lo[4] = {nib16<0>(w4, mask_f0), nib16<1>(w4, mask_f0),
+                                                nib16<2>(w4, mask_f0), nib16<3>(w4, mask_f0)};
+                    const unsigned off_hi[4] = {nib16<0>(w, mask_f0), nib16<1>(w, mask_f0),
+                                                nib16<2>(w, mask_f0), nib16<3>(w, mask_f0)};
                     const int row = (4 * i + k) * 8;  // first nibble row of the dword
 #pragma unroll
                     for (int h = 0; h < 2; ++h) {  // four lookups per table in flight
                         int4 e[TABLES][4];
 #pragma unroll
                         for (int b = 2 * h; b < 2 * h + 2; ++b) {
-                            const char* pe = lbase + (row + 2 * b) * 256 + ((even >> (8 * b)) & 0xFFu);
-                            const char* po = lbase + (row + 2 * b + 1) * 256 + ((odd >> (8 * b)) & 0xFFu);
+                            const char* pe = lbase + (row + 2 * b) * 256 + off_lo[b];
+                            const char* po = lbase + (row + 2 * b + 1) * 256 + off_hi[b];
 #pragma unroll
                             for (int tb = 0; tb < TABLES; ++tb) {
                                 e[tb][2 * (b - 2 * h)] = *reinterpret_cast<const int4*>(pe + tb * ENT * 16);
