@@ -23,8 +23,7 @@ import numpy as np  # noqa: E402
 METRIC = "queries/s, p50 query latency, scored embeddings/s (% of HBM peak BW)"
 HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
-# LDS read peak: 256 CUs x 256 B/clk (one 64-lane ds_read_b128 every 4 cycles) x 2.4 GHz
-LDS_PEAK_GBS = 256 * 256 * 2.4
+INT8_MFMA_PEAK_TOPS = 5000.0
 CSRC = os.path.join(ROOT, "paper_2501_17788_amd", "csrc")
 TRAFFIC_TABLE = os.path.join(ROOT, "profiles", "traffic.md")
 
@@ -173,21 +172,13 @@ def main() -> int:
     launches_per_step = max(scan_n, 1) / args.steps
     pairs_per_launch = float(scored.sum()) / launches_per_step  # scored (token, embedding) pairs
     hbm_equiv = pairs_per_launch * row_bytes / scan_avg_s / 1e9  # 16b + 4 bytes per scored pair
-    cluster_major = os.environ.get("WARP_SCAN", "cluster") != "token"
-    if cluster_major:
-        # one 16-byte table entry (four tokens) per code nibble: 4 * 32 * b bytes of LDS per pair
-        lds_bytes = pairs_per_launch * 4.0 * 32 * wl.nbits
-        roofline = {"bound": "alu", "kernel": "k_scan_cm", "resource": "LDS table reads",
-                    "achieved": lds_bytes / scan_avg_s / 1e9, "peak": LDS_PEAK_GBS, "unit": "GB/s",
-                    "frac": lds_bytes / scan_avg_s / 1e9 / LDS_PEAK_GBS,
-                    "traffic": measured_traffic("k_scan_cm", wl.name),
-                    "algorithmic_bytes_per_launch": lds_bytes, "avg_launch_ms": scan_avg_s * 1e3}
-    else:
-        roofline = {"bound": "hbm", "kernel": "k_scan", "achieved": hbm_equiv, "peak": HBM_PEAK_GBS,
-                    "unit": "GB/s", "frac": hbm_equiv / HBM_PEAK_GBS,
-                    "traffic": measured_traffic("k_scan", wl.name),
-                    "algorithmic_bytes_per_launch": pairs_per_launch * row_bytes,
-                    "avg_launch_ms": scan_avg_s * 1e3}
+    # int8 matrix-core work of the scan: 9 digit products x 128 dimensions per pair
+    mac = pairs_per_launch * 9 * 128
+    roofline = {"bound": "mfma", "kernel": "k_scan_mx", "resource": "int8 MFMA (exact 3 x 3 digit products)",
+                "achieved": 2 * mac / scan_avg_s / 1e12, "peak": INT8_MFMA_PEAK_TOPS, "unit": "TOP/s",
+                "frac": 2 * mac / scan_avg_s / 1e12 / INT8_MFMA_PEAK_TOPS,
+                "traffic": measured_traffic("k_scan_mx", wl.name),
+                "algorithmic_ops_per_launch": 2 * mac, "avg_launch_ms": scan_avg_s * 1e3}
     gemm_ms, gemm_n = stages["filter_gemm"]
     gemm_flops = 2.0 * nq * wl.n_qtok * wl.n_centroids * 128 / (max(gemm_n, 1) / args.steps)
     gemm_tflops = gemm_flops / (gemm_ms / 1e3 / max(gemm_n, 1)) / 1e12 if gemm_n else None

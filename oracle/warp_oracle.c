@@ -82,20 +82,27 @@ void oracle_select(const double* scores, const int64_t* offsets, int32_t n_c, in
     free(order);
 }
 
-/* upsilon[d][beta] = R(q_d * omega_beta): the per-token bucket-weight table */
+/* Q(x) = round-half-even(x * 2^22): query values and bucket weights quantised to
+ * 2^-22 before they are multiplied */
+static int64_t quant(double x) { return (int64_t)nearbyint(ldexp(x, ORACLE_PROD_BITS)); }
+
+/* upsilon[d][beta] = Q(q_d) * Q(omega_beta): the per-token bucket-weight table, as
+ * exact integers in units of 2^-44 */
 static void build_lut(const float* q, int32_t dim, const float* w, int32_t nbits, int64_t* lut) {
     int nb = 1 << nbits;
     for (int32_t d = 0; d < dim; ++d)
-        for (int b = 0; b < nb; ++b) lut[d * nb + b] = fixed((double)q[d] * (double)w[b]);
+        for (int b = 0; b < nb; ++b) lut[d * nb + b] = quant((double)q[d]) * quant((double)w[b]);
 }
 
-/* selective sum: centroid term plus one table entry per dimension */
+/* selective sum: one table entry per dimension, summed exactly, then rounded once to
+ * the 2^-26 grid and added to the centroid term */
 static int64_t token_score(const int64_t* lut, int32_t dim, int32_t nbits, int64_t centroid_term,
                            const uint8_t* row) {
     int nb = 1 << nbits;
-    int64_t t = centroid_term;
-    for (int32_t d = 0; d < dim; ++d) t += lut[d * nb + code_at(row, nbits, d)];
-    return t;
+    int64_t v = 0;
+    for (int32_t d = 0; d < dim; ++d) v += lut[d * nb + code_at(row, nbits, d)];
+    /* |v| < 2^53, so the scaling below is exact and nearbyint rounds half to even */
+    return centroid_term + (int64_t)nearbyint(ldexp((double)v, ORACLE_FRAC_BITS - 2 * ORACLE_PROD_BITS));
 }
 
 void oracle_token_scores(const float* q, int32_t dim, double centroid_score, const uint8_t* codes,

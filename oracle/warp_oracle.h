@@ -10,7 +10,10 @@
  *   - centroid score S64 = sum_d (double)C[c][d] * (double)q[d], accumulated in
  *     fp64 in increasing d order (each fp32 x fp32 product is exact in fp64);
  *   - R(x) = round-half-even(x * 2^26) in fp64, converted to an integer;
- *   - token score t = R(S64) + sum_d R((double)q[d] * (double)w[code_d]) (int32);
+ *   - Q(x) = round-half-even(x * 2^22): query values and bucket weights quantised
+ *     to 2^-22; the selective sum V = sum_d Q(q[d]) * Q(w[code_d]) is an exact
+ *     integer in units of 2^-44 (|V| < 2^53);
+ *   - token score t = R(S64) + round-half-even(V * 2^-18) (int32, units of 2^-26);
  *   - document score = sum over query tokens of (token max, else R(m_i)) (int64);
  *   - reported score = (float)(score * 2^-26).
  */
@@ -24,6 +27,7 @@ extern "C" {
 #endif
 
 #define ORACLE_FRAC_BITS 26
+#define ORACLE_PROD_BITS 22
 
 /* flags for oracle_search */
 #define ORACLE_EQ1_LITERAL     1  /* Eq. 1 read literally: max(m_i, retrieved) when some doc token is unretrieved */

@@ -32,16 +32,15 @@ __device__ __forceinline__ int score_bin(float f) {
     return b < 0 ? 0 : (b >= kSelBins ? kSelBins - 1 : b);
 }
 
-// Residual scan work split: a tile is kScanIters iterations of one embedding per thread.
-constexpr int kScanBlock = 512;
-constexpr int kScanIters = 8;
-constexpr int kScanTile = kScanBlock * kScanIters;
-
-// Cluster-major residual scan: a work item is (cluster, chunk of kCmChunk embeddings
-// held in registers, group of kCmGroup probing tokens scored kCmPack at a time).
-constexpr int kCmBlock = 512;  // also the chunk: one embedding per thread
-constexpr int kCmGroup = 16;
-constexpr int kCmPack = 4;     // tokens scored per table pass (4 or 8)
+// Residual scan on the matrix cores: a work item is (cluster, chunk of kMxChunk
+// embeddings, group of up to kMxGroup probing tokens), run by kMxBlock threads.
+constexpr int kMxChunk = 256;
+constexpr int kMxGroup = 64;
+constexpr int kMxBlock = 256;
+constexpr int kQdigBytes = 3 * kDim;  // three base-256 digit planes of a query token
+// Largest bucket weight magnitude: Q(omega) = round(omega * 2^22) must have three
+// signed base-256 digits, i.e. lie in [-8421504, 8355711].
+constexpr float kMaxWeight = 1.99f;
 constexpr int kPlanBlock = 1024;  // clusters per block of the pairing prefix sums
 
 // Error bits the device reports through the index's flag word.
@@ -67,10 +66,8 @@ struct WaveArgs {
     uint16_t* filter_bins;      // [n_tok][n_c] histogram bin of each filter score
     int32_t* sel;               // [n_tok][nprobe]
     int32_t* base;              // [n_tok][nprobe]  R(S64) of the probed centroids
-    int64_t* seg_start;         // [n_tok][nprobe]  first embedding of each probed cluster
     int64_t* seg_pref;          // [n_tok][nprobe + 1] cumulative probed sizes
     int64_t* m_fixed;           // [n_tok]
-    int64_t* tile_start;        // [n_tok + 1]
     int32_t* tokmax;            // [n_tok][n_docs], kAbsent when not retrieved
     uint64_t* keys;             // [n_q][n_docs]
     int32_t* err;               // device flag word
@@ -80,6 +77,7 @@ struct WaveArgs {
     int64_t* item_start;        // [n_c + 1] exclusive prefix of work items
     int32_t* pair_start;        // [n_c + 1] exclusive prefix of pairs
     int32_t* plist;             // [n_tok * nprobe][2]: (wave token, R(S64)) grouped by cluster
+    int8_t* qdig;               // [n_tok][kQdigBytes] query digit planes in operand order
     int64_t* blk;               // [2 * ceil(n_c / kPlanBlock)] block sums of items and pairs
     // outputs (device; the debug ones may be null)
     int32_t* out_ids;           // [n_q][k]
@@ -91,23 +89,21 @@ struct WaveArgs {
     uint32_t* dbg_bitmap;       // [n_q][ceil(n_docs / 32)] or null
     int64_t* dbg_scored;        // [n_q] or null
     int32_t scan_grid;          // persistent workgroups of the residual scan
-    int32_t cm_pack;            // tokens per table pass of the cluster-major scan (4 or 8)
 };
 
 // out_bins [n_tok][n_c] u16 bins (the search path) or, if null, out_scores fp32
 void launch_filter_gemm(const float* q, int32_t n_tok, const float* c, int32_t n_c, uint16_t* out_bins,
                         float* out_scores, hipStream_t s);
 void launch_select(const WaveArgs& a, hipStream_t s);
-void launch_plan(const WaveArgs& a, hipStream_t s);
-void launch_scan(const WaveArgs& a, hipStream_t s);
+void launch_scored(const WaveArgs& a, hipStream_t s);
 void launch_pairing(const WaveArgs& a, hipStream_t s);
-void launch_scan_cm(const WaveArgs& a, hipStream_t s);
-int scan_cm_blocks_per_cu(int nbits, int pack);
+void launch_qdigits(const WaveArgs& a, hipStream_t s);
+void launch_scan_mx(const WaveArgs& a, hipStream_t s);
+int scan_mx_blocks_per_cu(int nbits);
 void launch_fold(const WaveArgs& a, hipStream_t s);
 void launch_topk(const WaveArgs& a, hipStream_t s);
 void launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
 void launch_check_docs(const int32_t* ids, int64_t n, int32_t n_docs, int32_t* err, hipStream_t s);
 void launch_check_queries(const float* q, int64_t n_tok, int32_t* err, hipStream_t s);
-int scan_blocks_per_cu(int nbits);
 
 }  // namespace warp

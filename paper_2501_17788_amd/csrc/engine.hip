@@ -62,11 +62,10 @@ struct warp_index {
     float* weights = nullptr;
     int32_t* err = nullptr;
     hipStream_t stream = nullptr;
-    int scan_grid = 0;     // persistent workgroups of the token-major scan
-    int scan_cm_grid[2] = {0, 0};  // persistent workgroups of the cluster-major scan, pack 4 and 8
+    int scan_grid = 0;     // persistent workgroups of the residual scan
     // per-search scratch, grown on demand
-    DevBuf filter, sel, base, seg_start, seg_pref, m_fixed, tile_start, tokmax, keys;
-    DevBuf ccount, cursor, item_start, pair_start, plist, blk;
+    DevBuf filter, sel, base, seg_pref, m_fixed, tokmax, keys;
+    DevBuf ccount, cursor, item_start, pair_start, plist, qdig, blk;
     int64_t tokmax_ready = 0;  // leading elements of tokmax holding kAbsent
     // staging of the host-pointer calls
     DevBuf st_q, st_ids, st_scores, st_fixed, st_counts, st_sel, st_m, st_bitmap, st_scored;
@@ -136,8 +135,9 @@ int validate_index_host(const float* C, int32_t n_c, int32_t dim, const int64_t*
     }
     if (off[n_c] >= (1ll << 40)) return fail(WARP_EINVAL, "more than 2^40 embeddings");
     for (int b = 0; b < (1 << nbits); ++b)
-        if (!std::isfinite(w[b]) || std::fabs(w[b]) > 2.0f)
-            return fail(WARP_EINVAL, "bucket weight %d is not finite or exceeds 2 in magnitude", b);
+        if (!std::isfinite(w[b]) || std::fabs(w[b]) > kMaxWeight)
+            return fail(WARP_EINVAL, "bucket weight %d is not finite or exceeds %.2f in magnitude", b,
+                        (double)kMaxWeight);
     for (int32_t c = 0; c < n_c; ++c) {
         double s = 0;
         for (int d = 0; d < kDim; ++d) {
@@ -190,9 +190,7 @@ int finish_load(warp_index* idx, const int64_t* off_host) {
     if (err & kErrDocRange) return fail(WARP_EINVAL, "a document id is outside [0, n_docs)");
     int cus = 0;
     HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, idx->device));
-    idx->scan_grid = cus * scan_blocks_per_cu(idx->nbits);
-    idx->scan_cm_grid[0] = cus * scan_cm_blocks_per_cu(idx->nbits, 4);
-    idx->scan_cm_grid[1] = cus * scan_cm_blocks_per_cu(idx->nbits, 8);
+    idx->scan_grid = cus * scan_mx_blocks_per_cu(idx->nbits);
     return WARP_OK;
 }
 
@@ -281,10 +279,8 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P) {
     if (!rc) rc = grow(idx->filter, (size_t)n_tok * idx->n_c * 2);
     if (!rc) rc = grow(idx->sel, (size_t)n_tok * P * 4);
     if (!rc) rc = grow(idx->base, (size_t)n_tok * P * 4);
-    if (!rc) rc = grow(idx->seg_start, (size_t)n_tok * P * 8);
     if (!rc) rc = grow(idx->seg_pref, (size_t)n_tok * (P + 1) * 8);
     if (!rc) rc = grow(idx->m_fixed, (size_t)n_tok * 8);
-    if (!rc) rc = grow(idx->tile_start, (size_t)(n_tok + 1) * 8);
     if (!rc) rc = grow(idx->keys, (size_t)qw * idx->n_docs * 8);
     const int64_t nblk = ((int64_t)idx->n_c + kPlanBlock - 1) / kPlanBlock;
     if (!rc) rc = grow(idx->ccount, (size_t)idx->n_c * 4);
@@ -292,6 +288,7 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P) {
     if (!rc) rc = grow(idx->item_start, ((size_t)idx->n_c + 1) * 8);
     if (!rc) rc = grow(idx->pair_start, ((size_t)idx->n_c + 1) * 4);
     if (!rc) rc = grow(idx->plist, (size_t)n_tok * P * 8);
+    if (!rc) rc = grow(idx->qdig, (size_t)n_tok * kQdigBytes);
     if (!rc) rc = grow(idx->blk, (size_t)nblk * 16);
     if (rc) return rc;
     const int64_t need = n_tok * idx->n_docs;
@@ -313,7 +310,7 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P) {
 // held as scratch by this index. A larger wave lets the cluster-major scan read
 // each probed cluster once for more queries.
 int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T) {
-    const size_t held = idx->tokmax.bytes + idx->filter.bytes + idx->keys.bytes + idx->plist.bytes;
+    const size_t held = idx->tokmax.bytes + idx->filter.bytes + idx->keys.bytes + idx->plist.bytes + idx->qdig.bytes;
     size_t budget = 0;
     if (const char* s = std::getenv("WARP_SCRATCH_MB")) {
         budget = (size_t)std::atoll(s) << 20;
@@ -378,10 +375,6 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
     int rc = reserve(idx, qw, T, P);
     if (rc) return rc;
     launch_check_queries(dq, (int64_t)n_queries * T, idx->err, s);
-    const char* scan_env = std::getenv("WARP_SCAN");
-    const bool cluster_major = !(scan_env && std::strcmp(scan_env, "token") == 0);
-    const char* pack_env = std::getenv("WARP_CM_PACK");
-    const int cm_pack = pack_env ? (std::atoi(pack_env) == 8 ? 8 : 4) : kCmPack;
     const int64_t words = ((int64_t)idx->n_docs + 31) / 32;
     for (int32_t q0 = 0; q0 < n_queries; q0 += qw) {
         const int32_t nq = n_queries - q0 < qw ? n_queries - q0 : qw;
@@ -404,10 +397,8 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         a.filter_bins = (uint16_t*)idx->filter.p;
         a.sel = (int32_t*)idx->sel.p;
         a.base = (int32_t*)idx->base.p;
-        a.seg_start = (int64_t*)idx->seg_start.p;
         a.seg_pref = (int64_t*)idx->seg_pref.p;
         a.m_fixed = (int64_t*)idx->m_fixed.p;
-        a.tile_start = (int64_t*)idx->tile_start.p;
         a.tokmax = (int32_t*)idx->tokmax.p;
         a.keys = (uint64_t*)idx->keys.p;
         a.err = idx->err;
@@ -425,8 +416,8 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         a.pair_start = (int32_t*)idx->pair_start.p;
         a.plist = (int32_t*)idx->plist.p;
         a.blk = (int64_t*)idx->blk.p;
-        a.cm_pack = cm_pack;
-        a.scan_grid = cluster_major ? idx->scan_cm_grid[cm_pack == 8 ? 1 : 0] : idx->scan_grid;
+        a.qdig = (int8_t*)idx->qdig.p;
+        a.scan_grid = idx->scan_grid;
 
         hipEvent_t ev[kStages + 1] = {};
         if (idx->timing)
@@ -439,11 +430,11 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         mark(1);
         launch_select(a, s);
         mark(2);
-        launch_plan(a, s);
-        if (cluster_major) launch_pairing(a, s);
+        launch_scored(a, s);
+        launch_pairing(a, s);
+        launch_qdigits(a, s);
         mark(3);
-        if (cluster_major) launch_scan_cm(a, s);
-        else launch_scan(a, s);
+        launch_scan_mx(a, s);
         mark(4);
         launch_fold(a, s);
         mark(5);
@@ -546,9 +537,9 @@ void warp_index_free(warp_index* idx) {
         for (void* p : {(void*)idx->centroids, (void*)idx->offsets, (void*)idx->sizes, (void*)idx->doc_ids,
                         (void*)idx->codes, (void*)idx->weights, (void*)idx->err})
             if (p) (void)hipFree(p);
-        for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_start, &idx->seg_pref, &idx->m_fixed,
-                          &idx->tile_start, &idx->tokmax, &idx->keys, &idx->ccount, &idx->cursor, &idx->item_start,
-                          &idx->pair_start, &idx->plist, &idx->blk, &idx->st_q, &idx->st_ids, &idx->st_scores,
+        for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_pref, &idx->m_fixed,
+                          &idx->tokmax, &idx->keys, &idx->ccount, &idx->cursor, &idx->item_start,
+                          &idx->pair_start, &idx->plist, &idx->qdig, &idx->blk, &idx->st_q, &idx->st_ids, &idx->st_scores,
                           &idx->st_fixed, &idx->st_counts, &idx->st_sel, &idx->st_m, &idx->st_bitmap,
                           &idx->st_scored})
             release(*b);

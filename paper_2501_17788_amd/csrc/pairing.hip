@@ -1,6 +1,6 @@
 // Cluster-major work plan of one wave of queries: every (query token, probed
 // cluster) pair is bucketed by cluster (a counting sort), and each probed
-// cluster is cut into work items of (kCmBlock embeddings) x (kCmGroup tokens),
+// cluster is cut into work items of (kMxChunk embeddings) x (kMxGroup tokens),
 // so that the residual scan reads a cluster chunk once for all the tokens that
 // probe it. Pair order inside a bucket follows atomic arrival and does not
 // affect results: the token-level max is exact and commutative.
@@ -19,7 +19,7 @@ __global__ __launch_bounds__(256) void k_pair_count(WaveArgs a) {
 
 __device__ __forceinline__ int64_t cluster_items(int32_t n_tok, int32_t size) {
     if (n_tok <= 0 || size <= 0) return 0;
-    return (int64_t)((size + kCmBlock - 1) / kCmBlock) * ((n_tok + kCmGroup - 1) / kCmGroup);
+    return (int64_t)((size + kMxChunk - 1) / kMxChunk) * ((n_tok + kMxGroup - 1) / kMxGroup);
 }
 
 // exclusive scans of items and pairs inside each block of kPlanBlock clusters

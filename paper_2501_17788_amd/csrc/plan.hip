@@ -1,53 +1,21 @@
-// Work plan of one wave of queries: the probed embeddings of query token t
-// (the concatenation of its n_probe clusters) are cut into tiles of kScanTile
-// embeddings; tile_start is the exclusive prefix sum of tiles over tokens, so
-// the residual scan can split all tiles evenly over a persistent grid. Also
-// counts the embeddings scored per query.
+// Embeddings scored per query (a debug output): the sum over its tokens of the
+// sizes of their probed clusters. Also the small fill and check kernels.
 #include "engine.h"
 
 namespace warp {
 
-__global__ __launch_bounds__(1024) void k_plan(WaveArgs a) {
-    constexpr int NT = 1024;
-    __shared__ int64_t part[NT];
-    const int n_tok = a.n_q * a.n_qtok;
+__global__ __launch_bounds__(256) void k_scored(WaveArgs a) {
+    const int q = blockIdx.x * 256 + threadIdx.x;
+    if (q >= a.n_q) return;
     const int P = a.nprobe;
-    const int tid = threadIdx.x;
-    const int per = (n_tok + NT - 1) / NT;
-    const int lo = tid * per < n_tok ? tid * per : n_tok;
-    const int hi = lo + per < n_tok ? lo + per : n_tok;
-    int64_t mine = 0;
-    for (int t = lo; t < hi; ++t) {
-        const int64_t n = a.seg_pref[(int64_t)t * (P + 1) + P];
-        mine += (n + kScanTile - 1) / kScanTile;
-    }
-    part[tid] = mine;
-    __syncthreads();
-    for (int off = 1; off < NT; off <<= 1) {  // inclusive prefix over threads
-        const int64_t v = tid >= off ? part[tid - off] : 0;
-        __syncthreads();
-        part[tid] += v;
-        __syncthreads();
-    }
-    int64_t run = part[tid] - mine;
-    for (int t = lo; t < hi; ++t) {
-        a.tile_start[t] = run;
-        const int64_t n = a.seg_pref[(int64_t)t * (P + 1) + P];
-        run += (n + kScanTile - 1) / kScanTile;
-    }
-    if (tid == NT - 1) a.tile_start[n_tok] = part[NT - 1];
-    if (a.dbg_scored) {
-        for (int q = tid; q < a.n_q; q += NT) {
-            int64_t s = 0;
-            for (int i = 0; i < a.n_qtok; ++i)
-                s += a.seg_pref[((int64_t)q * a.n_qtok + i) * (P + 1) + P];
-            a.dbg_scored[q] = s;
-        }
-    }
+    int64_t s = 0;
+    for (int i = 0; i < a.n_qtok; ++i) s += a.seg_pref[((int64_t)q * a.n_qtok + i) * (P + 1) + P];
+    a.dbg_scored[q] = s;
 }
 
-void launch_plan(const WaveArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(k_plan, dim3(1), dim3(1024), 0, s, a);
+void launch_scored(const WaveArgs& a, hipStream_t s) {
+    if (!a.dbg_scored) return;
+    hipLaunchKernelGGL(k_scored, dim3((a.n_q + 255) / 256), dim3(256), 0, s, a);
 }
 
 __global__ void k_fill_i32(int32_t* p, int64_t n, int32_t v) {

@@ -1,0 +1,324 @@
+// Residual scan on the matrix cores: implicit decompression, selective sum and
+// token-level max (Sections 4.4 and 4.5) for every (probing token, probed
+// embedding) pair of a wave of queries.
+//
+// Arithmetic. With Q(x) = round-half-even(x * 2^22), the residual part of the
+// score of query token i against embedding e is the exact integer
+//     V = sum_d Q(q_{i,d}) * Q(omega[code_{e,d}])            (units of 2^-44)
+// and the token score is t = R(S64[i][c]) + round-half-even(V * 2^-18), an int32
+// in units of 2^-26. Both factors lie in [-8421504, 8355711] (|q_d| <= 1 + 1e-3
+// and |omega| <= 1.99 are checked on entry), so each is three signed base-256
+// digits x = x2 2^16 + x1 2^8 + x0 with x_j in [-128, 127], and
+//     V = sum_s 2^(8 s) A_s,   A_s = sum_{i + j = s} sum_d qdig_i[d] * wdig_j[d]
+// for s = 0..4. Every A_s is an int8 matrix product over d, computed by
+// v_mfma_i32_16x16x64_i8 with embedding digits as rows and query digits as
+// columns (|A_s| <= 3 * 128 * 2^14 < 2^23: no overflow), and mx_round recombines
+// the five class sums and rounds in int32 without loss. The result does not
+// depend on the order of any summation, so it equals the CPU definition bit for bit.
+//
+// Work. A work item is (cluster, chunk of kMxChunk embeddings, group of up to
+// kMxGroup probing tokens); a persistent workgroup of four waves walks a
+// contiguous range of items. Per item, the query digit planes of the group are
+// staged in LDS in operand order; each wave takes 16-embedding tiles of the
+// chunk, decodes their codes into weight digits in registers (v_perm_b32 lookups
+// in a 16-byte table per digit plane), and runs the 18 MFMAs of every 16-token
+// tile of the group. The 16 x 16 score tile then goes through a per-wave LDS
+// transpose so that a 16-lane row holds one token against the tile's 16
+// embeddings, a DPP segmented max merges runs of equal document ids, and the
+// run's last lane issues one atomicMax into the token-max table.
+#include "engine.h"
+
+namespace warp {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+// Q(x): x * 2^22 is exact in fp32 and v_rndne_f32 rounds half to even.
+__device__ __forceinline__ int quant22(float x) { return (int)__builtin_rintf(x * 4194304.0f); }
+
+// Balanced base-256 digits of x in [-8421504, 8355711].
+__device__ __forceinline__ void digits3(int x, int& d0, int& d1, int& d2) {
+    d0 = ((x + 128) & 255) - 128;
+    x = (x - d0) >> 8;
+    d1 = ((x + 128) & 255) - 128;
+    d2 = (x - d1) >> 8;
+}
+
+// round-half-even((A0 + 2^8 A1 + 2^16 A2 + 2^24 A3 + 2^32 A4) / 2^18) in int32.
+// Writing A2 = 4 alpha + rho and N = A0 + 2^8 A1 + 2^16 rho = 2^18 beta + f with
+// 0 <= f < 2^18 gives V = 2^18 (2^14 A4 + 2^6 A3 + alpha + beta) + f. N fits in
+// int32 (|A1| <= 2^22), and the floor term is exact modulo 2^32, hence exact,
+// since the rounded score itself fits in int32.
+__device__ __forceinline__ int mx_round(int a0, int a1, int a2, int a3, int a4) {
+    const unsigned m = (unsigned)a0 + ((unsigned)a1 << 8);
+    const int alpha = a2 >> 2;
+    const unsigned rho = (unsigned)a2 & 3u;
+    const int n = (int)(m + (rho << 16));
+    const int beta = n >> 18;
+    const unsigned f = (unsigned)n & 0x3FFFFu;
+    const unsigned fl = ((unsigned)a4 << 14) + ((unsigned)a3 << 6) + (unsigned)alpha + (unsigned)beta;
+    return (int)(fl + ((f + (fl & 1u)) > 0x20000u ? 1u : 0u));
+}
+
+// Operand slot of dimension d: lane group g = d / 32 of the 16 x 64 operands,
+// K slice s (two MFMAs of 64 dimensions), byte j of the lane's 16 bytes. The
+// order follows the code layout so that decoding needs no byte shuffles:
+//   b = 4: code byte 16 g + 4 m + t holds dimensions 32 g + 8 m + 2 t (high
+//          nibble) and + 1 (low nibble); slice s takes code words m = 2 s, 2 s + 1
+//          as [high nibbles of 2 s, low of 2 s, high of 2 s + 1, low of 2 s + 1];
+//   b = 2: code byte 8 g + 4 s + t holds dimensions 32 g + 16 s + 4 t + u, u = 0
+//          in the top bits; slice s holds the four fields u = 0..3 in that order.
+template <int NBITS>
+__device__ __forceinline__ void slot_of_dim(int d, int& s, int& g, int& j) {
+    g = d >> 5;
+    const int r = d & 31;
+    if (NBITS == 4) {
+        const int m = r >> 3, t = (r & 7) >> 1, lo = r & 1;
+        s = m >> 1;
+        j = 4 * (2 * (m & 1) + lo) + t;
+    } else {
+        s = r >> 4;
+        j = 4 * (r & 3) + ((r & 15) >> 2);
+    }
+}
+
+// Query digit planes of every wave token: qdig[t][(p * 2 + s) * 4 + g][16] bytes.
+template <int NBITS>
+__global__ __launch_bounds__(256) void k_qdigits(const float* __restrict__ q, int64_t n_tok,
+                                                 int8_t* __restrict__ qdig) {
+    const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (x >= n_tok * kDim) return;
+    const int64_t t = x / kDim;
+    const int d = (int)(x % kDim);
+    int s, g, j, d0, d1, d2;
+    slot_of_dim<NBITS>(d, s, g, j);
+    digits3(quant22(q[x]), d0, d1, d2);
+    int8_t* row = qdig + t * kQdigBytes;
+    row[((0 * 2 + s) * 4 + g) * 16 + j] = (int8_t)d0;
+    row[((1 * 2 + s) * 4 + g) * 16 + j] = (int8_t)d1;
+    row[((2 * 2 + s) * 4 + g) * 16 + j] = (int8_t)d2;
+}
+
+struct MxItem {
+    int c;        // cluster
+    int64_t e0;   // first embedding of the chunk
+    int64_t e1;   // end of the chunk
+    int p0, np;   // pairs [p0, p0 + np) of the token group
+};
+
+__device__ __forceinline__ MxItem mx_decode(const WaveArgs& a, int64_t item, int c) {
+    MxItem it;
+    const int nt = a.ccount[c];
+    const int groups = (nt + kMxGroup - 1) / kMxGroup;
+    const int64_t l = item - a.item_start[c];
+    const int64_t chunk = l / groups;
+    const int grp = (int)(l - chunk * groups);
+    it.c = c;
+    it.e0 = a.offsets[c] + chunk * kMxChunk;
+    const int64_t end = a.offsets[c + 1];
+    it.e1 = it.e0 + kMxChunk < end ? it.e0 + kMxChunk : end;
+    it.p0 = a.pair_start[c] + grp * kMxGroup;
+    it.np = nt - grp * kMxGroup < kMxGroup ? nt - grp * kMxGroup : kMxGroup;
+    return it;
+}
+
+// DPP row_shr:k source (k = 1, 2, 4, 8) inside rows of 16 lanes; lanes whose
+// source falls outside the row read INT32_MIN.
+template <int K>
+__device__ __forceinline__ int row_shr(int v) {
+    return __builtin_amdgcn_update_dpp(INT32_MIN, v, 0x110 + K, 0xf, 0xf, false);
+}
+__device__ __forceinline__ int row_shl1(int v) {
+    return __builtin_amdgcn_update_dpp(INT32_MIN, v, 0x101, 0xf, 0xf, false);
+}
+
+// Segmented max over runs of equal documents inside a 16-lane row. Document ids
+// are ascending along a cluster, so a run is contiguous and a step that merges
+// only same-document sources leaves each lane the max over its run prefix.
+__device__ __forceinline__ int seg_max16(int v, unsigned same) {
+    int s;
+    s = row_shr<1>(v); v = (same & 1u) && s > v ? s : v;
+    s = row_shr<2>(v); v = (same & 2u) && s > v ? s : v;
+    s = row_shr<4>(v); v = (same & 4u) && s > v ? s : v;
+    s = row_shr<8>(v); v = (same & 8u) && s > v ? s : v;
+    return v;
+}
+
+// In-order LDS access of one wave: complete this lane's LDS operations and keep
+// the compiler from moving memory operations across this point.
+__device__ __forceinline__ void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+template <int NBITS>
+__global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
+    constexpr int BYTES = kDim * NBITS / 8;  // code bytes per embedding
+    constexpr int NSLOT = 24;                // (plane, slice, lane group) slots of 16 bytes
+    __shared__ v4i s_q[NSLOT][kMxGroup];     // query digit planes of the item's tokens
+    __shared__ int s_tok[kMxGroup];
+    __shared__ int s_base[kMxGroup];
+    __shared__ __attribute__((aligned(16))) int s_x[kMxBlock / 64][16][16];  // per-wave transpose of a score tile
+
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6;
+    const int lane = tid & 63;
+    const int li = lane & 15;  // MFMA row / column inside the tile; embedding in the transposed tile
+    const int lg = lane >> 4;  // MFMA lane group; token quarter in the transposed tile
+
+    // weight digit tables: tab[p][k] holds digit p of Q(omega[v]) for v = 4 k .. 4 k + 3
+    unsigned tab[3][4] = {};
+#pragma unroll
+    for (int v = 0; v < (1 << NBITS); ++v) {
+        int d[3];
+        digits3(quant22(a.weights[v]), d[0], d[1], d[2]);
+#pragma unroll
+        for (int p = 0; p < 3; ++p) tab[p][v >> 2] |= ((unsigned)d[p] & 255u) << (8 * (v & 3));
+    }
+
+    const int n_c = a.n_c;
+    const int64_t* item_start = a.item_start;
+    const int64_t total = item_start[n_c];
+    const int64_t G = gridDim.x;
+    const int64_t first = total * blockIdx.x / G;
+    const int64_t last = total * (blockIdx.x + 1) / G;
+    if (first >= last) return;
+    int lo = 0, hi = n_c;  // cluster of the first item: item_start[c] <= first < item_start[c + 1]
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (item_start[mid] <= first) lo = mid;
+        else hi = mid;
+    }
+    int c = lo;
+    const v4i* qdig = reinterpret_cast<const v4i*>(a.qdig);
+    const uint8_t* __restrict__ codes = a.codes;
+    const int64_t n_docs = a.n_docs;
+
+    for (int64_t item = first; item < last; ++item) {
+        while (item_start[c + 1] <= item) ++c;
+        const MxItem it = mx_decode(a, item, c);
+        __syncthreads();  // the previous item's tokens are no longer read
+        if (tid < kMxGroup) {
+            const bool in = tid < it.np;
+            s_tok[tid] = in ? a.plist[2 * (int64_t)(it.p0 + tid)] : 0;
+            s_base[tid] = in ? a.plist[2 * (int64_t)(it.p0 + tid) + 1] : 0;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < NSLOT * kMxGroup / kMxBlock; ++i) {
+            const int k = tid + kMxBlock * i;
+            const int tk = k / NSLOT, slot = k - tk * NSLOT;
+            v4i v = {0, 0, 0, 0};
+            if (tk < it.np) v = qdig[(int64_t)s_tok[tk] * NSLOT + slot];
+            s_q[slot][tk] = v;
+        }
+        __syncthreads();
+
+        const int n_et = (int)((it.e1 - it.e0 + 15) >> 4);
+        const int n_tt = (it.np + 15) >> 4;
+        for (int et = wave; et < n_et; et += kMxBlock / 64) {  // wave-uniform
+            const int64_t tile0 = it.e0 + 16 * et;
+            // this lane's operand rows: embedding tile0 + li, dimensions 32 lg .. 32 lg + 31
+            const int64_t e_row = tile0 + li;
+            const bool row_in = e_row < it.e1;
+            v4i A[3][2];
+            if (NBITS == 4) {
+                uint4 cw = make_uint4(0, 0, 0, 0);
+                if (row_in) cw = *reinterpret_cast<const uint4*>(codes + e_row * BYTES + 16 * lg);
+                const unsigned w[4] = {cw.x, cw.y, cw.z, cw.w};
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const unsigned x = h == 0 ? (w[m] >> 4) & 0x0F0F0F0Fu : w[m] & 0x0F0F0F0Fu;
+                        const unsigned x7 = x & 0x07070707u;
+                        const unsigned pick = ((x >> 1) & 0x04040404u) | 0x03020100u;
+#pragma unroll
+                        for (int p = 0; p < 3; ++p) {
+                            const unsigned lo8 = __builtin_amdgcn_perm(tab[p][1], tab[p][0], x7);
+                            const unsigned hi8 = __builtin_amdgcn_perm(tab[p][3], tab[p][2], x7);
+                            A[p][m >> 1][2 * (m & 1) + h] = (int)__builtin_amdgcn_perm(hi8, lo8, pick);
+                        }
+                    }
+                }
+            } else {
+                uint2 cw = make_uint2(0, 0);
+                if (row_in) cw = *reinterpret_cast<const uint2*>(codes + e_row * BYTES + 8 * lg);
+                const unsigned w[2] = {cw.x, cw.y};
+#pragma unroll
+                for (int s = 0; s < 2; ++s) {
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const unsigned x = (w[s] >> (6 - 2 * u)) & 0x03030303u;
+#pragma unroll
+                        for (int p = 0; p < 3; ++p)
+                            A[p][s][u] = (int)__builtin_amdgcn_perm(tab[p][0], tab[p][0], x);
+                    }
+                }
+            }
+            // documents of the transposed layout: lane (li, lg) holds embedding tile0 + li
+            const bool emb_in = tile0 + li < it.e1;
+            const int doc = emb_in ? a.doc_ids[tile0 + li] : -1 - li;
+            unsigned same = 0;
+            same |= row_shr<1>(doc) == doc ? 1u : 0u;
+            same |= row_shr<2>(doc) == doc ? 2u : 0u;
+            same |= row_shr<4>(doc) == doc ? 4u : 0u;
+            same |= row_shr<8>(doc) == doc ? 8u : 0u;
+            const bool run_end = emb_in && row_shl1(doc) != doc;
+
+            for (int tt = 0; tt < n_tt; ++tt) {
+                v4i B[3][2];
+#pragma unroll
+                for (int p = 0; p < 3; ++p)
+#pragma unroll
+                    for (int s = 0; s < 2; ++s) B[p][s] = s_q[(p * 2 + s) * 4 + lg][16 * tt + li];
+                v4i acc[5];
+#pragma unroll
+                for (int k = 0; k < 5; ++k) acc[k] = (v4i){0, 0, 0, 0};
+#pragma unroll
+                for (int s = 0; s < 2; ++s)
+#pragma unroll
+                    for (int i = 0; i < 3; ++i)
+#pragma unroll
+                        for (int j = 0; j < 3; ++j)
+                            acc[i + j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[j][s], B[i][s], acc[i + j], 0, 0, 0);
+                // acc[k][r] of lane (li, lg): embedding tile0 + 4 lg + r against token 16 tt + li
+                const int base = s_base[16 * tt + li];
+                int v[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] = mx_round(acc[0][r], acc[1][r], acc[2][r], acc[3][r], acc[4][r]) + base;
+                *reinterpret_cast<int4*>(&s_x[wave][li][4 * lg]) = make_int4(v[0], v[1], v[2], v[3]);
+                wave_lds_sync();
+                int u[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) u[j] = s_x[wave][lg + 4 * j][li];
+                wave_lds_sync();
+#pragma unroll
+                for (int j = 0; j < 4; ++j) u[j] = seg_max16(u[j], same);
+                if (run_end) {
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int tk = 16 * tt + lg + 4 * j;
+                        if (tk < it.np) atomicMax(&a.tokmax[(int64_t)s_tok[tk] * n_docs + doc], u[j]);
+                    }
+                }
+            }
+        }
+    }
+}
+
+void launch_qdigits(const WaveArgs& a, hipStream_t s) {
+    const int64_t n_tok = (int64_t)a.n_q * a.n_qtok;
+    const dim3 grid((unsigned)((n_tok * kDim + 255) / 256));
+    if (a.nbits == 4) hipLaunchKernelGGL(k_qdigits<4>, grid, dim3(256), 0, s, a.queries, n_tok, a.qdig);
+    else hipLaunchKernelGGL(k_qdigits<2>, grid, dim3(256), 0, s, a.queries, n_tok, a.qdig);
+}
+
+void launch_scan_mx(const WaveArgs& a, hipStream_t s) {
+    if (a.nbits == 4) hipLaunchKernelGGL(k_scan_mx<4>, dim3(a.scan_grid), dim3(kMxBlock), 0, s, a);
+    else hipLaunchKernelGGL(k_scan_mx<2>, dim3(a.scan_grid), dim3(kMxBlock), 0, s, a);
+}
+
+int scan_mx_blocks_per_cu(int nbits) {
+    int n = 0;
+    (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, nbits == 4 ? k_scan_mx<4> : k_scan_mx<2>, kMxBlock, 0);
+    return n > 0 ? n : 1;
+}
+
+}  // namespace warp

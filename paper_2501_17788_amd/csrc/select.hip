@@ -252,14 +252,12 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
     const int nA = s_nA, nB = s_nB;
     int32_t* sel = a.sel + (int64_t)t * P;
     int32_t* base = a.base + (int64_t)t * P;
-    int64_t* seg_start = a.seg_start + (int64_t)t * P;
     int64_t* seg_pref = a.seg_pref + (int64_t)t * (P + 1);
     if (nA > kSelCap || nB > kSelCap || nA < P || nB < 1) {
         // degenerate score distribution: leave a token that probes and scans nothing
         for (int j = tid; j < P; j += NT) {
             sel[j] = -1;
             base[j] = 0;
-            seg_start[j] = 0;
         }
         for (int j = tid; j <= P; j += NT) seg_pref[j] = 0;
         if (tid == 0) {
@@ -292,7 +290,6 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
         const int c = idA[j];
         sel[j] = c;
         base[j] = (int32_t)to_fixed(sA[j]);
-        seg_start[j] = a.offsets[c];
         cum[j] = sizes[c];
         if (a.dbg_sel) a.dbg_sel[(int64_t)t * P + j] = c;
     }

@@ -21,16 +21,6 @@ pytestmark = pytest.mark.gpu
 EXACT = ("ids", "fixed", "counts", "sel", "m_fixed", "cand_bitmap", "n_scored")
 
 
-@pytest.fixture(autouse=True, params=["cluster", "cluster8", "token"])
-def scan_variant(request, monkeypatch):
-    """Every parity test runs with each residual scan: cluster-major scoring four
-    or eight tokens per table pass, and token-major."""
-    monkeypatch.setenv("WARP_SCAN", "token" if request.param == "token" else "cluster")
-    monkeypatch.setenv("WARP_CM_PACK", "8" if request.param == "cluster8" else "4")
-    print(f"[scan={request.param}]", flush=True)
-    return request.param
-
-
 def _engine():
     import paper_2501_17788_amd as w
     return w

@@ -27,8 +27,23 @@ import synth
 from helpers import (FRAC, bruteforce_maxsim, cluster_of_embeddings, explicit_decompress,
                      load_dyadic, topp_by_score, unpack_msb_first, weighted_order_statistic)
 
-TOK_TOL = 129 * 2.0 ** -27      # 129 roundings of at most half a unit of 2^-26 each
-DOC_TOL = 32 * TOK_TOL
+
+
+def tok_tol(q, w):
+    """Largest gap between a fixed-point token score and the real-valued one.
+
+    Each product q_d * w uses q_d and w rounded to 2^-22 (error at most
+    (|q_d| + |w|) 2^-23 + 2^-46 per dimension); the centroid term and the summed
+    residual term are each rounded once to 2^-26.
+    """
+    q = np.asarray(q, np.float64)
+    return ((np.abs(q).sum() + q.size * float(np.abs(w).max())) * 2.0 ** -23
+            + q.size * 2.0 ** -46 + 2 * 2.0 ** -27)
+
+
+def doc_tol(Q, w):
+    """A document score sums one token score (or estimate) per query token."""
+    return sum(tok_tol(q, w) for q in Q)
 
 
 def _index(seed=0, **kw):
@@ -80,7 +95,7 @@ def test_o1_explicit_equals_implicit(nbits):
         for c in range(len(idx.offsets) - 1):
             e0, e1 = int(idx.offsets[c]), int(idx.offsets[c + 1])
             t = oracle.token_scores(q, S[c], idx.codes, nbits, idx.bucket_weights, e0, e1)
-            assert np.all(np.abs(t / FRAC - direct[e0:e1]) <= TOK_TOL)
+            assert np.all(np.abs(t / FRAC - direct[e0:e1]) <= tok_tol(q, idx.bucket_weights))
 
 
 def test_o1_planted_mistake_is_caught():
@@ -93,7 +108,7 @@ def test_o1_planted_mistake_is_caught():
     swapped = ((swapped >> 4) | (swapped << 4)).astype(np.uint8)  # nibble order flipped
     e1 = int(idx.offsets[1])
     t = oracle.token_scores(q, S[0], swapped, 4, idx.bucket_weights, 0, e1)
-    assert np.any(np.abs(t / FRAC - X[:e1] @ q.astype(np.float64)) > TOK_TOL)
+    assert np.any(np.abs(t / FRAC - X[:e1] @ q.astype(np.float64)) > tok_tol(q, idx.bucket_weights))
 
 
 # ----------------------------------------------------------------------------- O2
@@ -103,6 +118,7 @@ def _check_against_bruteforce(idx, r, k):
     for qi, Q in enumerate(idx.queries):
         docs, bf = bruteforce_maxsim(X, idx.doc_ids, idx.n_docs, Q)
         bf_of = dict(zip(docs.tolist(), bf.tolist()))
+        DOC_TOL = doc_tol(Q, idx.bucket_weights)
         n = int(r["counts"][qi])
         assert n == min(k, len(docs))
         ids = r["ids"][qi, :n]
