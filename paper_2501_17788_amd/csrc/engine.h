@@ -14,7 +14,9 @@ constexpr int kMaxQtok = 32;       // query_maxlen
 constexpr int kMaxProbe = 256;     // largest n_probe the selection and scan kernels hold
 constexpr int kMaxK = 4096;        // largest k the device top-k sorts
 constexpr int kMaxDocs = 1 << 24;  // document ids packed into the low 24 bits of a sort key
-constexpr int32_t kAbsent = INT32_MIN;  // "no retrieved embedding" in the token-max table
+// Token-max cells hold t + 2^31 as unsigned (an order-preserving bias); 0 marks
+// "no retrieved embedding", as no token score reaches -2^31.
+constexpr uint32_t kTokAbsent = 0;
 
 // Centroid selection: the fp32 matrix-core scores are within kFilterEps of the
 // fp64 scores; bins of the score histogram are wider than 2 * kFilterEps.
@@ -68,7 +70,7 @@ struct WaveArgs {
     int32_t* base;              // [n_tok][nprobe]  R(S64) of the probed centroids
     int64_t* seg_pref;          // [n_tok][nprobe + 1] cumulative probed sizes
     int64_t* m_fixed;           // [n_tok]
-    int32_t* tokmax;            // [n_tok][n_docs], kAbsent when not retrieved
+    uint32_t* tokmax;           // [n_tok][n_docs] biased token maxima, kTokAbsent when not retrieved
     uint64_t* keys;             // [n_q][n_docs]
     int32_t* err;               // device flag word
     // cluster-major pairing

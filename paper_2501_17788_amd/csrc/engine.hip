@@ -66,7 +66,7 @@ struct warp_index {
     // per-search scratch, grown on demand
     DevBuf filter, sel, base, seg_pref, m_fixed, tokmax, keys;
     DevBuf ccount, cursor, item_start, pair_start, plist, qdig, blk;
-    int64_t tokmax_ready = 0;  // leading elements of tokmax holding kAbsent
+    int64_t tokmax_ready = 0;  // leading elements of tokmax holding kTokAbsent
     // staging of the host-pointer calls
     DevBuf st_q, st_ids, st_scores, st_fixed, st_counts, st_sel, st_m, st_bitmap, st_scored;
     std::mutex lock;
@@ -298,7 +298,7 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P) {
         idx->tokmax_ready = 0;
     }
     if (idx->tokmax_ready < need) {
-        launch_fill_i32((int32_t*)idx->tokmax.p, need, kAbsent, idx->stream);
+        launch_fill_i32((int32_t*)idx->tokmax.p, need, (int32_t)kTokAbsent, idx->stream);
         HIP_TRY(hipStreamSynchronize(idx->stream));
         idx->tokmax_ready = need;
     }
@@ -399,7 +399,7 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         a.base = (int32_t*)idx->base.p;
         a.seg_pref = (int64_t*)idx->seg_pref.p;
         a.m_fixed = (int64_t*)idx->m_fixed.p;
-        a.tokmax = (int32_t*)idx->tokmax.p;
+        a.tokmax = (uint32_t*)idx->tokmax.p;
         a.keys = (uint64_t*)idx->keys.p;
         a.err = idx->err;
         a.out_ids = o.ids + (int64_t)q0 * k;

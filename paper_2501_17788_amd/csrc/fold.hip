@@ -4,7 +4,7 @@
 // the token strides gives this sum, so one pass per document computes it.
 //
 // One thread per (query, document); the n_qtok token rows are read with
-// coalesced loads and reset to kAbsent for the next wave. The output is a sort
+// coalesced loads and reset to kTokAbsent for the next wave. The output is a sort
 // key per document: ((score + 2^39) << 24) | (2^24 - 1 - doc), larger is
 // better and equal scores order by lower document id; 0 marks a non-candidate.
 #include "engine.h"
@@ -19,14 +19,14 @@ __global__ __launch_bounds__(256) void k_fold(WaveArgs a) {
     if (in) {
         int64_t sum = 0;
         const int T = a.n_qtok;
-        int32_t* col = a.tokmax + (int64_t)q * T * a.n_docs + doc;
+        uint32_t* col = a.tokmax + (int64_t)q * T * a.n_docs + doc;
         const int64_t* m = a.m_fixed + (int64_t)q * T;
         for (int i = 0; i < T; ++i) {
-            const int32_t v = col[(int64_t)i * a.n_docs];
-            if (v != kAbsent) {
+            const uint32_t v = col[(int64_t)i * a.n_docs];
+            if (v != kTokAbsent) {
                 any = true;
-                sum += v;
-                col[(int64_t)i * a.n_docs] = kAbsent;
+                sum += (int32_t)(v ^ 0x80000000u);
+                col[(int64_t)i * a.n_docs] = kTokAbsent;
             } else {
                 sum += m[i];
             }

@@ -22,10 +22,10 @@
 // staged in LDS in operand order; each wave takes 16-embedding tiles of the
 // chunk, decodes their codes into weight digits in registers (v_perm_b32 lookups
 // in a 16-byte table per digit plane), and runs the 18 MFMAs of every 16-token
-// tile of the group. The 16 x 16 score tile then goes through a per-wave LDS
-// transpose so that a 16-lane row holds one token against the tile's 16
-// embeddings, a DPP segmented max merges runs of equal document ids, and the
-// run's last lane issues one atomicMax into the token-max table.
+// tile of the group, query digits as rows and weight digits as columns, so that
+// each 16-lane row of the result holds four tokens against the tile's 16
+// embeddings: a DPP segmented max along the row merges runs of equal document
+// ids, and the run's last lane issues one atomicMax into the token-max table.
 #include "engine.h"
 
 namespace warp {
@@ -121,46 +121,39 @@ __device__ __forceinline__ MxItem mx_decode(const WaveArgs& a, int64_t item, int
     return it;
 }
 
-// DPP row_shr:k source (k = 1, 2, 4, 8) inside rows of 16 lanes; lanes whose
-// source falls outside the row read INT32_MIN.
+// DPP row_shr:k source (k = 1, 2, 4, 8) of a document id inside rows of 16
+// lanes; lanes whose source falls outside the row read INT32_MIN.
 template <int K>
-__device__ __forceinline__ int row_shr(int v) {
+__device__ __forceinline__ int doc_shr(int v) {
     return __builtin_amdgcn_update_dpp(INT32_MIN, v, 0x110 + K, 0xf, 0xf, false);
 }
-__device__ __forceinline__ int row_shl1(int v) {
+__device__ __forceinline__ int doc_shl1(int v) {
     return __builtin_amdgcn_update_dpp(INT32_MIN, v, 0x101, 0xf, 0xf, false);
 }
 
-// Segmented max over runs of equal documents inside a 16-lane row. Document ids
-// are ascending along a cluster, so a run is contiguous and a step that merges
-// only same-document sources leaves each lane the max over its run prefix.
-__device__ __forceinline__ int seg_max16(int v, unsigned same) {
-    int s;
-    s = row_shr<1>(v); v = (same & 1u) && s > v ? s : v;
-    s = row_shr<2>(v); v = (same & 2u) && s > v ? s : v;
-    s = row_shr<4>(v); v = (same & 4u) && s > v ? s : v;
-    s = row_shr<8>(v); v = (same & 8u) && s > v ? s : v;
-    return v;
+// Same for a biased score: lanes outside the row read 0, the identity of max.
+template <int K>
+__device__ __forceinline__ unsigned val_shr(unsigned v) {
+    return (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x110 + K, 0xf, 0xf, true);
 }
 
-// In-order LDS access of one wave: complete this lane's LDS operations and keep
-// the compiler from moving memory operations across this point.
-__device__ __forceinline__ void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// Token-max cells hold t + 2^31 as unsigned (order preserving; 0 = absent).
+__device__ __forceinline__ unsigned bias(int t) { return (unsigned)t ^ 0x80000000u; }
 
 template <int NBITS>
 __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
     constexpr int BYTES = kDim * NBITS / 8;  // code bytes per embedding
+    constexpr int CW = BYTES / 16 * 4;       // code words per lane: 16 bytes (b = 4) or 8 (b = 2)
     constexpr int NSLOT = 24;                // (plane, slice, lane group) slots of 16 bytes
     __shared__ v4i s_q[NSLOT][kMxGroup];     // query digit planes of the item's tokens
-    __shared__ int s_tok[kMxGroup];
-    __shared__ int s_base[kMxGroup];
-    __shared__ __attribute__((aligned(16))) int s_x[kMxBlock / 64][16][16];  // per-wave transpose of a score tile
+    __shared__ __attribute__((aligned(16))) int s_base[kMxGroup];   // R(S64) + 2^31 of each token
+    __shared__ __attribute__((aligned(16))) int64_t s_row[kMxGroup];  // its token-max row offset
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
     const int lane = tid & 63;
-    const int li = lane & 15;  // MFMA row / column inside the tile; embedding in the transposed tile
-    const int lg = lane >> 4;  // MFMA lane group; token quarter in the transposed tile
+    const int li = lane & 15;  // operand row / column inside a 16 x 16 tile
+    const int lg = lane >> 4;  // operand lane group
 
     // weight digit tables: tab[p][k] holds digit p of Q(omega[v]) for v = 4 k .. 4 k + 3
     unsigned tab[3][4] = {};
@@ -188,7 +181,25 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
     int c = lo;
     const v4i* qdig = reinterpret_cast<const v4i*>(a.qdig);
     const uint8_t* __restrict__ codes = a.codes;
-    const int64_t n_docs = a.n_docs;
+    unsigned* __restrict__ tokmax = a.tokmax;
+
+    // this lane's code words of embedding tile0 + li, dimensions 32 lg .. 32 lg + 31
+    auto load_codes = [&](int64_t tile0, int64_t e1, unsigned (&w)[CW], int& doc) {
+        const int64_t e = tile0 + li;
+#pragma unroll
+        for (int m = 0; m < CW; ++m) w[m] = 0;
+        doc = -1 - li;  // padding rows never match a neighbour
+        if (e < e1) {
+            if (NBITS == 4) {
+                const uint4 v = *reinterpret_cast<const uint4*>(codes + e * BYTES + 16 * lg);
+                w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+            } else {
+                const uint2 v = *reinterpret_cast<const uint2*>(codes + e * BYTES + 8 * lg);
+                w[0] = v.x; w[1] = v.y;
+            }
+            doc = a.doc_ids[e];
+        }
+    };
 
     for (int64_t item = first; item < last; ++item) {
         while (item_start[c + 1] <= item) ++c;
@@ -196,32 +207,29 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
         __syncthreads();  // the previous item's tokens are no longer read
         if (tid < kMxGroup) {
             const bool in = tid < it.np;
-            s_tok[tid] = in ? a.plist[2 * (int64_t)(it.p0 + tid)] : 0;
-            s_base[tid] = in ? a.plist[2 * (int64_t)(it.p0 + tid) + 1] : 0;
+            const int tok = in ? a.plist[2 * (int64_t)(it.p0 + tid)] : 0;
+            s_base[tid] = in ? (int)bias(a.plist[2 * (int64_t)(it.p0 + tid) + 1]) : 0;
+            s_row[tid] = (int64_t)tok * a.n_docs;
         }
-        __syncthreads();
 #pragma unroll
         for (int i = 0; i < NSLOT * kMxGroup / kMxBlock; ++i) {
             const int k = tid + kMxBlock * i;
             const int tk = k / NSLOT, slot = k - tk * NSLOT;
             v4i v = {0, 0, 0, 0};
-            if (tk < it.np) v = qdig[(int64_t)s_tok[tk] * NSLOT + slot];
+            if (tk < it.np) v = qdig[(int64_t)a.plist[2 * (int64_t)(it.p0 + tk)] * NSLOT + slot];
             s_q[slot][tk] = v;
         }
         __syncthreads();
 
         const int n_et = (int)((it.e1 - it.e0 + 15) >> 4);
         const int n_tt = (it.np + 15) >> 4;
+        unsigned w[CW];
+        int doc;
+        if (wave < n_et) load_codes(it.e0 + 16 * wave, it.e1, w, doc);
         for (int et = wave; et < n_et; et += kMxBlock / 64) {  // wave-uniform
-            const int64_t tile0 = it.e0 + 16 * et;
-            // this lane's operand rows: embedding tile0 + li, dimensions 32 lg .. 32 lg + 31
-            const int64_t e_row = tile0 + li;
-            const bool row_in = e_row < it.e1;
+            // weight digits of the tile (MFMA B operand: column li = embedding tile0 + li)
             v4i A[3][2];
             if (NBITS == 4) {
-                uint4 cw = make_uint4(0, 0, 0, 0);
-                if (row_in) cw = *reinterpret_cast<const uint4*>(codes + e_row * BYTES + 16 * lg);
-                const unsigned w[4] = {cw.x, cw.y, cw.z, cw.w};
 #pragma unroll
                 for (int m = 0; m < 4; ++m) {
 #pragma unroll
@@ -238,9 +246,6 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
                     }
                 }
             } else {
-                uint2 cw = make_uint2(0, 0);
-                if (row_in) cw = *reinterpret_cast<const uint2*>(codes + e_row * BYTES + 8 * lg);
-                const unsigned w[2] = {cw.x, cw.y};
 #pragma unroll
                 for (int s = 0; s < 2; ++s) {
 #pragma unroll
@@ -252,50 +257,51 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
                     }
                 }
             }
-            // documents of the transposed layout: lane (li, lg) holds embedding tile0 + li
-            const bool emb_in = tile0 + li < it.e1;
-            const int doc = emb_in ? a.doc_ids[tile0 + li] : -1 - li;
-            unsigned same = 0;
-            same |= row_shr<1>(doc) == doc ? 1u : 0u;
-            same |= row_shr<2>(doc) == doc ? 2u : 0u;
-            same |= row_shr<4>(doc) == doc ? 4u : 0u;
-            same |= row_shr<8>(doc) == doc ? 8u : 0u;
-            const bool run_end = emb_in && row_shl1(doc) != doc;
+            // runs of equal documents along the row (embedding li of the tile)
+            const bool same1 = doc_shr<1>(doc) == doc, same2 = doc_shr<2>(doc) == doc;
+            const bool same4 = doc_shr<4>(doc) == doc, same8 = doc_shr<8>(doc) == doc;
+            const bool run_end = doc >= 0 && doc_shl1(doc) != doc;
+            const int my_doc = doc;
+            // prefetch the wave's next tile
+            if (et + kMxBlock / 64 < n_et) load_codes(it.e0 + 16 * (et + kMxBlock / 64), it.e1, w, doc);
 
             for (int tt = 0; tt < n_tt; ++tt) {
-                v4i B[3][2];
-#pragma unroll
-                for (int p = 0; p < 3; ++p)
-#pragma unroll
-                    for (int s = 0; s < 2; ++s) B[p][s] = s_q[(p * 2 + s) * 4 + lg][16 * tt + li];
                 v4i acc[5];
 #pragma unroll
                 for (int k = 0; k < 5; ++k) acc[k] = (v4i){0, 0, 0, 0};
 #pragma unroll
-                for (int s = 0; s < 2; ++s)
+                for (int s = 0; s < 2; ++s) {
+                    // query digits of slice s (MFMA A operand: row li = token 16 tt + li)
+                    v4i B[3];
+#pragma unroll
+                    for (int p = 0; p < 3; ++p) B[p] = s_q[(p * 2 + s) * 4 + lg][16 * tt + li];
 #pragma unroll
                     for (int i = 0; i < 3; ++i)
 #pragma unroll
                         for (int j = 0; j < 3; ++j)
-                            acc[i + j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[j][s], B[i][s], acc[i + j], 0, 0, 0);
-                // acc[k][r] of lane (li, lg): embedding tile0 + 4 lg + r against token 16 tt + li
-                const int base = s_base[16 * tt + li];
-                int v[4];
+                            acc[i + j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(B[i], A[j][s], acc[i + j], 0, 0, 0);
+                }
+                // acc[k][r] of lane (li, lg): token 16 tt + 4 lg + r against embedding tile0 + li
+                const int4 bs = *reinterpret_cast<const int4*>(&s_base[16 * tt + 4 * lg]);
+                const int bsr[4] = {bs.x, bs.y, bs.z, bs.w};
+                unsigned v[4];
 #pragma unroll
-                for (int r = 0; r < 4; ++r) v[r] = mx_round(acc[0][r], acc[1][r], acc[2][r], acc[3][r], acc[4][r]) + base;
-                *reinterpret_cast<int4*>(&s_x[wave][li][4 * lg]) = make_int4(v[0], v[1], v[2], v[3]);
-                wave_lds_sync();
-                int u[4];
+                for (int r = 0; r < 4; ++r)
+                    v[r] = (unsigned)mx_round(acc[0][r], acc[1][r], acc[2][r], acc[3][r], acc[4][r]) + (unsigned)bsr[r];
+                // segmented max over the run prefix: a step merges a same-document source only
 #pragma unroll
-                for (int j = 0; j < 4; ++j) u[j] = s_x[wave][lg + 4 * j][li];
-                wave_lds_sync();
-#pragma unroll
-                for (int j = 0; j < 4; ++j) u[j] = seg_max16(u[j], same);
+                for (int r = 0; r < 4; ++r) {
+                    unsigned t;
+                    t = val_shr<1>(v[r]); v[r] = same1 && t > v[r] ? t : v[r];
+                    t = val_shr<2>(v[r]); v[r] = same2 && t > v[r] ? t : v[r];
+                    t = val_shr<4>(v[r]); v[r] = same4 && t > v[r] ? t : v[r];
+                    t = val_shr<8>(v[r]); v[r] = same8 && t > v[r] ? t : v[r];
+                }
                 if (run_end) {
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const int tk = 16 * tt + lg + 4 * j;
-                        if (tk < it.np) atomicMax(&a.tokmax[(int64_t)s_tok[tk] * n_docs + doc], u[j]);
+                    for (int r = 0; r < 4; ++r) {
+                        const int tk = 16 * tt + 4 * lg + r;
+                        if (tk < it.np) atomicMax(&tokmax[s_row[tk] + my_doc], v[r]);
                     }
                 }
             }
