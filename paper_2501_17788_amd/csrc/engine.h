@@ -37,7 +37,7 @@ __device__ __forceinline__ int score_bin(float f) {
 // Residual scan on the matrix cores: a work item is (cluster, chunk of kMxChunk
 // embeddings, group of up to kMxGroup probing tokens), run by kMxBlock threads.
 constexpr int kMxChunk = 256;
-constexpr int kMxGroup = 64;
+constexpr int kMxGroup = 32;
 constexpr int kMxBlock = 256;
 constexpr int kQdigBytes = 3 * kDim;  // three base-256 digit planes of a query token
 // Largest bucket weight magnitude: Q(omega) = round(omega * 2^22) must have three

@@ -121,22 +121,6 @@ __device__ __forceinline__ MxItem mx_decode(const WaveArgs& a, int64_t item, int
     return it;
 }
 
-// DPP row_shr:k source (k = 1, 2, 4, 8) of a document id inside rows of 16
-// lanes; lanes whose source falls outside the row read INT32_MIN.
-template <int K>
-__device__ __forceinline__ int doc_shr(int v) {
-    return __builtin_amdgcn_update_dpp(INT32_MIN, v, 0x110 + K, 0xf, 0xf, false);
-}
-__device__ __forceinline__ int doc_shl1(int v) {
-    return __builtin_amdgcn_update_dpp(INT32_MIN, v, 0x101, 0xf, 0xf, false);
-}
-
-// Same for a biased score: lanes outside the row read 0, the identity of max.
-template <int K>
-__device__ __forceinline__ unsigned val_shr(unsigned v) {
-    return (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x110 + K, 0xf, 0xf, true);
-}
-
 // Token-max cells hold t + 2^31 as unsigned (order preserving; 0 = absent).
 __device__ __forceinline__ unsigned bias(int t) { return (unsigned)t ^ 0x80000000u; }
 
@@ -145,9 +129,15 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
     constexpr int BYTES = kDim * NBITS / 8;  // code bytes per embedding
     constexpr int CW = BYTES / 16 * 4;       // code words per lane: 16 bytes (b = 4) or 8 (b = 2)
     constexpr int NSLOT = 24;                // (plane, slice, lane group) slots of 16 bytes
+    constexpr int TPAD = kMxChunk + 1;       // row of the run table, padded against bank conflicts
+    constexpr int NW = kMxBlock / 64;
     __shared__ v4i s_q[NSLOT][kMxGroup];     // query digit planes of the item's tokens
     __shared__ __attribute__((aligned(16))) int s_base[kMxGroup];   // R(S64) + 2^31 of each token
     __shared__ __attribute__((aligned(16))) int64_t s_row[kMxGroup];  // its token-max row offset
+    __shared__ unsigned s_tab[kMxGroup * TPAD];  // max score of (token, document run of the chunk)
+    __shared__ int s_run[kMxChunk];          // run of each chunk embedding
+    __shared__ int s_rdoc[kMxChunk];         // document of each run
+    __shared__ int s_wruns[NW];              // runs starting in each wave's quarter of the chunk
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
@@ -181,30 +171,14 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
     int c = lo;
     const v4i* qdig = reinterpret_cast<const v4i*>(a.qdig);
     const uint8_t* __restrict__ codes = a.codes;
+    const int32_t* __restrict__ doc_ids = a.doc_ids;
     unsigned* __restrict__ tokmax = a.tokmax;
-
-    // this lane's code words of embedding tile0 + li, dimensions 32 lg .. 32 lg + 31
-    auto load_codes = [&](int64_t tile0, int64_t e1, unsigned (&w)[CW], int& doc) {
-        const int64_t e = tile0 + li;
-#pragma unroll
-        for (int m = 0; m < CW; ++m) w[m] = 0;
-        doc = -1 - li;  // padding rows never match a neighbour
-        if (e < e1) {
-            if (NBITS == 4) {
-                const uint4 v = *reinterpret_cast<const uint4*>(codes + e * BYTES + 16 * lg);
-                w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
-            } else {
-                const uint2 v = *reinterpret_cast<const uint2*>(codes + e * BYTES + 8 * lg);
-                w[0] = v.x; w[1] = v.y;
-            }
-            doc = a.doc_ids[e];
-        }
-    };
+    for (int i = tid; i < kMxGroup * TPAD; i += kMxBlock) s_tab[i] = kTokAbsent;
 
     for (int64_t item = first; item < last; ++item) {
         while (item_start[c + 1] <= item) ++c;
         const MxItem it = mx_decode(a, item, c);
-        __syncthreads();  // the previous item's tokens are no longer read
+        __syncthreads();  // the previous item's table is flushed and its tokens are no longer read
         if (tid < kMxGroup) {
             const bool in = tid < it.np;
             const int tok = in ? a.plist[2 * (int64_t)(it.p0 + tid)] : 0;
@@ -219,15 +193,45 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
             if (tk < it.np) v = qdig[(int64_t)a.plist[2 * (int64_t)(it.p0 + tk)] * NSLOT + slot];
             s_q[slot][tk] = v;
         }
+        // runs of equal documents along the chunk (ids ascend inside a cluster)
+        const int64_t e = it.e0 + tid;
+        const bool e_in = e < it.e1;
+        const int doc = e_in ? doc_ids[e] : -1;
+        const bool start = e_in && (tid == 0 || doc_ids[e - 1] != doc);
+        const unsigned long long starts = __ballot(start);
+        if (lane == 0) s_wruns[wave] = __popcll(starts);
+        __syncthreads();
+        int run = __popcll(starts & ((2ull << lane) - 1)) - 1;  // starts in this wave up to this lane, minus one
+        int n_runs = 0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+            run += w < wave ? s_wruns[w] : 0;
+            n_runs += s_wruns[w];
+        }
+        if (e_in) {
+            s_run[tid] = run;
+            if (start) s_rdoc[run] = doc;
+        }
         __syncthreads();
 
         const int n_et = (int)((it.e1 - it.e0 + 15) >> 4);
         const int n_tt = (it.np + 15) >> 4;
-        unsigned w[CW];
-        int doc;
-        if (wave < n_et) load_codes(it.e0 + 16 * wave, it.e1, w, doc);
-        for (int et = wave; et < n_et; et += kMxBlock / 64) {  // wave-uniform
-            // weight digits of the tile (MFMA B operand: column li = embedding tile0 + li)
+        for (int et = wave; et < n_et; et += NW) {  // wave-uniform
+            // weight digits of the tile (MFMA B operand: column li = embedding e0 + 16 et + li)
+            const int64_t er = it.e0 + 16 * et + li;
+            const bool row_in = er < it.e1;
+            unsigned w[CW];
+#pragma unroll
+            for (int m = 0; m < CW; ++m) w[m] = 0;
+            if (row_in) {
+                if (NBITS == 4) {
+                    const uint4 v = *reinterpret_cast<const uint4*>(codes + er * BYTES + 16 * lg);
+                    w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+                } else {
+                    const uint2 v = *reinterpret_cast<const uint2*>(codes + er * BYTES + 8 * lg);
+                    w[0] = v.x; w[1] = v.y;
+                }
+            }
             v4i A[3][2];
             if (NBITS == 4) {
 #pragma unroll
@@ -257,13 +261,7 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
                     }
                 }
             }
-            // runs of equal documents along the row (embedding li of the tile)
-            const bool same1 = doc_shr<1>(doc) == doc, same2 = doc_shr<2>(doc) == doc;
-            const bool same4 = doc_shr<4>(doc) == doc, same8 = doc_shr<8>(doc) == doc;
-            const bool run_end = doc >= 0 && doc_shl1(doc) != doc;
-            const int my_doc = doc;
-            // prefetch the wave's next tile
-            if (et + kMxBlock / 64 < n_et) load_codes(it.e0 + 16 * (et + kMxBlock / 64), it.e1, w, doc);
+            const int my_run = row_in ? s_run[16 * et + li] : 0;
 
             for (int tt = 0; tt < n_tt; ++tt) {
                 v4i acc[5];
@@ -281,30 +279,28 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
                         for (int j = 0; j < 3; ++j)
                             acc[i + j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(B[i], A[j][s], acc[i + j], 0, 0, 0);
                 }
-                // acc[k][r] of lane (li, lg): token 16 tt + 4 lg + r against embedding tile0 + li
+                // acc[k][r] of lane (li, lg): token 16 tt + 4 lg + r against embedding e0 + 16 et + li;
+                // merge into the (token, run) table
                 const int4 bs = *reinterpret_cast<const int4*>(&s_base[16 * tt + 4 * lg]);
                 const int bsr[4] = {bs.x, bs.y, bs.z, bs.w};
-                unsigned v[4];
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    v[r] = (unsigned)mx_round(acc[0][r], acc[1][r], acc[2][r], acc[3][r], acc[4][r]) + (unsigned)bsr[r];
-                // segmented max over the run prefix: a step merges a same-document source only
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    unsigned t;
-                    t = val_shr<1>(v[r]); v[r] = same1 && t > v[r] ? t : v[r];
-                    t = val_shr<2>(v[r]); v[r] = same2 && t > v[r] ? t : v[r];
-                    t = val_shr<4>(v[r]); v[r] = same4 && t > v[r] ? t : v[r];
-                    t = val_shr<8>(v[r]); v[r] = same8 && t > v[r] ? t : v[r];
-                }
-                if (run_end) {
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int tk = 16 * tt + 4 * lg + r;
-                        if (tk < it.np) atomicMax(&tokmax[s_row[tk] + my_doc], v[r]);
-                    }
+                    const int tk = 16 * tt + 4 * lg + r;
+                    const unsigned v =
+                        (unsigned)mx_round(acc[0][r], acc[1][r], acc[2][r], acc[3][r], acc[4][r]) + (unsigned)bsr[r];
+                    if (row_in && tk < it.np) atomicMax(&s_tab[tk * TPAD + my_run], v);
                 }
             }
+        }
+        __syncthreads();
+        // flush: one device atomic per (token, run); consecutive threads take consecutive
+        // runs of one token, i.e. ascending documents of one token-max row
+        const int cells = it.np * n_runs;
+        for (int x = tid; x < cells; x += kMxBlock) {
+            const int tk = x / n_runs, rn = x - tk * n_runs;
+            const unsigned v = s_tab[tk * TPAD + rn];
+            s_tab[tk * TPAD + rn] = kTokAbsent;
+            atomicMax(&tokmax[s_row[tk] + s_rdoc[rn]], v);
         }
     }
 }
