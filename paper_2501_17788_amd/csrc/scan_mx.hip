@@ -131,6 +131,10 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
     constexpr int NSLOT = 24;                // (plane, slice, lane group) slots of 16 bytes
     constexpr int TPAD = kMxChunk + 1;       // row of the run table, padded against bank conflicts
     constexpr int NW = kMxBlock / 64;
+    // the run pass gives each thread at most one embedding of the chunk, and the query
+    // staging splits evenly over the threads
+    static_assert(kMxChunk <= kMxBlock, "one thread per chunk embedding");
+    static_assert(NSLOT * kMxGroup % kMxBlock == 0, "query staging");
     __shared__ v4i s_q[NSLOT][kMxGroup];     // query digit planes of the item's tokens
     __shared__ __attribute__((aligned(16))) int s_base[kMxGroup];   // R(S64) + 2^31 of each token
     __shared__ __attribute__((aligned(16))) int64_t s_row[kMxGroup];  // its token-max row offset
