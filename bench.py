@@ -94,7 +94,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="small")
     ap.add_argument("--latency-runs", type=int, default=100)
-    ap.add_argument("--cpu-queries", type=int, default=48)
+    ap.add_argument("--cpu-queries", type=int, default=128)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the run, copy a buffer of this size 3 times on the device (a kernel of "

@@ -17,10 +17,14 @@
  *
  * Arithmetic. Centroid scores are computed in fp64 in dimension order; every
  * token score and document score is held in fixed point with
- * warp_fixed_point_bits() fraction bits (R(x) = round-half-even(x * 2^F)):
- *   token score  t = R(S_{c,q_i}) + sum_d R(q_{i,d} * omega[code_d])   (int32)
+ * warp_fixed_point_bits() fraction bits (R(x) = round-half-even(x * 2^F)).
+ * The table entries of Section 4.4 are exact products of query values and
+ * bucket weights quantised to 2^-22 (Q(x) = round-half-even(x * 2^22)):
+ *   token score  t = R(S_{c,q_i}) + round-half-even(2^(F-44) * V),
+ *                V = sum_d Q(q_{i,d}) * Q(omega[code_d])                (int32)
  *   doc score    s = sum_i (max retrieved t, or R(m_i) if none)        (int64)
- * so every max and sum is exact and independent of the order of evaluation.
+ * so every product, max and sum is exact and independent of the order of
+ * evaluation.
  * The reported float score is (float)(s * 2^-F). Ties between documents are
  * broken by the lower document id; ties between centroids by the lower id.
  *
@@ -73,7 +77,8 @@ const char* warp_last_error(void);
  *   doc_ids          [N] int32, 0 <= id < n_docs, grouped by cluster
  *   codes            [N][dim * nbits / 8] uint8, grouped by cluster
  *   nbits            2 or 4 (1 and 8: WARP_ENOTSUP)
- *   bucket_weights   [2^nbits] fp32, finite, |w| <= 2
+ *   bucket_weights   [2^nbits] fp32, finite, |w| <= 1.99 (so that Q(w) has three
+ *                    signed base-256 digits)
  *   n_docs           1 <= n_docs <= 2^24
  *   out              receives the index on WARP_OK; untouched otherwise
  *
