@@ -72,6 +72,7 @@ struct WaveArgs {
     int64_t* m_fixed;           // [n_tok]
     uint32_t* tokmax;           // [n_tok][n_docs] biased token maxima, kTokAbsent when not retrieved
     uint64_t* keys;             // [n_q][n_docs]
+    uint64_t* qpart;            // [n_q][ceil(n_docs / 256)][2]: candidate count and largest key of each fold block
     int32_t* err;               // device flag word
     // cluster-major pairing
     int32_t* ccount;            // [n_c] probing tokens per cluster

@@ -64,7 +64,7 @@ struct warp_index {
     hipStream_t stream = nullptr;
     int scan_grid = 0;     // persistent workgroups of the residual scan
     // per-search scratch, grown on demand
-    DevBuf filter, sel, base, seg_pref, m_fixed, tokmax, keys;
+    DevBuf filter, sel, base, seg_pref, m_fixed, tokmax, keys, qpart;
     DevBuf ccount, cursor, item_start, pair_start, plist, qdig, blk;
     int64_t tokmax_ready = 0;  // leading elements of tokmax holding kTokAbsent
     // staging of the host-pointer calls
@@ -282,6 +282,7 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P) {
     if (!rc) rc = grow(idx->seg_pref, (size_t)n_tok * (P + 1) * 8);
     if (!rc) rc = grow(idx->m_fixed, (size_t)n_tok * 8);
     if (!rc) rc = grow(idx->keys, (size_t)qw * idx->n_docs * 8);
+    if (!rc) rc = grow(idx->qpart, (size_t)qw * (((size_t)idx->n_docs + 255) / 256) * 16);
     const int64_t nblk = ((int64_t)idx->n_c + kPlanBlock - 1) / kPlanBlock;
     if (!rc) rc = grow(idx->ccount, (size_t)idx->n_c * 4);
     if (!rc) rc = grow(idx->cursor, (size_t)idx->n_c * 4);
@@ -401,6 +402,7 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         a.m_fixed = (int64_t*)idx->m_fixed.p;
         a.tokmax = (uint32_t*)idx->tokmax.p;
         a.keys = (uint64_t*)idx->keys.p;
+        a.qpart = (uint64_t*)idx->qpart.p;
         a.err = idx->err;
         a.out_ids = o.ids + (int64_t)q0 * k;
         a.out_scores = o.scores + (int64_t)q0 * k;
@@ -538,7 +540,7 @@ void warp_index_free(warp_index* idx) {
                         (void*)idx->codes, (void*)idx->weights, (void*)idx->err})
             if (p) (void)hipFree(p);
         for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_pref, &idx->m_fixed,
-                          &idx->tokmax, &idx->keys, &idx->ccount, &idx->cursor, &idx->item_start,
+                          &idx->tokmax, &idx->keys, &idx->qpart, &idx->ccount, &idx->cursor, &idx->item_start,
                           &idx->pair_start, &idx->plist, &idx->qdig, &idx->blk, &idx->st_q, &idx->st_ids, &idx->st_scores,
                           &idx->st_fixed, &idx->st_counts, &idx->st_sel, &idx->st_m, &idx->st_bitmap,
                           &idx->st_scored})

@@ -16,6 +16,7 @@ __global__ __launch_bounds__(256) void k_fold(WaveArgs a) {
     const int64_t doc = (int64_t)blockIdx.x * 256 + threadIdx.x;
     const bool in = doc < a.n_docs;
     bool any = false;
+    uint64_t key = 0;
     if (in) {
         int64_t sum = 0;
         const int T = a.n_qtok;
@@ -31,9 +32,33 @@ __global__ __launch_bounds__(256) void k_fold(WaveArgs a) {
                 sum += m[i];
             }
         }
-        const uint64_t key =
-            any ? ((uint64_t)(sum + (1ll << 39)) << 24) | (uint64_t)(kMaxDocs - 1 - (int32_t)doc) : 0;
+        key = any ? ((uint64_t)(sum + (1ll << 39)) << 24) | (uint64_t)(kMaxDocs - 1 - (int32_t)doc) : 0;
         a.keys[(int64_t)q * a.n_docs + doc] = key;
+    }
+    // candidate count and largest key of the block, for the top-k's histogram
+    __shared__ unsigned long long s_max[4];
+    __shared__ int s_cnt[4];
+    unsigned long long kmax = key;
+    for (int off = 32; off > 0; off >>= 1) {
+        const unsigned long long o = __shfl_xor(kmax, off, 64);
+        kmax = o > kmax ? o : kmax;
+    }
+    const int n_any = __popcll(__ballot(in && any));
+    if ((threadIdx.x & 63) == 0) {
+        s_max[threadIdx.x >> 6] = kmax;
+        s_cnt[threadIdx.x >> 6] = n_any;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long m = 0;
+        long long cnt = 0;
+        for (int w = 0; w < 4; ++w) {
+            m = s_max[w] > m ? s_max[w] : m;
+            cnt += s_cnt[w];
+        }
+        uint64_t* part = a.qpart + 2 * ((int64_t)q * gridDim.x + blockIdx.x);
+        part[0] = (uint64_t)cnt;
+        part[1] = m;
     }
     if (a.dbg_bitmap) {
         const unsigned long long bits = __ballot(in && any);

@@ -1,43 +1,160 @@
 // Final top-k (Section 4.5: the k best candidate documents by score).
 //
-// One workgroup per query over its n_docs sort keys (fold kernel): keys are
-// distinct, so the K-th largest key (K = min(k, candidates)) is found exactly
-// by an MSB-first radix select, 8 bits per pass, with an LDS histogram of the
-// keys that match the digits fixed so far. The K keys >= that key are gathered
-// and sorted in LDS; each decodes to (document id, fixed-point score).
+// One workgroup per query over its n_docs sort keys (fold kernel). A key is
+// ((score + 2^39) << 24) | (2^24 - 1 - doc): keys are distinct, larger is
+// better, and the score is key >> 24 (offset). The fold leaves, per block of
+// 256 documents, the candidate count and the largest key.
+//
+// With K = min(k, candidates), the K largest keys are found in one or two
+// histogram passes over the keys: bins of the distance below the largest score
+// (4096 bins of 2^-6, then, inside the bin holding the K-th key, 4096 bins of
+// 2^-18), after which every key at or above the bin holding the K-th key is
+// gathered (at most kMaxK), sorted in LDS, and the first K decoded. When the
+// K-th key lies more than 64 below the best, or its fine bin alone would overflow
+// the gather buffer, an MSB-first radix select over the whole key (8 bits per
+// pass) finds the K-th key exactly instead.
 #include "engine.h"
 
 namespace warp {
 
 constexpr int kTopkThreads = 1024;
+constexpr int kTopkBins = 4096;
+constexpr int kCoarseShift = 20;  // coarse bin width: 2^20 units of 2^-26
+constexpr int kFineShift = 8;     // fine bin width inside one coarse bin: 2^8 units
+
+// Smallest bin b with hist[0] + ... + hist[b] >= need, and the count of bins
+// before it; b = -1 if the total is below need. Every thread calls it.
+__device__ void find_crossing(const uint32_t* hist, uint32_t need, uint32_t* scan, int* s_bin,
+                              uint32_t* s_before) {
+    const int tid = threadIdx.x;
+    constexpr int PER = kTopkBins / kTopkThreads;
+    uint32_t mine = 0;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) mine += hist[PER * tid + i];
+    scan[tid] = mine;
+    if (tid == 0) *s_bin = -1;
+    __syncthreads();
+    for (int off = 1; off < kTopkThreads; off <<= 1) {
+        const uint32_t v = tid >= off ? scan[tid - off] : 0;
+        __syncthreads();
+        scan[tid] += v;
+        __syncthreads();
+    }
+    const uint32_t incl = scan[tid], excl = incl - mine;
+    if (excl < need && incl >= need) {
+        uint32_t cum = excl;
+        for (int i = 0; i < PER; ++i) {
+            const uint32_t h = hist[PER * tid + i];
+            if (cum + h >= need) {
+                *s_bin = PER * tid + i;
+                *s_before = cum;
+                break;
+            }
+            cum += h;
+        }
+    }
+    __syncthreads();
+}
 
 __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
-    __shared__ uint32_t hist[256];
+    __shared__ uint32_t hist[kTopkBins];
+    __shared__ uint32_t scan[kTopkThreads];
     __shared__ unsigned long long buf[kMaxK];
-    __shared__ unsigned long long s_prefix, s_mask;
-    __shared__ uint32_t s_need, s_count, s_ncand;
+    __shared__ unsigned long long s_prefix, s_mask, s_max, s_lim;
+    __shared__ uint32_t s_need, s_count, s_ncand, s_before;
+    __shared__ int s_bin;
 
     const int q = blockIdx.x;
     const int tid = threadIdx.x;
     const int64_t n = a.n_docs;
     const unsigned long long* keys = reinterpret_cast<const unsigned long long*>(a.keys) + (int64_t)q * n;
+
+    // candidates and the largest key, from the fold's per-block partials
     if (tid == 0) {
         s_ncand = 0;
+        s_max = 0;
         s_count = 0;
-        s_prefix = 0;
-        s_mask = 0;
     }
     __syncthreads();
-    uint32_t mine = 0;
-    for (int64_t x = tid; x < n; x += kTopkThreads) mine += keys[x] != 0;
-    atomicAdd(&s_ncand, mine);
+    {
+        const int64_t nb = (n + 255) / 256;
+        const uint64_t* part = a.qpart + 2 * (int64_t)q * nb;
+        unsigned long long cnt = 0, mx = 0;
+        for (int64_t b = tid; b < nb; b += kTopkThreads) {
+            cnt += part[2 * b];
+            mx = part[2 * b + 1] > mx ? part[2 * b + 1] : mx;
+        }
+        atomicAdd(&s_ncand, (uint32_t)cnt);
+        atomicMax(&s_max, mx);
+    }
     __syncthreads();
     const uint32_t ncand = s_ncand;
     const int K = (int)(ncand < (uint32_t)a.k ? ncand : (uint32_t)a.k);
-    if (tid == 0) s_need = (uint32_t)K;
-    __syncthreads();
+    const unsigned long long smax = s_max >> 24;  // the best (offset) score
 
-    if (K > 0) {
+    bool done = K == 0;
+    // level 1: coarse bins of the distance below the best score
+    if (!done) {
+        for (int i = tid; i < kTopkBins; i += kTopkThreads) hist[i] = 0;
+        __syncthreads();
+        for (int64_t x = tid; x < n; x += kTopkThreads) {
+            const unsigned long long key = keys[x];
+            if (key == 0) continue;
+            const unsigned long long d = smax - (key >> 24);
+            if (d < ((unsigned long long)kTopkBins << kCoarseShift)) atomicAdd(&hist[d >> kCoarseShift], 1u);
+        }
+        __syncthreads();
+        find_crossing(hist, (uint32_t)K, scan, &s_bin, &s_before);
+        const int b1 = s_bin;
+        if (b1 >= 0) {
+            const uint32_t above = s_before;
+            unsigned long long lim = 0;  // gather every key with distance < lim
+            if (above + hist[b1] <= (uint32_t)kMaxK) {
+                lim = (unsigned long long)(b1 + 1) << kCoarseShift;
+            } else {
+                // level 2: fine bins inside coarse bin b1
+                __syncthreads();
+                for (int i = tid; i < kTopkBins; i += kTopkThreads) hist[i] = 0;
+                __syncthreads();
+                const unsigned long long base = (unsigned long long)b1 << kCoarseShift;
+                for (int64_t x = tid; x < n; x += kTopkThreads) {
+                    const unsigned long long key = keys[x];
+                    if (key == 0) continue;
+                    const unsigned long long d = smax - (key >> 24);
+                    if (d >= base && d - base < (1ull << kCoarseShift))
+                        atomicAdd(&hist[(d - base) >> kFineShift], 1u);
+                }
+                __syncthreads();
+                find_crossing(hist, (uint32_t)K - above, scan, &s_bin, &s_before);
+                const int b2 = s_bin;
+                if (b2 >= 0 && above + s_before + hist[b2] <= (uint32_t)kMaxK)
+                    lim = base + ((unsigned long long)(b2 + 1) << kFineShift);
+            }
+            if (tid == 0) s_lim = lim;
+            __syncthreads();
+            lim = s_lim;
+            if (lim != 0) {
+                for (int64_t x = tid; x < n; x += kTopkThreads) {
+                    const unsigned long long key = keys[x];
+                    if (key != 0 && smax - (key >> 24) < lim) {
+                        const uint32_t p = atomicAdd(&s_count, 1u);
+                        if (p < (uint32_t)kMaxK) buf[p] = key;
+                    }
+                }
+                done = true;
+            }
+        }
+        __syncthreads();
+    }
+    // fallback: exact radix select of the K-th key, 8 bits per pass
+    if (!done) {
+        if (tid == 0) {
+            s_need = (uint32_t)K;
+            s_prefix = 0;
+            s_mask = 0;
+            s_count = 0;
+        }
+        __syncthreads();
         for (int shift = 56; shift >= 0; shift -= 8) {
             for (int i = tid; i < 256; i += kTopkThreads) hist[i] = 0;
             __syncthreads();
@@ -73,13 +190,14 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
         }
         __syncthreads();
     }
-    // bitonic sort, descending, of the K gathered keys padded with zeros
+    // bitonic sort, descending, of the gathered keys padded with zeros; the first K are the result
+    const int cnt = K == 0 ? 0 : (int)(s_count < (uint32_t)kMaxK ? s_count : (uint32_t)kMaxK);
     int np = 2;
-    while (np < K) np <<= 1;
+    while (np < cnt) np <<= 1;
     for (int i = tid; i < np; i += kTopkThreads)
-        if (i >= K) buf[i] = 0;
+        if (i >= cnt) buf[i] = 0;
     __syncthreads();
-    if (K > 1) {
+    if (cnt > 1) {
         for (int kk = 2; kk <= np; kk <<= 1) {
             for (int j = kk >> 1; j > 0; j >>= 1) {
                 for (int i = tid; i < np; i += kTopkThreads) {
