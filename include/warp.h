@@ -76,7 +76,7 @@ const char* warp_last_error(void);
  *                    N = offsets[n_centroids] embeddings, N < 2^40
  *   doc_ids          [N] int32, 0 <= id < n_docs, grouped by cluster
  *   codes            [N][dim * nbits / 8] uint8, grouped by cluster
- *   nbits            2 or 4 (1 and 8: WARP_ENOTSUP)
+ *   nbits            1, 2, 4 or 8
  *   bucket_weights   [2^nbits] fp32, finite, |w| <= 1.99 (so that Q(w) has three
  *                    signed base-256 digits)
  *   n_docs           1 <= n_docs <= 2^24

@@ -123,8 +123,8 @@ int validate_index_host(const float* C, int32_t n_c, int32_t dim, const int64_t*
                         const float* w, int32_t n_docs) {
     if (n_c < 1) return fail(WARP_EINVAL, "n_centroids must be >= 1 (got %d)", n_c);
     if (dim != kDim) return fail(WARP_ENOTSUP, "dim must be 128 (got %d)", dim);
-    if (nbits == 1 || nbits == 8) return fail(WARP_ENOTSUP, "nbits = %d is not implemented (2 or 4)", nbits);
-    if (nbits != 2 && nbits != 4) return fail(WARP_EINVAL, "nbits must be 2 or 4 (got %d)", nbits);
+    if (nbits != 1 && nbits != 2 && nbits != 4 && nbits != 8)
+        return fail(WARP_EINVAL, "nbits must be 1, 2, 4 or 8 (got %d)", nbits);
     if (n_docs < 1 || n_docs > kMaxDocs) return fail(WARP_EINVAL, "n_docs must be in [1, 2^24] (got %d)", n_docs);
     if (!C || !off || !w) return fail(WARP_EINVAL, "null index array");
     if (off[0] != 0) return fail(WARP_EINVAL, "cluster_offsets[0] must be 0");

@@ -66,7 +66,10 @@ __device__ __forceinline__ int mx_round(int a0, int a1, int a2, int a3, int a4) 
 //          nibble) and + 1 (low nibble); slice s takes code words m = 2 s, 2 s + 1
 //          as [high nibbles of 2 s, low of 2 s, high of 2 s + 1, low of 2 s + 1];
 //   b = 2: code byte 8 g + 4 s + t holds dimensions 32 g + 16 s + 4 t + u, u = 0
-//          in the top bits; slice s holds the four fields u = 0..3 in that order.
+//          in the top bits; slice s holds the four fields u = 0..3 in that order;
+//   b = 1: code byte 4 g + t holds dimensions 32 g + 8 t + (7 - k) in bit k; word
+//          u of slice s holds bit k = 4 s + u of the four bytes;
+//   b = 8: code byte 32 g + 16 s + j is dimension 32 g + 16 s + j.
 template <int NBITS>
 __device__ __forceinline__ void slot_of_dim(int d, int& s, int& g, int& j) {
     g = d >> 5;
@@ -75,9 +78,16 @@ __device__ __forceinline__ void slot_of_dim(int d, int& s, int& g, int& j) {
         const int m = r >> 3, t = (r & 7) >> 1, lo = r & 1;
         s = m >> 1;
         j = 4 * (2 * (m & 1) + lo) + t;
-    } else {
+    } else if (NBITS == 2) {
         s = r >> 4;
         j = 4 * (r & 3) + ((r & 15) >> 2);
+    } else if (NBITS == 1) {
+        const int k = 7 - (r & 7);
+        s = k >> 2;
+        j = 4 * (k & 3) + (r >> 3);
+    } else {
+        s = r >> 4;
+        j = r & 15;
     }
 }
 
@@ -127,7 +137,7 @@ __device__ __forceinline__ unsigned bias(int t) { return (unsigned)t ^ 0x8000000
 template <int NBITS>
 __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
     constexpr int BYTES = kDim * NBITS / 8;  // code bytes per embedding
-    constexpr int CW = BYTES / 16 * 4;       // code words per lane: 16 bytes (b = 4) or 8 (b = 2)
+    constexpr int CW = NBITS;                // code words per lane: 32 dimensions of b bits
     constexpr int NSLOT = 24;                // (plane, slice, lane group) slots of 16 bytes
     constexpr int TPAD = kMxChunk + 1;       // row of the run table, padded against bank conflicts
     constexpr int NW = kMxBlock / 64;
@@ -142,6 +152,7 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
     __shared__ int s_run[kMxChunk];          // run of each chunk embedding
     __shared__ int s_rdoc[kMxChunk];         // document of each run
     __shared__ int s_wruns[NW];              // runs starting in each wave's quarter of the chunk
+    __shared__ unsigned s_wd[NBITS == 8 ? 256 : 1];  // b = 8: the three digits of Q(omega[v]) in bytes 0..2
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
@@ -150,13 +161,20 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
     const int lg = lane >> 4;  // operand lane group
 
     // weight digit tables: tab[p][k] holds digit p of Q(omega[v]) for v = 4 k .. 4 k + 3
+    // (b <= 4); for b = 8 a 256-entry table in LDS, ordered by the first barrier below
     unsigned tab[3][4] = {};
+    if (NBITS <= 4) {
 #pragma unroll
-    for (int v = 0; v < (1 << NBITS); ++v) {
+        for (int v = 0; v < (NBITS <= 4 ? 1 << NBITS : 0); ++v) {
+            int d[3];
+            digits3(quant22(a.weights[v]), d[0], d[1], d[2]);
+#pragma unroll
+            for (int p = 0; p < 3; ++p) tab[p][v >> 2] |= ((unsigned)d[p] & 255u) << (8 * (v & 3));
+        }
+    } else if (tid < 256) {
         int d[3];
-        digits3(quant22(a.weights[v]), d[0], d[1], d[2]);
-#pragma unroll
-        for (int p = 0; p < 3; ++p) tab[p][v >> 2] |= ((unsigned)d[p] & 255u) << (8 * (v & 3));
+        digits3(quant22(a.weights[tid]), d[0], d[1], d[2]);
+        s_wd[tid] = ((unsigned)d[0] & 255u) | (((unsigned)d[1] & 255u) << 8) | (((unsigned)d[2] & 255u) << 16);
     }
 
     const int n_c = a.n_c;
@@ -228,12 +246,20 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
 #pragma unroll
             for (int m = 0; m < CW; ++m) w[m] = 0;
             if (row_in) {
-                if (NBITS == 4) {
-                    const uint4 v = *reinterpret_cast<const uint4*>(codes + er * BYTES + 16 * lg);
+                const uint8_t* row = codes + er * BYTES + 4 * NBITS * lg;
+                if (NBITS == 8) {
+                    const uint4 v0 = reinterpret_cast<const uint4*>(row)[0];
+                    const uint4 v1 = reinterpret_cast<const uint4*>(row)[1];
+                    w[0] = v0.x; w[1] = v0.y; w[2] = v0.z; w[3] = v0.w;
+                    w[4] = v1.x; w[5] = v1.y; w[6] = v1.z; w[7] = v1.w;
+                } else if (NBITS == 4) {
+                    const uint4 v = *reinterpret_cast<const uint4*>(row);
                     w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
-                } else {
-                    const uint2 v = *reinterpret_cast<const uint2*>(codes + er * BYTES + 8 * lg);
+                } else if (NBITS == 2) {
+                    const uint2 v = *reinterpret_cast<const uint2*>(row);
                     w[0] = v.x; w[1] = v.y;
+                } else {
+                    w[0] = *reinterpret_cast<const unsigned*>(row);
                 }
             }
             v4i A[3][2];
@@ -253,7 +279,7 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
                         }
                     }
                 }
-            } else {
+            } else if (NBITS == 2) {
 #pragma unroll
                 for (int s = 0; s < 2; ++s) {
 #pragma unroll
@@ -262,6 +288,28 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
 #pragma unroll
                         for (int p = 0; p < 3; ++p)
                             A[p][s][u] = (int)__builtin_amdgcn_perm(tab[p][0], tab[p][0], x);
+                    }
+                }
+            } else if (NBITS == 1) {
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    const unsigned x = (w[0] >> k) & 0x01010101u;  // bit k of each byte: 0 or 1
+#pragma unroll
+                    for (int p = 0; p < 3; ++p)
+                        A[p][k >> 2][k & 3] = (int)__builtin_amdgcn_perm(tab[p][0], tab[p][0], x);
+                }
+            } else {
+                // b = 8: one table lookup per code byte, then gather digit p of four entries
+#pragma unroll
+                for (int m = 0; m < 8; ++m) {
+                    const unsigned e0 = s_wd[w[m] & 255u], e1 = s_wd[(w[m] >> 8) & 255u];
+                    const unsigned e2 = s_wd[(w[m] >> 16) & 255u], e3 = s_wd[w[m] >> 24];
+#pragma unroll
+                    for (int p = 0; p < 3; ++p) {
+                        const unsigned sel = 0x0C0C0000u | ((unsigned)(4 + p) << 8) | (unsigned)p;
+                        const unsigned lo2 = __builtin_amdgcn_perm(e1, e0, sel);  // bytes 0, 1: digit p of e0, e1
+                        const unsigned hi2 = __builtin_amdgcn_perm(e3, e2, sel);
+                        A[p][m >> 2][m & 3] = (int)__builtin_amdgcn_perm(hi2, lo2, 0x05040100u);
                     }
                 }
             }
@@ -312,18 +360,31 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
 void launch_qdigits(const WaveArgs& a, hipStream_t s) {
     const int64_t n_tok = (int64_t)a.n_q * a.n_qtok;
     const dim3 grid((unsigned)((n_tok * kDim + 255) / 256));
-    if (a.nbits == 4) hipLaunchKernelGGL(k_qdigits<4>, grid, dim3(256), 0, s, a.queries, n_tok, a.qdig);
-    else hipLaunchKernelGGL(k_qdigits<2>, grid, dim3(256), 0, s, a.queries, n_tok, a.qdig);
+    switch (a.nbits) {
+        case 1: hipLaunchKernelGGL(k_qdigits<1>, grid, dim3(256), 0, s, a.queries, n_tok, a.qdig); break;
+        case 2: hipLaunchKernelGGL(k_qdigits<2>, grid, dim3(256), 0, s, a.queries, n_tok, a.qdig); break;
+        case 4: hipLaunchKernelGGL(k_qdigits<4>, grid, dim3(256), 0, s, a.queries, n_tok, a.qdig); break;
+        default: hipLaunchKernelGGL(k_qdigits<8>, grid, dim3(256), 0, s, a.queries, n_tok, a.qdig); break;
+    }
 }
 
 void launch_scan_mx(const WaveArgs& a, hipStream_t s) {
-    if (a.nbits == 4) hipLaunchKernelGGL(k_scan_mx<4>, dim3(a.scan_grid), dim3(kMxBlock), 0, s, a);
-    else hipLaunchKernelGGL(k_scan_mx<2>, dim3(a.scan_grid), dim3(kMxBlock), 0, s, a);
+    const dim3 grid(a.scan_grid), block(kMxBlock);
+    switch (a.nbits) {
+        case 1: hipLaunchKernelGGL(k_scan_mx<1>, grid, block, 0, s, a); break;
+        case 2: hipLaunchKernelGGL(k_scan_mx<2>, grid, block, 0, s, a); break;
+        case 4: hipLaunchKernelGGL(k_scan_mx<4>, grid, block, 0, s, a); break;
+        default: hipLaunchKernelGGL(k_scan_mx<8>, grid, block, 0, s, a); break;
+    }
 }
 
 int scan_mx_blocks_per_cu(int nbits) {
     int n = 0;
-    (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, nbits == 4 ? k_scan_mx<4> : k_scan_mx<2>, kMxBlock, 0);
+    const void* k = nbits == 1   ? (const void*)k_scan_mx<1>
+                    : nbits == 2 ? (const void*)k_scan_mx<2>
+                    : nbits == 4 ? (const void*)k_scan_mx<4>
+                                 : (const void*)k_scan_mx<8>;
+    (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, kMxBlock, 0);
     return n > 0 ? n : 1;
 }
 

@@ -66,6 +66,7 @@ def _load_rc(a):
     ("bad_offsets", w.EINVAL, "decrease"),
     ("first_offset", w.EINVAL, "offsets[0]"),
     ("big_weight", w.EINVAL, "bucket weight"),
+    ("weight_above_1.99", w.EINVAL, "bucket weight"),
     ("nan_weight", w.EINVAL, "bucket weight"),
     ("non_unit", w.EINVAL, "unit norm"),
     ("n_docs_zero", w.EINVAL, "n_docs"),
@@ -84,6 +85,9 @@ def test_index_validation_before_device(case, code, needle):
     elif case == "big_weight":
         a["bucket_weights"] = a["bucket_weights"].copy()
         a["bucket_weights"][0] = -2.5
+    elif case == "weight_above_1.99":
+        a["bucket_weights"] = a["bucket_weights"].copy()
+        a["bucket_weights"][-1] = 1.995
     elif case == "nan_weight":
         a["bucket_weights"] = a["bucket_weights"].copy()
         a["bucket_weights"][1] = np.nan
@@ -117,10 +121,6 @@ def test_unsupported_shapes():
                                a["doc_ids"].ctypes.data_as(P), a["codes"].ctypes.data_as(P), 4,
                                a["bucket_weights"].ctypes.data_as(P), 20, ctypes.byref(h))
     assert rc == w.ENOTSUP and "dim" in w.last_error()
-    rc = w.lib.warp_index_load(a["centroids"].ctypes.data_as(P), 6, 128, a["offsets"].ctypes.data_as(P),
-                               a["doc_ids"].ctypes.data_as(P), a["codes"].ctypes.data_as(P), 8,
-                               a["bucket_weights"].ctypes.data_as(P), 20, ctypes.byref(h))
-    assert rc == w.ENOTSUP
 
 
 @pytest.mark.skipif(HAS_GPU, reason="checks the no-device error path")

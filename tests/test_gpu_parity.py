@@ -109,6 +109,9 @@ CASES = [
     (7, 200, 1000, 20, 2, 7, 1, 3, 50, 1),      # one query token, k = 1
     (8, 300, 5000, 30, 4, 3, 32, 256, 2000, 4096),  # largest nprobe and k
     (9, 40, 100000, 1, 4, 2, 8, 5, 7, 10),      # most documents have no embedding at all
+    (10, 60, 400, 12, 1, 4, 32, 9, 100, 30),    # one bit per dimension
+    (11, 60, 400, 12, 8, 4, 32, 9, 100, 30),    # eight bits per dimension
+    (12, 300, 3000, 40, 8, 3, 32, 48, 800, 200),
 ]
 
 
@@ -150,8 +153,8 @@ def test_tiny_workload_exact_and_real_valued():
     assert got["ids"][0, 0] == data.query_targets[0]
 
 
-@pytest.mark.parametrize("nbits", [2, 4])
-def test_tiny_workload_both_code_widths(nbits):
+@pytest.mark.parametrize("nbits", [1, 2, 4, 8])
+def test_tiny_workload_code_widths(nbits):
     wl = synth.with_overrides(synth.WORKLOADS["tiny"], nbits=nbits, n_queries=3, nprobe=32, k=100)
     run_both(synth.make_index(wl, workers=1), label=f"tiny nbits={nbits}")
 
