@@ -66,6 +66,16 @@ int warp_fixed_point_bits(void);
 const char* warp_last_error(void);
 
 /*
+ * The t' policy of Section 4.6 (hyperparameters): t' grows with the square root
+ * of the number of indexed embeddings and is bounded by t'_max:
+ *   *out = min(t_max, floor(c * sqrt(n_embeddings)))
+ * The paper fixes neither c nor t_max; the caller passes both. Host-only, no
+ * device call. WARP_EINVAL for a null out, n_embeddings < 0, c negative or not
+ * finite, or t_max < 0.
+ */
+int warp_t_prime_policy(int64_t n_embeddings, double c, int64_t t_max, int64_t* out);
+
+/*
  * Build a device-resident index (Section 4.1's index: centroids, per-cluster
  * document ids and packed residual codes, bucket weights).
  *

@@ -516,6 +516,16 @@ int warp_fixed_point_bits(void) { return kFrac; }
 
 const char* warp_last_error(void) { return g_err.c_str(); }
 
+int warp_t_prime_policy(int64_t n_embeddings, double c, int64_t t_max, int64_t* out) {
+    if (!out) return fail(WARP_EINVAL, "out is null");
+    if (n_embeddings < 0) return fail(WARP_EINVAL, "n_embeddings must be >= 0");
+    if (!(c >= 0.0) || !std::isfinite(c)) return fail(WARP_EINVAL, "c must be finite and >= 0");
+    if (t_max < 0) return fail(WARP_EINVAL, "t_max must be >= 0");
+    const double t = std::floor(c * std::sqrt((double)n_embeddings));
+    *out = t >= (double)t_max ? t_max : (int64_t)t;
+    return WARP_OK;
+}
+
 int warp_index_load(const float* centroids, int32_t n_centroids, int32_t dim, const int64_t* cluster_offsets,
                     const int32_t* doc_ids, const uint8_t* codes, int32_t nbits, const float* bucket_weights,
                     int32_t n_docs, warp_index** out) {

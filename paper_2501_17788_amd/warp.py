@@ -24,6 +24,7 @@ EXPORTS = (
     "warp_fixed_point_bits", "warp_last_error", "warp_index_load", "warp_index_load_device",
     "warp_index_free", "warp_index_info", "warp_search", "warp_search_async", "warp_index_sync",
     "warp_search_debug", "warp_centroid_filter_scores", "warp_set_timing", "warp_stage_timings",
+    "warp_t_prime_policy",
 )
 
 
@@ -60,6 +61,7 @@ def _load() -> ctypes.CDLL:
         "warp_centroid_filter_scores": ([P, P, i32, P], ctypes.c_int),
         "warp_set_timing": ([P, i32], ctypes.c_int),
         "warp_stage_timings": ([P, P, P, i32], ctypes.c_int),
+        "warp_t_prime_policy": ([i64, ctypes.c_double, i64, P], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -70,6 +72,19 @@ def _load() -> ctypes.CDLL:
 
 lib = _load()
 FRAC_BITS = lib.warp_fixed_point_bits()
+
+
+# Section 4.6 leaves the constants of its t' policy open; these defaults reproduce the
+# t' of the synthetic workloads (40,000 for 6.3M embeddings, capped at 100,000 above).
+T_PRIME_C = 15.8
+T_PRIME_MAX = 100_000
+
+
+def t_prime_policy(n_embeddings: int, c: float = T_PRIME_C, t_max: int = T_PRIME_MAX) -> int:
+    """t' = min(t_max, floor(c * sqrt(n_embeddings))) (Section 4.6), computed by the library."""
+    out = ctypes.c_int64()
+    _check(lib.warp_t_prime_policy(int(n_embeddings), float(c), int(t_max), ctypes.byref(out)))
+    return out.value
 
 
 def last_error() -> str:

@@ -127,3 +127,25 @@ def test_unsupported_shapes():
 def test_valid_index_without_device_reports_edevice():
     rc, msg = _load_rc(_arrays())
     assert rc == w.EDEVICE and "device" in msg
+
+
+def test_t_prime_policy():
+    """Section 4.6: t' proportional to sqrt(N), bounded by t'_max (computed on the host)."""
+    import math
+
+    from paper_2501_17788_amd import t_prime_policy
+
+    for n in (0, 1, 99, 10_000, 6_305_539, 70_000_000, 10 ** 12):
+        for c in (0.0, 1.0, 15.8, 100.0):
+            for t_max in (0, 1000, 100_000, 10 ** 15):
+                want = min(t_max, math.floor(c * math.sqrt(n)))
+                assert t_prime_policy(n, c, t_max) == want, (n, c, t_max)
+    # proportional to sqrt(N) below the cap, constant above it
+    assert t_prime_policy(4 * 1_000_000, 10.0, 10 ** 9) == 2 * t_prime_policy(1_000_000, 10.0, 10 ** 9)
+    assert t_prime_policy(10 ** 12, 15.8, 100_000) == 100_000
+    # the defaults give the synthetic workloads' t': 40,000 for small (capped at 100,000 beyond)
+    assert abs(t_prime_policy(6_305_539) - 40_000) < 1000
+    for bad in ((-1, 1.0, 10), (10, -1.0, 10), (10, float("nan"), 10), (10, 1.0, -1)):
+        with pytest.raises(w.WarpError) as e:
+            t_prime_policy(*bad)
+        assert e.value.code == w.EINVAL
