@@ -87,6 +87,84 @@ def describe(wl) -> str:
             f"t'={wl.t_prime}, k={wl.k}")
 
 
+def recall_study(args) -> int:
+    """The hyperparameter study of Section 4.6 on synthetic data: nRecall@k of the engine's top-k
+    against exhaustive MaxSim over the uncompressed fp32 token vectors, as nprobe, t' and b vary,
+    plus the rank of each query's target document. Prints a markdown table (and writes JSON)."""
+    import torch
+
+    import synth
+    from paper_2501_17788_amd import Index, t_prime_policy
+
+    base = synth.with_overrides(synth.WORKLOADS[args.workload], query_noise=args.query_noise)
+    dev = torch.device("cuda:0")
+    data = {}
+    for b in (4, 2):
+        t0 = time.time()
+        data[b] = synth.make_index(synth.with_overrides(base, nbits=b), workers=min(16, host_threads()))
+        log(f"recall: generated b={b} index in {time.time() - t0:.1f} s")
+    ref = data[4]
+    assert np.array_equal(ref.queries, data[2].queries)
+    lens = ref.doc_lengths.astype(np.int64)
+    n_docs, L = len(lens), int(lens.max())
+    N = int(lens.sum())
+    t0 = time.time()
+    X = torch.from_numpy(synth.token_vectors(ref.workload, np.arange(N))).to(dev)
+    log(f"recall: regenerated {N} token vectors in {time.time() - t0:.1f} s")
+    # documents padded to L tokens; padding rows score -inf
+    starts = np.zeros(n_docs + 1, np.int64)
+    np.cumsum(lens, out=starts[1:])
+    doc_of = np.repeat(np.arange(n_docs), lens)
+    slot = torch.from_numpy(doc_of * L + (np.arange(N) - starts[doc_of])).to(dev)
+    pad = torch.zeros(n_docs * L, 128, device=dev)
+    pad[slot] = X
+    del X
+    valid = torch.zeros(n_docs * L, dtype=torch.bool, device=dev)
+    valid[slot] = True
+    valid = valid.view(n_docs, L, 1)
+    Q = torch.from_numpy(ref.queries).to(dev)  # [nq, T, 128]
+    nq, T = Q.shape[0], Q.shape[1]
+    kmax = 100
+    exh = []
+    qc = max(1, 256 // T)
+    for q0 in range(0, nq, qc):
+        qq = Q[q0:q0 + qc].reshape(-1, 128)
+        S = (pad @ qq.T).view(n_docs, L, -1).masked_fill(~valid, float("-inf")).amax(dim=1)
+        scores = S.view(n_docs, -1, T).sum(dim=2)  # [n_docs, queries of the chunk]
+        exh.append(torch.topk(scores.T, kmax, dim=1).indices.cpu().numpy())
+    exh = np.concatenate(exh)
+    log("recall: exhaustive MaxSim done")
+    targets = ref.query_targets
+    tp_policy = t_prime_policy(N)
+    rows = []
+    for b in (4, 2):
+        ix = Index.from_synthetic(data[b])
+        for nprobe in (1, 2, 4, 8, 16, 32, 64):
+            log(f"recall: b={b} nprobe={nprobe}")
+            for tp in sorted({1_000, 10_000, tp_policy, 100_000, 400_000}):
+                ids = ix.search(data[b].queries, nprobe, tp, kmax)[0]
+                r10 = np.mean([len(set(ids[i, :10]) & set(exh[i, :10])) / 10 for i in range(nq)])
+                r100 = np.mean([len(set(ids[i]) & set(exh[i])) / 100 for i in range(nq)])
+                s1 = float(np.mean(ids[:, 0] == targets))
+                s10 = float(np.mean([targets[i] in ids[i, :10] for i in range(nq)]))
+                rows.append({"b": b, "nprobe": nprobe, "t_prime": tp, "nrecall10": r10, "nrecall100": r100,
+                             "target_at_1": s1, "target_in_10": s10})
+        ix.close()
+    ex1 = float(np.mean(exh[:, 0] == targets))
+    print(f"| b | nprobe | t' | nRecall@10 | nRecall@100 | target at 1 | target in top 10 |")
+    print("|---|---|---|---|---|---|---|")
+    for r in rows:
+        print(f"| {r['b']} | {r['nprobe']} | {r['t_prime']:,} | {r['nrecall10']:.3f} | {r['nrecall100']:.3f} | "
+              f"{r['target_at_1']:.3f} | {r['target_in_10']:.3f} |")
+    print(f"\nquery noise {args.query_noise}: exhaustive MaxSim over the uncompressed vectors ranks the target "
+          f"first for {ex1:.3f} of {nq} queries; t' policy value {tp_policy:,}")
+    if args.recall_out:
+        with open(args.recall_out, "w") as f:
+            json.dump({"workload": describe(base), "rows": rows, "exhaustive_target_at_1": ex1,
+                       "t_prime_policy": tp_policy}, f)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -99,11 +177,19 @@ def main() -> int:
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the run, copy a buffer of this size 3 times on the device (a kernel of "
                          "known traffic to scale HBM counters against)")
+    ap.add_argument("--recall-study", action="store_true",
+                    help="instead of the benchmark, run the nprobe / t' / b recall study (Section 4.6)")
+    ap.add_argument("--recall-out", default="", help="JSON output of the recall study")
+    ap.add_argument("--query-noise", type=float, default=0.05,
+                    help="recall study: per-component noise of the query tokens around their document's tokens")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the search path has no multi-GPU mode (--gpus {args.gpus} "
               f"requested). Run with --gpus 1.", file=sys.stderr)
         return 2
+
+    if args.recall_study:
+        return recall_study(args)
 
     import torch
 
