@@ -59,6 +59,14 @@ enum {
 
 typedef struct warp_index warp_index; /* opaque; owns all of its device memory */
 
+/* Scoring modes (warp_set_scoring). */
+enum {
+    WARP_SCORING_PAPER = 0,      /* Section 4.5: a missing (token, document) entry takes m_i */
+    WARP_SCORING_EQ1_LITERAL = 1 /* Eq. 1 read literally: a retrieved entry is also raised to m_i
+                                    while some of the document's embeddings were not retrieved for
+                                    that query token */
+};
+
 /* Number of fraction bits F of the fixed-point token and document scores (26). */
 int warp_fixed_point_bits(void);
 
@@ -172,6 +180,18 @@ int warp_search_debug(warp_index* idx, const float* queries, int32_t n_queries, 
  * scores and recomputes every centroid near a selection boundary in fp64.
  */
 int warp_centroid_filter_scores(warp_index* idx, const float* queries, int32_t n_tok, float* out);
+
+/*
+ * Scoring of a (query token, document) entry (Section 4.5 versus Eq. 1).
+ * WARP_SCORING_PAPER (the default) replaces only missing entries by m_i.
+ * WARP_SCORING_EQ1_LITERAL reads Eq. 1 literally: a document with a retrieved
+ * score v for query token i, but with some embeddings not retrieved for i (the
+ * retrieved count is below the document's number of embeddings), takes
+ * max(v, m_i). That mode keeps a second [tokens][documents] count table per wave
+ * and more device atomics. Applies to later searches on the index.
+ * WARP_EINVAL for an invalid handle or mode.
+ */
+int warp_set_scoring(warp_index* index, int32_t mode);
 
 /*
  * Per-stage device time, measured with HIP events on the stream each search

@@ -5,6 +5,6 @@ top-k) runs in hand-written HIP kernels behind the C ABI of include/warp.h;
 `warp` is its Python binding.
 """
 from .warp import (  # noqa: F401
-    EINVAL, EDEVICE, ENOMEM, ENOTSUP, EXPORTS, FRAC_BITS, STAGES, T_PRIME_C, T_PRIME_MAX, Index, WarpError,
-    last_error, lib, t_prime_policy,
+    EINVAL, EDEVICE, ENOMEM, ENOTSUP, EXPORTS, FRAC_BITS, SCORING_EQ1_LITERAL, SCORING_PAPER, STAGES, T_PRIME_C,
+    T_PRIME_MAX, Index, WarpError, last_error, lib, t_prime_policy,
 )

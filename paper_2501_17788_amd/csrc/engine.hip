@@ -67,6 +67,10 @@ struct warp_index {
     DevBuf filter, sel, base, seg_pref, m_fixed, tokmax, keys, qpart;
     DevBuf ccount, cursor, item_start, pair_start, plist, qdig, blk;
     int64_t tokmax_ready = 0;  // leading elements of tokmax holding kTokAbsent
+    int32_t scoring = WARP_SCORING_PAPER;
+    DevBuf tokcnt, doc_len;    // Eq.-1-literal scoring only
+    int64_t tokcnt_ready = 0;  // leading elements of tokcnt holding 0
+    bool doc_len_ready = false;
     // staging of the host-pointer calls
     DevBuf st_q, st_ids, st_scores, st_fixed, st_counts, st_sel, st_m, st_bitmap, st_scored;
     std::mutex lock;
@@ -303,6 +307,22 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P) {
         HIP_TRY(hipStreamSynchronize(idx->stream));
         idx->tokmax_ready = need;
     }
+    if (idx->scoring == WARP_SCORING_EQ1_LITERAL) {
+        if ((int64_t)(idx->tokcnt.bytes / 4) < need) {
+            rc = grow(idx->tokcnt, (size_t)need * 4);
+            if (rc) return rc;
+            idx->tokcnt_ready = 0;
+        }
+        if (!idx->doc_len_ready) {
+            rc = grow(idx->doc_len, (size_t)idx->n_docs * 4);
+            if (rc) return rc;
+            launch_doc_len(idx->doc_ids, idx->n_emb, (int32_t*)idx->doc_len.p, idx->n_docs, idx->stream);
+        }
+        if (idx->tokcnt_ready < need) launch_fill_i32((int32_t*)idx->tokcnt.p, need, 0, idx->stream);
+        HIP_TRY(hipStreamSynchronize(idx->stream));
+        idx->doc_len_ready = true;
+        idx->tokcnt_ready = need;
+    }
     return WARP_OK;
 }
 
@@ -323,8 +343,9 @@ int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T) {
         }
         budget = (size_t)(0.6 * (double)(free_b + held));
     }
-    const size_t per = (size_t)T * idx->n_docs * 4 + (size_t)idx->n_docs * 8 + (size_t)T * idx->n_c * 2 +
-                       (size_t)T * kMaxProbe * 32 + (size_t)T * 1024;
+    const size_t per = (size_t)T * idx->n_docs * (idx->scoring == WARP_SCORING_EQ1_LITERAL ? 8 : 4) +
+                       (size_t)idx->n_docs * 8 + (size_t)T * idx->n_c * 2 + (size_t)T * kMaxProbe * 32 +
+                       (size_t)T * 1024;
     int64_t qw = (int64_t)(budget / per);
     if (qw < 1) qw = 1;
     if (qw > n_queries) qw = n_queries;
@@ -401,6 +422,8 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         a.seg_pref = (int64_t*)idx->seg_pref.p;
         a.m_fixed = (int64_t*)idx->m_fixed.p;
         a.tokmax = (uint32_t*)idx->tokmax.p;
+        a.tokcnt = idx->scoring == WARP_SCORING_EQ1_LITERAL ? (uint32_t*)idx->tokcnt.p : nullptr;
+        a.doc_len = (const int32_t*)idx->doc_len.p;
         a.keys = (uint64_t*)idx->keys.p;
         a.qpart = (uint64_t*)idx->qpart.p;
         a.err = idx->err;
@@ -550,7 +573,7 @@ void warp_index_free(warp_index* idx) {
                         (void*)idx->codes, (void*)idx->weights, (void*)idx->err})
             if (p) (void)hipFree(p);
         for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_pref, &idx->m_fixed,
-                          &idx->tokmax, &idx->keys, &idx->qpart, &idx->ccount, &idx->cursor, &idx->item_start,
+                          &idx->tokmax, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount, &idx->cursor, &idx->item_start,
                           &idx->pair_start, &idx->plist, &idx->qdig, &idx->blk, &idx->st_q, &idx->st_ids, &idx->st_scores,
                           &idx->st_fixed, &idx->st_counts, &idx->st_sel, &idx->st_m, &idx->st_bitmap,
                           &idx->st_scored})
@@ -626,6 +649,15 @@ int warp_centroid_filter_scores(warp_index* idx, const float* queries, int32_t n
     release(q);
     release(f);
     return rc;
+}
+
+int warp_set_scoring(warp_index* idx, int32_t mode) {
+    if (!is_index(idx)) return fail(WARP_EINVAL, "invalid or freed index handle");
+    if (mode != WARP_SCORING_PAPER && mode != WARP_SCORING_EQ1_LITERAL)
+        return fail(WARP_EINVAL, "unknown scoring mode %d", mode);
+    std::lock_guard<std::mutex> g(idx->lock);
+    idx->scoring = mode;
+    return WARP_OK;
 }
 
 int warp_set_timing(warp_index* idx, int32_t enable) {

@@ -22,12 +22,21 @@ __global__ __launch_bounds__(256) void k_fold(WaveArgs a) {
         const int T = a.n_qtok;
         uint32_t* col = a.tokmax + (int64_t)q * T * a.n_docs + doc;
         const int64_t* m = a.m_fixed + (int64_t)q * T;
+        uint32_t* cnt = a.tokcnt ? a.tokcnt + (int64_t)q * T * a.n_docs + doc : nullptr;
+        const int32_t len = cnt ? a.doc_len[doc] : 0;
         for (int i = 0; i < T; ++i) {
             const uint32_t v = col[(int64_t)i * a.n_docs];
             if (v != kTokAbsent) {
                 any = true;
-                sum += (int32_t)(v ^ 0x80000000u);
+                int64_t t = (int32_t)(v ^ 0x80000000u);
                 col[(int64_t)i * a.n_docs] = kTokAbsent;
+                if (cnt) {
+                    // Eq. 1 read literally: while some of the document's tokens were not
+                    // retrieved for this query token, the estimate m_i bounds it from below
+                    if ((int32_t)cnt[(int64_t)i * a.n_docs] < len && t < m[i]) t = m[i];
+                    cnt[(int64_t)i * a.n_docs] = 0;
+                }
+                sum += t;
             } else {
                 sum += m[i];
             }

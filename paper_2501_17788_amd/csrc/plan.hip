@@ -69,4 +69,18 @@ void launch_check_queries(const float* q, int64_t n_tok, int32_t* err, hipStream
     hipLaunchKernelGGL(k_check_queries, dim3((unsigned)((n_tok + 3) / 4)), dim3(256), 0, s, q, n_tok, err);
 }
 
+__global__ void k_doc_len(const int32_t* ids, int64_t n, int32_t* doc_len) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) atomicAdd(&doc_len[ids[i]], 1);
+}
+
+// embeddings per document (doc ids were checked to lie in [0, n_docs) on load)
+void launch_doc_len(const int32_t* doc_ids, int64_t n, int32_t* doc_len, int32_t n_docs, hipStream_t s) {
+    launch_fill_i32(doc_len, n_docs, 0, s);
+    if (n <= 0) return;
+    int64_t blocks = (n + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    hipLaunchKernelGGL(k_doc_len, dim3((unsigned)blocks), dim3(256), 0, s, doc_ids, n, doc_len);
+}
+
 }  // namespace warp

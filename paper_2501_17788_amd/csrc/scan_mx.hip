@@ -151,6 +151,7 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
     __shared__ unsigned s_tab[kMxGroup * TPAD];  // max score of (token, document run of the chunk)
     __shared__ int s_run[kMxChunk];          // run of each chunk embedding
     __shared__ int s_rdoc[kMxChunk];         // document of each run
+    __shared__ int s_rstart[kMxChunk];       // its first embedding in the chunk
     __shared__ int s_wruns[NW];              // runs starting in each wave's quarter of the chunk
     __shared__ unsigned s_wd[NBITS == 8 ? 256 : 1];  // b = 8: the three digits of Q(omega[v]) in bytes 0..2
 
@@ -232,7 +233,10 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
         }
         if (e_in) {
             s_run[tid] = run;
-            if (start) s_rdoc[run] = doc;
+            if (start) {
+                s_rdoc[run] = doc;
+                s_rstart[run] = tid;
+            }
         }
         __syncthreads();
 
@@ -353,6 +357,10 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
             const unsigned v = s_tab[tk * TPAD + rn];
             s_tab[tk * TPAD + rn] = kTokAbsent;
             atomicMax(&tokmax[s_row[tk] + s_rdoc[rn]], v);
+            if (a.tokcnt) {  // Eq.-1-literal scoring: embeddings of the run retrieved for the token
+                const int len = (rn + 1 < n_runs ? s_rstart[rn + 1] : (int)(it.e1 - it.e0)) - s_rstart[rn];
+                atomicAdd(&a.tokcnt[s_row[tk] + s_rdoc[rn]], (unsigned)len);
+            }
         }
     }
 }

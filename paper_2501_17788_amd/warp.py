@@ -19,12 +19,13 @@ LIB_PATH = os.path.join(_PKG, "libwarp.so")
 OK, EINVAL, ENOMEM, EDEVICE, ENOTSUP = 0, -1, -2, -3, -4
 _NAMES = {EINVAL: "EINVAL", ENOMEM: "ENOMEM", EDEVICE: "EDEVICE", ENOTSUP: "ENOTSUP"}
 STAGES = ("filter_gemm", "select", "plan", "scan", "fold", "topk")
+SCORING_PAPER, SCORING_EQ1_LITERAL = 0, 1  # warp_set_scoring modes
 
 EXPORTS = (
     "warp_fixed_point_bits", "warp_last_error", "warp_index_load", "warp_index_load_device",
     "warp_index_free", "warp_index_info", "warp_search", "warp_search_async", "warp_index_sync",
     "warp_search_debug", "warp_centroid_filter_scores", "warp_set_timing", "warp_stage_timings",
-    "warp_t_prime_policy",
+    "warp_t_prime_policy", "warp_set_scoring",
 )
 
 
@@ -62,6 +63,7 @@ def _load() -> ctypes.CDLL:
         "warp_set_timing": ([P, i32], ctypes.c_int),
         "warp_stage_timings": ([P, P, P, i32], ctypes.c_int),
         "warp_t_prime_policy": ([i64, ctypes.c_double, i64, P], ctypes.c_int),
+        "warp_set_scoring": ([P, i32], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -255,6 +257,10 @@ class Index:
         out = np.empty((T.shape[0], self.n_centroids), np.float32)
         _check(lib.warp_centroid_filter_scores(self._h, _ptr(T), T.shape[0], _ptr(out)))
         return out
+
+    def set_scoring(self, mode: int) -> None:
+        """SCORING_PAPER (Section 4.5, the default) or SCORING_EQ1_LITERAL (Eq. 1 read literally)."""
+        _check(lib.warp_set_scoring(self._h, int(mode)))
 
     def set_timing(self, enable: bool) -> None:
         _check(lib.warp_set_timing(self._h, 1 if enable else 0))

@@ -40,7 +40,7 @@ def compare(got: dict, want: dict, rows=None, label=""):
     np.testing.assert_array_equal(g, want["scores"])
 
 
-def run_both(data, queries=None, nprobe=None, t_prime=None, k=None, label=""):
+def run_both(data, queries=None, nprobe=None, t_prime=None, k=None, label="", literal=False):
     w = _engine()
     wl = data.workload
     Q = data.queries if queries is None else queries
@@ -48,10 +48,13 @@ def run_both(data, queries=None, nprobe=None, t_prime=None, k=None, label=""):
     t_prime = wl.t_prime if t_prime is None else t_prime
     k = wl.k if k is None else k
     say(f"[{label}] n_emb={data.n_embeddings} n_c={len(data.offsets) - 1} nbits={data.nbits} "
-        f"queries={Q.shape} nprobe={nprobe} t'={t_prime} k={k}")
+        f"queries={Q.shape} nprobe={nprobe} t'={t_prime} k={k} literal={literal}")
     with w.Index.from_synthetic(data) as ix:
+        if literal:
+            ix.set_scoring(w.SCORING_EQ1_LITERAL)
         got = ix.search_debug(Q, nprobe, t_prime, k)
-    want = oracle.search_index(data, queries=Q, nprobe=nprobe, t_prime=t_prime, k=k)
+    want = oracle.search_index(data, queries=Q, nprobe=nprobe, t_prime=t_prime, k=k,
+                               flags=oracle.EQ1_LITERAL if literal else 0)
     compare(got, want, label=label)
     return got
 
@@ -282,3 +285,42 @@ def test_small_workload_sampled_queries(small_data):
     hit = (got["ids"][:, 0] == data.query_targets).mean()
     say(f"[small] target doc ranked first for {hit:.1%} of queries; mean scored/query "
         f"{got['n_scored'].mean():.3g}")
+
+
+# ----------------------------------------------------------------------------- Eq. 1 literal
+
+LITERAL_CASES = [
+    # seed, n_centroids, n_docs, max_len, nbits, nprobe, t_prime, k: short documents and many probes
+    # make fully retrieved documents common, so both branches of the literal rule occur
+    (20, 12, 200, 4, 4, 6, 50, 40),
+    (21, 30, 500, 6, 2, 10, 200, 60),
+    (22, 64, 1000, 12, 4, 32, 1000, 100),
+    (23, 8, 100, 3, 1, 8, 0, 30),   # every cluster probed: every candidate fully retrieved
+]
+
+
+@pytest.mark.parametrize("case", LITERAL_CASES, ids=[f"seed{c[0]}" for c in LITERAL_CASES])
+def test_eq1_literal_scoring(case):
+    seed, n_c, n_docs, max_len, nbits, nprobe, tp, k = case
+    wl = synth.random_small_workload(seed, n_centroids=n_c, n_docs=n_docs, max_len=max_len, nbits=nbits,
+                                     n_queries=4, n_qtok=32, nprobe=nprobe, t_prime=tp, k=k)
+    data = synth.make_index(wl, workers=1)
+    lit = run_both(data, label=f"literal seed {seed}", literal=True)
+    paper = run_both(data, label=f"paper seed {seed}")
+    if seed != 23:  # with partial retrieval the two readings must differ somewhere
+        assert not np.array_equal(lit["fixed"], paper["fixed"])
+
+
+def test_eq1_literal_tiny_and_switch_back():
+    data = synth.make_index(synth.with_overrides(synth.WORKLOADS["tiny"], n_queries=3, nprobe=64, k=50),
+                            workers=1)
+    w = _engine()
+    with w.Index.from_synthetic(data) as ix:
+        ix.set_scoring(w.SCORING_EQ1_LITERAL)
+        compare(ix.search_debug(data.queries, 64, 10_000, 50),
+                oracle.search_index(data, k=50, flags=oracle.EQ1_LITERAL), label="tiny literal")
+        ix.set_scoring(w.SCORING_PAPER)
+        compare(ix.search_debug(data.queries, 64, 10_000, 50), oracle.search_index(data, k=50),
+                label="tiny paper after literal")
+        with pytest.raises(w.WarpError):
+            ix.set_scoring(7)
