@@ -182,6 +182,43 @@ int warp_search_debug(warp_index* idx, const float* queries, int32_t n_queries, 
 int warp_centroid_filter_scores(warp_index* idx, const float* queries, int32_t n_tok, float* out);
 
 /*
+ * Index construction on the device (Section 4.1): k-means on a sample of the
+ * token embeddings, then every token encoded as a b-bit quantised residual to
+ * its nearest centroid. Every pointer is device memory; the call blocks.
+ *
+ *   tokens           [n_tokens][128] fp32, finite, norm <= 1 + 1e-3
+ *   token_docs       [n_tokens] document id of each token, in [0, n_docs)
+ *   init_centroids   [n_centroids][128] fp32 starting centroids, unit norm
+ *   sample_ids       [n_sample] token ids (in [0, n_tokens)) used by k-means; Section
+ *                    4.1 samples passages in proportion to the square root of the
+ *                    collection size (the caller's choice)
+ *   iterations       k-means steps (assign the sample, then recompute every centroid)
+ *   n_quant          the residuals of tokens [0, n_quant) fit the quantile buckets
+ * Outputs (caller-allocated, device):
+ *   centroids        [n_centroids][128] fp32
+ *   cluster_offsets  [n_centroids + 1]
+ *   doc_ids          [n_tokens] and codes [n_tokens][16 * nbits]: the embeddings grouped by
+ *                    cluster, in input order inside a cluster (the layout warp_index_load takes)
+ *   bucket_weights   [2^nbits], bucket_cutoffs [2^nbits - 1] fp32
+ *   assignment       [n_tokens] cluster of each input token, or null
+ * Definitions (exact; the result does not depend on the order of evaluation):
+ *   assignment = argmax_c S64(c, x), lowest id on ties (S64: fp64 dot product in
+ *   dimension order); a k-means step replaces a centroid with a token by
+ *   normalise(sum of round(x * 2^30)) (int64 sums, fp64 norm, rounded to fp32) and
+ *   keeps a centroid without one; with r the fp32 residual components of the first
+ *   n_quant tokens (n values), the cutoff j (1 <= j < 2^b) is the ceil(n j / 2^b)-th
+ *   smallest and the weight j (0 <= j < 2^b) the ceil(n (2j + 1) / 2^(b+1))-th
+ *   smallest; a code is the number of cutoffs <= the residual component.
+ * WARP_EINVAL for an argument out of range, WARP_ENOTSUP if more than 1,024
+ * centroids score within 2.5 * 2^-13 of a token's best, WARP_ENOMEM, WARP_EDEVICE.
+ */
+int warp_build_index(const float* tokens, const int32_t* token_docs, int64_t n_tokens, int32_t n_docs,
+                     const float* init_centroids, int32_t n_centroids, const int64_t* sample_ids,
+                     int64_t n_sample, int32_t iterations, int32_t nbits, int64_t n_quant, float* centroids,
+                     int64_t* cluster_offsets, int32_t* doc_ids, uint8_t* codes, float* bucket_weights,
+                     float* bucket_cutoffs, int32_t* assignment);
+
+/*
  * Scoring of a (query token, document) entry (Section 4.5 versus Eq. 1).
  * WARP_SCORING_PAPER (the default) replaces only missing entries by m_i.
  * WARP_SCORING_EQ1_LITERAL reads Eq. 1 literally: a document with a retrieved

@@ -48,6 +48,8 @@ def _load():
         lib.oracle_search.argtypes = [P, i32, i32, P, P, P, i32, P, i32, P, i32, i32, i32, i64, i32,
                                       i32, P, P, P, P, P, P, P, P, P, i32]
         lib.oracle_search.restype = ctypes.c_int
+        lib.oracle_build_index.argtypes = [P, P, i64, P, i32, P, i64, i32, i32, i64, P, P, P, P, P, P, P, i32]
+        lib.oracle_build_index.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -132,3 +134,30 @@ def search_index(idx, queries=None, nprobe=None, t_prime=None, k=None, **kw) -> 
                   idx.n_docs, idx.queries if queries is None else queries,
                   w.nprobe if nprobe is None else nprobe, w.t_prime if t_prime is None else t_prime,
                   w.k if k is None else k, **kw)
+
+
+def build_index(tokens, token_docs, init_centroids, sample_ids, iterations: int, nbits: int, n_quant: int,
+                threads: int = 0) -> dict:
+    """Section 4.1's index construction (oracle_build_index) on host arrays."""
+    X = _c(tokens, np.float32)
+    docs = _c(token_docs, np.int32)
+    C0 = _c(init_centroids, np.float32)
+    S = _c(sample_ids, np.int64)
+    n, n_c = X.shape[0], C0.shape[0]
+    nb = 1 << nbits
+    r = {
+        "centroids": np.empty((n_c, 128), np.float32),
+        "offsets": np.empty(n_c + 1, np.int64),
+        "doc_ids": np.empty(n, np.int32),
+        "codes": np.empty((n, 16 * nbits), np.uint8),
+        "weights": np.empty(nb, np.float32),
+        "cutoffs": np.empty(nb - 1, np.float32),
+        "assign": np.empty(n, np.int32),
+    }
+    rc = _load().oracle_build_index(
+        _ptr(X), _ptr(docs), n, _ptr(C0), n_c, _ptr(S), len(S), int(iterations), int(nbits), int(n_quant),
+        _ptr(r["centroids"]), _ptr(r["offsets"]), _ptr(r["doc_ids"]), _ptr(r["codes"]), _ptr(r["weights"]),
+        _ptr(r["cutoffs"]), _ptr(r["assign"]), int(threads))
+    if rc != 0:
+        raise ValueError("oracle_build_index rejected its arguments")
+    return r

@@ -270,3 +270,106 @@ int oracle_search(const float* centroids, int32_t n_c, int32_t dim, const int64_
     free(doc_len);
     return 0;
 }
+
+/* ------------------------------------------------------------------ index construction (Section 4.1) */
+
+static int32_t nearest(const float* C, int32_t n_c, const float* x) {
+    int32_t best = 0;
+    double bs = 0.0;
+    for (int32_t c = 0; c < n_c; ++c) {
+        double s = 0.0;
+        for (int d = 0; d < ORACLE_DIM; ++d) s += (double)C[(int64_t)c * ORACLE_DIM + d] * (double)x[d];
+        if (c == 0 || s > bs) {
+            bs = s;
+            best = c;
+        }
+    }
+    return best;
+}
+
+static int by_float(const void* a, const void* b) {
+    float x = *(const float*)a, y = *(const float*)b;
+    return (x > y) - (x < y);
+}
+
+int oracle_build_index(const float* tokens, const int32_t* token_docs, int64_t n, const float* init,
+                       int32_t n_c, const int64_t* sample, int64_t n_sample, int32_t iterations,
+                       int32_t nbits, int64_t n_quant, float* centroids, int64_t* offsets,
+                       int32_t* doc_ids, uint8_t* codes, float* weights, float* cutoffs,
+                       int32_t* assign, int32_t n_threads) {
+    const int D = ORACLE_DIM;
+    if (n < 1 || n_c < 1 || n_sample < 1 || iterations < 0 || n_quant < 1 || n_quant > n) return -1;
+    if (nbits != 1 && nbits != 2 && nbits != 4 && nbits != 8) return -1;
+    if (n_threads > 0) omp_set_num_threads(n_threads);
+    memcpy(centroids, init, sizeof(float) * (size_t)n_c * D);
+
+    /* k-means on the sample */
+    int32_t* sa = (int32_t*)malloc(sizeof(int32_t) * (size_t)n_sample);
+    int64_t* sums = (int64_t*)malloc(sizeof(int64_t) * (size_t)n_c * D);
+    int64_t* cnt = (int64_t*)malloc(sizeof(int64_t) * (size_t)n_c);
+    for (int32_t it = 0; it < iterations; ++it) {
+#pragma omp parallel for schedule(dynamic, 64)
+        for (int64_t i = 0; i < n_sample; ++i) sa[i] = nearest(centroids, n_c, tokens + sample[i] * D);
+        memset(sums, 0, sizeof(int64_t) * (size_t)n_c * D);
+        memset(cnt, 0, sizeof(int64_t) * (size_t)n_c);
+        for (int64_t i = 0; i < n_sample; ++i) {
+            const float* x = tokens + sample[i] * D;
+            cnt[sa[i]] += 1;
+            for (int d = 0; d < D; ++d) sums[(int64_t)sa[i] * D + d] += (int64_t)nearbyint(ldexp((double)x[d], 30));
+        }
+        for (int32_t c = 0; c < n_c; ++c) {
+            if (cnt[c] == 0) continue;
+            double ss = 0.0;
+            for (int d = 0; d < D; ++d) ss += (double)sums[(int64_t)c * D + d] * (double)sums[(int64_t)c * D + d];
+            if (!(ss > 0.0)) continue;
+            double norm = sqrt(ss);
+            for (int d = 0; d < D; ++d) centroids[(int64_t)c * D + d] = (float)((double)sums[(int64_t)c * D + d] / norm);
+        }
+    }
+    free(sa);
+    free(sums);
+    free(cnt);
+
+    /* every token to its nearest centroid */
+#pragma omp parallel for schedule(dynamic, 256)
+    for (int64_t t = 0; t < n; ++t) assign[t] = nearest(centroids, n_c, tokens + t * D);
+
+    /* quantile buckets from the residual components of tokens [0, n_quant) */
+    const int64_t m = n_quant * D;
+    float* r = (float*)malloc(sizeof(float) * (size_t)m);
+    for (int64_t t = 0; t < n_quant; ++t)
+        for (int d = 0; d < D; ++d) r[t * D + d] = tokens[t * D + d] - centroids[(int64_t)assign[t] * D + d];
+    qsort(r, (size_t)m, sizeof(float), by_float);
+    const int nb = 1 << nbits;
+    for (int j = 1; j < nb; ++j) {
+        int64_t k = (m * j + nb - 1) / nb; /* ceil(m j / 2^b) */
+        cutoffs[j - 1] = r[(k < 1 ? 1 : k) - 1];
+    }
+    for (int j = 0; j < nb; ++j) {
+        int64_t k = (m * (2 * j + 1) + 2 * nb - 1) / (2 * nb); /* ceil(m (2j+1) / 2^(b+1)) */
+        weights[j] = r[(k < 1 ? 1 : k) - 1];
+    }
+    free(r);
+
+    /* grouping by cluster (stable) and codes */
+    int64_t* cur = (int64_t*)calloc((size_t)n_c + 1, sizeof(int64_t));
+    for (int64_t t = 0; t < n; ++t) cur[assign[t] + 1] += 1;
+    for (int32_t c = 0; c < n_c; ++c) cur[c + 1] += cur[c];
+    memcpy(offsets, cur, sizeof(int64_t) * ((size_t)n_c + 1));
+    const int64_t row_bytes = (int64_t)D * nbits / 8;
+    const int per_byte = 8 / nbits;
+    for (int64_t t = 0; t < n; ++t) {
+        int64_t p = cur[assign[t]]++;
+        doc_ids[p] = token_docs[t];
+        uint8_t* row = codes + p * row_bytes;
+        memset(row, 0, (size_t)row_bytes);
+        for (int d = 0; d < D; ++d) {
+            float x = tokens[t * D + d] - centroids[(int64_t)assign[t] * D + d];
+            int code = 0;
+            for (int j = 0; j < nb - 1; ++j) code += cutoffs[j] <= x;
+            row[d / per_byte] |= (uint8_t)(code << (8 - nbits * (d % per_byte + 1)));
+        }
+    }
+    free(cur);
+    return 0;
+}

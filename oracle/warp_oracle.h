@@ -27,6 +27,7 @@ extern "C" {
 #endif
 
 #define ORACLE_FRAC_BITS 26
+#define ORACLE_DIM 128  /* token dimension of the index construction */
 #define ORACLE_PROD_BITS 22
 
 /* flags for oracle_search */
@@ -67,6 +68,25 @@ int oracle_search(const float* centroids, int32_t n_c, int32_t dim,
                   int32_t* out_ids, int64_t* out_fixed, float* out_scores, int32_t* out_counts,
                   int32_t* sel, int64_t* m_fixed, uint32_t* cand_bitmap, int64_t* n_scored,
                   int64_t* doc_fixed, int32_t n_threads);
+
+/* Section 4.1 (index construction), written out plainly:
+ *   assign(x)   = argmax_c sum_d (double)C[c][d] * (double)x[d] (dimension order), lowest c on ties;
+ *   k-means     = `iterations` times: assign the sample tokens, then replace every centroid that
+ *                 has tokens by normalise(sum over them of round(x * 2^30)) (int64 sums, fp64
+ *                 norm in dimension order, rounded to fp32);
+ *   quantiles   = of the n fp32 residual components x - C[assign(x)] of tokens [0, n_quant):
+ *                 cutoff j (1 <= j < 2^b) = ceil(n j / 2^b)-th smallest,
+ *                 weight j (0 <= j < 2^b) = ceil(n (2j+1) / 2^(b+1))-th smallest;
+ *   codes       = per dimension the number of cutoffs <= the residual component, packed with the
+ *                 first dimension in the most significant bits;
+ *   layout      = embeddings grouped by cluster (offsets), input order inside a cluster.
+ * Outputs: centroids [n_c][128], offsets [n_c+1], doc_ids [n], codes [n][16b], weights [2^b],
+ * cutoffs [2^b - 1], assign [n]. Returns 0, or -1 on a bad argument. */
+int oracle_build_index(const float* tokens, const int32_t* token_docs, int64_t n, const float* init,
+                       int32_t n_c, const int64_t* sample, int64_t n_sample, int32_t iterations,
+                       int32_t nbits, int64_t n_quant, float* centroids, int64_t* offsets,
+                       int32_t* doc_ids, uint8_t* codes, float* weights, float* cutoffs,
+                       int32_t* assign, int32_t n_threads);
 
 #ifdef __cplusplus
 }

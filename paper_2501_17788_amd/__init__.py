@@ -6,5 +6,5 @@ top-k) runs in hand-written HIP kernels behind the C ABI of include/warp.h;
 """
 from .warp import (  # noqa: F401
     EINVAL, EDEVICE, ENOMEM, ENOTSUP, EXPORTS, FRAC_BITS, SCORING_EQ1_LITERAL, SCORING_PAPER, STAGES, T_PRIME_C,
-    T_PRIME_MAX, Index, WarpError, last_error, lib, t_prime_policy,
+    T_PRIME_MAX, Index, WarpError, build_index, initial_centroids, last_error, lib, sample_passages, t_prime_policy,
 )

@@ -113,4 +113,28 @@ void launch_check_docs(const int32_t* ids, int64_t n, int32_t n_docs, int32_t* e
 void launch_check_queries(const float* q, int64_t n_tok, int32_t* err, hipStream_t s);
 void launch_doc_len(const int32_t* doc_ids, int64_t n, int32_t* doc_len, int32_t n_docs, hipStream_t s);
 
+// index construction
+constexpr int kErrArgOverflow = 1 << 10;  // more than kArgCap centroids in one token's argmax band
+void launch_rows_argmax(const float* scores, int64_t n, int32_t n_c, const float* x, const float* cen,
+                        int32_t* assign, int32_t* err, hipStream_t s);
+void launch_gather_rows(const float* x, const int64_t* ids, int64_t n, float* out, hipStream_t s);
+void launch_kmeans_accum(const float* xs, const int32_t* assign, int64_t n, unsigned long long* sums,
+                         unsigned long long* counts, hipStream_t s);
+void launch_kmeans_normalize(const unsigned long long* sums, const unsigned long long* counts, int32_t n_c,
+                             float* cen, hipStream_t s);
+void launch_residuals(const float* x, const int32_t* assign, int64_t n, const float* cen, float* out,
+                      hipStream_t s);
+void launch_pick_quantiles(const float* sorted, int64_t n, int32_t nbits, float* cutoffs, float* weights,
+                           hipStream_t s);
+void launch_encode(int32_t nbits, const float* x, const int32_t* token_docs, const int32_t* assign,
+                   const int64_t* perm, int64_t n, const float* cen, const float* cutoffs, uint8_t* codes,
+                   int32_t* doc_ids, hipStream_t s);
+void launch_count_clusters(const int32_t* assign, int64_t n, unsigned long long* counts, hipStream_t s);
+void launch_iota64(int64_t* out, int64_t n, hipStream_t s);
+hipError_t sort_floats(void* temp, size_t* temp_bytes, const float* in, float* out, int64_t n, hipStream_t s);
+hipError_t sort_by_cluster(void* temp, size_t* temp_bytes, const int32_t* keys_in, int32_t* keys_out,
+                           const int64_t* vals_in, int64_t* vals_out, int64_t n, int end_bit, hipStream_t s);
+hipError_t exclusive_sum_u64(void* temp, size_t* temp_bytes, const unsigned long long* in, int64_t* out,
+                             int64_t n, hipStream_t s);
+
 }  // namespace warp

@@ -651,6 +651,145 @@ int warp_centroid_filter_scores(warp_index* idx, const float* queries, int32_t n
     return rc;
 }
 
+int warp_build_index(const float* tokens, const int32_t* token_docs, int64_t n_tokens, int32_t n_docs,
+                     const float* init_centroids, int32_t n_centroids, const int64_t* sample_ids, int64_t n_sample,
+                     int32_t iterations, int32_t nbits, int64_t n_quant, float* centroids, int64_t* cluster_offsets,
+                     int32_t* doc_ids, uint8_t* codes, float* bucket_weights, float* bucket_cutoffs,
+                     int32_t* assignment) {
+    if (!tokens || !token_docs || !init_centroids || !sample_ids || !centroids || !cluster_offsets || !doc_ids ||
+        !codes || !bucket_weights || !bucket_cutoffs)
+        return fail(WARP_EINVAL, "null pointer argument");
+    if (n_tokens < 1 || n_tokens > INT32_MAX / 2) return fail(WARP_EINVAL, "n_tokens must be in [1, 2^30]");
+    if (n_docs < 1 || n_docs > kMaxDocs) return fail(WARP_EINVAL, "n_docs must be in [1, 2^24]");
+    if (n_centroids < 1 || n_centroids > (1 << 24)) return fail(WARP_EINVAL, "n_centroids must be in [1, 2^24]");
+    if (nbits != 1 && nbits != 2 && nbits != 4 && nbits != 8)
+        return fail(WARP_EINVAL, "nbits must be 1, 2, 4 or 8 (got %d)", nbits);
+    if (iterations < 0 || iterations > 10000) return fail(WARP_EINVAL, "iterations must be in [0, 10000]");
+    if (n_sample < 1 || n_sample > (1 << 23)) return fail(WARP_EINVAL, "n_sample must be in [1, 2^23]");
+    if (n_quant < 1 || n_quant > n_tokens || n_quant > INT32_MAX / kDim)
+        return fail(WARP_EINVAL, "n_quant must be in [1, min(n_tokens, 2^24)]");
+    int rc = check_device();
+    if (rc) return rc;
+    const int64_t n_c = n_centroids;
+    // host checks of the small inputs
+    std::vector<float> hC((size_t)n_c * kDim);
+    std::vector<int64_t> hS((size_t)n_sample);
+    HIP_TRY(hipMemcpy(hC.data(), init_centroids, hC.size() * 4, hipMemcpyDefault));
+    HIP_TRY(hipMemcpy(hS.data(), sample_ids, hS.size() * 8, hipMemcpyDefault));
+    for (int64_t c = 0; c < n_c; ++c) {
+        double ss = 0;
+        for (int d = 0; d < kDim; ++d) {
+            const float v = hC[(size_t)c * kDim + d];
+            if (!std::isfinite(v)) return fail(WARP_EINVAL, "initial centroid %lld is not finite", (long long)c);
+            ss += (double)v * v;
+        }
+        if (std::fabs(std::sqrt(ss) - 1.0) > 1e-3)
+            return fail(WARP_EINVAL, "initial centroid %lld is not of unit norm", (long long)c);
+    }
+    for (int64_t i = 0; i < n_sample; ++i)
+        if (hS[i] < 0 || hS[i] >= n_tokens) return fail(WARP_EINVAL, "sample id %lld is out of range", (long long)i);
+
+    hipStream_t s = nullptr;
+    HIP_TRY(hipStreamCreateWithFlags(&s, hipStreamNonBlocking));
+    struct Scratch {
+        DevBuf err, assign, scores, xs, assign_s, sums, counts, resid, sorted, temp, perm_in, perm, keys;
+        ~Scratch() {
+            for (DevBuf* b : {&err, &assign, &scores, &xs, &assign_s, &sums, &counts, &resid, &sorted, &temp,
+                              &perm_in, &perm, &keys})
+                release(*b);
+        }
+    } w;
+    auto done = [&](int code) {
+        (void)hipStreamSynchronize(s);
+        (void)hipStreamDestroy(s);
+        return code;
+    };
+    const int64_t N = n_tokens;
+    const int64_t chunk = std::max<int64_t>(1, std::min<int64_t>(N, ((int64_t)1 << 31) / (n_c * 4)));
+    size_t tb = 0, t1 = 0, t2 = 0, t3 = 0;
+    if (!rc) rc = grow(w.err, 4);
+    if (!rc && !assignment) rc = grow(w.assign, (size_t)N * 4);
+    if (!rc) rc = grow(w.scores, (size_t)chunk * n_c * 4);
+    if (!rc) rc = grow(w.xs, (size_t)n_sample * kDim * 4);
+    if (!rc) rc = grow(w.assign_s, (size_t)n_sample * 4);
+    if (!rc) rc = grow(w.sums, (size_t)n_c * kDim * 8);
+    if (!rc) rc = grow(w.counts, ((size_t)n_c + 1) * 8);
+    if (!rc) rc = grow(w.resid, (size_t)n_quant * kDim * 4);
+    if (!rc) rc = grow(w.sorted, (size_t)n_quant * kDim * 4);
+    if (!rc) rc = grow(w.perm_in, (size_t)N * 8);
+    if (!rc) rc = grow(w.perm, (size_t)N * 8);
+    if (!rc) rc = grow(w.keys, (size_t)N * 4);
+    if (rc) return done(rc);
+    int end_bit = 1;
+    while (end_bit < 31 && ((int64_t)1 << end_bit) < n_c) ++end_bit;
+    if (sort_floats(nullptr, &t1, nullptr, nullptr, n_quant * kDim, s) != hipSuccess ||
+        sort_by_cluster(nullptr, &t2, nullptr, nullptr, nullptr, nullptr, N, end_bit, s) != hipSuccess ||
+        exclusive_sum_u64(nullptr, &t3, nullptr, nullptr, n_c + 1, s) != hipSuccess)
+        return done(fail(WARP_EDEVICE, "device primitive sizing failed"));
+    tb = std::max(t1, std::max(t2, t3));
+    rc = grow(w.temp, tb);
+    if (rc) return done(rc);
+    int32_t* err = (int32_t*)w.err.p;
+    int32_t* assign = assignment ? assignment : (int32_t*)w.assign.p;
+
+    // inputs: finite tokens of norm <= 1 + 1e-3, document ids in range
+    launch_fill_i32(err, 1, 0, s);
+    launch_check_queries(tokens, N, err, s);
+    launch_check_docs(token_docs, N, n_docs, err, s);
+    int32_t herr = 0;
+    HIP_TRY(hipMemcpyAsync(&herr, err, 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (herr & kErrQueryNorm) return done(fail(WARP_EINVAL, "a token is not finite or has norm > 1 + 1e-3"));
+    if (herr & kErrDocRange) return done(fail(WARP_EINVAL, "a token's document id is outside [0, n_docs)"));
+
+    HIP_TRY(hipMemcpyAsync(centroids, hC.data(), hC.size() * 4, hipMemcpyHostToDevice, s));
+    auto assign_rows = [&](const float* x, int64_t n, int32_t* out) {
+        for (int64_t t0 = 0; t0 < n; t0 += chunk) {
+            const int64_t nt = std::min(chunk, n - t0);
+            launch_filter_gemm(x + t0 * kDim, (int32_t)nt, centroids, n_centroids, nullptr, (float*)w.scores.p, s);
+            launch_rows_argmax((const float*)w.scores.p, nt, n_centroids, x + t0 * kDim, centroids, out + t0, err, s);
+        }
+    };
+    // k-means on the sample
+    float* xs = (float*)w.xs.p;
+    launch_gather_rows(tokens, sample_ids, n_sample, xs, s);
+    auto* sums = (unsigned long long*)w.sums.p;
+    auto* counts = (unsigned long long*)w.counts.p;
+    for (int it = 0; it < iterations; ++it) {
+        assign_rows(xs, n_sample, (int32_t*)w.assign_s.p);
+        launch_fill_i32((int32_t*)sums, n_c * kDim * 2, 0, s);
+        launch_fill_i32((int32_t*)counts, (n_c + 1) * 2, 0, s);
+        launch_kmeans_accum(xs, (const int32_t*)w.assign_s.p, n_sample, sums, counts, s);
+        launch_kmeans_normalize(sums, counts, n_centroids, centroids, s);
+    }
+    // every token to its nearest centroid; quantiles of the first n_quant tokens' residuals
+    assign_rows(tokens, N, assign);
+    launch_residuals(tokens, assign, n_quant, centroids, (float*)w.resid.p, s);
+    if (sort_floats(w.temp.p, &tb, (const float*)w.resid.p, (float*)w.sorted.p, n_quant * kDim, s) != hipSuccess)
+        return done(fail(WARP_EDEVICE, "residual sort failed"));
+    launch_pick_quantiles((const float*)w.sorted.p, n_quant * kDim, nbits, bucket_cutoffs, bucket_weights, s);
+    // embeddings grouped by cluster in input order, offsets, codes
+    launch_iota64((int64_t*)w.perm_in.p, N, s);
+    tb = w.temp.bytes;
+    if (sort_by_cluster(w.temp.p, &tb, assign, (int32_t*)w.keys.p, (const int64_t*)w.perm_in.p, (int64_t*)w.perm.p, N,
+                        end_bit, s) != hipSuccess)
+        return done(fail(WARP_EDEVICE, "cluster sort failed"));
+    launch_fill_i32((int32_t*)counts, (n_c + 1) * 2, 0, s);
+    launch_count_clusters(assign, N, counts, s);
+    tb = w.temp.bytes;
+    if (exclusive_sum_u64(w.temp.p, &tb, counts, cluster_offsets, n_c + 1, s) != hipSuccess)
+        return done(fail(WARP_EDEVICE, "offset scan failed"));
+    launch_encode(nbits, tokens, token_docs, assign, (const int64_t*)w.perm.p, N, centroids, bucket_cutoffs, codes,
+                  doc_ids, s);
+    HIP_TRY(hipMemcpyAsync(&herr, err, 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    const hipError_t le = hipGetLastError();
+    if (le != hipSuccess) return done(fail(WARP_EDEVICE, "index build failed: %s", hipGetErrorString(le)));
+    if (herr & kErrArgOverflow)
+        return done(fail(WARP_ENOTSUP, "more than 1024 centroids tie within 2.5 * 2^-13 of a token's best score"));
+    return done(WARP_OK);
+}
+
 int warp_set_scoring(warp_index* idx, int32_t mode) {
     if (!is_index(idx)) return fail(WARP_EINVAL, "invalid or freed index handle");
     if (mode != WARP_SCORING_PAPER && mode != WARP_SCORING_EQ1_LITERAL)

@@ -25,7 +25,7 @@ EXPORTS = (
     "warp_fixed_point_bits", "warp_last_error", "warp_index_load", "warp_index_load_device",
     "warp_index_free", "warp_index_info", "warp_search", "warp_search_async", "warp_index_sync",
     "warp_search_debug", "warp_centroid_filter_scores", "warp_set_timing", "warp_stage_timings",
-    "warp_t_prime_policy", "warp_set_scoring",
+    "warp_t_prime_policy", "warp_set_scoring", "warp_build_index",
 )
 
 
@@ -64,6 +64,7 @@ def _load() -> ctypes.CDLL:
         "warp_stage_timings": ([P, P, P, i32], ctypes.c_int),
         "warp_t_prime_policy": ([i64, ctypes.c_double, i64, P], ctypes.c_int),
         "warp_set_scoring": ([P, i32], ctypes.c_int),
+        "warp_build_index": ([P, P, i64, i32, P, i32, P, i64, i32, i32, i64, P, P, P, P, P, P, P], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -270,3 +271,66 @@ class Index:
         n = np.zeros(len(STAGES), np.int64)
         _check(lib.warp_stage_timings(self._h, _ptr(ms), _ptr(n), len(STAGES)))
         return {s: (float(ms[i]), int(n[i])) for i, s in enumerate(STAGES)}
+
+
+# ----------------------------------------------------------------------------- index construction
+
+def sample_passages(doc_lengths, c: float = 16.0, seed: int = 0) -> np.ndarray:
+    """Token ids (document-major order) of ceil(c * sqrt(n_docs)) passages drawn without
+    replacement: Section 4.1 clusters a sample of passages whose size grows with the square
+    root of the collection."""
+    lens = np.asarray(doc_lengths, np.int64)
+    n_docs = len(lens)
+    k = min(n_docs, int(np.ceil(c * np.sqrt(n_docs))))
+    docs = np.sort(np.random.default_rng(seed).choice(n_docs, size=k, replace=False))
+    starts = np.zeros(n_docs + 1, np.int64)
+    np.cumsum(lens, out=starts[1:])
+    return np.concatenate([np.arange(starts[d], starts[d + 1]) for d in docs]).astype(np.int64)
+
+
+def initial_centroids(tokens, sample_ids, n_centroids: int, seed: int = 0) -> np.ndarray:
+    """n_centroids distinct sample tokens, normalised (the k-means starting point)."""
+    ids = np.asarray(sample_ids, np.int64)
+    if n_centroids > len(ids):
+        raise ValueError("more centroids than sampled tokens")
+    pick = np.random.default_rng(seed).choice(len(ids), size=n_centroids, replace=False)
+    X = tokens[ids[np.sort(pick)]]
+    X = np.asarray(X.cpu() if hasattr(X, "cpu") else X, np.float64)
+    return (X / np.linalg.norm(X, axis=1, keepdims=True)).astype(np.float32)
+
+
+def build_index(tokens, token_docs, n_docs: int, init_centroids, sample_ids, iterations: int, nbits: int,
+                n_quant: int) -> dict:
+    """Index construction on the device (warp_build_index): torch tensors in, torch tensors out.
+
+    tokens [n, 128] float32 and token_docs [n] int32 on the device; init_centroids
+    [n_c, 128] and sample_ids [n_sample] int64 on the device or host. Returns the index
+    arrays (centroids, offsets, doc_ids, codes, weights, cutoffs, assign) as device tensors.
+    """
+    import torch
+
+    dev = tokens.device
+    X = tokens.contiguous()
+    docs = token_docs.to(torch.int32).contiguous()
+    C0 = torch.as_tensor(init_centroids, dtype=torch.float32).to(dev).contiguous()
+    S = torch.as_tensor(sample_ids, dtype=torch.int64).to(dev).contiguous()
+    n, n_c = X.shape[0], C0.shape[0]
+    out = {
+        "centroids": torch.empty((n_c, 128), dtype=torch.float32, device=dev),
+        "offsets": torch.empty(n_c + 1, dtype=torch.int64, device=dev),
+        "doc_ids": torch.empty(n, dtype=torch.int32, device=dev),
+        "codes": torch.empty((n, 16 * nbits), dtype=torch.uint8, device=dev),
+        "weights": torch.empty(1 << nbits, dtype=torch.float32, device=dev),
+        "cutoffs": torch.empty((1 << nbits) - 1, dtype=torch.float32, device=dev),
+        "assign": torch.empty(n, dtype=torch.int32, device=dev),
+    }
+    torch.cuda.synchronize(dev)
+    _check(lib.warp_build_index(
+        _tptr(X), _tptr(docs), n, int(n_docs), _tptr(C0), n_c, _tptr(S), S.numel(), int(iterations), int(nbits),
+        int(n_quant), _tptr(out["centroids"]), _tptr(out["offsets"]), _tptr(out["doc_ids"]), _tptr(out["codes"]),
+        _tptr(out["weights"]), _tptr(out["cutoffs"]), _tptr(out["assign"])))
+    return out
+
+
+def _tptr(t):
+    return ctypes.c_void_p(t.data_ptr())
