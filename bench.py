@@ -165,6 +165,46 @@ def recall_study(args) -> int:
     return 0
 
 
+def build_bench(args) -> int:
+    """Index construction on the device (Section 4.1) for the workload's tokens: k-means on a passage
+    sample proportional to sqrt(n_docs), assignment, quantiles, codes. Prints one JSON line."""
+    import torch
+
+    import synth
+    import paper_2501_17788_amd as w
+
+    wl = synth.with_overrides(synth.WORKLOADS[args.workload], nbits=args.build_nbits)
+    data = synth.make_index(wl, with_queries=True, workers=min(16, host_threads()))
+    lens = data.doc_lengths.astype(np.int64)
+    N = int(lens.sum())
+    t0 = time.time()
+    X = torch.from_numpy(synth.token_vectors(wl, np.arange(N))).cuda()
+    docs = torch.from_numpy(np.repeat(np.arange(len(lens)), lens).astype(np.int32)).cuda()
+    log(f"build: {N} tokens regenerated in {time.time() - t0:.1f} s")
+    sample = w.sample_passages(lens, c=16.0, seed=0)
+    C0 = w.initial_centroids(X, sample, wl.n_centroids, seed=0)
+    n_quant = min(N, 1 << 16)
+    times = {}
+    for it in (0, args.build_iterations):  # the difference isolates the k-means steps
+        torch.cuda.synchronize()
+        a = time.perf_counter()
+        built = w.build_index(X, docs, len(lens), C0, sample, it, wl.nbits, n_quant)
+        torch.cuda.synchronize()
+        times[it] = time.perf_counter() - a
+        log(f"build: {it} k-means steps: {times[it]:.2f} s")
+    with w.Index.from_device(built["centroids"], built["offsets"], built["doc_ids"], built["codes"], wl.nbits,
+                             built["weights"], len(lens)) as ix:
+        ids = ix.search(data.queries, wl.nprobe, wl.t_prime, wl.k)[0]
+    hit = float(np.mean(ids[:, 0] == data.query_targets))
+    rec = {"mode": "index construction", "workload": describe(wl), "n_tokens": N, "n_centroids": wl.n_centroids,
+           "sample_tokens": int(len(sample)), "iterations": args.build_iterations, "n_quant_tokens": n_quant,
+           "seconds_total": times[args.build_iterations], "seconds_without_kmeans": times[0],
+           "seconds_per_kmeans_step": (times[args.build_iterations] - times[0]) / max(1, args.build_iterations),
+           "tokens_per_s_encode": N / times[0], "target_first_after_search": hit}
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -180,6 +220,9 @@ def main() -> int:
     ap.add_argument("--recall-study", action="store_true",
                     help="instead of the benchmark, run the nprobe / t' / b recall study (Section 4.6)")
     ap.add_argument("--recall-out", default="", help="JSON output of the recall study")
+    ap.add_argument("--build", action="store_true", help="instead of the benchmark, time index construction")
+    ap.add_argument("--build-iterations", type=int, default=8)
+    ap.add_argument("--build-nbits", type=int, default=4)
     ap.add_argument("--query-noise", type=float, default=0.05,
                     help="recall study: per-component noise of the query tokens around their document's tokens")
     args = ap.parse_args()
@@ -190,6 +233,8 @@ def main() -> int:
 
     if args.recall_study:
         return recall_study(args)
+    if args.build:
+        return build_bench(args)
 
     import torch
 
