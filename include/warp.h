@@ -20,7 +20,7 @@
  * warp_fixed_point_bits() fraction bits (R(x) = round-half-even(x * 2^F)).
  * The table entries of Section 4.4 are exact products of query values and
  * bucket weights quantised to 2^-22 (Q(x) = round-half-even(x * 2^22)):
- *   token score  t = R(S_{c,q_i}) + round-half-even(2^(F-44) * V),
+ *   token score  t = R(S_{c,q_i}) + floor(2^(F-44) * V + 1/2),
  *                V = sum_d Q(q_{i,d}) * Q(omega[code_d])                (int32)
  *   doc score    s = sum_i (max retrieved t, or R(m_i) if none)        (int64)
  * so every product, max and sum is exact and independent of the order of

@@ -95,14 +95,16 @@ static void build_lut(const float* q, int32_t dim, const float* w, int32_t nbits
 }
 
 /* selective sum: one table entry per dimension, summed exactly, then rounded once to
- * the 2^-26 grid and added to the centroid term */
+ * the 2^-26 grid (halves upward) and added to the centroid term */
 static int64_t token_score(const int64_t* lut, int32_t dim, int32_t nbits, int64_t centroid_term,
                            const uint8_t* row) {
     int nb = 1 << nbits;
     int64_t v = 0;
     for (int32_t d = 0; d < dim; ++d) v += lut[d * nb + code_at(row, nbits, d)];
-    /* |v| < 2^53, so the scaling below is exact and nearbyint rounds half to even */
-    return centroid_term + (int64_t)nearbyint(ldexp((double)v, ORACLE_FRAC_BITS - 2 * ORACLE_PROD_BITS));
+    /* |v| < 2^52, so v + 2^17 and its scaling by 2^-18 are exact in fp64, and
+     * floor(x + 1/2) rounds x to the nearest integer, halves upward */
+    const int shift = 2 * ORACLE_PROD_BITS - ORACLE_FRAC_BITS;
+    return centroid_term + (int64_t)floor(ldexp((double)v + ldexp(1.0, shift - 1), -shift));
 }
 
 void oracle_token_scores(const float* q, int32_t dim, double centroid_score, const uint8_t* codes,

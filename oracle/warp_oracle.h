@@ -13,7 +13,8 @@
  *   - Q(x) = round-half-even(x * 2^22): query values and bucket weights quantised
  *     to 2^-22; the selective sum V = sum_d Q(q[d]) * Q(w[code_d]) is an exact
  *     integer in units of 2^-44 (|V| < 2^53);
- *   - token score t = R(S64) + round-half-even(V * 2^-18) (int32, units of 2^-26);
+ *   - token score t = R(S64) + floor(V * 2^-18 + 1/2) (int32, units of 2^-26): the
+ *     residual term is rounded to nearest with halves upward;
  *   - document score = sum over query tokens of (token max, else R(m_i)) (int64);
  *   - reported score = (float)(score * 2^-26).
  */

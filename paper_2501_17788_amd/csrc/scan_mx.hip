@@ -5,27 +5,31 @@
 // Arithmetic. With Q(x) = round-half-even(x * 2^22), the residual part of the
 // score of query token i against embedding e is the exact integer
 //     V = sum_d Q(q_{i,d}) * Q(omega[code_{e,d}])            (units of 2^-44)
-// and the token score is t = R(S64[i][c]) + round-half-even(V * 2^-18), an int32
-// in units of 2^-26. Both factors lie in [-8421504, 8355711] (|q_d| <= 1 + 1e-3
+// and the token score is t = R(S64[i][c]) + floor(V * 2^-18 + 1/2), an int32 in
+// units of 2^-26. Both factors lie in [-8421504, 8355711] (|q_d| <= 1 + 1e-3
 // and |omega| <= 1.99 are checked on entry), so each is three signed base-256
 // digits x = x2 2^16 + x1 2^8 + x0 with x_j in [-128, 127], and
 //     V = sum_s 2^(8 s) A_s,   A_s = sum_{i + j = s} sum_d qdig_i[d] * wdig_j[d]
 // for s = 0..4. Every A_s is an int8 matrix product over d, computed by
-// v_mfma_i32_16x16x64_i8 with embedding digits as rows and query digits as
-// columns (|A_s| <= 3 * 128 * 2^14 < 2^23: no overflow), and mx_round recombines
-// the five class sums and rounds in int32 without loss. The result does not
-// depend on the order of any summation, so it equals the CPU definition bit for bit.
+// v_mfma_i32_16x16x64_i8 with query digits as rows and embedding digits as
+// columns (|A_s| <= 3 * 128 * 2^14 < 2^23: no overflow). The accumulators start
+// from the rounding half and the token's centroid term, and mx_fold turns the
+// five class sums into the biased token score in int32 without loss. No result
+// depends on the order of a summation, so the scan equals the CPU definition bit
+// for bit.
 //
 // Work. A work item is (cluster, chunk of kMxChunk embeddings, group of up to
 // kMxGroup probing tokens); a persistent workgroup of four waves walks a
-// contiguous range of items. Per item, the query digit planes of the group are
-// staged in LDS in operand order; each wave takes 16-embedding tiles of the
-// chunk, decodes their codes into weight digits in registers (v_perm_b32 lookups
-// in a 16-byte table per digit plane), and runs the 18 MFMAs of every 16-token
-// tile of the group, query digits as rows and weight digits as columns, so that
-// each 16-lane row of the result holds four tokens against the tile's 16
-// embeddings: a DPP segmented max along the row merges runs of equal document
-// ids, and the run's last lane issues one atomicMax into the token-max table.
+// contiguous range of items and loads the next item's data while it scores the
+// current one. Per item, the query digit planes of the group are staged in LDS in
+// operand order and the runs of equal document ids along the chunk are numbered.
+// Each wave takes 16-embedding tiles of the chunk, decodes their codes into
+// weight digits in registers (v_perm_b32 lookups in 16-byte digit tables, or a
+// 256-entry LDS table at b = 8) and runs the 18 MFMAs of every 16-token tile of
+// the group, so that each 16-lane row of the result holds four tokens against the
+// tile's 16 embeddings. Every score goes into an LDS table of (token, run) maxima
+// by an LDS atomic max; at the end of the item the table is flushed with one
+// device atomicMax per (token, run) into the token-max table.
 #include "engine.h"
 
 namespace warp {
@@ -43,20 +47,17 @@ __device__ __forceinline__ void digits3(int x, int& d0, int& d1, int& d2) {
     d2 = (x - d1) >> 8;
 }
 
-// round-half-even((A0 + 2^8 A1 + 2^16 A2 + 2^24 A3 + 2^32 A4) / 2^18) in int32.
-// Writing A2 = 4 alpha + rho and N = A0 + 2^8 A1 + 2^16 rho = 2^18 beta + f with
-// 0 <= f < 2^18 gives V = 2^18 (2^14 A4 + 2^6 A3 + alpha + beta) + f. N fits in
-// int32 (|A1| <= 2^22), and the floor term is exact modulo 2^32, hence exact,
-// since the rounded score itself fits in int32.
-__device__ __forceinline__ int mx_round(int a0, int a1, int a2, int a3, int a4) {
-    const unsigned m = (unsigned)a0 + ((unsigned)a1 << 8);
-    const int alpha = a2 >> 2;
-    const unsigned rho = (unsigned)a2 & 3u;
-    const int n = (int)(m + (rho << 16));
-    const int beta = n >> 18;
-    const unsigned f = (unsigned)n & 0x3FFFFu;
-    const unsigned fl = ((unsigned)a4 << 14) + ((unsigned)a3 << 6) + (unsigned)alpha + (unsigned)beta;
-    return (int)(fl + ((f + (fl & 1u)) > 0x20000u ? 1u : 0u));
+// floor((a0 + 2^8 a1 + 2^16 a2 + 2^24 a3 + 2^32 a4) / 2^18) modulo 2^32. Writing
+// a2 = 4 alpha + rho (0 <= rho < 4) and n = a0 + 2^8 a1 + 2^16 rho, the quotient is
+// 2^14 a4 + 2^6 a3 + alpha + floor(n / 2^18); n fits in int32 for |a0| <= 2^22 and
+// |a1| <= 2^22, and the other terms are exact modulo 2^32. The scan seeds the class
+// accumulators so that this one expression is the rounded token score plus its bias:
+// a0 = A0 + 2^17 (round half up), and with the biased centroid term split as
+// 2^14 h + 2^6 m + l (0 <= m < 2^8, 0 <= l < 2^6), a2 = A2 + 4 l, a3 = A3 + m, a4 = A4 + h.
+// The result is below 2^32, hence exact.
+__device__ __forceinline__ unsigned mx_fold(int a0, int a1, int a2, int a3, int a4) {
+    const int n = (int)((unsigned)a0 + ((unsigned)a1 << 8) + (((unsigned)a2 & 3u) << 16));
+    return ((unsigned)a4 << 14) + ((unsigned)a3 << 6) + (unsigned)(a2 >> 2) + (unsigned)(n >> 18);
 }
 
 // Operand slot of dimension d: lane group g = d / 32 of the 16 x 64 operands,
@@ -115,18 +116,26 @@ struct MxItem {
     int p0, np;   // pairs [p0, p0 + np) of the token group
 };
 
+// A wave-uniform load of the work plan through the scalar cache. The plan is read-only
+// here (earlier kernels wrote it), and scalar loads are waited for on their own counter,
+// so reading it never waits for the vector loads and atomics in flight.
+template <typename T>
+__device__ __forceinline__ T plan_load(const T* p, int64_t i) {
+    return ((const __attribute__((address_space(4))) T*)p)[i];
+}
+
 __device__ __forceinline__ MxItem mx_decode(const WaveArgs& a, int64_t item, int c) {
     MxItem it;
-    const int nt = a.ccount[c];
-    const int groups = (nt + kMxGroup - 1) / kMxGroup;
-    const int64_t l = item - a.item_start[c];
-    const int64_t chunk = l / groups;
+    const int nt = plan_load(a.ccount, c);
+    const unsigned groups = (unsigned)(nt + kMxGroup - 1) / kMxGroup;
+    const unsigned l = (unsigned)(item - plan_load(a.item_start, c));  // below 2^31: chunks x groups
+    const unsigned chunk = l / groups;
     const int grp = (int)(l - chunk * groups);
     it.c = c;
-    it.e0 = a.offsets[c] + chunk * kMxChunk;
-    const int64_t end = a.offsets[c + 1];
+    it.e0 = plan_load(a.offsets, c) + (int64_t)chunk * kMxChunk;
+    const int64_t end = plan_load(a.offsets, c + 1);
     it.e1 = it.e0 + kMxChunk < end ? it.e0 + kMxChunk : end;
-    it.p0 = a.pair_start[c] + grp * kMxGroup;
+    it.p0 = plan_load(a.pair_start, c) + grp * kMxGroup;
     it.np = nt - grp * kMxGroup < kMxGroup ? nt - grp * kMxGroup : kMxGroup;
     return it;
 }
@@ -134,19 +143,36 @@ __device__ __forceinline__ MxItem mx_decode(const WaveArgs& a, int64_t item, int
 // Token-max cells hold t + 2^31 as unsigned (order preserving; 0 = absent).
 __device__ __forceinline__ unsigned bias(int t) { return (unsigned)t ^ 0x80000000u; }
 
+// Registers that carry an item's global data from its prefetch, one item ahead,
+// to its staging in LDS.
+template <int QPT>
+struct MxStage {
+    v4i q[QPT];     // query digit slots tid + kMxBlock i of the group
+    int tok, base;  // thread tid < kMxGroup: wave token and R(S64) of group token tid
+    int doc, prev;  // documents of chunk embeddings tid and tid - 1 (-1 outside the chunk)
+};
+
 template <int NBITS>
-__global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
+__global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
     constexpr int BYTES = kDim * NBITS / 8;  // code bytes per embedding
     constexpr int CW = NBITS;                // code words per lane: 32 dimensions of b bits
     constexpr int NSLOT = 24;                // (plane, slice, lane group) slots of 16 bytes
-    constexpr int TPAD = kMxChunk + 1;       // row of the run table, padded against bank conflicts
+    // row of the run table: the four token rows a lane group writes together start 16 banks
+    // apart; column kMxChunk takes the scores of tile rows past the chunk's end and is never read
+    constexpr int TPAD = kMxChunk + 4;
     constexpr int NW = kMxBlock / 64;
-    // the run pass gives each thread at most one embedding of the chunk, and the query
-    // staging splits evenly over the threads
+    constexpr int QPT = NSLOT * kMxGroup / kMxBlock;  // query slots staged per thread
+    constexpr int TPW = kMxChunk / (16 * NW);          // 16-embedding tiles per wave
+    // the run pass gives each thread at most one embedding of the chunk, the query staging
+    // splits evenly over the threads, and the waves split the tiles evenly
     static_assert(kMxChunk <= kMxBlock, "one thread per chunk embedding");
     static_assert(NSLOT * kMxGroup % kMxBlock == 0, "query staging");
+    static_assert(kMxChunk % (16 * NW) == 0, "tiles per wave");
     __shared__ v4i s_q[NSLOT][kMxGroup];     // query digit planes of the item's tokens
-    __shared__ __attribute__((aligned(16))) int s_base[kMxGroup];   // R(S64) + 2^31 of each token
+    // accumulator seeds of each token: R(S64) + 2^31 = 2^14 h + 2^6 m + l
+    __shared__ __attribute__((aligned(16))) int s_seed_h[kMxGroup];  // h
+    __shared__ __attribute__((aligned(16))) int s_seed_m[kMxGroup];  // m
+    __shared__ __attribute__((aligned(16))) int s_seed_l[kMxGroup];  // 4 l
     __shared__ __attribute__((aligned(16))) int64_t s_row[kMxGroup];  // its token-max row offset
     __shared__ unsigned s_tab[kMxGroup * TPAD];  // max score of (token, document run of the chunk)
     __shared__ int s_run[kMxChunk];          // run of each chunk embedding
@@ -180,7 +206,7 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
 
     const int n_c = a.n_c;
     const int64_t* item_start = a.item_start;
-    const int64_t total = item_start[n_c];
+    const int64_t total = plan_load(item_start, n_c);
     const int64_t G = gridDim.x;
     const int64_t first = total * blockIdx.x / G;
     const int64_t last = total * (blockIdx.x + 1) / G;
@@ -188,48 +214,110 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
     int lo = 0, hi = n_c;  // cluster of the first item: item_start[c] <= first < item_start[c + 1]
     while (hi - lo > 1) {
         const int mid = (lo + hi) >> 1;
-        if (item_start[mid] <= first) lo = mid;
+        if (plan_load(item_start, mid) <= first) lo = mid;
         else hi = mid;
     }
-    int c = lo;
+    int c = lo;  // cluster of the newest decoded item
     const v4i* qdig = reinterpret_cast<const v4i*>(a.qdig);
+    const int32_t* __restrict__ plist = a.plist;
     const uint8_t* __restrict__ codes = a.codes;
     const int32_t* __restrict__ doc_ids = a.doc_ids;
     unsigned* __restrict__ tokmax = a.tokmax;
     for (int i = tid; i < kMxGroup * TPAD; i += kMxBlock) s_tab[i] = kTokAbsent;
 
+    // the software pipeline: while item i is scored, the query digits, bases and documents of
+    // item i + 1 are in flight, its codes are loaded before item i's flush, and the wave
+    // tokens of item i + 2 (which address item i + 2's query digits) are loaded
+    auto load_tokens = [&](const MxItem& x, int (&ptok)[QPT]) {
+#pragma unroll
+        for (int i = 0; i < QPT; ++i) {
+            const int tk = (tid + kMxBlock * i) / NSLOT;
+            ptok[i] = tk < x.np ? plist[2 * (int64_t)(x.p0 + tk)] : -1;
+        }
+    };
+    auto load_stage = [&](const MxItem& x, const int (&ptok)[QPT], MxStage<QPT>& st) {
+#pragma unroll
+        for (int i = 0; i < QPT; ++i) {
+            const int slot = (tid + kMxBlock * i) % NSLOT;
+            st.q[i] = ptok[i] >= 0 ? qdig[(unsigned)(ptok[i] * NSLOT + slot)] : (v4i){0, 0, 0, 0};
+        }
+        const bool in = tid < x.np;
+        st.tok = in ? plist[2 * (int64_t)(x.p0 + tid)] : 0;
+        st.base = in ? plist[2 * (int64_t)(x.p0 + tid) + 1] : 0;
+        const int64_t e = x.e0 + tid;
+        st.doc = e < x.e1 ? doc_ids[e] : -1;
+        st.prev = tid > 0 && e < x.e1 ? doc_ids[e - 1] : -1;
+    };
+    auto load_codes = [&](const MxItem& x, unsigned (&w)[TPW][CW]) {
+#pragma unroll
+        for (int j = 0; j < TPW; ++j) {
+            const int64_t er = x.e0 + 16 * (wave + NW * j) + li;
+#pragma unroll
+            for (int m = 0; m < CW; ++m) w[j][m] = 0;
+            if (er < x.e1) {
+                const uint8_t* row = codes + er * BYTES + 4 * NBITS * lg;
+                if (NBITS == 8) {
+                    const uint4 v0 = reinterpret_cast<const uint4*>(row)[0];
+                    const uint4 v1 = reinterpret_cast<const uint4*>(row)[1];
+                    w[j][0] = v0.x; w[j][1] = v0.y; w[j][2] = v0.z; w[j][3] = v0.w;
+                    w[j][4 % CW] = v1.x; w[j][5 % CW] = v1.y; w[j][6 % CW] = v1.z; w[j][7 % CW] = v1.w;
+                } else if (NBITS == 4) {
+                    const uint4 v = *reinterpret_cast<const uint4*>(row);
+                    w[j][0] = v.x; w[j][1 % CW] = v.y; w[j][2 % CW] = v.z; w[j][3 % CW] = v.w;
+                } else if (NBITS == 2) {
+                    const uint2 v = *reinterpret_cast<const uint2*>(row);
+                    w[j][0] = v.x; w[j][1 % CW] = v.y;
+                } else {
+                    w[j][0] = *reinterpret_cast<const unsigned*>(row);
+                }
+            }
+        }
+    };
+    auto decode_item = [&](int64_t item) {
+        while (plan_load(item_start, c + 1) <= item) ++c;
+        return mx_decode(a, item, c);
+    };
+
+    MxItem it = mx_decode(a, first, c), nx = it;
+    int ptok[QPT];
+    MxStage<QPT> st;
+    unsigned w[TPW][CW];
+    load_tokens(it, ptok);
+    load_stage(it, ptok, st);
+    load_codes(it, w);
+    if (first + 1 < last) {
+        nx = decode_item(first + 1);
+        load_tokens(nx, ptok);
+    }
+
     for (int64_t item = first; item < last; ++item) {
-        while (item_start[c + 1] <= item) ++c;
-        const MxItem it = mx_decode(a, item, c);
         __syncthreads();  // the previous item's table is flushed and its tokens are no longer read
-        if (tid < kMxGroup) {
-            const bool in = tid < it.np;
-            const int tok = in ? a.plist[2 * (int64_t)(it.p0 + tid)] : 0;
-            s_base[tid] = in ? (int)bias(a.plist[2 * (int64_t)(it.p0 + tid) + 1]) : 0;
-            s_row[tid] = (int64_t)tok * a.n_docs;
+        // stage the item from registers
+        if (tid < kMxGroup) {  // tokens past the group's end have zero digits and seeds: score 0 = absent
+            const unsigned b = tid < it.np ? bias(st.base) : 0u;
+            s_seed_h[tid] = (int)(b >> 14);
+            s_seed_m[tid] = (int)((b >> 6) & 255u);
+            s_seed_l[tid] = (int)((b & 63u) << 2);
+            s_row[tid] = (int64_t)st.tok * a.n_docs;
         }
 #pragma unroll
-        for (int i = 0; i < NSLOT * kMxGroup / kMxBlock; ++i) {
+        for (int i = 0; i < QPT; ++i) {
             const int k = tid + kMxBlock * i;
-            const int tk = k / NSLOT, slot = k - tk * NSLOT;
-            v4i v = {0, 0, 0, 0};
-            if (tk < it.np) v = qdig[(int64_t)a.plist[2 * (int64_t)(it.p0 + tk)] * NSLOT + slot];
-            s_q[slot][tk] = v;
+            s_q[k % NSLOT][k / NSLOT] = st.q[i];
         }
         // runs of equal documents along the chunk (ids ascend inside a cluster)
-        const int64_t e = it.e0 + tid;
-        const bool e_in = e < it.e1;
-        const int doc = e_in ? doc_ids[e] : -1;
-        const bool start = e_in && (tid == 0 || doc_ids[e - 1] != doc);
+        const bool e_in = st.doc >= 0;
+        const int doc = st.doc;
+        const bool start = e_in && (tid == 0 || st.prev != doc);
         const unsigned long long starts = __ballot(start);
         if (lane == 0) s_wruns[wave] = __popcll(starts);
         __syncthreads();
         int run = __popcll(starts & ((2ull << lane) - 1)) - 1;  // starts in this wave up to this lane, minus one
         int n_runs = 0;
 #pragma unroll
-        for (int w = 0; w < NW; ++w) {
-            run += w < wave ? s_wruns[w] : 0;
-            n_runs += s_wruns[w];
+        for (int w8 = 0; w8 < NW; ++w8) {
+            run += w8 < wave ? s_wruns[w8] : 0;
+            n_runs += s_wruns[w8];
         }
         if (e_in) {
             s_run[tid] = run;
@@ -238,41 +326,32 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
                 s_rstart[run] = tid;
             }
         }
+        // prefetch: the next item's query digits, bases and documents, then the tokens of the
+        // item after it
+        const bool has_next = item + 1 < last;
+        if (has_next) load_stage(nx, ptok, st);
+        MxItem nn = nx;
+        if (item + 2 < last) {
+            nn = decode_item(item + 2);
+            load_tokens(nn, ptok);
+        }
         __syncthreads();
 
         const int n_et = (int)((it.e1 - it.e0 + 15) >> 4);
         const int n_tt = (it.np + 15) >> 4;
-        for (int et = wave; et < n_et; et += NW) {  // wave-uniform
-            // weight digits of the tile (MFMA B operand: column li = embedding e0 + 16 et + li)
-            const int64_t er = it.e0 + 16 * et + li;
-            const bool row_in = er < it.e1;
-            unsigned w[CW];
 #pragma unroll
-            for (int m = 0; m < CW; ++m) w[m] = 0;
-            if (row_in) {
-                const uint8_t* row = codes + er * BYTES + 4 * NBITS * lg;
-                if (NBITS == 8) {
-                    const uint4 v0 = reinterpret_cast<const uint4*>(row)[0];
-                    const uint4 v1 = reinterpret_cast<const uint4*>(row)[1];
-                    w[0] = v0.x; w[1] = v0.y; w[2] = v0.z; w[3] = v0.w;
-                    w[4] = v1.x; w[5] = v1.y; w[6] = v1.z; w[7] = v1.w;
-                } else if (NBITS == 4) {
-                    const uint4 v = *reinterpret_cast<const uint4*>(row);
-                    w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
-                } else if (NBITS == 2) {
-                    const uint2 v = *reinterpret_cast<const uint2*>(row);
-                    w[0] = v.x; w[1] = v.y;
-                } else {
-                    w[0] = *reinterpret_cast<const unsigned*>(row);
-                }
-            }
+        for (int j = 0; j < TPW; ++j) {
+            const int et = wave + NW * j;
+            if (et >= n_et) break;  // wave-uniform
+            const bool row_in = it.e0 + 16 * et + li < it.e1;
+            // weight digits of the tile (MFMA B operand: column li = embedding e0 + 16 et + li)
             v4i A[3][2];
             if (NBITS == 4) {
 #pragma unroll
                 for (int m = 0; m < 4; ++m) {
 #pragma unroll
                     for (int h = 0; h < 2; ++h) {
-                        const unsigned x = h == 0 ? (w[m] >> 4) & 0x0F0F0F0Fu : w[m] & 0x0F0F0F0Fu;
+                        const unsigned x = h == 0 ? (w[j][m % CW] >> 4) & 0x0F0F0F0Fu : w[j][m % CW] & 0x0F0F0F0Fu;
                         const unsigned x7 = x & 0x07070707u;
                         const unsigned pick = ((x >> 1) & 0x04040404u) | 0x03020100u;
 #pragma unroll
@@ -288,7 +367,7 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
                 for (int s = 0; s < 2; ++s) {
 #pragma unroll
                     for (int u = 0; u < 4; ++u) {
-                        const unsigned x = (w[s] >> (6 - 2 * u)) & 0x03030303u;
+                        const unsigned x = (w[j][s % CW] >> (6 - 2 * u)) & 0x03030303u;
 #pragma unroll
                         for (int p = 0; p < 3; ++p)
                             A[p][s][u] = (int)__builtin_amdgcn_perm(tab[p][0], tab[p][0], x);
@@ -297,7 +376,7 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
             } else if (NBITS == 1) {
 #pragma unroll
                 for (int k = 0; k < 8; ++k) {
-                    const unsigned x = (w[0] >> k) & 0x01010101u;  // bit k of each byte: 0 or 1
+                    const unsigned x = (w[j][0] >> k) & 0x01010101u;  // bit k of each byte: 0 or 1
 #pragma unroll
                     for (int p = 0; p < 3; ++p)
                         A[p][k >> 2][k & 3] = (int)__builtin_amdgcn_perm(tab[p][0], tab[p][0], x);
@@ -306,8 +385,9 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
                 // b = 8: one table lookup per code byte, then gather digit p of four entries
 #pragma unroll
                 for (int m = 0; m < 8; ++m) {
-                    const unsigned e0 = s_wd[w[m] & 255u], e1 = s_wd[(w[m] >> 8) & 255u];
-                    const unsigned e2 = s_wd[(w[m] >> 16) & 255u], e3 = s_wd[w[m] >> 24];
+                    const unsigned wm = w[j][m % CW];
+                    const unsigned e0 = s_wd[wm & 255u], e1 = s_wd[(wm >> 8) & 255u];
+                    const unsigned e2 = s_wd[(wm >> 16) & 255u], e3 = s_wd[wm >> 24];
 #pragma unroll
                     for (int p = 0; p < 3; ++p) {
                         const unsigned sel = 0x0C0C0000u | ((unsigned)(4 + p) << 8) | (unsigned)p;
@@ -317,12 +397,16 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
                     }
                 }
             }
-            const int my_run = row_in ? s_run[16 * et + li] : 0;
+            const int my_run = row_in ? s_run[16 * et + li] : kMxChunk;
 
             for (int tt = 0; tt < n_tt; ++tt) {
+                // class accumulators, seeded with the rounding half and the tokens' centroid terms
                 v4i acc[5];
-#pragma unroll
-                for (int k = 0; k < 5; ++k) acc[k] = (v4i){0, 0, 0, 0};
+                acc[0] = (v4i){1 << 17, 1 << 17, 1 << 17, 1 << 17};
+                acc[1] = (v4i){0, 0, 0, 0};
+                acc[2] = *reinterpret_cast<const v4i*>(&s_seed_l[16 * tt + 4 * lg]);
+                acc[3] = *reinterpret_cast<const v4i*>(&s_seed_m[16 * tt + 4 * lg]);
+                acc[4] = *reinterpret_cast<const v4i*>(&s_seed_h[16 * tt + 4 * lg]);
 #pragma unroll
                 for (int s = 0; s < 2; ++s) {
                     // query digits of slice s (MFMA A operand: row li = token 16 tt + li)
@@ -332,36 +416,43 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_mx(WaveArgs a) {
 #pragma unroll
                     for (int i = 0; i < 3; ++i)
 #pragma unroll
-                        for (int j = 0; j < 3; ++j)
-                            acc[i + j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(B[i], A[j][s], acc[i + j], 0, 0, 0);
+                        for (int jj = 0; jj < 3; ++jj)
+                            acc[i + jj] = __builtin_amdgcn_mfma_i32_16x16x64_i8(B[i], A[jj][s], acc[i + jj], 0, 0, 0);
                 }
                 // acc[k][r] of lane (li, lg): token 16 tt + 4 lg + r against embedding e0 + 16 et + li;
                 // merge into the (token, run) table
-                const int4 bs = *reinterpret_cast<const int4*>(&s_base[16 * tt + 4 * lg]);
-                const int bsr[4] = {bs.x, bs.y, bs.z, bs.w};
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int tk = 16 * tt + 4 * lg + r;
-                    const unsigned v =
-                        (unsigned)mx_round(acc[0][r], acc[1][r], acc[2][r], acc[3][r], acc[4][r]) + (unsigned)bsr[r];
-                    if (row_in && tk < it.np) atomicMax(&s_tab[tk * TPAD + my_run], v);
-                }
+                for (int r = 0; r < 4; ++r)
+                    atomicMax(&s_tab[(16 * tt + 4 * lg + r) * TPAD + my_run],
+                              mx_fold(acc[0][r], acc[1][r], acc[2][r], acc[3][r], acc[4][r]));
             }
         }
+        // the next item's codes, in flight during the flush
+        if (has_next) load_codes(nx, w);
         __syncthreads();
-        // flush: one device atomic per (token, run); consecutive threads take consecutive
-        // runs of one token, i.e. ascending documents of one token-max row
-        const int cells = it.np * n_runs;
-        for (int x = tid; x < cells; x += kMxBlock) {
-            const int tk = x / n_runs, rn = x - tk * n_runs;
-            const unsigned v = s_tab[tk * TPAD + rn];
-            s_tab[tk * TPAD + rn] = kTokAbsent;
-            atomicMax(&tokmax[s_row[tk] + s_rdoc[rn]], v);
-            if (a.tokcnt) {  // Eq.-1-literal scoring: embeddings of the run retrieved for the token
-                const int len = (rn + 1 < n_runs ? s_rstart[rn + 1] : (int)(it.e1 - it.e0)) - s_rstart[rn];
-                atomicAdd(&a.tokcnt[s_row[tk] + s_rdoc[rn]], (unsigned)len);
+        // flush: one device atomic per (token, run). With R = 2^lr the power of two at or above
+        // the run count, thread tid takes run tid mod R of tokens tid / R, tid / R + 256 / R, ...:
+        // consecutive lanes take consecutive runs of one token (ascending documents of one
+        // token-max row), and no thread divides
+        const int lr = n_runs <= 1 ? 0 : 32 - __builtin_clz((unsigned)(n_runs - 1));
+        const int rn = tid & ((1 << lr) - 1);
+        if (rn < n_runs) {
+            const int rdoc = s_rdoc[rn];
+            // Eq.-1-literal scoring: embeddings of the run retrieved for each token
+            const unsigned len =
+                (unsigned)((rn + 1 < n_runs ? s_rstart[rn + 1] : (int)(it.e1 - it.e0)) - s_rstart[rn]);
+            const int step = kMxBlock >> lr;
+            for (int tk = tid >> lr; tk < it.np; tk += step) {
+                unsigned* cell = &s_tab[tk * TPAD + rn];
+                const unsigned v = *cell;
+                *cell = kTokAbsent;
+                const int64_t o = s_row[tk] + rdoc;
+                atomicMax(&tokmax[o], v);
+                if (a.tokcnt) atomicAdd(&a.tokcnt[o], len);
             }
         }
+        it = nx;
+        nx = nn;
     }
 }
 

@@ -14,7 +14,7 @@ import pytest
 
 import oracle
 import synth
-from helpers import FRAC, explicit_decompress, load_dyadic
+from helpers import FRAC, explicit_decompress, load_dyadic, unpack_msb_first
 
 pytestmark = pytest.mark.gpu
 
@@ -324,3 +324,21 @@ def test_eq1_literal_tiny_and_switch_back():
                 label="tiny paper after literal")
         with pytest.raises(w.WarpError):
             ix.set_scoring(7)
+
+
+def test_exact_halves_in_the_residual_term():
+    # query values on a 2^-13 grid and bucket weights on a 2^-14 grid make every residual
+    # term V = 2^17 sum_d k_d m_d, so V 2^-18 is an exact half whenever the sum is odd:
+    # the engine must round those halves upward like the oracle
+    wl = synth.random_small_workload(31, n_centroids=60, n_docs=500, max_len=14, nbits=4, n_queries=5,
+                                     n_qtok=32, nprobe=12, t_prime=200, k=40)
+    data = synth.make_index(wl, workers=1)
+    data.bucket_weights = (np.round(data.bucket_weights.astype(np.float64) * 2 ** 14) / 2 ** 14).astype(np.float32)
+    Q = (np.round(data.queries.astype(np.float64) * 0.999 * 2 ** 13) / 2 ** 13).astype(np.float32)
+    k = np.round(Q.astype(np.float64) * 2 ** 13).astype(np.int64).reshape(-1, 128)
+    m = np.round(data.bucket_weights.astype(np.float64) * 2 ** 14).astype(np.int64)
+    per_dim = m[unpack_msb_first(data.codes[:200], data.nbits)]  # [200, 128]
+    odd = ((k @ per_dim.T) % 2 != 0).mean()
+    say(f"[halves] fraction of exact halves among sampled residual terms: {odd:.2f}")
+    assert odd > 0.2
+    run_both(data, queries=Q, label="exact halves")

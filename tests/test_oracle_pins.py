@@ -307,3 +307,28 @@ def test_o6_invariances():
     for key in ("ids", "fixed", "counts", "m_fixed", "n_scored", "cand_bitmap"):
         np.testing.assert_array_equal(base[key], r[key])
     np.testing.assert_array_equal(lab[base["sel"]], r["sel"])
+
+
+# ----------------------------------------------------------------------------- O8
+
+def test_o8_residual_rounding_of_exact_halves():
+    """Token score = R(S64) + floor(V 2^-18 + 1/2), halves upward (reading 11).
+
+    q_0 = 2^-13 and bucket weight m 2^-14 quantise exactly to 2^9 and m 2^8, so an
+    embedding whose dimension 0 takes that bucket (every other q_d = 0) has
+    V = m 2^17: V 2^-18 = m / 2. Worked by hand for m = 1, 3, -1, -3, 2, 0:
+    0.5 -> 1, 1.5 -> 2, -0.5 -> 0, -1.5 -> -1, 1 -> 1, 0 -> 0 (half to even would
+    give 0, 2, 0, -2, 1, 0).
+    """
+    m = [1, 3, -1, -3, 2, 0]
+    w = np.zeros(16, np.float32)
+    w[:len(m)] = np.asarray(m, np.float64) * 2.0 ** -14
+    q = np.zeros(128, np.float32)
+    q[0] = 2.0 ** -13
+    codes = np.zeros((len(m), 64), np.uint8)
+    codes[:, 0] = np.arange(len(m), dtype=np.uint8) << 4  # dimension 0 is the high nibble of byte 0
+    t = oracle.token_scores(q, 0.0, codes, 4, w, 0, len(m))
+    assert t.tolist() == [1, 2, 0, -1, 1, 0]
+    # the centroid term R(2^-26) = 1 is added to the rounded residual term
+    t = oracle.token_scores(q, 2.0 ** -26, codes, 4, w, 0, len(m))
+    assert t.tolist() == [2, 3, 1, 0, 2, 1]
