@@ -39,6 +39,16 @@
  * error the outputs are unspecified and warp_last_error() describes the cause.
  *
  * Threads. Calls on one index are serialised by a lock inside the index.
+ *
+ * Scratch. An index grows device scratch on demand and keeps it until freed. A
+ * search runs in waves of as many queries as the scratch budget holds: the value
+ * of the environment variable WARP_SCRATCH_MB (MiB) if set, else 60% of the free
+ * device memory. The dominant scratch is a [tokens][documents] table of token
+ * maxima per wave. When the whole batch fits one wave even with two such tables,
+ * and a table is at least WARP_TWO_TABLES_MIN_MB MiB (default 64), waves
+ * alternate between two tables and a table is zeroed after its fold on a second
+ * stream of the index (default priority), ordered by events; otherwise the fold
+ * resets the table it reads.
  */
 #ifndef WARP_H
 #define WARP_H

@@ -71,6 +71,7 @@ struct WaveArgs {
     int64_t* seg_pref;          // [n_tok][nprobe + 1] cumulative probed sizes
     int64_t* m_fixed;           // [n_tok]
     uint32_t* tokmax;           // [n_tok][n_docs] biased token maxima, kTokAbsent when not retrieved
+    int32_t fold_reset;         // 1: the fold resets the cells it reads; 0: the table is zeroed on a side stream
     uint32_t* tokcnt;           // [n_tok][n_docs] retrieved embeddings per (token, doc); only for the
                                 // Eq.-1-literal scoring, else null
     const int32_t* doc_len;     // [n_docs] embeddings per document (Eq.-1-literal scoring)
@@ -109,6 +110,7 @@ int scan_mx_blocks_per_cu(int nbits);
 void launch_fold(const WaveArgs& a, hipStream_t s);
 void launch_topk(const WaveArgs& a, hipStream_t s);
 void launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
+void launch_zero16(void* p, int64_t units, hipStream_t s);  // units of 16 bytes, streaming stores
 void launch_check_docs(const int32_t* ids, int64_t n, int32_t n_docs, int32_t* err, hipStream_t s);
 void launch_check_queries(const float* q, int64_t n_tok, int32_t* err, hipStream_t s);
 void launch_doc_len(const int32_t* doc_ids, int64_t n, int32_t* doc_len, int32_t n_docs, hipStream_t s);

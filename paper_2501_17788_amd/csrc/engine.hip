@@ -65,8 +65,17 @@ struct warp_index {
     int scan_grid = 0;     // persistent workgroups of the residual scan
     // per-search scratch, grown on demand
     DevBuf filter, sel, base, seg_pref, m_fixed, tokmax, keys, qpart;
+    // A second token-max table: when the whole batch fits one wave even with two tables,
+    // waves alternate between them and the fold only reads; a folded table is zeroed on a
+    // side stream while the next wave selects centroids on the other one, and the wave
+    // after that waits for the zeroing before its scan writes the table.
+    DevBuf tokmax2;
+    int64_t tab_ready[2] = {0, 0};     // leading cells of each table that hold kTokAbsent once zeroed
+    bool tab_zeroing[2] = {false, false};  // a zeroing of the table is enqueued on the side stream
+    hipEvent_t tab_folded[2] = {}, tab_zeroed[2] = {};
+    hipStream_t side = nullptr;
+    int tab_cur = 0;                   // table of the next wave in two-table mode
     DevBuf ccount, cursor, item_start, pair_start, plist, qdig, blk;
-    int64_t tokmax_ready = 0;  // leading elements of tokmax holding kTokAbsent
     int32_t scoring = WARP_SCORING_PAPER;
     DevBuf tokcnt, doc_len;    // Eq.-1-literal scoring only
     int64_t tokcnt_ready = 0;  // leading elements of tokcnt holding 0
@@ -276,8 +285,9 @@ int load_common(const float* C, int32_t n_c, int32_t dim, const int64_t* off, co
     return WARP_OK;
 }
 
-// Device scratch for a wave of `qw` queries of `T` tokens.
-int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P) {
+// Device scratch for a wave of `qw` queries of `T` tokens; the fills are enqueued on the
+// search stream `s`, after the searches before it.
+int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, bool two_tables, hipStream_t s) {
     const int64_t n_tok = (int64_t)qw * T;
     int rc = WARP_OK;
     if (!rc) rc = grow(idx->filter, (size_t)n_tok * idx->n_c * 2);
@@ -296,16 +306,29 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P) {
     if (!rc) rc = grow(idx->qdig, (size_t)n_tok * kQdigBytes);
     if (!rc) rc = grow(idx->blk, (size_t)nblk * 16);
     if (rc) return rc;
-    const int64_t need = n_tok * idx->n_docs;
-    if ((int64_t)(idx->tokmax.bytes / 4) < need) {
-        rc = grow(idx->tokmax, (size_t)need * 4);
-        if (rc) return rc;
-        idx->tokmax_ready = 0;
+    // token-max tables: cells rounded up to whole 16-byte units (the scan zeroes units);
+    // every cell the wave can touch holds kTokAbsent when it starts
+    const int64_t need = (n_tok * idx->n_docs + 3) & ~(int64_t)3;
+    for (int t = 0; t < (two_tables ? 2 : 1); ++t) {
+        DevBuf& tab = t ? idx->tokmax2 : idx->tokmax;
+        if ((int64_t)(tab.bytes / 4) < need) {
+            rc = grow(tab, (size_t)need * 4);  // hipFree waits for the device, zeroings included
+            if (rc) return rc;
+            idx->tab_ready[t] = 0;
+            idx->tab_zeroing[t] = false;
+        }
+        if (idx->tab_ready[t] < need) {
+            launch_fill_i32((int32_t*)tab.p, need, (int32_t)kTokAbsent, s);
+            idx->tab_ready[t] = need;
+        }
     }
-    if (idx->tokmax_ready < need) {
-        launch_fill_i32((int32_t*)idx->tokmax.p, need, (int32_t)kTokAbsent, idx->stream);
-        HIP_TRY(hipStreamSynchronize(idx->stream));
-        idx->tokmax_ready = need;
+    if (two_tables && !idx->side) {
+        if (hipStreamCreateWithFlags(&idx->side, hipStreamNonBlocking) != hipSuccess)
+            return fail(WARP_EDEVICE, "hipStreamCreate failed");
+        for (int t = 0; t < 2; ++t)
+            if (hipEventCreateWithFlags(&idx->tab_folded[t], hipEventDisableTiming) != hipSuccess ||
+                hipEventCreateWithFlags(&idx->tab_zeroed[t], hipEventDisableTiming) != hipSuccess)
+                return fail(WARP_EDEVICE, "hipEventCreate failed");
     }
     if (idx->scoring == WARP_SCORING_EQ1_LITERAL) {
         if ((int64_t)(idx->tokcnt.bytes / 4) < need) {
@@ -316,10 +339,9 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P) {
         if (!idx->doc_len_ready) {
             rc = grow(idx->doc_len, (size_t)idx->n_docs * 4);
             if (rc) return rc;
-            launch_doc_len(idx->doc_ids, idx->n_emb, (int32_t*)idx->doc_len.p, idx->n_docs, idx->stream);
+            launch_doc_len(idx->doc_ids, idx->n_emb, (int32_t*)idx->doc_len.p, idx->n_docs, s);
         }
-        if (idx->tokcnt_ready < need) launch_fill_i32((int32_t*)idx->tokcnt.p, need, 0, idx->stream);
-        HIP_TRY(hipStreamSynchronize(idx->stream));
+        if (idx->tokcnt_ready < need) launch_fill_i32((int32_t*)idx->tokcnt.p, need, 0, s);
         idx->doc_len_ready = true;
         idx->tokcnt_ready = need;
     }
@@ -330,8 +352,12 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P) {
 // WARP_SCRATCH_MB if set, else 60% of the device memory that is free or already
 // held as scratch by this index. A larger wave lets the cluster-major scan read
 // each probed cluster once for more queries.
-int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T) {
-    const size_t held = idx->tokmax.bytes + idx->filter.bytes + idx->keys.bytes + idx->plist.bytes + idx->qdig.bytes;
+// Two-table mode (see the index) is taken when the second table does not shrink the
+// wave and a table is large enough (WARP_TWO_TABLES_MIN_MB, default 64 MiB) for the
+// fold's resets to cost more than the side-stream zeroing and its synchronisation.
+int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T, bool* two_tables) {
+    const size_t held = idx->tokmax.bytes + idx->tokmax2.bytes + idx->filter.bytes + idx->keys.bytes +
+                        idx->plist.bytes + idx->qdig.bytes;
     size_t budget = 0;
     if (const char* s = std::getenv("WARP_SCRATCH_MB")) {
         budget = (size_t)std::atoll(s) << 20;
@@ -346,10 +372,16 @@ int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T) {
     const size_t per = (size_t)T * idx->n_docs * (idx->scoring == WARP_SCORING_EQ1_LITERAL ? 8 : 4) +
                        (size_t)idx->n_docs * 8 + (size_t)T * idx->n_c * 2 + (size_t)T * kMaxProbe * 32 +
                        (size_t)T * 1024;
-    int64_t qw = (int64_t)(budget / per);
-    if (qw < 1) qw = 1;
-    if (qw > n_queries) qw = n_queries;
-    if (qw > 65535) qw = 65535;
+    auto clamp = [&](int64_t q) {
+        if (q > n_queries) q = n_queries;
+        if (q > 65535) q = 65535;
+        return q < 1 ? (int64_t)1 : q;
+    };
+    const int64_t qw = clamp((int64_t)(budget / per));
+    const int64_t qw2 = clamp((int64_t)(budget / (per + (size_t)T * idx->n_docs * 4)));
+    int64_t min_mb = 64;
+    if (const char* s = std::getenv("WARP_TWO_TABLES_MIN_MB")) min_mb = std::atoll(s);
+    *two_tables = idx->scoring == WARP_SCORING_PAPER && qw2 >= qw && qw * T * idx->n_docs * 4 >= (min_mb << 20);
     return (int32_t)qw;
 }
 
@@ -393,8 +425,9 @@ struct SearchOut {
 // Enqueue a whole search on `s`; every pointer is device memory.
 int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t T, int32_t P,
                    int64_t t_prime, int32_t k, const SearchOut& o, hipStream_t s) {
-    const int32_t qw = wave_queries(idx, n_queries, T);
-    int rc = reserve(idx, qw, T, P);
+    bool two = false;
+    const int32_t qw = wave_queries(idx, n_queries, T, &two);
+    int rc = reserve(idx, qw, T, P, two, s);
     if (rc) return rc;
     launch_check_queries(dq, (int64_t)n_queries * T, idx->err, s);
     const int64_t words = ((int64_t)idx->n_docs + 31) / 32;
@@ -421,7 +454,9 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         a.base = (int32_t*)idx->base.p;
         a.seg_pref = (int64_t*)idx->seg_pref.p;
         a.m_fixed = (int64_t*)idx->m_fixed.p;
-        a.tokmax = (uint32_t*)idx->tokmax.p;
+        const int tab = two ? idx->tab_cur : 0;
+        a.tokmax = (uint32_t*)(tab ? idx->tokmax2.p : idx->tokmax.p);
+        a.fold_reset = two ? 0 : 1;
         a.tokcnt = idx->scoring == WARP_SCORING_EQ1_LITERAL ? (uint32_t*)idx->tokcnt.p : nullptr;
         a.doc_len = (const int32_t*)idx->doc_len.p;
         a.keys = (uint64_t*)idx->keys.p;
@@ -459,12 +494,24 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         launch_pairing(a, s);
         launch_qdigits(a, s);
         mark(3);
+        if (idx->tab_zeroing[tab]) {  // the table's zeroing precedes its next scan
+            HIP_TRY(hipStreamWaitEvent(s, idx->tab_zeroed[tab], 0));
+            idx->tab_zeroing[tab] = false;
+        }
         launch_scan_mx(a, s);
         mark(4);
         launch_fold(a, s);
         mark(5);
         launch_topk(a, s);
         mark(6);
+        if (two) {  // zero the folded table on the side stream
+            HIP_TRY(hipEventRecord(idx->tab_folded[tab], s));
+            HIP_TRY(hipStreamWaitEvent(idx->side, idx->tab_folded[tab], 0));
+            launch_zero16(a.tokmax, ((int64_t)nq * T * idx->n_docs + 3) / 4, idx->side);
+            HIP_TRY(hipEventRecord(idx->tab_zeroed[tab], idx->side));
+            idx->tab_zeroing[tab] = true;
+            idx->tab_cur = 1 - tab;
+        }
         if (idx->timing)
             for (int e = 0; e <= kStages; ++e) idx->ev_pending.push_back(ev[e]);
         hipError_t le = hipGetLastError();
@@ -573,13 +620,21 @@ void warp_index_free(warp_index* idx) {
                         (void*)idx->codes, (void*)idx->weights, (void*)idx->err})
             if (p) (void)hipFree(p);
         for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_pref, &idx->m_fixed,
-                          &idx->tokmax, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount, &idx->cursor, &idx->item_start,
+                          &idx->tokmax, &idx->tokmax2, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount, &idx->cursor, &idx->item_start,
                           &idx->pair_start, &idx->plist, &idx->qdig, &idx->blk, &idx->st_q, &idx->st_ids, &idx->st_scores,
                           &idx->st_fixed, &idx->st_counts, &idx->st_sel, &idx->st_m, &idx->st_bitmap,
                           &idx->st_scored})
             release(*b);
         for (hipEvent_t e : idx->ev_pool) (void)hipEventDestroy(e);
         for (hipEvent_t e : idx->ev_pending) (void)hipEventDestroy(e);
+        if (idx->side) {
+            (void)hipStreamSynchronize(idx->side);
+            for (int t = 0; t < 2; ++t) {
+                if (idx->tab_folded[t]) (void)hipEventDestroy(idx->tab_folded[t]);
+                if (idx->tab_zeroed[t]) (void)hipEventDestroy(idx->tab_zeroed[t]);
+            }
+            (void)hipStreamDestroy(idx->side);
+        }
         if (idx->stream) (void)hipStreamDestroy(idx->stream);
         idx->magic = 0;
     }

@@ -3,10 +3,12 @@
 // over the candidate documents (at least one retrieved token). Every split of
 // the token strides gives this sum, so one pass per document computes it.
 //
-// One thread per (query, document); the n_qtok token rows are read with
-// coalesced loads and reset to kTokAbsent for the next wave. The output is a sort
-// key per document: ((score + 2^39) << 24) | (2^24 - 1 - doc), larger is
-// better and equal scores order by lower document id; 0 marks a non-candidate.
+// One thread per (query, document): the n_qtok token rows are read with coalesced
+// loads, all issued before the first is used. With one token-max table the fold
+// resets the cells it read to kTokAbsent for the next wave; with two, the next
+// wave's scan zeroes this table and the fold only reads. The output is a sort key
+// per document: ((score + 2^39) << 24) | (2^24 - 1 - doc), larger is better and
+// equal scores order by lower document id; 0 marks a non-candidate.
 #include "engine.h"
 
 namespace warp {
@@ -18,31 +20,49 @@ __global__ __launch_bounds__(256) void k_fold(WaveArgs a) {
     bool any = false;
     uint64_t key = 0;
     if (in) {
-        int64_t sum = 0;
         const int T = a.n_qtok;
-        uint32_t* col = a.tokmax + (int64_t)q * T * a.n_docs + doc;
-        const int64_t* m = a.m_fixed + (int64_t)q * T;
-        uint32_t* cnt = a.tokcnt ? a.tokcnt + (int64_t)q * T * a.n_docs + doc : nullptr;
-        const int32_t len = cnt ? a.doc_len[doc] : 0;
-        for (int i = 0; i < T; ++i) {
-            const uint32_t v = col[(int64_t)i * a.n_docs];
-            if (v != kTokAbsent) {
-                any = true;
-                int64_t t = (int32_t)(v ^ 0x80000000u);
-                col[(int64_t)i * a.n_docs] = kTokAbsent;
-                if (cnt) {
-                    // Eq. 1 read literally: while some of the document's tokens were not
-                    // retrieved for this query token, the estimate m_i bounds it from below
-                    if ((int32_t)cnt[(int64_t)i * a.n_docs] < len && t < m[i]) t = m[i];
-                    cnt[(int64_t)i * a.n_docs] = 0;
+        const int64_t nd = a.n_docs;
+        uint32_t* col = a.tokmax + (int64_t)q * T * nd + doc;
+        // R(m_i) of the query's tokens: wave-uniform, read through the scalar cache
+        const auto* m = (const __attribute__((address_space(4))) int64_t*)(a.m_fixed + (int64_t)q * T);
+        uint32_t* cnt = a.tokcnt ? a.tokcnt + (int64_t)q * T * nd + doc : nullptr;
+        uint32_t v[kMaxQtok];
+#pragma unroll
+        for (int i = 0; i < kMaxQtok; ++i) v[i] = i < T ? col[i * nd] : kTokAbsent;
+        int64_t sum = 0;
+        if (!cnt) {
+#pragma unroll
+            for (int i = 0; i < kMaxQtok; ++i) {
+                if (i < T) {
+                    any |= v[i] != kTokAbsent;
+                    sum += v[i] != kTokAbsent ? (int64_t)(int32_t)(v[i] ^ 0x80000000u) : m[i];
                 }
-                sum += t;
-            } else {
-                sum += m[i];
+            }
+            if (a.fold_reset) {
+#pragma unroll
+                for (int i = 0; i < kMaxQtok; ++i)
+                    if (i < T && v[i] != kTokAbsent) col[i * nd] = kTokAbsent;
+            }
+        } else {
+            // Eq. 1 read literally: while some of the document's tokens were not retrieved
+            // for this query token, the estimate m_i bounds it from below
+            const int32_t len = a.doc_len[doc];
+            for (int i = 0; i < T; ++i) {
+                const uint32_t n = cnt[i * nd];
+                if (v[i] != kTokAbsent) {
+                    any = true;
+                    int64_t t = (int32_t)(v[i] ^ 0x80000000u);
+                    if ((int32_t)n < len && t < m[i]) t = m[i];
+                    sum += t;
+                    col[i * nd] = kTokAbsent;
+                } else {
+                    sum += m[i];
+                }
+                cnt[i * nd] = 0;
             }
         }
         key = any ? ((uint64_t)(sum + (1ll << 39)) << 24) | (uint64_t)(kMaxDocs - 1 - (int32_t)doc) : 0;
-        a.keys[(int64_t)q * a.n_docs + doc] = key;
+        a.keys[(int64_t)q * nd + doc] = key;
     }
     // candidate count and largest key of the block, for the top-k's histogram
     __shared__ unsigned long long s_max[4];

@@ -342,3 +342,28 @@ def test_exact_halves_in_the_residual_term():
     say(f"[halves] fraction of exact halves among sampled residual terms: {odd:.2f}")
     assert odd > 0.2
     run_both(data, queries=Q, label="exact halves")
+
+
+def test_consecutive_searches_reuse_the_token_max_tables(monkeypatch):
+    # waves alternate between two token-max tables when the batch fits one wave; a folded table
+    # is zeroed on a side stream before its next scan. Every search of a sequence with changing
+    # query counts must match the oracle, also around a search with one table (the Eq.-1-literal
+    # scoring resets in the fold) and with one query per wave (a 1 MiB scratch budget)
+    w = _engine()
+    data = synth.make_index(synth.with_overrides(synth.WORKLOADS["tiny"], n_queries=9), workers=1)
+    wl = data.workload
+    rng = np.random.default_rng(5)
+    batches = [data.queries[:5], data.queries[5:7], data.queries[:9], data.queries[2:3],
+               data.queries[rng.permutation(9)[:7]], data.queries[1:8]]
+    monkeypatch.setenv("WARP_TWO_TABLES_MIN_MB", "0")  # two tables also for these small tables
+    with w.Index.from_synthetic(data) as ix:
+        for j, Q in enumerate(batches):
+            literal = j == 3
+            ix.set_scoring(w.SCORING_EQ1_LITERAL if literal else w.SCORING_PAPER)
+            if j == 5:
+                monkeypatch.setenv("WARP_SCRATCH_MB", "1")
+            say(f"[tables] search {j}: {len(Q)} queries, literal={literal}")
+            got = ix.search_debug(Q, wl.nprobe, wl.t_prime, wl.k)
+            want = oracle.search_index(data, queries=Q, nprobe=wl.nprobe, t_prime=wl.t_prime, k=wl.k,
+                                       flags=oracle.EQ1_LITERAL if literal else 0)
+            compare(got, want, label=f"tables search {j}")
