@@ -235,7 +235,8 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
             ptok[i] = tk < x.np ? plist[2 * (int64_t)(x.p0 + tk)] : -1;
         }
     };
-    auto load_stage = [&](const MxItem& x, const int (&ptok)[QPT], MxStage<QPT>& st) {
+    // the documents are loaded only for a new chunk: items of one chunk follow each other
+    auto load_stage = [&](const MxItem& x, const int (&ptok)[QPT], MxStage<QPT>& st, bool new_chunk) {
 #pragma unroll
         for (int i = 0; i < QPT; ++i) {
             const int slot = (tid + kMxBlock * i) % NSLOT;
@@ -244,9 +245,11 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
         const bool in = tid < x.np;
         st.tok = in ? plist[2 * (int64_t)(x.p0 + tid)] : 0;
         st.base = in ? plist[2 * (int64_t)(x.p0 + tid) + 1] : 0;
-        const int64_t e = x.e0 + tid;
-        st.doc = e < x.e1 ? doc_ids[e] : -1;
-        st.prev = tid > 0 && e < x.e1 ? doc_ids[e - 1] : -1;
+        if (new_chunk) {
+            const int64_t e = x.e0 + tid;
+            st.doc = e < x.e1 ? doc_ids[e] : -1;
+            st.prev = tid > 0 && e < x.e1 ? doc_ids[e - 1] : -1;
+        }
     };
     auto load_codes = [&](const MxItem& x, unsigned (&w)[TPW][CW]) {
 #pragma unroll
@@ -283,13 +286,17 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
     MxStage<QPT> st;
     unsigned w[TPW][CW];
     load_tokens(it, ptok);
-    load_stage(it, ptok, st);
+    load_stage(it, ptok, st, true);
     load_codes(it, w);
     if (first + 1 < last) {
         nx = decode_item(first + 1);
         load_tokens(nx, ptok);
     }
 
+    // The runs of the chunk in LDS (s_run, s_rdoc, s_rstart, n_runs) and the codes in w stay
+    // valid while consecutive items share a chunk (the token groups of one chunk).
+    int64_t run_e0 = -1;  // first embedding of the chunk whose runs are in LDS
+    int n_runs = 0;
     for (int64_t item = first; item < last; ++item) {
         __syncthreads();  // the previous item's table is flushed and its tokens are no longer read
         // stage the item from registers
@@ -305,31 +312,34 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
             const int k = tid + kMxBlock * i;
             s_q[k % NSLOT][k / NSLOT] = st.q[i];
         }
-        // runs of equal documents along the chunk (ids ascend inside a cluster)
-        const bool e_in = st.doc >= 0;
-        const int doc = st.doc;
-        const bool start = e_in && (tid == 0 || st.prev != doc);
-        const unsigned long long starts = __ballot(start);
-        if (lane == 0) s_wruns[wave] = __popcll(starts);
-        __syncthreads();
-        int run = __popcll(starts & ((2ull << lane) - 1)) - 1;  // starts in this wave up to this lane, minus one
-        int n_runs = 0;
+        // runs of equal documents along a new chunk (ids ascend inside a cluster)
+        if (it.e0 != run_e0) {  // wave-uniform
+            run_e0 = it.e0;
+            const bool e_in = st.doc >= 0;
+            const int doc = st.doc;
+            const bool start = e_in && (tid == 0 || st.prev != doc);
+            const unsigned long long starts = __ballot(start);
+            if (lane == 0) s_wruns[wave] = __popcll(starts);
+            __syncthreads();
+            int run = __popcll(starts & ((2ull << lane) - 1)) - 1;  // starts in this wave up to this lane, minus one
+            n_runs = 0;
 #pragma unroll
-        for (int w8 = 0; w8 < NW; ++w8) {
-            run += w8 < wave ? s_wruns[w8] : 0;
-            n_runs += s_wruns[w8];
-        }
-        if (e_in) {
-            s_run[tid] = run;
-            if (start) {
-                s_rdoc[run] = doc;
-                s_rstart[run] = tid;
+            for (int w8 = 0; w8 < NW; ++w8) {
+                run += w8 < wave ? s_wruns[w8] : 0;
+                n_runs += s_wruns[w8];
+            }
+            if (e_in) {
+                s_run[tid] = run;
+                if (start) {
+                    s_rdoc[run] = doc;
+                    s_rstart[run] = tid;
+                }
             }
         }
         // prefetch: the next item's query digits, bases and documents, then the tokens of the
         // item after it
         const bool has_next = item + 1 < last;
-        if (has_next) load_stage(nx, ptok, st);
+        if (has_next) load_stage(nx, ptok, st, nx.e0 != it.e0);
         MxItem nn = nx;
         if (item + 2 < last) {
             nn = decode_item(item + 2);
@@ -427,8 +437,8 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
                               mx_fold(acc[0][r], acc[1][r], acc[2][r], acc[3][r], acc[4][r]));
             }
         }
-        // the next item's codes, in flight during the flush
-        if (has_next) load_codes(nx, w);
+        // the next item's codes, in flight during the flush (the same codes for the same chunk)
+        if (has_next && nx.e0 != it.e0) load_codes(nx, w);
         __syncthreads();
         // flush: one device atomic per (token, run). With R = 2^lr the power of two at or above
         // the run count, thread tid takes run tid mod R of tokens tid / R, tid / R + 256 / R, ...:
