@@ -1,35 +1,51 @@
 // Query-token x centroid scores on the matrix cores (Section 4.3: S = C q^T,
 // a matrix product since both sides are normalised).
 //
-// out[t][c] = sum_d q[t][d] * centroids[c][d] in fp32 with v_mfma_f32_16x16x4_f32.
-// These scores only steer centroid selection: every centroid that lands near a
-// selection boundary is rescored in fp64 by the selection kernel, so the result
-// of the search does not depend on the accumulation order used here.
+// Every fp32 operand x is split into two fp16 parts, hi = fp16(x) and
+// lo = fp16(x - hi), so that |x - hi - lo| <= 2^-22 |x| + 2^-25 for |x| <= 1.001
+// (the second term from fp16 subnormals), and
+//     out[t][c] = sum_d (q_hi c_hi + q_hi c_lo + q_lo c_hi)[t][c][d]
+// is accumulated in fp32 by v_mfma_f32_16x16x32_f16 (every fp16 product is exact in
+// fp32). The split and the dropped lo x lo term change a score by at most
+// 3 * 2^-22 sum_d |q_d c_d| + 2^-24 sqrt(128), about 1.4e-6 for unit vectors, and the
+// fp32 accumulation of the 384 products by at most gamma_384 sum_d |q_d c_d| (2.3e-5):
+// within the 2^-13 that centroid selection and the index build assume. These scores
+// only steer selection: every centroid that lands near a selection boundary is
+// rescored in fp64, so no result depends on how they were accumulated.
 //
-// Tiling: a workgroup of 4 waves owns a 128-token x 128-centroid tile; K = 128
-// is staged through LDS in two halves of 64 with coalesced 16-byte loads, rows
-// padded to 68 floats so that the 16 lanes of each ds_read_b128 pass hit 16
-// distinct 4-bank groups. Each wave computes a 64 x 64 block as 4 x 4 MFMA
-// blocks of 16 x 16. Lane group g = lane / 16 reads 4 consecutive k with one
-// 16-byte LDS read and feeds them to 4 successive MFMA steps: step s of a
-// 16-wide k slice uses k = 4 g + s on both operands, so every k is summed once.
+// Tiling: a workgroup of 4 waves owns a 128-token x 128-centroid tile; K = 128 is
+// staged through LDS in two halves of 64, each fp32 row split into hi and lo fp16 rows
+// padded to 72 halves (144 bytes: the 16 rows of a 16-lane ds_read_b128 start in 16
+// distinct 4-bank groups). Each wave computes a 64 x 64 block as 4 x 4 MFMA blocks of
+// 16 x 16; lane group g = lane / 16 supplies the 8 consecutive k = ks + 8 g .. ks + 8 g + 7
+// of both operands to each 32-wide k step ks, so every k is summed once.
 #include "engine.h"
 
 namespace warp {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half4 __attribute__((ext_vector_type(4)));
 
-constexpr int kGT = 128;       // tile rows (tokens) and columns (centroids)
-constexpr int kGK = 64;        // k staged per half
-constexpr int kGPad = kGK + 4;  // padded LDS row (floats)
+constexpr int kGT = 128;        // tile rows (tokens) and columns (centroids)
+constexpr int kGK = 64;         // k staged per half
+constexpr int kGPad = kGK + 8;  // padded LDS row (halves)
+
+__device__ __forceinline__ void split4(const float4 v, half4& hi, half4& lo) {
+    hi = (half4){(_Float16)v.x, (_Float16)v.y, (_Float16)v.z, (_Float16)v.w};
+    lo = (half4){(_Float16)(v.x - (float)hi.x), (_Float16)(v.y - (float)hi.y), (_Float16)(v.z - (float)hi.z),
+                 (_Float16)(v.w - (float)hi.w)};
+}
 
 // BINS: write the selection histogram bin of each score (u16); else the fp32 score.
 template <bool BINS>
 __global__ __launch_bounds__(256) void k_filter_gemm(const float* __restrict__ q, int32_t n_tok,
                                                      const float* __restrict__ cen, int32_t n_c,
                                                      void* __restrict__ out) {
-    __shared__ float As[kGT * kGPad];
-    __shared__ float Bs[kGT * kGPad];
+    __shared__ __attribute__((aligned(16))) _Float16 Ah[kGT * kGPad];
+    __shared__ __attribute__((aligned(16))) _Float16 Al[kGT * kGPad];
+    __shared__ __attribute__((aligned(16))) _Float16 Bh[kGT * kGPad];
+    __shared__ __attribute__((aligned(16))) _Float16 Bl[kGT * kGPad];
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
     const int lane = tid & 63;
@@ -49,7 +65,7 @@ __global__ __launch_bounds__(256) void k_filter_gemm(const float* __restrict__ q
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
         if (half) __syncthreads();
-        // stage: 128 rows x 64 floats per operand = 2048 float4, 8 per thread
+        // stage: 128 rows x 64 floats per operand = 2048 float4, 8 per thread, split on the way
 #pragma unroll
         for (int it = 0; it < 8; ++it) {
             const int f = tid + 256 * it;
@@ -58,28 +74,34 @@ __global__ __launch_bounds__(256) void k_filter_gemm(const float* __restrict__ q
             float4 va = make_float4(0.f, 0.f, 0.f, 0.f), vb = va;
             if (tr < n_tok) va = *reinterpret_cast<const float4*>(q + tr * kDim + half * kGK + 4 * c4);
             if (cr < n_c) vb = *reinterpret_cast<const float4*>(cen + cr * kDim + half * kGK + 4 * c4);
-            *reinterpret_cast<float4*>(&As[row * kGPad + 4 * c4]) = va;
-            *reinterpret_cast<float4*>(&Bs[row * kGPad + 4 * c4]) = vb;
+            half4 hi, lo;
+            split4(va, hi, lo);
+            *reinterpret_cast<half4*>(&Ah[row * kGPad + 4 * c4]) = hi;
+            *reinterpret_cast<half4*>(&Al[row * kGPad + 4 * c4]) = lo;
+            split4(vb, hi, lo);
+            *reinterpret_cast<half4*>(&Bh[row * kGPad + 4 * c4]) = hi;
+            *reinterpret_cast<half4*>(&Bl[row * kGPad + 4 * c4]) = lo;
         }
         __syncthreads();
 #pragma unroll
-        for (int ks = 0; ks < kGK; ks += 16) {
-            float4 a[4], b[4];
+        for (int ks = 0; ks < kGK; ks += 32) {
+            half8 ah[4], al[4], bh[4], bl[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                a[i] = *reinterpret_cast<const float4*>(&As[(wr + 16 * i + li) * kGPad + ks + 4 * g]);
-                b[i] = *reinterpret_cast<const float4*>(&Bs[(wc + 16 * i + li) * kGPad + ks + 4 * g]);
+                const int ra = (wr + 16 * i + li) * kGPad + ks + 8 * g;
+                const int rb = (wc + 16 * i + li) * kGPad + ks + 8 * g;
+                ah[i] = *reinterpret_cast<const half8*>(&Ah[ra]);
+                al[i] = *reinterpret_cast<const half8*>(&Al[ra]);
+                bh[i] = *reinterpret_cast<const half8*>(&Bh[rb]);
+                bl[i] = *reinterpret_cast<const half8*>(&Bl[rb]);
             }
 #pragma unroll
-            for (int s = 0; s < 4; ++s) {
+            for (int i = 0; i < 4; ++i) {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float av = s == 0 ? a[i].x : s == 1 ? a[i].y : s == 2 ? a[i].z : a[i].w;
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const float bv = s == 0 ? b[j].x : s == 1 ? b[j].y : s == 2 ? b[j].z : b[j].w;
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[i][j], 0, 0, 0);
-                    }
+                for (int j = 0; j < 4; ++j) {
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[i], bh[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[i], bl[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[i], bh[j], acc[i][j], 0, 0, 0);
                 }
             }
         }
