@@ -11,7 +11,7 @@
 //   2. from the top bin down: the bin b_P where the centroid count reaches
 //      n_probe and the bin b_t where the size sum first exceeds t';
 //   3. every centroid whose bin is within 2 of b_t, or at least b_P - 2, is
-//      rescored in fp64 and sorted by (S64 desc, id asc).
+//      rescored in fp64 and placed in (S64 desc, id asc) order by its rank.
 // Since |f - S64| <= kFilterEps and a bin is wider than 2 kFilterEps, a centroid
 // three or more bins above (below) b_t scores strictly above (below) m_i, and no
 // centroid below bin b_P - 2 can be among the n_probe best. Walking the rescored
@@ -32,29 +32,12 @@ __device__ __forceinline__ bool before(double xs, int xi, double ys, int yi) {
     return xs > ys || (xs == ys && xi < yi);
 }
 
-// Bitonic sort of n (a power of two) LDS entries in (score desc, id asc) order.
-__device__ void sort_desc(double* s, int* id, int n) {
-    for (int k = 2; k <= n; k <<= 1) {
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int i = threadIdx.x; i < n; i += blockDim.x) {
-                const int ixj = i ^ j;
-                if (ixj > i) {
-                    const bool asc = (i & k) == 0;
-                    const bool swap = asc ? before(s[ixj], id[ixj], s[i], id[i])
-                                          : before(s[i], id[i], s[ixj], id[ixj]);
-                    if (swap) {
-                        const double ts = s[i];
-                        s[i] = s[ixj];
-                        s[ixj] = ts;
-                        const int ti = id[i];
-                        id[i] = id[ixj];
-                        id[ixj] = ti;
-                    }
-                }
-            }
-            __syncthreads();
-        }
-    }
+// Number of the n LDS entries that come before entry (xs, xi) in (score desc, id asc)
+// order: its position in that order, since ids are distinct.
+__device__ __forceinline__ int rank_of(const double* s, const int* id, int n, double xs, int xi) {
+    int r = 0;
+    for (int j = 0; j < n; ++j) r += before(s[j], id[j], xs, xi) ? 1 : 0;
+    return r;
 }
 
 // fp64 centroid score, accumulated in dimension order (each product is exact).
@@ -79,36 +62,42 @@ __device__ __noinline__ double score64(const float* __restrict__ cen, int c, con
     return s;
 }
 
-__device__ __forceinline__ int pow2_at_least(int n) {
-    int p = 2;
-    while (p < n) p <<= 1;
-    return p;
-}
-
 constexpr int kSelThreads = 512;
 
-// Inclusive prefix sum of n <= kSelCap int64 values in LDS.
-__device__ void block_inclusive_scan(int64_t* v, int n, int64_t* tmp) {
-    constexpr int NT = kSelThreads;
-    const int tid = threadIdx.x;
-    const int per = (n + NT - 1) / NT;
-    const int lo = tid * per < n ? tid * per : n;
-    const int hi = lo + per < n ? lo + per : n;
-    int64_t run = 0;
-    for (int i = lo; i < hi; ++i) run += v[i];
-    tmp[tid] = run;
+// Inclusive prefix sum over the block of one value per thread: shuffle scans inside
+// each wave, then the wave totals through LDS (wtot: one entry per wave). Also returns
+// the block total. Every thread calls it.
+__device__ unsigned long long block_scan(unsigned long long v, unsigned long long* wtot,
+                                         unsigned long long* total) {
+    constexpr int NW = kSelThreads / 64;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const unsigned long long t = __shfl_up(v, off, 64);
+        if (lane >= off) v += t;
+    }
+    if (lane == 63) wtot[w] = v;
     __syncthreads();
-    for (int off = 1; off < NT; off <<= 1) {
-        const int64_t x = tid >= off ? tmp[tid - off] : 0;
-        __syncthreads();
-        tmp[tid] += x;
-        __syncthreads();
+    unsigned long long base = 0, all = 0;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+        base += i < w ? wtot[i] : 0;
+        all += wtot[i];
     }
-    run = tmp[tid] - run;
-    for (int i = lo; i < hi; ++i) {
-        run += v[i];
-        v[i] = run;
-    }
+    __syncthreads();  // wtot is free again
+    *total = all;
+    return v + base;
+}
+
+// Inclusive prefix sum of n <= 2 kSelThreads int64 values in LDS.
+__device__ void block_inclusive_scan(int64_t* v, int n, unsigned long long* wtot) {
+    const int i0 = 2 * threadIdx.x;
+    const int64_t a = i0 < n ? v[i0] : 0, b = i0 + 1 < n ? v[i0 + 1] : 0;
+    unsigned long long total;
+    const unsigned long long incl = block_scan((unsigned long long)(a + b), wtot, &total);
+    const int64_t excl = (int64_t)incl - (a + b);
+    if (i0 < n) v[i0] = excl + a;
+    if (i0 + 1 < n) v[i0 + 1] = excl + a + b;
     __syncthreads();
 }
 
@@ -152,14 +141,13 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
     constexpr int NT = kSelThreads;
     constexpr int PER = kSelBins / NT;
     __shared__ unsigned long long hist[kSelBins];
-    __shared__ unsigned long long sfx[NT];
+    __shared__ unsigned long long wtot[NT / 64];
     __shared__ float qs[kDim];
     __shared__ double sA[kSelCap], sB[kSelCap];
     __shared__ int idA[kSelCap], idB[kSelCap];
     __shared__ int64_t cum[kSelCap];
     __shared__ int s_bP, s_bt, s_blo, s_nA, s_nB, s_cross;
     __shared__ unsigned long long s_wabove;
-    int64_t* scan_tmp = reinterpret_cast<int64_t*>(sfx);  // free once the bin suffix sums are used
 
     const int t = blockIdx.x;
     const int tid = threadIdx.x;
@@ -190,15 +178,9 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
     //    Packed words add field by field: sizes total < 2^40, counts < 2^24.
     unsigned long long own = 0;
     for (int j = 0; j < PER; ++j) own += hist[PER * tid + j];
-    sfx[tid] = own;
-    __syncthreads();
-    for (int off = 1; off < NT; off <<= 1) {
-        const unsigned long long x = tid + off < NT ? sfx[tid + off] : 0;
-        __syncthreads();
-        sfx[tid] += x;
-        __syncthreads();
-    }
-    const unsigned long long above = sfx[tid] - own;
+    unsigned long long total;
+    const unsigned long long incl = block_scan(own, wtot, &total);
+    const unsigned long long above = total - incl;  // every bin above this thread's
     const uint32_t above_c = (uint32_t)(above >> 40), own_c = (uint32_t)(own >> 40);
     const unsigned long long above_w = above & kSizeMask, own_w = own & kSizeMask;
     if (above_c < (uint32_t)P && above_c + own_c >= (uint32_t)P) {
@@ -267,42 +249,40 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
         return;
     }
 
-    // 4. fp64 rescoring (both lists in one pass) and exact order
-    const int pA = pow2_at_least(nA), pB = pow2_at_least(nB);
-    for (int p = tid; p < pA + pB; p += NT) {
-        const bool in_a = p < pA;
-        const int q = in_a ? p : p - pA;
-        int* ids = in_a ? idA : idB;
-        double* ss = in_a ? sA : sB;
-        if (q < (in_a ? nA : nB)) {
-            ss[q] = score64(a.centroids, ids[q], qs);
-        } else {
-            ss[q] = -__builtin_inf();
-            ids[q] = 0x7fffffff;
+    // 4. fp64 rescoring of both lists
+    for (int p = tid; p < nA + nB; p += NT) {
+        if (p < nA) sA[p] = score64(a.centroids, idA[p], qs);
+        else sB[p - nA] = score64(a.centroids, idB[p - nA], qs);
+    }
+    __syncthreads();
+
+    // 5. the n_probe best in exact order (an entry's position is its rank among the rescored
+    //    entries), their fixed-point scores and the prefix of their sizes
+    for (int p = tid; p < nA; p += NT) {
+        const int r = rank_of(sA, idA, nA, sA[p], idA[p]);
+        if (r < P) {
+            const int c = idA[p];
+            sel[r] = c;
+            base[r] = (int32_t)to_fixed(sA[p]);
+            cum[r] = sizes[c];
+            if (a.dbg_sel) a.dbg_sel[(int64_t)t * P + r] = c;
         }
     }
     __syncthreads();
-    sort_desc(sA, idA, pA);
-    sort_desc(sB, idB, pB);
-
-    // 5. the n_probe best, their fixed-point scores and the prefix of their sizes
-    for (int j = tid; j < P; j += NT) {
-        const int c = idA[j];
-        sel[j] = c;
-        base[j] = (int32_t)to_fixed(sA[j]);
-        cum[j] = sizes[c];
-        if (a.dbg_sel) a.dbg_sel[(int64_t)t * P + j] = c;
-    }
-    __syncthreads();
-    block_inclusive_scan(cum, P, scan_tmp);
+    block_inclusive_scan(cum, P, wtot);
     for (int j = tid; j <= P; j += NT) seg_pref[j] = j == 0 ? 0 : cum[j - 1];
     __syncthreads();
 
-    // 6. m_i: the first band entry, in exact order, whose cumulative size (from the
-    //    size of everything above the band) exceeds t'
-    for (int p = tid; p < nB; p += NT) cum[p] = sizes[idB[p]];
+    // 6. m_i: the band in exact order (its scores placed by rank into sA, free now), and the
+    //    first entry whose cumulative size (from the size of everything above the band)
+    //    exceeds t'
+    for (int p = tid; p < nB; p += NT) {
+        const int r = rank_of(sB, idB, nB, sB[p], idB[p]);
+        sA[r] = sB[p];
+        cum[r] = sizes[idB[p]];
+    }
     __syncthreads();
-    block_inclusive_scan(cum, nB, scan_tmp);
+    block_inclusive_scan(cum, nB, wtot);
     if (!clamp) {
         unsigned long long band_above = s_wabove;
         for (int b = s_bt + 1; b <= bt_hi; ++b) band_above -= hist[b] & kSizeMask;
@@ -311,9 +291,9 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
     }
     __syncthreads();
     if (tid == 0) {
-        double m = sB[nB - 1];  // clamp: the lowest score
+        double m = sA[nB - 1];  // clamp: the lowest score
         if (!clamp) {
-            if (s_cross < nB) m = sB[s_cross];
+            if (s_cross < nB) m = sA[s_cross];
             else atomicOr(a.err, kErrSelNoCrossing);
         }
         a.m_fixed[t] = to_fixed(m);
