@@ -39,11 +39,14 @@ __device__ __forceinline__ int score_bin(float f) {
 constexpr int kMxChunk = 256;
 constexpr int kMxGroup = 32;
 constexpr int kMxBlock = 256;
+// The persistent scan grid takes its items in batches of kScanBatch consecutive items:
+// workgroup b starts with batch b, and every later batch comes from a device counter.
+constexpr int kScanBatch = 4;
 constexpr int kQdigBytes = 3 * kDim;  // three base-256 digit planes of a query token
 // Largest bucket weight magnitude: Q(omega) = round(omega * 2^22) must have three
 // signed base-256 digits, i.e. lie in [-8421504, 8355711].
 constexpr float kMaxWeight = 1.99f;
-constexpr int kPlanBlock = 1024;  // clusters per block of the pairing prefix sums
+constexpr int kPlanBlock = 1024;  // clusters (chunks) per block of the work plan's prefix sums
 
 // Error bits the device reports through the index's flag word.
 constexpr int kErrSelOverflow = 1;
@@ -86,6 +89,18 @@ struct WaveArgs {
     int32_t* plist;             // [n_tok * nprobe][2]: (wave token, R(S64)) grouped by cluster
     int8_t* qdig;               // [n_tok][kQdigBytes] query digit planes in operand order
     int64_t* blk;               // [2 * ceil(n_c / kPlanBlock)] block sums of items and pairs
+    // The scan's items run over the probed chunks in the index's fixed pseudo-random chunk
+    // order, the token groups of one chunk consecutively, so that the equal shares of the
+    // persistent grid hold similar mixes of dense and sparse chunks of all clusters.
+    const int32_t* chunk_c;     // [n_chunks] cluster of each chunk of the index, in that order
+    const int32_t* chunk_k;     // [n_chunks] its chunk within the cluster
+    int64_t n_chunks;
+    int32_t* list_c;            // [n_chunks] the probed chunks of the wave, in that order: cluster
+    int32_t* list_k;            // [n_chunks] and chunk
+    int64_t* list_item;         // [n_chunks + 1] exclusive prefix of their items; list_item[*list_n] = total
+    int64_t* list_n;            // [1] number of probed chunks
+    int64_t* cblk;              // [2 * ceil(n_chunks / kPlanBlock)] block sums of probed chunks and items
+    uint32_t* scan_queue;       // [1] next unclaimed batch of the scan's items
     // outputs (device; the debug ones may be null)
     int32_t* out_ids;           // [n_q][k]
     float* out_scores;          // [n_q][k]

@@ -12,6 +12,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "engine.h"
@@ -57,6 +58,9 @@ struct warp_index {
     float* centroids = nullptr;
     int64_t* offsets = nullptr;
     int32_t* sizes = nullptr;
+    int32_t* chunk_c = nullptr;  // the index's chunks in a fixed pseudo-random order (see WaveArgs)
+    int32_t* chunk_k = nullptr;
+    int64_t n_chunks = 0;
     int32_t* doc_ids = nullptr;
     uint8_t* codes = nullptr;
     float* weights = nullptr;
@@ -76,6 +80,8 @@ struct warp_index {
     hipStream_t side = nullptr;
     int tab_cur = 0;                   // table of the next wave in two-table mode
     DevBuf ccount, cursor, item_start, pair_start, plist, qdig, blk;
+    DevBuf list_c, list_k, list_item, cblk;  // the wave's probed chunks (see WaveArgs)
+    DevBuf scan_queue;
     int32_t scoring = WARP_SCORING_PAPER;
     DevBuf tokcnt, doc_len;    // Eq.-1-literal scoring only
     int64_t tokcnt_ready = 0;  // leading elements of tokcnt holding 0
@@ -195,6 +201,31 @@ int finish_load(warp_index* idx, const int64_t* off_host) {
     std::vector<int32_t> sz(idx->n_c);
     for (int32_t c = 0; c < idx->n_c; ++c) sz[c] = (int32_t)(off_host[c + 1] - off_host[c]);
     HIP_TRY(hipMemcpy(idx->sizes, sz.data(), sizeof(int32_t) * idx->n_c, hipMemcpyHostToDevice));
+    // the chunks of kMxChunk embeddings of every cluster, shuffled (Fisher-Yates with a fixed
+    // xorshift64 stream): the scan's items follow this order
+    std::vector<int32_t> cc, ck;
+    for (int32_t c = 0; c < idx->n_c; ++c)
+        for (int64_t k = 0; k * kMxChunk < sz[c]; ++k) {
+            cc.push_back(c);
+            ck.push_back((int32_t)k);
+        }
+    uint64_t x = 0x9E3779B97F4A7C15ull;
+    for (int64_t i = (int64_t)cc.size() - 1; i > 0; --i) {
+        x ^= x << 13;
+        x ^= x >> 7;
+        x ^= x << 17;
+        const int64_t j = (int64_t)(x % (uint64_t)(i + 1));
+        std::swap(cc[i], cc[j]);
+        std::swap(ck[i], ck[j]);
+    }
+    idx->n_chunks = (int64_t)cc.size();
+    if (hipMalloc((void**)&idx->chunk_c, cc.size() * 4 + 16) != hipSuccess ||
+        hipMalloc((void**)&idx->chunk_k, ck.size() * 4 + 16) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(WARP_ENOMEM, "hipMalloc of the index's chunk order failed");
+    }
+    HIP_TRY(hipMemcpy(idx->chunk_c, cc.data(), cc.size() * 4, hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(idx->chunk_k, ck.data(), ck.size() * 4, hipMemcpyHostToDevice));
     launch_fill_i32(idx->err, 1, 0, idx->stream);
     launch_check_docs(idx->doc_ids, idx->n_emb, idx->n_docs, idx->err, idx->stream);
     int32_t err = 0;
@@ -305,6 +336,12 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, bool two_tables, 
     if (!rc) rc = grow(idx->plist, (size_t)n_tok * P * 8);
     if (!rc) rc = grow(idx->qdig, (size_t)n_tok * kQdigBytes);
     if (!rc) rc = grow(idx->blk, (size_t)nblk * 16);
+    const int64_t cblocks = (idx->n_chunks + kPlanBlock - 1) / kPlanBlock;
+    if (!rc) rc = grow(idx->list_c, (size_t)idx->n_chunks * 4);
+    if (!rc) rc = grow(idx->list_k, (size_t)idx->n_chunks * 4);
+    if (!rc) rc = grow(idx->list_item, ((size_t)idx->n_chunks + 2) * 8);  // + the count
+    if (!rc) rc = grow(idx->cblk, (size_t)cblocks * 16);
+    if (!rc) rc = grow(idx->scan_queue, 256);
     if (rc) return rc;
     // token-max tables: cells rounded up to whole 16-byte units (the scan zeroes units);
     // every cell the wave can touch holds kTokAbsent when it starts
@@ -476,6 +513,15 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         a.pair_start = (int32_t*)idx->pair_start.p;
         a.plist = (int32_t*)idx->plist.p;
         a.blk = (int64_t*)idx->blk.p;
+        a.chunk_c = idx->chunk_c;
+        a.chunk_k = idx->chunk_k;
+        a.n_chunks = idx->n_chunks;
+        a.list_c = (int32_t*)idx->list_c.p;
+        a.list_k = (int32_t*)idx->list_k.p;
+        a.list_item = (int64_t*)idx->list_item.p;
+        a.list_n = (int64_t*)idx->list_item.p + idx->n_chunks + 1;
+        a.cblk = (int64_t*)idx->cblk.p;
+        a.scan_queue = (uint32_t*)idx->scan_queue.p;
         a.qdig = (int8_t*)idx->qdig.p;
         a.scan_grid = idx->scan_grid;
 
@@ -616,12 +662,13 @@ void warp_index_free(warp_index* idx) {
         std::lock_guard<std::mutex> g(idx->lock);
         (void)hipSetDevice(idx->device);
         if (idx->stream) (void)hipStreamSynchronize(idx->stream);
-        for (void* p : {(void*)idx->centroids, (void*)idx->offsets, (void*)idx->sizes, (void*)idx->doc_ids,
+        for (void* p : {(void*)idx->centroids, (void*)idx->offsets, (void*)idx->sizes, (void*)idx->chunk_c,
+                        (void*)idx->chunk_k, (void*)idx->doc_ids,
                         (void*)idx->codes, (void*)idx->weights, (void*)idx->err})
             if (p) (void)hipFree(p);
         for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_pref, &idx->m_fixed,
                           &idx->tokmax, &idx->tokmax2, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount, &idx->cursor, &idx->item_start,
-                          &idx->pair_start, &idx->plist, &idx->qdig, &idx->blk, &idx->st_q, &idx->st_ids, &idx->st_scores,
+                          &idx->pair_start, &idx->plist, &idx->qdig, &idx->blk, &idx->list_c, &idx->list_k, &idx->list_item, &idx->cblk, &idx->scan_queue, &idx->st_q, &idx->st_ids, &idx->st_scores,
                           &idx->st_fixed, &idx->st_counts, &idx->st_sel, &idx->st_m, &idx->st_bitmap,
                           &idx->st_scored})
             release(*b);

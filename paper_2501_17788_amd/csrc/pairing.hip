@@ -99,6 +99,91 @@ __global__ __launch_bounds__(256) void k_pair_scatter(WaveArgs a) {
     a.plist[2 * p + 1] = a.base[i];           // R(S64) of (token, cluster)
 }
 
+// Probed chunks and their items (token groups of their cluster) in the index's chunk order.
+__device__ __forceinline__ void chunk_items(const WaveArgs& a, int64_t j, int64_t& flag, int64_t& items) {
+    flag = items = 0;
+    if (j < a.n_chunks) {
+        const int32_t nt = a.ccount[a.chunk_c[j]];
+        items = (nt + kMxGroup - 1) / kMxGroup;
+        flag = items > 0;
+    }
+}
+
+// Inclusive prefix sums of two values per thread over a block of kPlanBlock threads
+// (wave shuffles, then the wave totals through LDS).
+__device__ __forceinline__ void block_scan2(int64_t& f, int64_t& it, int64_t* wf, int64_t* wi) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int64_t tf = __shfl_up(f, off, 64), ti = __shfl_up(it, off, 64);
+        if (lane >= off) {
+            f += tf;
+            it += ti;
+        }
+    }
+    if (lane == 63) {
+        wf[w] = f;
+        wi[w] = it;
+    }
+    __syncthreads();
+    int64_t bf = 0, bi = 0;
+    for (int i = 0; i < w; ++i) {
+        bf += wf[i];
+        bi += wi[i];
+    }
+    f += bf;
+    it += bi;
+}
+
+// per block of kPlanBlock chunks: the number of probed chunks and their items
+__global__ __launch_bounds__(kPlanBlock) void k_chunk_count(WaveArgs a) {
+    __shared__ int64_t wf[kPlanBlock / 64], wi[kPlanBlock / 64];
+    int64_t f, it;
+    chunk_items(a, (int64_t)blockIdx.x * kPlanBlock + threadIdx.x, f, it);
+    block_scan2(f, it, wf, wi);
+    if (threadIdx.x == kPlanBlock - 1) {
+        a.cblk[2 * blockIdx.x] = f;
+        a.cblk[2 * blockIdx.x + 1] = it;
+    }
+}
+
+// the compacted list of probed chunks with the exclusive prefix of their items
+__global__ __launch_bounds__(kPlanBlock) void k_chunk_list(WaveArgs a) {
+    __shared__ int64_t wf[kPlanBlock / 64], wi[kPlanBlock / 64];
+    __shared__ unsigned long long s_of, s_oi;
+    const int tid = threadIdx.x;
+    const int b = blockIdx.x;
+    if (tid == 0) {
+        s_of = 0;
+        s_oi = 0;
+    }
+    __syncthreads();
+    {  // offsets of this block: the sums of the blocks before it
+        int64_t vf = 0, vi = 0;
+        for (int j = tid; j < b; j += kPlanBlock) {
+            vf += a.cblk[2 * j];
+            vi += a.cblk[2 * j + 1];
+        }
+        if (vf) atomicAdd(&s_of, (unsigned long long)vf);
+        if (vi) atomicAdd(&s_oi, (unsigned long long)vi);
+    }
+    const int64_t j = (int64_t)b * kPlanBlock + tid;
+    int64_t f0, it0;
+    chunk_items(a, j, f0, it0);
+    int64_t f = f0, it = it0;
+    block_scan2(f, it, wf, wi);  // its barrier also orders the offsets above
+    const int64_t pos = (int64_t)s_of + f - f0, item = (int64_t)s_oi + it - it0;
+    if (f0) {
+        a.list_c[pos] = a.chunk_c[j];
+        a.list_k[pos] = a.chunk_k[j];
+        a.list_item[pos] = item;
+    }
+    if (b == (int)gridDim.x - 1 && tid == kPlanBlock - 1) {
+        *a.list_n = (int64_t)s_of + f;
+        a.list_item[(int64_t)s_of + f] = (int64_t)s_oi + it;
+    }
+}
+
 void launch_pairing(const WaveArgs& a, hipStream_t s) {
     const int64_t n = (int64_t)a.n_q * a.n_qtok * a.nprobe;
     const unsigned pb = (unsigned)((n + 255) / 256);
@@ -108,6 +193,14 @@ void launch_pairing(const WaveArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(k_cplan_local, dim3(nblk), dim3(kPlanBlock), 0, s, a);
     hipLaunchKernelGGL(k_cplan_add, dim3(nblk), dim3(kPlanBlock), 0, s, a);
     hipLaunchKernelGGL(k_pair_scatter, dim3(pb), dim3(256), 0, s, a);
+    const unsigned cb = (unsigned)((a.n_chunks + kPlanBlock - 1) / kPlanBlock);
+    if (cb == 0) {  // an index without embeddings: no chunk, no item
+        launch_fill_i32(reinterpret_cast<int32_t*>(a.list_n), 2, 0, s);
+        launch_fill_i32(reinterpret_cast<int32_t*>(a.list_item), 2, 0, s);
+        return;
+    }
+    hipLaunchKernelGGL(k_chunk_count, dim3(cb), dim3(kPlanBlock), 0, s, a);
+    hipLaunchKernelGGL(k_chunk_list, dim3(cb), dim3(kPlanBlock), 0, s, a);
 }
 
 }  // namespace warp

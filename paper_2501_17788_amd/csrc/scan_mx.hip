@@ -124,15 +124,15 @@ __device__ __forceinline__ T plan_load(const T* p, int64_t i) {
     return ((const __attribute__((address_space(4))) T*)p)[i];
 }
 
-__device__ __forceinline__ MxItem mx_decode(const WaveArgs& a, int64_t item, int c) {
+// item of the wave's probed-chunk list entry p (its chunk's token group item - list_item[p])
+__device__ __forceinline__ MxItem mx_decode(const WaveArgs& a, int64_t item, int64_t p) {
     MxItem it;
+    const int c = plan_load(a.list_c, p);
+    const int k = plan_load(a.list_k, p);
+    const int grp = (int)(item - plan_load(a.list_item, p));
     const int nt = plan_load(a.ccount, c);
-    const unsigned groups = (unsigned)(nt + kMxGroup - 1) / kMxGroup;
-    const unsigned l = (unsigned)(item - plan_load(a.item_start, c));  // below 2^31: chunks x groups
-    const unsigned chunk = l / groups;
-    const int grp = (int)(l - chunk * groups);
     it.c = c;
-    it.e0 = plan_load(a.offsets, c) + (int64_t)chunk * kMxChunk;
+    it.e0 = plan_load(a.offsets, c) + (int64_t)k * kMxChunk;
     const int64_t end = plan_load(a.offsets, c + 1);
     it.e1 = it.e0 + kMxChunk < end ? it.e0 + kMxChunk : end;
     it.p0 = plan_load(a.pair_start, c) + grp * kMxGroup;
@@ -179,6 +179,7 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
     __shared__ int s_rdoc[kMxChunk];         // document of each run
     __shared__ int s_rstart[kMxChunk];       // its first embedding in the chunk
     __shared__ int s_wruns[NW];              // runs starting in each wave's quarter of the chunk
+    __shared__ unsigned s_claim;             // the batch thread 0 claimed
     __shared__ unsigned s_wd[NBITS == 8 ? 256 : 1];  // b = 8: the three digits of Q(omega[v]) in bytes 0..2
 
     const int tid = threadIdx.x;
@@ -204,20 +205,40 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
         s_wd[tid] = ((unsigned)d[0] & 255u) | (((unsigned)d[1] & 255u) << 8) | (((unsigned)d[2] & 255u) << 16);
     }
 
-    const int n_c = a.n_c;
-    const int64_t* item_start = a.item_start;
-    const int64_t total = plan_load(item_start, n_c);
-    const int64_t G = gridDim.x;
-    const int64_t first = total * blockIdx.x / G;
-    const int64_t last = total * (blockIdx.x + 1) / G;
-    if (first >= last) return;
-    int lo = 0, hi = n_c;  // cluster of the first item: item_start[c] <= first < item_start[c + 1]
-    while (hi - lo > 1) {
-        const int mid = (lo + hi) >> 1;
-        if (plan_load(item_start, mid) <= first) lo = mid;
-        else hi = mid;
-    }
-    int c = lo;  // cluster of the newest decoded item
+    // Items of the wave's probed chunks, in the index's chunk order, in batches of R =
+    // kScanBatch: workgroup b starts with batch b; every later batch is claimed from the
+    // batch counter (which starts at G) when the workgroup takes the first item of the batch
+    // before it. Thread 0 claims with a wrapping increment (which the compiler does not turn
+    // into a wave-wide add that waits for its result); the claimed batch reaches every wave
+    // through LDS after the next item's staging wait, so a claim adds no wait. Consecutive
+    // claims of the grid lie in unrelated clusters, since the chunk order is shuffled.
+    const int64_t n_list = plan_load(a.list_n, 0);
+    const int64_t* list_item = a.list_item;
+    const int64_t total = plan_load(list_item, n_list);
+    int64_t gpos = (int64_t)blockIdx.x * kScanBatch;
+    if (gpos >= total) return;
+    int64_t gend = gpos + kScanBatch < total ? gpos + kScanBatch : total;
+    int64_t nb = -1;       // first item of the next batch, once claimed and published
+    bool claimed = false;  // a claim is in flight (wave-uniform)
+    unsigned claim = 0;    // thread 0: the batch its claim returned
+    auto request = [&]() {
+        if (tid == 0) claim = atomicInc(a.scan_queue, 0xFFFFFFFFu);
+        claimed = true;
+    };
+    // The next item of the workgroup, or -1. A claim is issued on entering a batch and
+    // published before the next call, so the workgroup never runs out of known items
+    // while a batch remains; the prologue's claim is still in flight when the first batch
+    // ends only if that batch was cut short by the last item, and then nothing is left.
+    auto next_item = [&]() -> int64_t {
+        if (gpos < gend) return gpos++;
+        if (nb < 0 || nb >= total) return -1;
+        gpos = nb;
+        gend = nb + kScanBatch < total ? nb + kScanBatch : total;
+        nb = -1;
+        request();
+        return gpos++;
+    };
+    int64_t p = 0;  // list entry of the newest decoded item; items increase along the sequence
     const v4i* qdig = reinterpret_cast<const v4i*>(a.qdig);
     const int32_t* __restrict__ plist = a.plist;
     const uint8_t* __restrict__ codes = a.codes;
@@ -276,20 +297,37 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
             }
         }
     };
+    // the list entry of item (at or after p): galloping from p, then bisection
     auto decode_item = [&](int64_t item) {
-        while (plan_load(item_start, c + 1) <= item) ++c;
-        return mx_decode(a, item, c);
+        if (plan_load(list_item, p + 1) <= item) {
+            int64_t lo = p + 1, step = 1, hi = lo + 1;  // list_item[lo] <= item
+            while (hi < n_list && plan_load(list_item, hi) <= item) {
+                lo = hi;
+                step <<= 1;
+                hi = lo + step;
+            }
+            if (hi > n_list) hi = n_list;  // list_item[hi] > item
+            while (hi - lo > 1) {
+                const int64_t mid = (lo + hi) >> 1;
+                if (plan_load(list_item, mid) <= item) lo = mid;
+                else hi = mid;
+            }
+            p = lo;
+        }
+        return mx_decode(a, item, p);
     };
 
-    MxItem it = mx_decode(a, first, c), nx = it;
+    request();
+    MxItem it = decode_item(next_item()), nx = it;
     int ptok[QPT];
     MxStage<QPT> st;
     unsigned w[TPW][CW];
     load_tokens(it, ptok);
     load_stage(it, ptok, st, true);
     load_codes(it, w);
-    if (first + 1 < last) {
-        nx = decode_item(first + 1);
+    int64_t nxi = next_item();
+    if (nxi >= 0) {
+        nx = decode_item(nxi);
         load_tokens(nx, ptok);
     }
 
@@ -297,7 +335,7 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
     // valid while consecutive items share a chunk (the token groups of one chunk).
     int64_t run_e0 = -1;  // first embedding of the chunk whose runs are in LDS
     int n_runs = 0;
-    for (int64_t item = first; item < last; ++item) {
+    for (;;) {
         __syncthreads();  // the previous item's table is flushed and its tokens are no longer read
         // stage the item from registers
         if (tid < kMxGroup) {  // tokens past the group's end have zero digits and seeds: score 0 = absent
@@ -312,6 +350,7 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
             const int k = tid + kMxBlock * i;
             s_q[k % NSLOT][k / NSLOT] = st.q[i];
         }
+        if (tid == 0 && claimed) s_claim = claim;  // after the wait for the staged data
         // runs of equal documents along a new chunk (ids ascend inside a cluster)
         if (it.e0 != run_e0) {  // wave-uniform
             run_e0 = it.e0;
@@ -336,16 +375,21 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
                 }
             }
         }
-        // prefetch: the next item's query digits, bases and documents, then the tokens of the
-        // item after it
-        const bool has_next = item + 1 < last;
+        // prefetch: the next item's query digits, bases and documents, then (once a claim
+        // is published) the tokens of the item after it
+        const bool has_next = nxi >= 0;
         if (has_next) load_stage(nx, ptok, st, nx.e0 != it.e0);
+        __syncthreads();
+        if (claimed) {
+            nb = (int64_t)s_claim * kScanBatch;
+            claimed = false;
+        }
         MxItem nn = nx;
-        if (item + 2 < last) {
-            nn = decode_item(item + 2);
+        const int64_t nni = has_next ? next_item() : -1;
+        if (nni >= 0) {
+            nn = decode_item(nni);
             load_tokens(nn, ptok);
         }
-        __syncthreads();
 
         const int n_et = (int)((it.e1 - it.e0 + 15) >> 4);
         const int n_tt = (it.np + 15) >> 4;
@@ -461,8 +505,10 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
                 if (a.tokcnt) atomicAdd(&a.tokcnt[o], len);
             }
         }
+        if (!has_next) break;
         it = nx;
         nx = nn;
+        nxi = nni;
     }
 }
 
@@ -479,6 +525,8 @@ void launch_qdigits(const WaveArgs& a, hipStream_t s) {
 
 void launch_scan_mx(const WaveArgs& a, hipStream_t s) {
     const dim3 grid(a.scan_grid), block(kMxBlock);
+    // the first batch of every workgroup is fixed; the counter hands out the rest
+    launch_fill_i32(reinterpret_cast<int32_t*>(a.scan_queue), 1, a.scan_grid, s);
     switch (a.nbits) {
         case 1: hipLaunchKernelGGL(k_scan_mx<1>, grid, block, 0, s, a); break;
         case 2: hipLaunchKernelGGL(k_scan_mx<2>, grid, block, 0, s, a); break;
