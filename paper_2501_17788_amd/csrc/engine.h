@@ -47,6 +47,7 @@ constexpr int kQdigBytes = 3 * kDim;  // three base-256 digit planes of a query 
 // signed base-256 digits, i.e. lie in [-8421504, 8355711].
 constexpr float kMaxWeight = 1.99f;
 constexpr int kPlanBlock = 1024;  // clusters (chunks) per block of the work plan's prefix sums
+constexpr int kRecLenShift = 48;   // a chunk's length above its first embedding (< 2^40) in a list record
 
 // Error bits the device reports through the index's flag word.
 constexpr int kErrSelOverflow = 1;
@@ -95,8 +96,9 @@ struct WaveArgs {
     const int32_t* chunk_c;     // [n_chunks] cluster of each chunk of the index, in that order
     const int32_t* chunk_k;     // [n_chunks] its chunk within the cluster
     int64_t n_chunks;
-    int32_t* list_c;            // [n_chunks] the probed chunks of the wave, in that order: cluster
-    int32_t* list_k;            // [n_chunks] and chunk
+    int4* list_rec;             // [n_chunks] the probed chunks of the wave, in that order: first
+                                // embedding (x, y: low and high words; the chunk's length in the
+                                // top bits of y), first pair of the cluster (z), probing tokens (w)
     int64_t* list_item;         // [n_chunks + 1] exclusive prefix of their items; list_item[*list_n] = total
     int64_t* list_n;            // [1] number of probed chunks
     int64_t* cblk;              // [2 * ceil(n_chunks / kPlanBlock)] block sums of probed chunks and items

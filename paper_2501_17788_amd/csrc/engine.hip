@@ -80,7 +80,7 @@ struct warp_index {
     hipStream_t side = nullptr;
     int tab_cur = 0;                   // table of the next wave in two-table mode
     DevBuf ccount, cursor, item_start, pair_start, plist, qdig, blk;
-    DevBuf list_c, list_k, list_item, cblk;  // the wave's probed chunks (see WaveArgs)
+    DevBuf list_rec, list_item, cblk;  // the wave's probed chunks (see WaveArgs)
     DevBuf scan_queue;
     int32_t scoring = WARP_SCORING_PAPER;
     DevBuf tokcnt, doc_len;    // Eq.-1-literal scoring only
@@ -337,8 +337,7 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, bool two_tables, 
     if (!rc) rc = grow(idx->qdig, (size_t)n_tok * kQdigBytes);
     if (!rc) rc = grow(idx->blk, (size_t)nblk * 16);
     const int64_t cblocks = (idx->n_chunks + kPlanBlock - 1) / kPlanBlock;
-    if (!rc) rc = grow(idx->list_c, (size_t)idx->n_chunks * 4);
-    if (!rc) rc = grow(idx->list_k, (size_t)idx->n_chunks * 4);
+    if (!rc) rc = grow(idx->list_rec, (size_t)idx->n_chunks * 16);
     if (!rc) rc = grow(idx->list_item, ((size_t)idx->n_chunks + 2) * 8);  // + the count
     if (!rc) rc = grow(idx->cblk, (size_t)cblocks * 16);
     if (!rc) rc = grow(idx->scan_queue, 256);
@@ -516,8 +515,7 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         a.chunk_c = idx->chunk_c;
         a.chunk_k = idx->chunk_k;
         a.n_chunks = idx->n_chunks;
-        a.list_c = (int32_t*)idx->list_c.p;
-        a.list_k = (int32_t*)idx->list_k.p;
+        a.list_rec = (int4*)idx->list_rec.p;
         a.list_item = (int64_t*)idx->list_item.p;
         a.list_n = (int64_t*)idx->list_item.p + idx->n_chunks + 1;
         a.cblk = (int64_t*)idx->cblk.p;
@@ -668,7 +666,7 @@ void warp_index_free(warp_index* idx) {
             if (p) (void)hipFree(p);
         for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_pref, &idx->m_fixed,
                           &idx->tokmax, &idx->tokmax2, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount, &idx->cursor, &idx->item_start,
-                          &idx->pair_start, &idx->plist, &idx->qdig, &idx->blk, &idx->list_c, &idx->list_k, &idx->list_item, &idx->cblk, &idx->scan_queue, &idx->st_q, &idx->st_ids, &idx->st_scores,
+                          &idx->pair_start, &idx->plist, &idx->qdig, &idx->blk, &idx->list_rec, &idx->list_item, &idx->cblk, &idx->scan_queue, &idx->st_q, &idx->st_ids, &idx->st_scores,
                           &idx->st_fixed, &idx->st_counts, &idx->st_sel, &idx->st_m, &idx->st_bitmap,
                           &idx->st_scored})
             release(*b);

@@ -174,8 +174,12 @@ __global__ __launch_bounds__(kPlanBlock) void k_chunk_list(WaveArgs a) {
     block_scan2(f, it, wf, wi);  // its barrier also orders the offsets above
     const int64_t pos = (int64_t)s_of + f - f0, item = (int64_t)s_oi + it - it0;
     if (f0) {
-        a.list_c[pos] = a.chunk_c[j];
-        a.list_k[pos] = a.chunk_k[j];
+        const int c = a.chunk_c[j];
+        const int64_t e0 = a.offsets[c] + (int64_t)a.chunk_k[j] * kMxChunk;
+        const int64_t e1 = a.offsets[c + 1];
+        const int64_t len = e1 - e0 < kMxChunk ? e1 - e0 : kMxChunk;  // 1 .. kMxChunk
+        const uint64_t ew = (uint64_t)e0 | ((uint64_t)len << kRecLenShift);
+        a.list_rec[pos] = make_int4((int)(uint32_t)ew, (int)(uint32_t)(ew >> 32), a.pair_start[c], a.ccount[c]);
         a.list_item[pos] = item;
     }
     if (b == (int)gridDim.x - 1 && tid == kPlanBlock - 1) {

@@ -110,7 +110,6 @@ __global__ __launch_bounds__(256) void k_qdigits(const float* __restrict__ q, in
 }
 
 struct MxItem {
-    int c;        // cluster
     int64_t e0;   // first embedding of the chunk
     int64_t e1;   // end of the chunk
     int p0, np;   // pairs [p0, p0 + np) of the token group
@@ -124,18 +123,16 @@ __device__ __forceinline__ T plan_load(const T* p, int64_t i) {
     return ((const __attribute__((address_space(4))) T*)p)[i];
 }
 
-// item of the wave's probed-chunk list entry p (its chunk's token group item - list_item[p])
-__device__ __forceinline__ MxItem mx_decode(const WaveArgs& a, int64_t item, int64_t p) {
+// item of the wave's probed-chunk list entry p, whose record is rec (its chunk's token
+// group item - list_item[p])
+__device__ __forceinline__ MxItem mx_decode(const v4i rec, int64_t item, int64_t item0) {
     MxItem it;
-    const int c = plan_load(a.list_c, p);
-    const int k = plan_load(a.list_k, p);
-    const int grp = (int)(item - plan_load(a.list_item, p));
-    const int nt = plan_load(a.ccount, c);
-    it.c = c;
-    it.e0 = plan_load(a.offsets, c) + (int64_t)k * kMxChunk;
-    const int64_t end = plan_load(a.offsets, c + 1);
-    it.e1 = it.e0 + kMxChunk < end ? it.e0 + kMxChunk : end;
-    it.p0 = plan_load(a.pair_start, c) + grp * kMxGroup;
+    const uint64_t ew = (uint64_t)(uint32_t)rec[0] | ((uint64_t)(uint32_t)rec[1] << 32);
+    const int grp = (int)(item - item0);
+    const int nt = rec[3];
+    it.e0 = (int64_t)(ew & ((1ull << kRecLenShift) - 1));
+    it.e1 = it.e0 + (int64_t)(ew >> kRecLenShift);
+    it.p0 = rec[2] + grp * kMxGroup;
     it.np = nt - grp * kMxGroup < kMxGroup ? nt - grp * kMxGroup : kMxGroup;
     return it;
 }
@@ -297,7 +294,10 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
             }
         }
     };
-    // the list entry of item (at or after p): galloping from p, then bisection
+    // the list entry of item (at or after p): galloping from p, then bisection; the entry's
+    // record and first item are read once per entry
+    v4i rec = {0, 0, 0, 0};
+    int64_t rec_p = -1, rec_item = 0;
     auto decode_item = [&](int64_t item) {
         if (plan_load(list_item, p + 1) <= item) {
             int64_t lo = p + 1, step = 1, hi = lo + 1;  // list_item[lo] <= item
@@ -314,7 +314,12 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
             }
             p = lo;
         }
-        return mx_decode(a, item, p);
+        if (p != rec_p) {
+            rec_p = p;
+            rec = plan_load(reinterpret_cast<const v4i*>(a.list_rec), p);
+            rec_item = plan_load(list_item, p);
+        }
+        return mx_decode(rec, item, rec_item);
     };
 
     request();
