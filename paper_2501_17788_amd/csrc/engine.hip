@@ -42,6 +42,7 @@ int fail(int code, const char* fmt, ...) {
 
 constexpr uint64_t kMagic = 0x5741525049445831ull;  // "WARPIDX1"
 constexpr int kStages = 6;
+constexpr int64_t kTwoTableMinWave = 256;  // queries
 
 struct DevBuf {
     void* p = nullptr;
@@ -388,9 +389,11 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, bool two_tables, 
 // WARP_SCRATCH_MB if set, else 60% of the device memory that is free or already
 // held as scratch by this index. A larger wave lets the cluster-major scan read
 // each probed cluster once for more queries.
-// Two-table mode (see the index) is taken when the second table does not shrink the
-// wave and a table is large enough (WARP_TWO_TABLES_MIN_MB, default 64 MiB) for the
-// fold's resets to cost more than the side-stream zeroing and its synchronisation.
+// Two-table mode (see the index) is taken when a table is large enough
+// (WARP_TWO_TABLES_MIN_MB, default 64 MiB) for the fold's resets to cost more than the
+// side-stream zeroing and its synchronisation, and the second table either does not
+// shrink the wave or leaves it at least kTwoTableMinWave queries: a smaller wave costs the
+// cluster-major scan a little reuse, which the fold's read-only pass repays.
 int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T, bool* two_tables) {
     const size_t held = idx->tokmax.bytes + idx->tokmax2.bytes + idx->filter.bytes + idx->keys.bytes +
                         idx->plist.bytes + idx->qdig.bytes;
@@ -417,8 +420,9 @@ int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T, bool* 
     const int64_t qw2 = clamp((int64_t)(budget / (per + (size_t)T * idx->n_docs * 4)));
     int64_t min_mb = 64;
     if (const char* s = std::getenv("WARP_TWO_TABLES_MIN_MB")) min_mb = std::atoll(s);
-    *two_tables = idx->scoring == WARP_SCORING_PAPER && qw2 >= qw && qw * T * idx->n_docs * 4 >= (min_mb << 20);
-    return (int32_t)qw;
+    *two_tables = idx->scoring == WARP_SCORING_PAPER && (qw2 >= qw || qw2 >= kTwoTableMinWave) &&
+                  qw2 * T * idx->n_docs * 4 >= (min_mb << 20);
+    return (int32_t)(*two_tables ? qw2 : qw);
 }
 
 hipEvent_t take_event(warp_index* idx) {

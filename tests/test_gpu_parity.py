@@ -115,6 +115,7 @@ CASES = [
     (10, 60, 400, 12, 1, 4, 32, 9, 100, 30),    # one bit per dimension
     (11, 60, 400, 12, 8, 4, 32, 9, 100, 30),    # eight bits per dimension
     (12, 300, 3000, 40, 8, 3, 32, 48, 800, 200),
+    (13, 40, 303, 12, 4, 3, 32, 9, 100, 30),     # a document count that is not a multiple of 4
 ]
 
 
