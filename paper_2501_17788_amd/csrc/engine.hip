@@ -77,7 +77,8 @@ struct warp_index {
     DevBuf tokmax2;
     int64_t tab_ready[2] = {0, 0};     // leading cells of each table that hold kTokAbsent once zeroed
     bool tab_zeroing[2] = {false, false};  // a zeroing of the table is enqueued on the side stream
-    hipEvent_t tab_folded[2] = {}, tab_zeroed[2] = {};
+    int64_t tab_pending[2] = {0, 0};       // 16-byte units of a folded table still to be zeroed
+    hipEvent_t tab_folded[2] = {}, tab_zeroed[2] = {}, tab_filter = nullptr;
     hipStream_t side = nullptr;
     int tab_cur = 0;                   // table of the next wave in two-table mode
     DevBuf ccount, cursor, item_start, pair_start, plist, qdig, blk;
@@ -353,6 +354,7 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, bool two_tables, 
             if (rc) return rc;
             idx->tab_ready[t] = 0;
             idx->tab_zeroing[t] = false;
+            idx->tab_pending[t] = 0;
         }
         if (idx->tab_ready[t] < need) {
             launch_fill_i32((int32_t*)tab.p, need, (int32_t)kTokAbsent, s);
@@ -366,6 +368,8 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, bool two_tables, 
             if (hipEventCreateWithFlags(&idx->tab_folded[t], hipEventDisableTiming) != hipSuccess ||
                 hipEventCreateWithFlags(&idx->tab_zeroed[t], hipEventDisableTiming) != hipSuccess)
                 return fail(WARP_EDEVICE, "hipEventCreate failed");
+        if (hipEventCreateWithFlags(&idx->tab_filter, hipEventDisableTiming) != hipSuccess)
+            return fail(WARP_EDEVICE, "hipEventCreate failed");
     }
     if (idx->scoring == WARP_SCORING_EQ1_LITERAL) {
         if ((int64_t)(idx->tokcnt.bytes / 4) < need) {
@@ -536,6 +540,20 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         mark(0);
         launch_filter_gemm(a.queries, nq * T, idx->centroids, idx->n_c, a.filter_bins, nullptr, s);
         mark(1);
+        for (int t = 0; t < 2; ++t) {  // zero folded tables on the side stream, after this filter
+            if (!idx->tab_pending[t]) continue;
+            if (t == tab && !two) {  // one-table mode writes this table next: zero it in order
+                launch_zero16(t ? idx->tokmax2.p : idx->tokmax.p, idx->tab_pending[t], s);
+            } else {
+                HIP_TRY(hipEventRecord(idx->tab_filter, s));
+                HIP_TRY(hipStreamWaitEvent(idx->side, idx->tab_folded[t], 0));
+                HIP_TRY(hipStreamWaitEvent(idx->side, idx->tab_filter, 0));
+                launch_zero16(t ? idx->tokmax2.p : idx->tokmax.p, idx->tab_pending[t], idx->side);
+                HIP_TRY(hipEventRecord(idx->tab_zeroed[t], idx->side));
+                idx->tab_zeroing[t] = true;
+            }
+            idx->tab_pending[t] = 0;
+        }
         launch_select(a, s);
         mark(2);
         launch_scored(a, s);
@@ -552,12 +570,9 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         mark(5);
         launch_topk(a, s);
         mark(6);
-        if (two) {  // zero the folded table on the side stream
+        if (two) {  // the folded table is zeroed after the next wave's filter
             HIP_TRY(hipEventRecord(idx->tab_folded[tab], s));
-            HIP_TRY(hipStreamWaitEvent(idx->side, idx->tab_folded[tab], 0));
-            launch_zero16(a.tokmax, ((int64_t)nq * T * idx->n_docs + 3) / 4, idx->side);
-            HIP_TRY(hipEventRecord(idx->tab_zeroed[tab], idx->side));
-            idx->tab_zeroing[tab] = true;
+            idx->tab_pending[tab] = ((int64_t)nq * T * idx->n_docs + 3) / 4;
             idx->tab_cur = 1 - tab;
         }
         if (idx->timing)
@@ -682,6 +697,7 @@ void warp_index_free(warp_index* idx) {
                 if (idx->tab_folded[t]) (void)hipEventDestroy(idx->tab_folded[t]);
                 if (idx->tab_zeroed[t]) (void)hipEventDestroy(idx->tab_zeroed[t]);
             }
+            if (idx->tab_filter) (void)hipEventDestroy(idx->tab_filter);
             (void)hipStreamDestroy(idx->side);
         }
         if (idx->stream) (void)hipStreamDestroy(idx->stream);
