@@ -44,11 +44,15 @@
  * search runs in waves of as many queries as the scratch budget holds: the value
  * of the environment variable WARP_SCRATCH_MB (MiB) if set, else 60% of the free
  * device memory. The dominant scratch is a [tokens][documents] table of token
- * maxima per wave. When the whole batch fits one wave even with two such tables,
- * and a table is at least WARP_TWO_TABLES_MIN_MB MiB (default 64), waves
- * alternate between two tables and a table is zeroed after its fold on a second
- * stream of the index (default priority), ordered by events; otherwise the fold
- * resets the table it reads.
+ * maxima per wave. When a table is at least WARP_TWO_TABLES_MIN_MB MiB (default
+ * 64) and a second table either leaves the wave as large or at least 256 queries,
+ * waves alternate between two tables, and a folded table is zeroed on a second
+ * stream of the index (default priority), ordered by events, while the next wave
+ * runs; otherwise the fold resets the table it reads.
+ *
+ * Top-k. The final selection visits only the blocks of 256 documents whose best
+ * score can reach the k-th, when at most WARP_TOPK_LIST_BLOCKS (default and
+ * largest 4096; 0 turns this off) such blocks exist; results do not depend on it.
  */
 #ifndef WARP_H
 #define WARP_H

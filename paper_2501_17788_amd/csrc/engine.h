@@ -14,6 +14,7 @@ constexpr int kMaxQtok = 32;       // query_maxlen
 constexpr int kMaxProbe = 256;     // largest n_probe the selection and scan kernels hold
 constexpr int kMaxK = 4096;        // largest k the device top-k sorts
 constexpr int kMaxDocs = 1 << 24;  // document ids packed into the low 24 bits of a sort key
+constexpr int kTopkListCap = 4096;  // blocks of 256 documents the top-k's pruned passes can list
 // Token-max cells hold t + 2^31 as unsigned (an order-preserving bias); 0 marks
 // "no retrieved embedding", as no token score reaches -2^31.
 constexpr uint32_t kTokAbsent = 0;
@@ -113,6 +114,7 @@ struct WaveArgs {
     uint32_t* dbg_bitmap;       // [n_q][ceil(n_docs / 32)] or null
     int64_t* dbg_scored;        // [n_q] or null
     int32_t scan_grid;          // persistent workgroups of the residual scan
+    int32_t topk_list_cap;      // at most kTopkListCap; the top-k visits every block when more pass
 };
 
 // out_bins [n_tok][n_c] u16 bins (the search path) or, if null, out_scores fp32

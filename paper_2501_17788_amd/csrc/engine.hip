@@ -429,6 +429,14 @@ int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T, bool* 
     return (int32_t)(*two_tables ? qw2 : qw);
 }
 
+// Blocks the top-k may list for its pruned passes: kTopkListCap, or fewer with
+// WARP_TOPK_LIST_BLOCKS (0 turns the pruning off).
+int32_t topk_list_cap() {
+    int64_t v = kTopkListCap;
+    if (const char* s = std::getenv("WARP_TOPK_LIST_BLOCKS")) v = std::atoll(s);
+    return (int32_t)(v < 0 ? 0 : (v > kTopkListCap ? kTopkListCap : v));
+}
+
 hipEvent_t take_event(warp_index* idx) {
     if (!idx->ev_pool.empty()) {
         hipEvent_t e = idx->ev_pool.back();
@@ -530,6 +538,7 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         a.scan_queue = (uint32_t*)idx->scan_queue.p;
         a.qdig = (int8_t*)idx->qdig.p;
         a.scan_grid = idx->scan_grid;
+        a.topk_list_cap = topk_list_cap();
 
         hipEvent_t ev[kStages + 1] = {};
         if (idx->timing)

@@ -5,8 +5,13 @@
 // better, and the score is key >> 24 (offset). The fold leaves, per block of
 // 256 documents, the candidate count and the largest key.
 //
-// With K = min(k, candidates), the K largest keys are found in one or two
-// histogram passes over the keys: bins of the distance below the largest score
+// With K = min(k, candidates), histograms of the blocks' largest keys (coarse, then
+// fine inside the crossing bin) first give a distance D0 below the best score such
+// that at least K block maxima, hence at least K keys, lie within it: every one of the
+// K largest keys then lies in a block whose maximum is within D0, and the keys of any
+// other block are smaller than all of these. The passes below visit only those blocks,
+// listed in LDS (all blocks when more than kTopkListCap pass, or no D0 is found). The
+// K largest keys are found in one or two histogram passes over the keys: bins of the distance below the largest score
 // (4096 bins of 2^-6, then, inside the bin holding the K-th key, 4096 bins of
 // 2^-18), after which every key at or above the bin holding the K-th key is
 // gathered (at most kMaxK), sorted in LDS, and the first K decoded. When the
@@ -60,25 +65,27 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
     __shared__ uint32_t hist[kTopkBins];
     __shared__ uint32_t scan[kTopkThreads];
     __shared__ unsigned long long buf[kMaxK];
+    __shared__ int32_t blist[kTopkListCap];
     __shared__ unsigned long long s_prefix, s_mask, s_max, s_lim;
-    __shared__ uint32_t s_need, s_count, s_ncand, s_before;
+    __shared__ uint32_t s_need, s_count, s_ncand, s_before, s_nlist;
     __shared__ int s_bin;
 
     const int q = blockIdx.x;
     const int tid = threadIdx.x;
     const int64_t n = a.n_docs;
+    const int64_t nb = (n + 255) / 256;
     const unsigned long long* keys = reinterpret_cast<const unsigned long long*>(a.keys) + (int64_t)q * n;
+    const uint64_t* part = a.qpart + 2 * (int64_t)q * nb;
 
     // candidates and the largest key, from the fold's per-block partials
     if (tid == 0) {
         s_ncand = 0;
         s_max = 0;
         s_count = 0;
+        s_nlist = 0;
     }
     __syncthreads();
     {
-        const int64_t nb = (n + 255) / 256;
-        const uint64_t* part = a.qpart + 2 * (int64_t)q * nb;
         unsigned long long cnt = 0, mx = 0;
         for (int64_t b = tid; b < nb; b += kTopkThreads) {
             cnt += part[2 * b];
@@ -93,16 +100,74 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
     const unsigned long long smax = s_max >> 24;  // the best (offset) score
 
     bool done = K == 0;
+    // D0 from the block maxima: coarse bins, then fine bins inside the crossing one
+    unsigned long long d0 = 0;  // 0: no pruning
+    if (!done) {
+        for (int i = tid; i < kTopkBins; i += kTopkThreads) hist[i] = 0;
+        __syncthreads();
+        for (int64_t b = tid; b < nb; b += kTopkThreads) {
+            const unsigned long long mx = part[2 * b + 1];
+            if (mx == 0) continue;
+            const unsigned long long d = smax - (mx >> 24);
+            if (d < ((unsigned long long)kTopkBins << kCoarseShift)) atomicAdd(&hist[d >> kCoarseShift], 1u);
+        }
+        __syncthreads();
+        find_crossing(hist, (uint32_t)K, scan, &s_bin, &s_before);
+        const int b1 = s_bin;
+        if (b1 >= 0) {
+            const uint32_t need = (uint32_t)K - s_before;
+            __syncthreads();
+            for (int i = tid; i < kTopkBins; i += kTopkThreads) hist[i] = 0;
+            __syncthreads();
+            const unsigned long long base = (unsigned long long)b1 << kCoarseShift;
+            for (int64_t b = tid; b < nb; b += kTopkThreads) {
+                const unsigned long long mx = part[2 * b + 1];
+                if (mx == 0) continue;
+                const unsigned long long d = smax - (mx >> 24);
+                if (d >= base && d - base < (1ull << kCoarseShift)) atomicAdd(&hist[(d - base) >> kFineShift], 1u);
+            }
+            __syncthreads();
+            find_crossing(hist, need, scan, &s_bin, &s_before);
+            d0 = base + ((unsigned long long)(s_bin + 1) << kFineShift);  // the crossing exists
+        }
+        if (d0 != 0) {
+            for (int64_t b = tid; b < nb; b += kTopkThreads) {
+                const unsigned long long mx = part[2 * b + 1];
+                if (mx != 0 && smax - (mx >> 24) < d0) {
+                    const uint32_t p = atomicAdd(&s_nlist, 1u);
+                    if (p < (uint32_t)kTopkListCap) blist[p] = (int32_t)b;
+                }
+            }
+        }
+        __syncthreads();
+    }
+    const uint32_t nlist = s_nlist;
+    const bool pruned = d0 != 0 && nlist <= (uint32_t)a.topk_list_cap;
+    // every key of the listed blocks, or of all blocks
+    auto for_each_key = [&](auto&& f) {
+        if (pruned) {
+            for (int64_t j = tid; j < (int64_t)nlist * 256; j += kTopkThreads) {
+                const int64_t x = (int64_t)blist[j >> 8] * 256 + (j & 255);
+                if (x < n) {
+                    const unsigned long long key = keys[x];
+                    if (key != 0) f(key);
+                }
+            }
+        } else {
+            for (int64_t x = tid; x < n; x += kTopkThreads) {
+                const unsigned long long key = keys[x];
+                if (key != 0) f(key);
+            }
+        }
+    };
     // level 1: coarse bins of the distance below the best score
     if (!done) {
         for (int i = tid; i < kTopkBins; i += kTopkThreads) hist[i] = 0;
         __syncthreads();
-        for (int64_t x = tid; x < n; x += kTopkThreads) {
-            const unsigned long long key = keys[x];
-            if (key == 0) continue;
+        for_each_key([&](unsigned long long key) {
             const unsigned long long d = smax - (key >> 24);
             if (d < ((unsigned long long)kTopkBins << kCoarseShift)) atomicAdd(&hist[d >> kCoarseShift], 1u);
-        }
+        });
         __syncthreads();
         find_crossing(hist, (uint32_t)K, scan, &s_bin, &s_before);
         const int b1 = s_bin;
@@ -117,13 +182,11 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
                 for (int i = tid; i < kTopkBins; i += kTopkThreads) hist[i] = 0;
                 __syncthreads();
                 const unsigned long long base = (unsigned long long)b1 << kCoarseShift;
-                for (int64_t x = tid; x < n; x += kTopkThreads) {
-                    const unsigned long long key = keys[x];
-                    if (key == 0) continue;
+                for_each_key([&](unsigned long long key) {
                     const unsigned long long d = smax - (key >> 24);
                     if (d >= base && d - base < (1ull << kCoarseShift))
                         atomicAdd(&hist[(d - base) >> kFineShift], 1u);
-                }
+                });
                 __syncthreads();
                 find_crossing(hist, (uint32_t)K - above, scan, &s_bin, &s_before);
                 const int b2 = s_bin;
@@ -134,13 +197,12 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
             __syncthreads();
             lim = s_lim;
             if (lim != 0) {
-                for (int64_t x = tid; x < n; x += kTopkThreads) {
-                    const unsigned long long key = keys[x];
-                    if (key != 0 && smax - (key >> 24) < lim) {
+                for_each_key([&](unsigned long long key) {
+                    if (smax - (key >> 24) < lim) {
                         const uint32_t p = atomicAdd(&s_count, 1u);
                         if (p < (uint32_t)kMaxK) buf[p] = key;
                     }
-                }
+                });
                 done = true;
             }
         }
@@ -159,10 +221,9 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
             for (int i = tid; i < 256; i += kTopkThreads) hist[i] = 0;
             __syncthreads();
             const unsigned long long prefix = s_prefix, mask = s_mask;
-            for (int64_t x = tid; x < n; x += kTopkThreads) {
-                const unsigned long long key = keys[x];
-                if (key != 0 && (key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255], 1u);
-            }
+            for_each_key([&](unsigned long long key) {
+                if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255], 1u);
+            });
             __syncthreads();
             if (tid == 0) {
                 uint32_t need = s_need, cum = 0;
@@ -181,13 +242,12 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
             __syncthreads();
         }
         const unsigned long long kth = s_prefix;  // the K-th largest key
-        for (int64_t x = tid; x < n; x += kTopkThreads) {
-            const unsigned long long key = keys[x];
-            if (key != 0 && key >= kth) {
+        for_each_key([&](unsigned long long key) {
+            if (key >= kth) {
                 const uint32_t p = atomicAdd(&s_count, 1u);
                 if (p < (uint32_t)kMaxK) buf[p] = key;
             }
-        }
+        });
         __syncthreads();
     }
     // bitonic sort, descending, of the gathered keys padded with zeros; the first K are the result

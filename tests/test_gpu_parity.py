@@ -368,3 +368,47 @@ def test_consecutive_searches_reuse_the_token_max_tables(monkeypatch):
             want = oracle.search_index(data, queries=Q, nprobe=wl.nprobe, t_prime=wl.t_prime, k=wl.k,
                                        flags=oracle.EQ1_LITERAL if literal else 0)
             compare(got, want, label=f"tables search {j}")
+
+
+# ----------------------------------------------------------------------------- top-k
+
+def _tied_index(seed=21, n_tied=5000, n_other=1000, nbits=2):
+    """n_tied documents with one identical embedding each (equal scores, so the k-th
+    key sits in a tie far wider than the gather buffer) and n_other documents with
+    random codes in two other clusters."""
+    rng = np.random.default_rng(seed)
+    C = rng.standard_normal((4, 128))
+    C = (C / np.linalg.norm(C, axis=1, keepdims=True)).astype(np.float32)
+    other = rng.integers(1, 3, n_other)
+    order = np.argsort(other, kind="stable")
+    clusters = np.concatenate([np.zeros(n_tied, np.int64), other[order]])
+    doc_ids = np.concatenate([rng.permutation(n_tied), n_tied + order]).astype(np.int32)
+    per_dim = np.zeros((n_tied + n_other, 128), np.int64)
+    per_dim[n_tied:] = rng.integers(0, 1 << nbits, (n_other, 128))
+    from helpers import pack_msb_first
+    offsets = np.zeros(5, np.int64)
+    np.cumsum(np.bincount(clusters, minlength=4), out=offsets[1:])
+    w = np.array([-0.05, -0.01, 0.01, 0.05], np.float32)
+    Q = rng.standard_normal((3, 8, 128))
+    Q = (Q / np.linalg.norm(Q, axis=2, keepdims=True)).astype(np.float32)
+    return dict(centroids=C, offsets=offsets, doc_ids=doc_ids, codes=pack_msb_first(per_dim, nbits),
+                nbits=nbits, bucket_weights=w, n_docs=n_tied + n_other), Q
+
+
+@pytest.mark.parametrize("cap", [None, "1", "0"], ids=["pruned", "cap1", "unpruned"])
+def test_topk_ties_and_block_pruning(cap, monkeypatch):
+    """The top-k's pruned passes (blocks whose best key can reach the k-th), its
+    fallback to every block, and its exact radix select inside a wide tie."""
+    w = _engine()
+    if cap is not None:
+        monkeypatch.setenv("WARP_TOPK_LIST_BLOCKS", cap)
+    arrays, Q = _tied_index()
+    for k in (4096, 100, 1):
+        say(f"[topk ties cap={cap}] k={k}")
+        with w.Index(**arrays) as ix:
+            got = ix.search_debug(Q, 4, 0, k)
+        want = oracle.search(queries=Q, nprobe=4, t_prime=0, k=k, **arrays)
+        compare(got, want, label=f"ties cap={cap} k={k}")
+    wl = synth.random_small_workload(8, n_centroids=300, n_docs=5000, max_len=30, nbits=4, n_queries=3,
+                                     n_qtok=32, nprobe=256, t_prime=2000, k=4096)
+    run_both(synth.make_index(wl, workers=1), label=f"seed 8 cap={cap}")
