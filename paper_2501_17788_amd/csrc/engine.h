@@ -15,8 +15,8 @@ constexpr int kMaxProbe = 256;     // largest n_probe the selection and scan ker
 constexpr int kMaxK = 4096;        // largest k the device top-k sorts
 constexpr int kMaxDocs = 1 << 24;  // document ids packed into the low 24 bits of a sort key
 constexpr int kTopkListCap = 4096;  // blocks of 256 documents the top-k's pruned passes can list
-// Token-max cells hold t + 2^31 as unsigned (an order-preserving bias); 0 marks
-// "no retrieved embedding", as no token score reaches -2^31.
+// A token-max cell holds t + tok_bias of the wave that wrote it (an order-preserving bias);
+// the wave's cells below tok_vmin hold no retrieved embedding. A zeroed cell holds kTokAbsent.
 constexpr uint32_t kTokAbsent = 0;
 
 // Centroid selection: the fp32 matrix-core scores are within kFilterEps of the
@@ -75,8 +75,10 @@ struct WaveArgs {
     int32_t* base;              // [n_tok][nprobe]  R(S64) of the probed centroids
     int64_t* seg_pref;          // [n_tok][nprobe + 1] cumulative probed sizes
     int64_t* m_fixed;           // [n_tok]
-    uint32_t* tokmax;           // [n_tok][n_docs] biased token maxima, kTokAbsent when not retrieved
-    int32_t fold_reset;         // 1: the fold resets the cells it reads; 0: the table is zeroed on a side stream
+    uint32_t* tokmax;           // [n_tok][n_docs] biased token maxima
+    uint32_t tok_bias;          // e 2^w + 2^(w-1) for a wave of epoch e >= 1; 2^31 when cells are reset
+    uint32_t tok_vmin;          // e 2^w; 1 when cells are reset
+    int32_t fold_reset;         // 1: the fold resets the cells it reads to kTokAbsent
     uint32_t* tokcnt;           // [n_tok][n_docs] retrieved embeddings per (token, doc); only for the
                                 // Eq.-1-literal scoring, else null
     const int32_t* doc_len;     // [n_docs] embeddings per document (Eq.-1-literal scoring)

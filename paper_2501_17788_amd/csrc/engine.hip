@@ -42,7 +42,7 @@ int fail(int code, const char* fmt, ...) {
 
 constexpr uint64_t kMagic = 0x5741525049445831ull;  // "WARPIDX1"
 constexpr int kStages = 6;
-constexpr int64_t kTwoTableMinWave = 256;  // queries
+constexpr int32_t kTabForceZero = 1 << 30;  // tab_epoch value that makes the next search zero the table
 
 struct DevBuf {
     void* p = nullptr;
@@ -70,17 +70,17 @@ struct warp_index {
     int scan_grid = 0;     // persistent workgroups of the residual scan
     // per-search scratch, grown on demand
     DevBuf filter, sel, base, seg_pref, m_fixed, tokmax, keys, qpart;
-    // A second token-max table: when the whole batch fits one wave even with two tables,
-    // waves alternate between them and the fold only reads; a folded table is zeroed on a
-    // side stream while the next wave selects centroids on the other one, and the wave
-    // after that waits for the zeroing before its scan writes the table.
-    DevBuf tokmax2;
-    int64_t tab_ready[2] = {0, 0};     // leading cells of each table that hold kTokAbsent once zeroed
-    bool tab_zeroing[2] = {false, false};  // a zeroing of the table is enqueued on the side stream
-    int64_t tab_pending[2] = {0, 0};       // 16-byte units of a folded table still to be zeroed
-    hipEvent_t tab_folded[2] = {}, tab_zeroed[2] = {}, tab_filter = nullptr;
-    hipStream_t side = nullptr;
-    int tab_cur = 0;                   // table of the next wave in two-table mode
+    // Token-max table. A wave of epoch e >= 1 stores t + e 2^w + 2^(w-1) in a cell, where
+    // 2^(w-1) exceeds every |t| that the bucket weights and the norm limits allow: values of
+    // earlier epochs all lie below e 2^w, so the fold reads them as absent and never resets a
+    // cell. After the last epoch, 2^(32-w) - 1, the cells written since the last zeroing are
+    // zeroed. When no bit is spare (w = 32) and in the Eq.-1-literal mode, a cell holds
+    // t + 2^31, 0 is absent, and the fold resets every cell it reads.
+    int32_t tab_w = 32;
+    int32_t tab_epochs = 0;  // 2^(32-w) - 1, if at least 2; 0: the fold resets cells
+    int32_t tab_epoch = 0;   // epoch of the last wave since the last zeroing (kTabForceZero: zero first)
+    int64_t tab_cells = 0;   // cells the table holds; all were zeroed when it was allocated
+    int64_t tab_hi = 0;      // cells below this may hold values written since the last zeroing
     DevBuf ccount, cursor, item_start, pair_start, plist, qdig, blk;
     DevBuf list_rec, list_item, cblk;  // the wave's probed chunks (see WaveArgs)
     DevBuf scan_queue;
@@ -169,6 +169,22 @@ int validate_index_host(const float* C, int32_t n_c, int32_t dim, const int64_t*
         if (std::fabs(std::sqrt(s) - 1.0) > 1e-3) return fail(WARP_EINVAL, "centroid %d is not of unit norm", c);
     }
     return WARP_OK;
+}
+
+// Width w of a token-max cell's value field: the smallest w with 2^(w-1) above a bound B on
+// |t| (units of 2^-26) for queries and centroids of norm at most 1 + 1e-3 and these bucket
+// weights: |R(S64)| <= 1.001^2 2^26 + 1 and |floor(V 2^-18 + 1/2)| <= (sum_d |Q(q_d)|)
+// (max_b |Q(omega_b)|) 2^-18 + 1, with sum_d |Q(q_d)| <= sqrt(128) 1.001 2^22 + 64 and
+// |Q(omega_b)| <= |omega_b| 2^22 + 1/2. At the largest weights accepted, w = 32.
+int32_t token_value_width(const float* w, int32_t nbits) {
+    double wmax = 0;
+    for (int b = 0; b < (1 << nbits); ++b) wmax = std::fmax(wmax, std::fabs((double)w[b]));
+    const double qsum = std::sqrt((double)kDim) * 1.001 * 4194304.0 + 0.5 * kDim;
+    const double bound = 1.001 * 1.001 * 67108864.0 + 1.0 + qsum * (wmax * 4194304.0 + 0.5) / 262144.0 + 1.0;
+    const double b = bound * (1.0 + 1e-5) + 64.0;
+    int32_t width = 2;
+    while (width < 32 && std::ldexp(1.0, width - 1) <= b) ++width;
+    return width;
 }
 
 int validate_queries_host(const float* q, int64_t n_tok) {
@@ -283,6 +299,9 @@ int load_common(const float* C, int32_t n_c, int32_t dim, const int64_t* off, co
     idx->n_docs = n_docs;
     idx->nbits = nbits;
     idx->n_emb = voff[n_c];
+    idx->tab_w = token_value_width(vw, nbits);
+    const int32_t epochs = (int32_t)((1ll << (32 - idx->tab_w)) - 1);
+    idx->tab_epochs = epochs >= 2 ? epochs : 0;  // one epoch per zeroing saves nothing over resets
     const size_t row = (size_t)kDim * nbits / 8;
     const hipMemcpyKind kind = device_ptrs ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
     auto alloc = [&](void** p, size_t bytes) -> int {
@@ -320,7 +339,7 @@ int load_common(const float* C, int32_t n_c, int32_t dim, const int64_t* off, co
 
 // Device scratch for a wave of `qw` queries of `T` tokens; the fills are enqueued on the
 // search stream `s`, after the searches before it.
-int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, bool two_tables, hipStream_t s) {
+int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, hipStream_t s) {
     const int64_t n_tok = (int64_t)qw * T;
     int rc = WARP_OK;
     if (!rc) rc = grow(idx->filter, (size_t)n_tok * idx->n_c * 2);
@@ -344,32 +363,24 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, bool two_tables, 
     if (!rc) rc = grow(idx->cblk, (size_t)cblocks * 16);
     if (!rc) rc = grow(idx->scan_queue, 256);
     if (rc) return rc;
-    // token-max tables: cells rounded up to whole 16-byte units (the scan zeroes units);
-    // every cell the wave can touch holds kTokAbsent when it starts
+    // the token-max table, in cells rounded up to whole 16-byte units (zeroed in units)
     const int64_t need = (n_tok * idx->n_docs + 3) & ~(int64_t)3;
-    for (int t = 0; t < (two_tables ? 2 : 1); ++t) {
-        DevBuf& tab = t ? idx->tokmax2 : idx->tokmax;
-        if ((int64_t)(tab.bytes / 4) < need) {
-            rc = grow(tab, (size_t)need * 4);  // hipFree waits for the device, zeroings included
-            if (rc) return rc;
-            idx->tab_ready[t] = 0;
-            idx->tab_zeroing[t] = false;
-            idx->tab_pending[t] = 0;
-        }
-        if (idx->tab_ready[t] < need) {
-            launch_fill_i32((int32_t*)tab.p, need, (int32_t)kTokAbsent, s);
-            idx->tab_ready[t] = need;
-        }
+    if (idx->tab_cells < need) {
+        idx->tab_cells = 0;
+        rc = grow(idx->tokmax, (size_t)need * 4);
+        if (rc) return rc;
+        launch_zero16(idx->tokmax.p, need / 4, s);
+        idx->tab_cells = need;
+        idx->tab_epoch = 0;
+        idx->tab_hi = 0;
     }
-    if (two_tables && !idx->side) {
-        if (hipStreamCreateWithFlags(&idx->side, hipStreamNonBlocking) != hipSuccess)
-            return fail(WARP_EDEVICE, "hipStreamCreate failed");
-        for (int t = 0; t < 2; ++t)
-            if (hipEventCreateWithFlags(&idx->tab_folded[t], hipEventDisableTiming) != hipSuccess ||
-                hipEventCreateWithFlags(&idx->tab_zeroed[t], hipEventDisableTiming) != hipSuccess)
-                return fail(WARP_EDEVICE, "hipEventCreate failed");
-        if (hipEventCreateWithFlags(&idx->tab_filter, hipEventDisableTiming) != hipSuccess)
-            return fail(WARP_EDEVICE, "hipEventCreate failed");
+    // a table holding values of some epoch is zeroed before a search that resets cells, and
+    // after a search whose queries failed the norm check (their scores can exceed 2^(w-1))
+    const bool resets = idx->scoring == WARP_SCORING_EQ1_LITERAL || idx->tab_epochs == 0;
+    if (idx->tab_epoch == kTabForceZero || (resets && idx->tab_epoch != 0)) {
+        launch_zero16(idx->tokmax.p, idx->tab_hi / 4, s);
+        idx->tab_epoch = 0;
+        idx->tab_hi = 0;
     }
     if (idx->scoring == WARP_SCORING_EQ1_LITERAL) {
         if ((int64_t)(idx->tokcnt.bytes / 4) < need) {
@@ -393,14 +404,9 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, bool two_tables, 
 // WARP_SCRATCH_MB if set, else 60% of the device memory that is free or already
 // held as scratch by this index. A larger wave lets the cluster-major scan read
 // each probed cluster once for more queries.
-// Two-table mode (see the index) is taken when a table is large enough
-// (WARP_TWO_TABLES_MIN_MB, default 64 MiB) for the fold's resets to cost more than the
-// side-stream zeroing and its synchronisation, and the second table either does not
-// shrink the wave or leaves it at least kTwoTableMinWave queries: a smaller wave costs the
-// cluster-major scan a little reuse, which the fold's read-only pass repays.
-int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T, bool* two_tables) {
-    const size_t held = idx->tokmax.bytes + idx->tokmax2.bytes + idx->filter.bytes + idx->keys.bytes +
-                        idx->plist.bytes + idx->qdig.bytes;
+int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T) {
+    const size_t held = idx->tokmax.bytes + idx->filter.bytes + idx->keys.bytes + idx->plist.bytes +
+                        idx->qdig.bytes;
     size_t budget = 0;
     if (const char* s = std::getenv("WARP_SCRATCH_MB")) {
         budget = (size_t)std::atoll(s) << 20;
@@ -420,13 +426,7 @@ int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T, bool* 
         if (q > 65535) q = 65535;
         return q < 1 ? (int64_t)1 : q;
     };
-    const int64_t qw = clamp((int64_t)(budget / per));
-    const int64_t qw2 = clamp((int64_t)(budget / (per + (size_t)T * idx->n_docs * 4)));
-    int64_t min_mb = 64;
-    if (const char* s = std::getenv("WARP_TWO_TABLES_MIN_MB")) min_mb = std::atoll(s);
-    *two_tables = idx->scoring == WARP_SCORING_PAPER && (qw2 >= qw || qw2 >= kTwoTableMinWave) &&
-                  qw2 * T * idx->n_docs * 4 >= (min_mb << 20);
-    return (int32_t)(*two_tables ? qw2 : qw);
+    return (int32_t)clamp((int64_t)(budget / per));
 }
 
 // Blocks the top-k may list for its pruned passes: kTopkListCap, or fewer with
@@ -477,9 +477,8 @@ struct SearchOut {
 // Enqueue a whole search on `s`; every pointer is device memory.
 int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t T, int32_t P,
                    int64_t t_prime, int32_t k, const SearchOut& o, hipStream_t s) {
-    bool two = false;
-    const int32_t qw = wave_queries(idx, n_queries, T, &two);
-    int rc = reserve(idx, qw, T, P, two, s);
+    const int32_t qw = wave_queries(idx, n_queries, T);
+    int rc = reserve(idx, qw, T, P, s);
     if (rc) return rc;
     launch_check_queries(dq, (int64_t)n_queries * T, idx->err, s);
     const int64_t words = ((int64_t)idx->n_docs + 31) / 32;
@@ -506,9 +505,19 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         a.base = (int32_t*)idx->base.p;
         a.seg_pref = (int64_t*)idx->seg_pref.p;
         a.m_fixed = (int64_t*)idx->m_fixed.p;
-        const int tab = two ? idx->tab_cur : 0;
-        a.tokmax = (uint32_t*)(tab ? idx->tokmax2.p : idx->tokmax.p);
-        a.fold_reset = two ? 0 : 1;
+        a.tokmax = (uint32_t*)idx->tokmax.p;
+        const int64_t wave_cells = ((int64_t)nq * T * idx->n_docs + 3) & ~(int64_t)3;
+        if (idx->scoring == WARP_SCORING_EQ1_LITERAL || idx->tab_epochs == 0) {
+            a.tok_bias = 1u << 31;
+            a.tok_vmin = 1;
+            a.fold_reset = 1;
+        } else {
+            const uint32_t e = (uint32_t)++idx->tab_epoch;
+            a.tok_bias = (e << idx->tab_w) + (1u << (idx->tab_w - 1));
+            a.tok_vmin = e << idx->tab_w;
+            a.fold_reset = 0;
+            if (idx->tab_hi < wave_cells) idx->tab_hi = wave_cells;
+        }
         a.tokcnt = idx->scoring == WARP_SCORING_EQ1_LITERAL ? (uint32_t*)idx->tokcnt.p : nullptr;
         a.doc_len = (const int32_t*)idx->doc_len.p;
         a.keys = (uint64_t*)idx->keys.p;
@@ -549,41 +558,23 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         mark(0);
         launch_filter_gemm(a.queries, nq * T, idx->centroids, idx->n_c, a.filter_bins, nullptr, s);
         mark(1);
-        for (int t = 0; t < 2; ++t) {  // zero folded tables on the side stream, after this filter
-            if (!idx->tab_pending[t]) continue;
-            if (t == tab && !two) {  // one-table mode writes this table next: zero it in order
-                launch_zero16(t ? idx->tokmax2.p : idx->tokmax.p, idx->tab_pending[t], s);
-            } else {
-                HIP_TRY(hipEventRecord(idx->tab_filter, s));
-                HIP_TRY(hipStreamWaitEvent(idx->side, idx->tab_folded[t], 0));
-                HIP_TRY(hipStreamWaitEvent(idx->side, idx->tab_filter, 0));
-                launch_zero16(t ? idx->tokmax2.p : idx->tokmax.p, idx->tab_pending[t], idx->side);
-                HIP_TRY(hipEventRecord(idx->tab_zeroed[t], idx->side));
-                idx->tab_zeroing[t] = true;
-            }
-            idx->tab_pending[t] = 0;
-        }
         launch_select(a, s);
         mark(2);
         launch_scored(a, s);
         launch_pairing(a, s);
         launch_qdigits(a, s);
         mark(3);
-        if (idx->tab_zeroing[tab]) {  // the table's zeroing precedes its next scan
-            HIP_TRY(hipStreamWaitEvent(s, idx->tab_zeroed[tab], 0));
-            idx->tab_zeroing[tab] = false;
-        }
         launch_scan_mx(a, s);
         mark(4);
         launch_fold(a, s);
+        if (idx->tab_epochs != 0 && idx->tab_epoch == idx->tab_epochs) {  // the last epoch is folded
+            launch_zero16(idx->tokmax.p, idx->tab_hi / 4, s);
+            idx->tab_epoch = 0;
+            idx->tab_hi = 0;
+        }
         mark(5);
         launch_topk(a, s);
         mark(6);
-        if (two) {  // the folded table is zeroed after the next wave's filter
-            HIP_TRY(hipEventRecord(idx->tab_folded[tab], s));
-            idx->tab_pending[tab] = ((int64_t)nq * T * idx->n_docs + 3) / 4;
-            idx->tab_cur = 1 - tab;
-        }
         if (idx->timing)
             for (int e = 0; e <= kStages; ++e) idx->ev_pending.push_back(ev[e]);
         hipError_t le = hipGetLastError();
@@ -598,6 +589,7 @@ int read_device_errors(warp_index* idx, hipStream_t s) {
     HIP_TRY(hipStreamSynchronize(s));
     if (idx->timing) settle_timings(idx);
     if (err) launch_fill_i32(idx->err, 1, 0, s);
+    if ((err & kErrQueryNorm) && idx->tab_epoch != 0) idx->tab_epoch = kTabForceZero;
     if (err & kErrQueryNorm)
         return fail(WARP_EINVAL, "a query token is not finite or has norm > 1 + 1e-3");
     if (err & kErrSelOverflow)
@@ -693,22 +685,13 @@ void warp_index_free(warp_index* idx) {
                         (void*)idx->codes, (void*)idx->weights, (void*)idx->err})
             if (p) (void)hipFree(p);
         for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_pref, &idx->m_fixed,
-                          &idx->tokmax, &idx->tokmax2, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount, &idx->cursor, &idx->item_start,
+                          &idx->tokmax, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount, &idx->cursor, &idx->item_start,
                           &idx->pair_start, &idx->plist, &idx->qdig, &idx->blk, &idx->list_rec, &idx->list_item, &idx->cblk, &idx->scan_queue, &idx->st_q, &idx->st_ids, &idx->st_scores,
                           &idx->st_fixed, &idx->st_counts, &idx->st_sel, &idx->st_m, &idx->st_bitmap,
                           &idx->st_scored})
             release(*b);
         for (hipEvent_t e : idx->ev_pool) (void)hipEventDestroy(e);
         for (hipEvent_t e : idx->ev_pending) (void)hipEventDestroy(e);
-        if (idx->side) {
-            (void)hipStreamSynchronize(idx->side);
-            for (int t = 0; t < 2; ++t) {
-                if (idx->tab_folded[t]) (void)hipEventDestroy(idx->tab_folded[t]);
-                if (idx->tab_zeroed[t]) (void)hipEventDestroy(idx->tab_zeroed[t]);
-            }
-            if (idx->tab_filter) (void)hipEventDestroy(idx->tab_filter);
-            (void)hipStreamDestroy(idx->side);
-        }
         if (idx->stream) (void)hipStreamDestroy(idx->stream);
         idx->magic = 0;
     }

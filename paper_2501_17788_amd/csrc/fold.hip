@@ -4,9 +4,10 @@
 // the token strides gives this sum, so one pass per document computes it.
 //
 // One thread per (query, document): the n_qtok token rows are read with coalesced
-// loads, all issued before the first is used. With one token-max table the fold
-// resets the cells it read to kTokAbsent for the next wave; with two, the next
-// wave's scan zeroes this table and the fold only reads. The output is a sort key
+// loads, all issued before the first is used. A cell at or above the wave's tok_vmin
+// holds t + tok_bias; a lower one (zeroed, or written by an earlier wave) is not
+// retrieved. The fold only reads, unless the wave resets cells (fold_reset), in
+// which case it zeroes every retrieved cell it read. The output is a sort key
 // per document: ((score + 2^39) << 24) | (2^24 - 1 - doc), larger is better and
 // equal scores order by lower document id; 0 marks a non-candidate.
 #include "engine.h"
@@ -26,6 +27,8 @@ __global__ __launch_bounds__(256) void k_fold(WaveArgs a) {
         // R(m_i) of the query's tokens: wave-uniform, read through the scalar cache
         const auto* m = (const __attribute__((address_space(4))) int64_t*)(a.m_fixed + (int64_t)q * T);
         uint32_t* cnt = a.tokcnt ? a.tokcnt + (int64_t)q * T * nd + doc : nullptr;
+        const uint32_t vmin = a.tok_vmin;
+        const int64_t bias = (int64_t)a.tok_bias;
         uint32_t v[kMaxQtok];
 #pragma unroll
         for (int i = 0; i < kMaxQtok; ++i) v[i] = i < T ? col[i * nd] : kTokAbsent;
@@ -34,24 +37,24 @@ __global__ __launch_bounds__(256) void k_fold(WaveArgs a) {
 #pragma unroll
             for (int i = 0; i < kMaxQtok; ++i) {
                 if (i < T) {
-                    any |= v[i] != kTokAbsent;
-                    sum += v[i] != kTokAbsent ? (int64_t)(int32_t)(v[i] ^ 0x80000000u) : m[i];
+                    any |= v[i] >= vmin;
+                    sum += v[i] >= vmin ? (int64_t)v[i] - bias : m[i];
                 }
             }
             if (a.fold_reset) {
 #pragma unroll
                 for (int i = 0; i < kMaxQtok; ++i)
-                    if (i < T && v[i] != kTokAbsent) col[i * nd] = kTokAbsent;
+                    if (i < T && v[i] >= vmin) col[i * nd] = kTokAbsent;
             }
         } else {
             // Eq. 1 read literally: while some of the document's tokens were not retrieved
-            // for this query token, the estimate m_i bounds it from below
+            // for this query token, the estimate m_i bounds it from below (cells are reset)
             const int32_t len = a.doc_len[doc];
             for (int i = 0; i < T; ++i) {
                 const uint32_t n = cnt[i * nd];
-                if (v[i] != kTokAbsent) {
+                if (v[i] >= vmin) {
                     any = true;
-                    int64_t t = (int32_t)(v[i] ^ 0x80000000u);
+                    int64_t t = (int64_t)v[i] - bias;
                     if ((int32_t)n < len && t < m[i]) t = m[i];
                     sum += t;
                     col[i * nd] = kTokAbsent;

@@ -30,8 +30,7 @@ void launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s) {
     hipLaunchKernelGGL(k_fill_i32, dim3((unsigned)blocks), dim3(256), 0, s, p, n, v);
 }
 
-// Zeroes `units` 16-byte units with non-temporal stores (no L2 allocation), from a grid
-// small enough to leave most of the GPU to the kernels it runs beside.
+// Zeroes `units` 16-byte units with non-temporal stores (no L2 allocation).
 __global__ __launch_bounds__(256) void k_zero16(unsigned __attribute__((ext_vector_type(4)))* p, int64_t units) {
     typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
     const u32x4 z = {0u, 0u, 0u, 0u};
@@ -43,7 +42,7 @@ __global__ __launch_bounds__(256) void k_zero16(unsigned __attribute__((ext_vect
 void launch_zero16(void* p, int64_t units, hipStream_t s) {
     if (units <= 0) return;
     int64_t blocks = (units + 255) / 256;
-    if (blocks > 128) blocks = 128;
+    if (blocks > 8192) blocks = 8192;
     hipLaunchKernelGGL(k_zero16, dim3((unsigned)blocks), dim3(256), 0, s,
                        reinterpret_cast<unsigned __attribute__((ext_vector_type(4)))*>(p), units);
 }

@@ -261,6 +261,9 @@ def test_async_query_norm_error_reported_by_sync():
         assert e.value.code == w.EINVAL and "norm" in e.value.msg
         ix.search_async(torch.from_numpy(data.queries).cuda(), 4, 10, 5)
         ix.sync()  # cleared
+        # the table written by the failed search is zeroed before it is used again
+        got = ix.search_debug(data.queries, 4, 10, 5)
+    compare(got, oracle.search_index(data, nprobe=4, t_prime=10, k=5), label="after a norm error")
 
 
 # ----------------------------------------------------------------------------- the 256-query workload
@@ -345,29 +348,36 @@ def test_exact_halves_in_the_residual_term():
     run_both(data, queries=Q, label="exact halves")
 
 
-def test_consecutive_searches_reuse_the_token_max_tables(monkeypatch):
-    # waves alternate between two token-max tables when the batch fits one wave; a folded table
-    # is zeroed on a side stream before its next scan. Every search of a sequence with changing
-    # query counts must match the oracle, also around a search with one table (the Eq.-1-literal
-    # scoring resets in the fold) and with one query per wave (a 1 MiB scratch budget)
+@pytest.mark.parametrize("weight_scale", [1.0, 11.0], ids=["epochs", "resets"])
+def test_consecutive_searches_reuse_the_token_max_table(weight_scale, monkeypatch):
+    # Waves tag their token-max cells with an epoch, so a cell of an earlier wave reads as
+    # absent and the table is zeroed only when the epochs run out (7 of them for the tiny
+    # workload's weights); with bucket weights too large for a spare bit (scaled by 11), the
+    # fold resets every cell instead. Every search of a sequence with changing query counts
+    # must match the oracle: across several zeroings, around Eq.-1-literal searches (which
+    # reset cells, so the table is zeroed before them) and with one query per wave (a 1 MiB
+    # scratch budget: nine waves in one search)
     w = _engine()
     data = synth.make_index(synth.with_overrides(synth.WORKLOADS["tiny"], n_queries=9), workers=1)
+    data.bucket_weights = (data.bucket_weights * weight_scale).astype(np.float32)
+    assert np.abs(data.bucket_weights).max() <= 1.99
     wl = data.workload
     rng = np.random.default_rng(5)
-    batches = [data.queries[:5], data.queries[5:7], data.queries[:9], data.queries[2:3],
-               data.queries[rng.permutation(9)[:7]], data.queries[1:8]]
-    monkeypatch.setenv("WARP_TWO_TABLES_MIN_MB", "0")  # two tables also for these small tables
+    sizes = [5, 2, 9, 1, 7, 7, 3, 9, 4, 6, 9, 2, 8, 1, 5, 9]
     with w.Index.from_synthetic(data) as ix:
-        for j, Q in enumerate(batches):
-            literal = j == 3
+        for j, n in enumerate(sizes):
+            Q = data.queries[rng.permutation(9)[:n]]
+            literal = j in (3, 12)
             ix.set_scoring(w.SCORING_EQ1_LITERAL if literal else w.SCORING_PAPER)
-            if j == 5:
+            if j == 9:
                 monkeypatch.setenv("WARP_SCRATCH_MB", "1")
-            say(f"[tables] search {j}: {len(Q)} queries, literal={literal}")
+            if j == 11:
+                monkeypatch.delenv("WARP_SCRATCH_MB")
+            say(f"[table x{weight_scale}] search {j}: {n} queries, literal={literal}")
             got = ix.search_debug(Q, wl.nprobe, wl.t_prime, wl.k)
             want = oracle.search_index(data, queries=Q, nprobe=wl.nprobe, t_prime=wl.t_prime, k=wl.k,
                                        flags=oracle.EQ1_LITERAL if literal else 0)
-            compare(got, want, label=f"tables search {j}")
+            compare(got, want, label=f"table x{weight_scale} search {j}")
 
 
 # ----------------------------------------------------------------------------- top-k
