@@ -44,11 +44,12 @@
  * search runs in waves of as many queries as the scratch budget holds: the value
  * of the environment variable WARP_SCRATCH_MB (MiB) if set, else 60% of the free
  * device memory. The dominant scratch is a [tokens][documents] table of token
- * maxima per wave. Each wave tags its cells with an epoch in the bits that the
- * score range leaves spare (the range follows from the bucket weights and the
- * norm limits), so that cells of earlier waves read as empty; the table is zeroed
- * on the index's stream when the epochs run out (every 7 to 15 waves for bucket
- * weights below about 0.2). With weights too large for a spare bit, and in the
+ * maxima per wave, one slot of rows per query of the wave. Each wave tags its
+ * cells with its slots' epochs, in the bits that the score range leaves spare
+ * (the range follows from the bucket weights and the norm limits), so that cells
+ * of earlier waves read as empty; a slot's rows are zeroed on the index's stream
+ * when its epochs run out (every 7 to 15 waves that use it, for bucket weights
+ * below about 0.2). With weights too large for a spare bit, and in the
  * Eq.-1-literal mode, the final reduction instead resets every cell it reads.
  *
  * Top-k. The final selection visits only the blocks of 256 documents whose best

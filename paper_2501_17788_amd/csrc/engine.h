@@ -15,8 +15,9 @@ constexpr int kMaxProbe = 256;     // largest n_probe the selection and scan ker
 constexpr int kMaxK = 4096;        // largest k the device top-k sorts
 constexpr int kMaxDocs = 1 << 24;  // document ids packed into the low 24 bits of a sort key
 constexpr int kTopkListCap = 4096;  // blocks of 256 documents the top-k's pruned passes can list
-// A token-max cell holds t + tok_bias of the wave that wrote it (an order-preserving bias);
-// the wave's cells below tok_vmin hold no retrieved embedding. A zeroed cell holds kTokAbsent.
+// A token-max cell holds t plus the bias of its query's epoch (an order-preserving bias, see
+// cell_code); cells below the epoch's threshold hold no retrieved embedding of the wave. A
+// zeroed cell holds kTokAbsent.
 constexpr uint32_t kTokAbsent = 0;
 
 // Centroid selection: the fp32 matrix-core scores are within kFilterEps of the
@@ -76,9 +77,8 @@ struct WaveArgs {
     int64_t* seg_pref;          // [n_tok][nprobe + 1] cumulative probed sizes
     int64_t* m_fixed;           // [n_tok]
     uint32_t* tokmax;           // [n_tok][n_docs] biased token maxima
-    uint32_t tok_bias;          // e 2^w + 2^(w-1) for a wave of epoch e >= 1; 2^31 when cells are reset
-    uint32_t tok_vmin;          // e 2^w; 1 when cells are reset
-    int32_t fold_reset;         // 1: the fold resets the cells it reads to kTokAbsent
+    const uint32_t* q_epoch;    // [n_q] epoch e >= 1 of each query's token-max rows; null: cells are reset
+    int32_t tok_w;              // width w of a cell's value field (epochs in the bits above it)
     uint32_t* tokcnt;           // [n_tok][n_docs] retrieved embeddings per (token, doc); only for the
                                 // Eq.-1-literal scoring, else null
     const int32_t* doc_len;     // [n_docs] embeddings per document (Eq.-1-literal scoring)
@@ -90,7 +90,7 @@ struct WaveArgs {
     int32_t* cursor;            // [n_c] scatter cursors
     int64_t* item_start;        // [n_c + 1] exclusive prefix of work items
     int32_t* pair_start;        // [n_c + 1] exclusive prefix of pairs
-    int32_t* plist;             // [n_tok * nprobe][2]: (wave token, R(S64)) grouped by cluster
+    int32_t* plist;             // [n_tok * nprobe][2]: (wave token, R(S64) + cell bias) grouped by cluster
     int8_t* qdig;               // [n_tok][kQdigBytes] query digit planes in operand order
     int64_t* blk;               // [2 * ceil(n_c / kPlanBlock)] block sums of items and pairs
     // The scan's items run over the probed chunks in the index's fixed pseudo-random chunk
@@ -119,6 +119,20 @@ struct WaveArgs {
     int32_t topk_list_cap;      // at most kTopkListCap; the top-k visits every block when more pass
 };
 
+// Bias and threshold of the token-max cells of wave query q: with epochs, a cell holds
+// t + e 2^w + 2^(w-1) and the query's retrieved cells are those at or above e 2^w, where
+// 2^(w-1) exceeds every |t| the index admits; without, t + 2^31 and every nonzero cell,
+// and the fold resets what it reads.
+__device__ __forceinline__ void cell_code(const WaveArgs& a, int q, uint32_t& bias, uint32_t& vmin) {
+    if (!a.q_epoch) {
+        bias = 1u << 31;
+        vmin = 1;
+        return;
+    }
+    vmin = a.q_epoch[q] << a.tok_w;
+    bias = vmin + (1u << (a.tok_w - 1));
+}
+
 // out_bins [n_tok][n_c] u16 bins (the search path) or, if null, out_scores fp32
 void launch_filter_gemm(const float* q, int32_t n_tok, const float* c, int32_t n_c, uint16_t* out_bins,
                         float* out_scores, hipStream_t s);
@@ -131,7 +145,8 @@ int scan_mx_blocks_per_cu(int nbits);
 void launch_fold(const WaveArgs& a, hipStream_t s);
 void launch_topk(const WaveArgs& a, hipStream_t s);
 void launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
-void launch_zero16(void* p, int64_t units, hipStream_t s);  // units of 16 bytes, streaming stores
+void launch_zero_cells(uint32_t* p, int64_t n, hipStream_t s);  // streaming stores
+void launch_epoch_step(uint32_t* ep, int32_t n, uint32_t last, hipStream_t s);
 void launch_check_docs(const int32_t* ids, int64_t n, int32_t n_docs, int32_t* err, hipStream_t s);
 void launch_check_queries(const float* q, int64_t n_tok, int32_t* err, hipStream_t s);
 void launch_doc_len(const int32_t* doc_ids, int64_t n, int32_t* doc_len, int32_t n_docs, hipStream_t s);

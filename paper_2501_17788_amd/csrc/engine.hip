@@ -5,6 +5,7 @@
 // row per query token and one sort key per document for each of its queries.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -42,7 +43,6 @@ int fail(int code, const char* fmt, ...) {
 
 constexpr uint64_t kMagic = 0x5741525049445831ull;  // "WARPIDX1"
 constexpr int kStages = 6;
-constexpr int32_t kTabForceZero = 1 << 30;  // tab_epoch value that makes the next search zero the table
 
 struct DevBuf {
     void* p = nullptr;
@@ -70,17 +70,20 @@ struct warp_index {
     int scan_grid = 0;     // persistent workgroups of the residual scan
     // per-search scratch, grown on demand
     DevBuf filter, sel, base, seg_pref, m_fixed, tokmax, keys, qpart;
-    // Token-max table. A wave of epoch e >= 1 stores t + e 2^w + 2^(w-1) in a cell, where
-    // 2^(w-1) exceeds every |t| that the bucket weights and the norm limits allow: values of
-    // earlier epochs all lie below e 2^w, so the fold reads them as absent and never resets a
-    // cell. After the last epoch, 2^(32-w) - 1, the cells written since the last zeroing are
-    // zeroed. When no bit is spare (w = 32) and in the Eq.-1-literal mode, a cell holds
-    // t + 2^31, 0 is absent, and the fold resets every cell it reads.
+    // Token-max table [wave query slot][token][document]. The rows of query slot q carry an
+    // epoch e_q >= 1 that every wave using the slot advances: its cells hold
+    // t + e_q 2^w + 2^(w-1), where 2^(w-1) exceeds every |t| that the bucket weights and the
+    // norm limits allow, so values of earlier epochs lie below e_q 2^w, the fold reads them as
+    // absent and never resets a cell. A slot's rows are zeroed before a wave would take it
+    // past the last epoch, 2^(32-w) - 1. When no bit is spare and in the Eq.-1-literal mode,
+    // a cell holds t + 2^31, 0 is absent, and the fold resets every cell it reads.
     int32_t tab_w = 32;
-    int32_t tab_epochs = 0;  // 2^(32-w) - 1, if at least 2; 0: the fold resets cells
-    int32_t tab_epoch = 0;   // epoch of the last wave since the last zeroing (kTabForceZero: zero first)
-    int64_t tab_cells = 0;   // cells the table holds; all were zeroed when it was allocated
-    int64_t tab_hi = 0;      // cells below this may hold values written since the last zeroing
+    int32_t tab_epochs = 0;        // 2^(32-w) - 1, if at least 2; 0: the fold resets cells
+    int64_t tab_cells = 0;         // cells the table holds
+    int32_t tab_T = 0;             // tokens per query slot of the epochs' layout
+    bool tab_force_zero = false;   // zero every slot first (after a query-norm error)
+    std::vector<uint32_t> slot_ep; // epoch of each query slot's rows; 0: all zero
+    DevBuf q_epoch;                // device copy of slot_ep
     DevBuf ccount, cursor, item_start, pair_start, plist, qdig, blk;
     DevBuf list_rec, list_item, cblk;  // the wave's probed chunks (see WaveArgs)
     DevBuf scan_queue;
@@ -337,6 +340,35 @@ int load_common(const float* C, int32_t n_c, int32_t dim, const int64_t* off, co
     return WARP_OK;
 }
 
+// Zero the rows of every query slot whose epoch is not 0 (runs of consecutive slots at once).
+// With `only_last`, only of the slots of the first n at the last epoch, which the next wave
+// takes back to epoch 1.
+void zero_slots(warp_index* idx, int32_t n, bool only_last, hipStream_t s) {
+    const int64_t cells = (int64_t)idx->tab_T * idx->n_docs;
+    auto hit = [&](int32_t q) {
+        return only_last ? idx->slot_ep[q] == (uint32_t)idx->tab_epochs : idx->slot_ep[q] != 0;
+    };
+    for (int32_t q = 0; q < n;) {
+        if (!hit(q)) {
+            ++q;
+            continue;
+        }
+        int32_t q1 = q + 1;
+        while (q1 < n && hit(q1)) ++q1;
+        launch_zero_cells((uint32_t*)idx->tokmax.p + q * cells, (int64_t)(q1 - q) * cells, s);
+        q = q1;
+    }
+}
+
+void clear_slots(warp_index* idx, hipStream_t s) {
+    bool any = false;
+    for (uint32_t e : idx->slot_ep) any |= e != 0;
+    if (!any) return;
+    zero_slots(idx, (int32_t)idx->slot_ep.size(), false, s);
+    std::fill(idx->slot_ep.begin(), idx->slot_ep.end(), 0u);
+    launch_fill_i32((int32_t*)idx->q_epoch.p, (int64_t)idx->slot_ep.size(), 0, s);
+}
+
 // Device scratch for a wave of `qw` queries of `T` tokens; the fills are enqueued on the
 // search stream `s`, after the searches before it.
 int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, hipStream_t s) {
@@ -363,24 +395,30 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, hipStream_t s) {
     if (!rc) rc = grow(idx->cblk, (size_t)cblocks * 16);
     if (!rc) rc = grow(idx->scan_queue, 256);
     if (rc) return rc;
-    // the token-max table, in cells rounded up to whole 16-byte units (zeroed in units)
-    const int64_t need = (n_tok * idx->n_docs + 3) & ~(int64_t)3;
+    // the token-max table and its query slots' epochs. All slots are zeroed before a search
+    // that resets cells or lays the table out with another token count, and after a search
+    // whose queries failed the norm check (their scores can exceed 2^(w-1)).
+    const int64_t need = n_tok * idx->n_docs;
     if (idx->tab_cells < need) {
         idx->tab_cells = 0;
         rc = grow(idx->tokmax, (size_t)need * 4);
         if (rc) return rc;
-        launch_zero16(idx->tokmax.p, need / 4, s);
+        launch_zero_cells((uint32_t*)idx->tokmax.p, need, s);
         idx->tab_cells = need;
-        idx->tab_epoch = 0;
-        idx->tab_hi = 0;
+        std::fill(idx->slot_ep.begin(), idx->slot_ep.end(), 0u);
+        if (idx->q_epoch.p) launch_fill_i32((int32_t*)idx->q_epoch.p, (int64_t)idx->slot_ep.size(), 0, s);
     }
-    // a table holding values of some epoch is zeroed before a search that resets cells, and
-    // after a search whose queries failed the norm check (their scores can exceed 2^(w-1))
     const bool resets = idx->scoring == WARP_SCORING_EQ1_LITERAL || idx->tab_epochs == 0;
-    if (idx->tab_epoch == kTabForceZero || (resets && idx->tab_epoch != 0)) {
-        launch_zero16(idx->tokmax.p, idx->tab_hi / 4, s);
-        idx->tab_epoch = 0;
-        idx->tab_hi = 0;
+    if (idx->tab_force_zero || resets || T != idx->tab_T || (int64_t)idx->slot_ep.size() < qw) {
+        clear_slots(idx, s);
+        idx->tab_force_zero = false;
+        idx->tab_T = T;
+    }
+    if ((int64_t)idx->slot_ep.size() < qw) {
+        rc = grow(idx->q_epoch, (size_t)qw * 4);
+        if (rc) return rc;
+        idx->slot_ep.assign((size_t)qw, 0u);
+        launch_fill_i32((int32_t*)idx->q_epoch.p, qw, 0, s);
     }
     if (idx->scoring == WARP_SCORING_EQ1_LITERAL) {
         if ((int64_t)(idx->tokcnt.bytes / 4) < need) {
@@ -506,18 +544,9 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         a.seg_pref = (int64_t*)idx->seg_pref.p;
         a.m_fixed = (int64_t*)idx->m_fixed.p;
         a.tokmax = (uint32_t*)idx->tokmax.p;
-        const int64_t wave_cells = ((int64_t)nq * T * idx->n_docs + 3) & ~(int64_t)3;
-        if (idx->scoring == WARP_SCORING_EQ1_LITERAL || idx->tab_epochs == 0) {
-            a.tok_bias = 1u << 31;
-            a.tok_vmin = 1;
-            a.fold_reset = 1;
-        } else {
-            const uint32_t e = (uint32_t)++idx->tab_epoch;
-            a.tok_bias = (e << idx->tab_w) + (1u << (idx->tab_w - 1));
-            a.tok_vmin = e << idx->tab_w;
-            a.fold_reset = 0;
-            if (idx->tab_hi < wave_cells) idx->tab_hi = wave_cells;
-        }
+        const bool epochs = idx->scoring == WARP_SCORING_PAPER && idx->tab_epochs != 0;
+        a.q_epoch = epochs ? (const uint32_t*)idx->q_epoch.p : nullptr;
+        a.tok_w = idx->tab_w;
         a.tokcnt = idx->scoring == WARP_SCORING_EQ1_LITERAL ? (uint32_t*)idx->tokcnt.p : nullptr;
         a.doc_len = (const int32_t*)idx->doc_len.p;
         a.keys = (uint64_t*)idx->keys.p;
@@ -560,6 +589,12 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         mark(1);
         launch_select(a, s);
         mark(2);
+        if (epochs) {  // the slots' next epochs, after zeroing those past the last one
+            zero_slots(idx, nq, true, s);
+            for (int32_t q = 0; q < nq; ++q)
+                idx->slot_ep[q] = idx->slot_ep[q] >= (uint32_t)idx->tab_epochs ? 1u : idx->slot_ep[q] + 1u;
+            launch_epoch_step((uint32_t*)idx->q_epoch.p, nq, (uint32_t)idx->tab_epochs, s);
+        }
         launch_scored(a, s);
         launch_pairing(a, s);
         launch_qdigits(a, s);
@@ -567,11 +602,6 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         launch_scan_mx(a, s);
         mark(4);
         launch_fold(a, s);
-        if (idx->tab_epochs != 0 && idx->tab_epoch == idx->tab_epochs) {  // the last epoch is folded
-            launch_zero16(idx->tokmax.p, idx->tab_hi / 4, s);
-            idx->tab_epoch = 0;
-            idx->tab_hi = 0;
-        }
         mark(5);
         launch_topk(a, s);
         mark(6);
@@ -589,7 +619,7 @@ int read_device_errors(warp_index* idx, hipStream_t s) {
     HIP_TRY(hipStreamSynchronize(s));
     if (idx->timing) settle_timings(idx);
     if (err) launch_fill_i32(idx->err, 1, 0, s);
-    if ((err & kErrQueryNorm) && idx->tab_epoch != 0) idx->tab_epoch = kTabForceZero;
+    if (err & kErrQueryNorm) idx->tab_force_zero = true;
     if (err & kErrQueryNorm)
         return fail(WARP_EINVAL, "a query token is not finite or has norm > 1 + 1e-3");
     if (err & kErrSelOverflow)
@@ -685,7 +715,7 @@ void warp_index_free(warp_index* idx) {
                         (void*)idx->codes, (void*)idx->weights, (void*)idx->err})
             if (p) (void)hipFree(p);
         for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_pref, &idx->m_fixed,
-                          &idx->tokmax, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount, &idx->cursor, &idx->item_start,
+                          &idx->tokmax, &idx->q_epoch, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount, &idx->cursor, &idx->item_start,
                           &idx->pair_start, &idx->plist, &idx->qdig, &idx->blk, &idx->list_rec, &idx->list_item, &idx->cblk, &idx->scan_queue, &idx->st_q, &idx->st_ids, &idx->st_scores,
                           &idx->st_fixed, &idx->st_counts, &idx->st_sel, &idx->st_m, &idx->st_bitmap,
                           &idx->st_scored})

@@ -4,10 +4,10 @@
 // the token strides gives this sum, so one pass per document computes it.
 //
 // One thread per (query, document): the n_qtok token rows are read with coalesced
-// loads, all issued before the first is used. A cell at or above the wave's tok_vmin
-// holds t + tok_bias; a lower one (zeroed, or written by an earlier wave) is not
-// retrieved. The fold only reads, unless the wave resets cells (fold_reset), in
-// which case it zeroes every retrieved cell it read. The output is a sort key
+// loads, all issued before the first is used. A cell at or above the query's
+// threshold holds t plus the query's bias; a lower one (zeroed, or written by an
+// earlier wave) is not retrieved (cell_code). With epochs the fold only reads;
+// without, it zeroes every retrieved cell it read. The output is a sort key
 // per document: ((score + 2^39) << 24) | (2^24 - 1 - doc), larger is better and
 // equal scores order by lower document id; 0 marks a non-candidate.
 #include "engine.h"
@@ -27,8 +27,9 @@ __global__ __launch_bounds__(256) void k_fold(WaveArgs a) {
         // R(m_i) of the query's tokens: wave-uniform, read through the scalar cache
         const auto* m = (const __attribute__((address_space(4))) int64_t*)(a.m_fixed + (int64_t)q * T);
         uint32_t* cnt = a.tokcnt ? a.tokcnt + (int64_t)q * T * nd + doc : nullptr;
-        const uint32_t vmin = a.tok_vmin;
-        const int64_t bias = (int64_t)a.tok_bias;
+        uint32_t ubias, vmin;
+        cell_code(a, q, ubias, vmin);
+        const int64_t bias = (int64_t)ubias;
         uint32_t v[kMaxQtok];
 #pragma unroll
         for (int i = 0; i < kMaxQtok; ++i) v[i] = i < T ? col[i * nd] : kTokAbsent;
@@ -41,7 +42,7 @@ __global__ __launch_bounds__(256) void k_fold(WaveArgs a) {
                     sum += v[i] >= vmin ? (int64_t)v[i] - bias : m[i];
                 }
             }
-            if (a.fold_reset) {
+            if (!a.q_epoch) {
 #pragma unroll
                 for (int i = 0; i < kMaxQtok; ++i)
                     if (i < T && v[i] >= vmin) col[i * nd] = kTokAbsent;

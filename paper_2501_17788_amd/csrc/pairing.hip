@@ -95,8 +95,11 @@ __global__ __launch_bounds__(256) void k_pair_scatter(WaveArgs a) {
     if (c < 0) return;
     const int slot = atomicAdd(&a.cursor[c], 1);
     const int64_t p = (int64_t)a.pair_start[c] + slot;
-    a.plist[2 * p] = (int32_t)(i / a.nprobe);  // wave token
-    a.plist[2 * p + 1] = a.base[i];           // R(S64) of (token, cluster)
+    const int32_t tok = (int32_t)(i / a.nprobe);
+    uint32_t bias, vmin;
+    cell_code(a, tok / a.n_qtok, bias, vmin);
+    a.plist[2 * p] = tok;                                   // wave token
+    a.plist[2 * p + 1] = (int32_t)((uint32_t)a.base[i] + bias);  // R(S64) of (token, cluster) + the cell bias
 }
 
 // Probed chunks and their items (token groups of their cluster) in the index's chunk order.

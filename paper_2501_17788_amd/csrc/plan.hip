@@ -39,12 +39,33 @@ __global__ __launch_bounds__(256) void k_zero16(unsigned __attribute__((ext_vect
         __builtin_nontemporal_store(z, p + i);
 }
 
-void launch_zero16(void* p, int64_t units, hipStream_t s) {
-    if (units <= 0) return;
-    int64_t blocks = (units + 255) / 256;
-    if (blocks > 8192) blocks = 8192;
-    hipLaunchKernelGGL(k_zero16, dim3((unsigned)blocks), dim3(256), 0, s,
-                       reinterpret_cast<unsigned __attribute__((ext_vector_type(4)))*>(p), units);
+// Zeroes n 32-bit cells from p (4-byte aligned): the 16-byte units inside the range with
+// k_zero16, the cells before and after them with k_fill_i32.
+void launch_zero_cells(uint32_t* p, int64_t n, hipStream_t s) {
+    if (n <= 0) return;
+    int64_t head = (int64_t)((16 - ((uintptr_t)p & 15)) & 15) / 4;
+    if (head > n) head = n;
+    launch_fill_i32(reinterpret_cast<int32_t*>(p), head, 0, s);
+    const int64_t units = (n - head) / 4;
+    if (units > 0) {
+        int64_t blocks = (units + 255) / 256;
+        if (blocks > 8192) blocks = 8192;
+        hipLaunchKernelGGL(k_zero16, dim3((unsigned)blocks), dim3(256), 0, s,
+                           reinterpret_cast<unsigned __attribute__((ext_vector_type(4)))*>(p + head), units);
+    }
+    launch_fill_i32(reinterpret_cast<int32_t*>(p + head + 4 * units), n - head - 4 * units, 0, s);
+}
+
+// The next epoch of every query slot of a wave: 1 after the last one (whose rows the host
+// has just zeroed), else one more.
+__global__ void k_epoch_step(uint32_t* ep, int32_t n, uint32_t last) {
+    const int32_t i = blockIdx.x * 256 + threadIdx.x;
+    if (i < n) ep[i] = ep[i] >= last ? 1u : ep[i] + 1u;
+}
+
+void launch_epoch_step(uint32_t* ep, int32_t n, uint32_t last, hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_epoch_step, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, ep, n, last);
 }
 
 }  // namespace warp

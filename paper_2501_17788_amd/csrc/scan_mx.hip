@@ -13,8 +13,9 @@
 // for s = 0..4. Every A_s is an int8 matrix product over d, computed by
 // v_mfma_i32_16x16x64_i8 with query digits as rows and embedding digits as
 // columns (|A_s| <= 3 * 128 * 2^14 < 2^23: no overflow). The accumulators start
-// from the rounding half and the token's centroid term plus the wave's bias, and
-// mx_fold turns the five class sums into t + tok_bias (below 2^32) without loss. No result
+// from the rounding half and the token's centroid term plus its query's cell bias
+// (added by the pairing), and mx_fold turns the five class sums into the biased
+// token score (below 2^32) without loss. No result
 // depends on the order of a summation, so the scan equals the CPU definition bit
 // for bit.
 //
@@ -52,7 +53,7 @@ __device__ __forceinline__ void digits3(int x, int& d0, int& d1, int& d2) {
 // 2^14 a4 + 2^6 a3 + alpha + floor(n / 2^18); n fits in int32 for |a0| <= 2^22 and
 // |a1| <= 2^22, and the other terms are exact modulo 2^32. The scan seeds the class
 // accumulators so that this one expression is the rounded token score plus its bias:
-// a0 = A0 + 2^17 (round half up), and with the centroid term plus the wave's bias split as
+// a0 = A0 + 2^17 (round half up), and with the centroid term plus the cell bias split as
 // 2^14 h + 2^6 m + l (0 <= m < 2^8, 0 <= l < 2^6), a2 = A2 + 4 l, a3 = A3 + m, a4 = A4 + h.
 // The result is below 2^32, hence exact.
 __device__ __forceinline__ unsigned mx_fold(int a0, int a1, int a2, int a3, int a4) {
@@ -142,7 +143,7 @@ __device__ __forceinline__ MxItem mx_decode(const v4i rec, int64_t item, int64_t
 template <int QPT>
 struct MxStage {
     v4i q[QPT];     // query digit slots tid + kMxBlock i of the group
-    int tok, base;  // thread tid < kMxGroup: wave token and R(S64) of group token tid
+    int tok, base;  // thread tid < kMxGroup: wave token and R(S64) + cell bias of group token tid
     int doc, prev;  // documents of chunk embeddings tid and tid - 1 (-1 outside the chunk)
 };
 
@@ -341,7 +342,7 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
         __syncthreads();  // the previous item's table is flushed and its tokens are no longer read
         // stage the item from registers
         if (tid < kMxGroup) {  // tokens past the group's end have zero digits and seeds: score 0 = absent
-            const unsigned b = tid < it.np ? (unsigned)st.base + a.tok_bias : 0u;
+            const unsigned b = tid < it.np ? (unsigned)st.base : 0u;  // R(S64) + the cell bias
             s_seed_h[tid] = (int)(b >> 14);
             s_seed_m[tid] = (int)((b >> 6) & 255u);
             s_seed_l[tid] = (int)((b & 63u) << 2);

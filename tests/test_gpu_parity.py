@@ -350,13 +350,14 @@ def test_exact_halves_in_the_residual_term():
 
 @pytest.mark.parametrize("weight_scale", [1.0, 11.0], ids=["epochs", "resets"])
 def test_consecutive_searches_reuse_the_token_max_table(weight_scale, monkeypatch):
-    # Waves tag their token-max cells with an epoch, so a cell of an earlier wave reads as
-    # absent and the table is zeroed only when the epochs run out (7 of them for the tiny
-    # workload's weights); with bucket weights too large for a spare bit (scaled by 11), the
-    # fold resets every cell instead. Every search of a sequence with changing query counts
-    # must match the oracle: across several zeroings, around Eq.-1-literal searches (which
-    # reset cells, so the table is zeroed before them) and with one query per wave (a 1 MiB
-    # scratch budget: nine waves in one search)
+    # Waves tag the token-max rows of each query slot with the slot's epoch, so a cell of an
+    # earlier wave reads as absent and a slot's rows are zeroed only when its epochs run out
+    # (7 of them for the tiny workload's weights); with bucket weights too large for a spare
+    # bit (scaled by 11), the fold resets every cell instead. Every search of a sequence with
+    # changing query counts (slots run out of epochs at different times) must match the
+    # oracle: across several zeroings, around Eq.-1-literal searches (which reset cells, so
+    # the table is zeroed before them), a search with 17 tokens per query (another layout of
+    # the slots) and one with one query per wave (a 1 MiB scratch budget: several waves)
     w = _engine()
     data = synth.make_index(synth.with_overrides(synth.WORKLOADS["tiny"], n_queries=9), workers=1)
     data.bucket_weights = (data.bucket_weights * weight_scale).astype(np.float32)
@@ -367,6 +368,8 @@ def test_consecutive_searches_reuse_the_token_max_table(weight_scale, monkeypatc
     with w.Index.from_synthetic(data) as ix:
         for j, n in enumerate(sizes):
             Q = data.queries[rng.permutation(9)[:n]]
+            if j == 6:
+                Q = np.ascontiguousarray(Q[:, :17])
             literal = j in (3, 12)
             ix.set_scoring(w.SCORING_EQ1_LITERAL if literal else w.SCORING_PAPER)
             if j == 9:
