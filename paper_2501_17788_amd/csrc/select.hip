@@ -40,24 +40,34 @@ __device__ __forceinline__ int rank_of(const double* s, const int* id, int n, do
     return r;
 }
 
-// fp64 centroid score, accumulated in dimension order (each product is exact).
-// The row is loaded in four slices of eight 16-byte loads, all in flight at once.
-__device__ __noinline__ double score64(const float* __restrict__ cen, int c, const float* qs) {
-    const float4* row = reinterpret_cast<const float4*>(cen + (int64_t)c * kDim);
+// fp64 centroid score, accumulated in dimension order (each product is exact), by the
+// four lanes 4 m .. 4 m + 3 of a wave that share centroid c: lane part loads dimensions
+// 32 part .. 32 part + 31 (one round trip for the whole row), and the running sum passes
+// from lane to lane in that order. Every lane of the four returns the score.
+__device__ __noinline__ double score64_quad(const float* __restrict__ cen, int c, const float* qs,
+                                               int part) {
+    const float4* row = reinterpret_cast<const float4*>(cen + (int64_t)c * kDim) + 8 * part;
+    float4 v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = row[k];
+    const int lead = (threadIdx.x & 63) & ~3;
+    const float* qp = qs + 32 * part;
     double s = 0.0;
+#pragma unroll 1
+    for (int seg = 0; seg < 4; ++seg) {
+        if (part == seg) {
 #pragma unroll
-    for (int sl = 0; sl < 4; ++sl) {
-        float4 v[8];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) v[k] = row[8 * sl + k];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int d = 32 * sl + 4 * k;
-            s = __builtin_fma((double)v[k].x, (double)qs[d + 0], s);
-            s = __builtin_fma((double)v[k].y, (double)qs[d + 1], s);
-            s = __builtin_fma((double)v[k].z, (double)qs[d + 2], s);
-            s = __builtin_fma((double)v[k].w, (double)qs[d + 3], s);
+            for (int k = 0; k < 8; ++k) {
+                float4 w = v[k];
+                // keeps the fp64 conversions inside the branch (else all 32 are hoisted)
+                asm volatile("" : "+v"(w.x), "+v"(w.y), "+v"(w.z), "+v"(w.w));
+                s = __builtin_fma((double)w.x, (double)qp[4 * k + 0], s);
+                s = __builtin_fma((double)w.y, (double)qp[4 * k + 1], s);
+                s = __builtin_fma((double)w.z, (double)qp[4 * k + 2], s);
+                s = __builtin_fma((double)w.w, (double)qp[4 * k + 3], s);
+            }
         }
+        s = __shfl(s, lead + seg, 64);
     }
     return s;
 }
@@ -146,8 +156,12 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
     __shared__ double sA[kSelCap], sB[kSelCap];
     __shared__ int idA[kSelCap], idB[kSelCap];
     __shared__ int64_t cum[kSelCap];
+    // from step 4 on, hist holds the sizes of the rescored centroids
+    int* const szA = reinterpret_cast<int*>(hist);
+    int* const szB = szA + kSelCap;
+    static_assert(2 * kSelCap * sizeof(int) <= sizeof(hist), "sizes must fit the histogram's LDS");
     __shared__ int s_bP, s_bt, s_blo, s_nA, s_nB, s_cross;
-    __shared__ unsigned long long s_wabove;
+    __shared__ unsigned long long s_wabove, s_band_above;
 
     const int t = blockIdx.x;
     const int tid = threadIdx.x;
@@ -230,6 +244,11 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
             if (p < kSelCap) idB[p] = c;
         }
     });
+    if (tid == 0 && !clamp) {  // size of every bin above the band (the histogram is reused below)
+        unsigned long long band_above = s_wabove;
+        for (int b = s_bt + 1; b <= bt_hi; ++b) band_above -= hist[b] & kSizeMask;
+        s_band_above = band_above;
+    }
     __syncthreads();
     const int nA = s_nA, nB = s_nB;
     int32_t* sel = a.sel + (int64_t)t * P;
@@ -249,10 +268,19 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
         return;
     }
 
-    // 4. fp64 rescoring of both lists
-    for (int p = tid; p < nA + nB; p += NT) {
-        if (p < nA) sA[p] = score64(a.centroids, idA[p], qs);
-        else sB[p - nA] = score64(a.centroids, idB[p - nA], qs);
+    // 4. fp64 rescoring of both lists, four lanes per centroid; the sizes come in beside
+    for (int p = tid >> 2; p < nA + nB; p += NT / 4) {  // uniform over each four lanes
+        const int c = p < nA ? idA[p] : idB[p - nA];
+        const double v = score64_quad(a.centroids, c, qs, tid & 3);
+        if ((tid & 3) == 0) {
+            if (p < nA) {
+                sA[p] = v;
+                szA[p] = sizes[c];
+            } else {
+                sB[p - nA] = v;
+                szB[p - nA] = sizes[c];
+            }
+        }
     }
     __syncthreads();
 
@@ -264,7 +292,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
             const int c = idA[p];
             sel[r] = c;
             base[r] = (int32_t)to_fixed(sA[p]);
-            cum[r] = sizes[c];
+            cum[r] = szA[p];
             if (a.dbg_sel) a.dbg_sel[(int64_t)t * P + r] = c;
         }
     }
@@ -279,13 +307,12 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
     for (int p = tid; p < nB; p += NT) {
         const int r = rank_of(sB, idB, nB, sB[p], idB[p]);
         sA[r] = sB[p];
-        cum[r] = sizes[idB[p]];
+        cum[r] = szB[p];
     }
     __syncthreads();
     block_inclusive_scan(cum, nB, wtot);
     if (!clamp) {
-        unsigned long long band_above = s_wabove;
-        for (int b = s_bt + 1; b <= bt_hi; ++b) band_above -= hist[b] & kSizeMask;
+        const unsigned long long band_above = s_band_above;
         for (int p = tid; p < nB; p += NT)
             if (band_above + (unsigned long long)cum[p] > tp) atomicMin(&s_cross, p);
     }
