@@ -4,12 +4,13 @@
 // the token strides gives this sum, so one pass per document computes it.
 //
 // One thread per (query, document): the n_qtok token rows are read with coalesced
-// loads, all issued before the first is used. A cell at or above the query's
-// threshold holds t plus the query's bias; a lower one (zeroed, or written by an
-// earlier wave) is not retrieved (cell_code). With epochs the fold only reads;
-// without, it zeroes every retrieved cell it read. The output is a sort key
-// per document: ((score + 2^39) << 24) | (2^24 - 1 - doc), larger is better and
-// equal scores order by lower document id; 0 marks a non-candidate.
+// non-temporal loads (nothing reads them again), all issued before the first is
+// used. A cell at or above the query's threshold holds t plus the query's bias; a
+// lower one (zeroed, or written by an earlier wave) is not retrieved (cell_code).
+// With epochs the fold only reads; without, it zeroes every retrieved cell it read.
+// The output is a sort key per document: ((score + 2^39) << 24) | (2^24 - 1 - doc),
+// larger is better and equal scores order by lower document id; 0 marks a
+// non-candidate.
 #include "engine.h"
 
 namespace warp {
@@ -32,7 +33,7 @@ __global__ __launch_bounds__(256) void k_fold(WaveArgs a) {
         const int64_t bias = (int64_t)ubias;
         uint32_t v[kMaxQtok];
 #pragma unroll
-        for (int i = 0; i < kMaxQtok; ++i) v[i] = i < T ? col[i * nd] : kTokAbsent;
+        for (int i = 0; i < kMaxQtok; ++i) v[i] = i < T ? __builtin_nontemporal_load(col + i * nd) : kTokAbsent;
         int64_t sum = 0;
         if (!cnt) {
 #pragma unroll
