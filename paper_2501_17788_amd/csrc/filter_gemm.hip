@@ -13,12 +13,11 @@
 // only steer selection: every centroid that lands near a selection boundary is
 // rescored in fp64, so no result depends on how they were accumulated.
 //
-// Tiling: a workgroup of 4 waves owns a 128-token x 128-centroid tile; K = 128 is
-// staged through LDS in two halves of 64, each fp32 row split into hi and lo fp16 rows
-// padded to 72 halves (144 bytes: the 16 rows of a 16-lane ds_read_b128 start in 16
-// distinct 4-bank groups). Each wave computes a 64 x 64 block as 4 x 4 MFMA blocks of
-// 16 x 16; lane group g = lane / 16 supplies the 8 consecutive k = ks + 8 g .. ks + 8 g + 7
-// of both operands to each 32-wide k step ks, so every k is summed once.
+// Tiling: a workgroup of 4 waves computes 128-token x 128-centroid tiles; K = 128 is
+// staged through LDS in quarters of 32, each fp32 row split into hi and lo fp16 rows
+// padded to 40 halves (80 bytes). Each wave computes a 64 x 64 block as 4 x 4 MFMA blocks
+// of 16 x 16; lane group g = lane / 16 supplies the 8 consecutive k = 8 g .. 8 g + 7 of
+// both operands to each 32-wide k step, so every k is summed once.
 #include "engine.h"
 
 namespace warp {
@@ -28,8 +27,8 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half4 __attribute__((ext_vector_type(4)));
 
 constexpr int kGT = 128;        // tile rows (tokens) and columns (centroids)
-constexpr int kGK = 64;         // k staged per half
-constexpr int kGPad = kGK + 8;  // padded LDS row (halves)
+constexpr int kGK = 32;         // k staged per quarter
+constexpr int kGPad = kGK + 8;  // padded LDS row (halves): 80 bytes
 
 __device__ __forceinline__ void split4(const float4 v, half4& hi, half4& lo) {
     hi = (half4){(_Float16)v.x, (_Float16)v.y, (_Float16)v.z, (_Float16)v.w};
@@ -38,8 +37,12 @@ __device__ __forceinline__ void split4(const float4 v, half4& hi, half4& lo) {
 }
 
 // BINS: write the selection histogram bin of each score (u16); else the fp32 score.
+// A persistent grid (as many workgroups as fit the GPU at once) walks the output tiles,
+// token tile major; workgroup b takes tiles b, b + G, ... While one quarter of K is
+// multiplied out of LDS, the fp32 rows of the next quarter (or of the next tile's first
+// quarter, during the epilogue as well) are in flight into registers.
 template <bool BINS>
-__global__ __launch_bounds__(256) void k_filter_gemm(const float* __restrict__ q, int32_t n_tok,
+__global__ __launch_bounds__(256, 2) void k_filter_gemm(const float* __restrict__ q, int32_t n_tok,
                                                      const float* __restrict__ cen, int32_t n_c,
                                                      void* __restrict__ out) {
     __shared__ __attribute__((aligned(16))) _Float16 Ah[kGT * kGPad];
@@ -51,82 +54,126 @@ __global__ __launch_bounds__(256) void k_filter_gemm(const float* __restrict__ q
     const int lane = tid & 63;
     const int li = lane & 15;
     const int g = lane >> 4;
-    const int64_t t_base = (int64_t)blockIdx.y * kGT;
-    const int64_t c_base = (int64_t)blockIdx.x * kGT;
     const int wr = (wave >> 1) * 64;  // this wave's rows within the tile
     const int wc = (wave & 1) * 64;   // and columns
+    const int64_t tiles_c = (n_c + kGT - 1) / kGT;
+    const int64_t n_tiles = tiles_c * ((n_tok + kGT - 1) / kGT);
 
-    floatx4 acc[4][4];
+    // 128 rows x 32 floats per operand = 1024 float4, 4 per thread
+    auto load = [&](int64_t tile, int quarter, float4 (&va)[4], float4 (&vb)[4]) {
+        const int64_t t_base = tile / tiles_c * kGT, c_base = tile % tiles_c * kGT;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = (floatx4){0.f, 0.f, 0.f, 0.f};
-
-#pragma unroll
-    for (int half = 0; half < 2; ++half) {
-        if (half) __syncthreads();
-        // stage: 128 rows x 64 floats per operand = 2048 float4, 8 per thread, split on the way
-#pragma unroll
-        for (int it = 0; it < 8; ++it) {
+        for (int it = 0; it < 4; ++it) {
             const int f = tid + 256 * it;
-            const int row = f >> 4, c4 = f & 15;
+            const int row = f >> 3, c4 = f & 7;
             const int64_t tr = t_base + row, cr = c_base + row;
-            float4 va = make_float4(0.f, 0.f, 0.f, 0.f), vb = va;
-            if (tr < n_tok) va = *reinterpret_cast<const float4*>(q + tr * kDim + half * kGK + 4 * c4);
-            if (cr < n_c) vb = *reinterpret_cast<const float4*>(cen + cr * kDim + half * kGK + 4 * c4);
+            va[it] = make_float4(0.f, 0.f, 0.f, 0.f);
+            vb[it] = va[it];
+            if (tr < n_tok) va[it] = *reinterpret_cast<const float4*>(q + tr * kDim + quarter * kGK + 4 * c4);
+            if (cr < n_c) vb[it] = *reinterpret_cast<const float4*>(cen + cr * kDim + quarter * kGK + 4 * c4);
+        }
+    };
+    auto stage = [&](const float4 (&va)[4], const float4 (&vb)[4]) {
+#pragma unroll
+        for (int it = 0; it < 4; ++it) {
+            const int f = tid + 256 * it;
+            const int row = f >> 3, c4 = f & 7;
             half4 hi, lo;
-            split4(va, hi, lo);
+            split4(va[it], hi, lo);
             *reinterpret_cast<half4*>(&Ah[row * kGPad + 4 * c4]) = hi;
             *reinterpret_cast<half4*>(&Al[row * kGPad + 4 * c4]) = lo;
-            split4(vb, hi, lo);
+            split4(vb[it], hi, lo);
             *reinterpret_cast<half4*>(&Bh[row * kGPad + 4 * c4]) = hi;
             *reinterpret_cast<half4*>(&Bl[row * kGPad + 4 * c4]) = lo;
         }
-        __syncthreads();
+    };
+    floatx4 acc[4][4];
+    auto multiply = [&]() {
 #pragma unroll
         for (int ks = 0; ks < kGK; ks += 32) {
-            half8 ah[4], al[4], bh[4], bl[4];
+            half8 bh[4], bl[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int rb = (wc + 16 * j + li) * kGPad + ks + 8 * g;
+                bh[j] = *reinterpret_cast<const half8*>(&Bh[rb]);
+                bl[j] = *reinterpret_cast<const half8*>(&Bl[rb]);
+            }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int ra = (wr + 16 * i + li) * kGPad + ks + 8 * g;
-                const int rb = (wc + 16 * i + li) * kGPad + ks + 8 * g;
-                ah[i] = *reinterpret_cast<const half8*>(&Ah[ra]);
-                al[i] = *reinterpret_cast<const half8*>(&Al[ra]);
-                bh[i] = *reinterpret_cast<const half8*>(&Bh[rb]);
-                bl[i] = *reinterpret_cast<const half8*>(&Bl[rb]);
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
+                const half8 ah = *reinterpret_cast<const half8*>(&Ah[ra]);
+                const half8 al = *reinterpret_cast<const half8*>(&Al[ra]);
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[i], bh[j], acc[i][j], 0, 0, 0);
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[i], bl[j], acc[i][j], 0, 0, 0);
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[i], bh[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bh[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bl[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al, bh[j], acc[i][j], 0, 0, 0);
                 }
             }
         }
-    }
-    // D[r][cidx] of a 16 x 16 block sits in lane cidx + 16 * (r / 4), element r % 4.
+    };
+
+    int64_t tile = blockIdx.x;
+    if (tile >= n_tiles) return;
+    float4 va[4], vb[4];
+    load(tile, 0, va, vb);
+    for (;;) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t c = c_base + wc + 16 * j + li;
-            if (c >= n_c) continue;
+            for (int j = 0; j < 4; ++j) acc[i][j] = (floatx4){0.f, 0.f, 0.f, 0.f};
+        const int64_t next = tile + gridDim.x;
+#pragma unroll 1
+        for (int h = 0; h < 4; ++h) {
+            stage(va, vb);
+            __syncthreads();
+            if (h < 3) load(tile, h + 1, va, vb);
+            else if (next < n_tiles) load(next, 0, va, vb);
+            multiply();
+            if (h < 3) __syncthreads();
+        }
+        // D[r][cidx] of a 16 x 16 block sits in lane cidx + 16 * (r / 4), element r % 4.
+        const int64_t t_base = tile / tiles_c * kGT, c_base = tile % tiles_c * kGT;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int64_t t = t_base + wr + 16 * i + 4 * g + r;
-                if (t >= n_tok) continue;
-                if (BINS) static_cast<uint16_t*>(out)[t * n_c + c] = (uint16_t)score_bin(acc[i][j][r]);
-                else static_cast<float*>(out)[t * n_c + c] = acc[i][j][r];
+        for (int i = 0; i < 4; ++i) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int64_t c = c_base + wc + 16 * j + li;
+                if (c >= n_c) continue;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int64_t t = t_base + wr + 16 * i + 4 * g + r;
+                    if (t >= n_tok) continue;
+                    if (BINS) static_cast<uint16_t*>(out)[t * n_c + c] = (uint16_t)score_bin(acc[i][j][r]);
+                    else static_cast<float*>(out)[t * n_c + c] = acc[i][j][r];
+                }
             }
         }
+        if (next >= n_tiles) break;
+        tile = next;
+        __syncthreads();  // every wave has read the LDS operands before they are replaced
     }
+}
+
+// Workgroups of the filter GEMM that fit the current device at once.
+int filter_gemm_grid() {
+    int dev = 0, cus = 0, per = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, k_filter_gemm<true>, 256, 0) != hipSuccess) {
+        (void)hipGetLastError();
+        return 512;
+    }
+    return cus * (per > 0 ? per : 1);
 }
 
 void launch_filter_gemm(const float* q, int32_t n_tok, const float* c, int32_t n_c, uint16_t* out_bins,
                         float* out_scores, hipStream_t s) {
-    dim3 grid((n_c + kGT - 1) / kGT, (n_tok + kGT - 1) / kGT);
+    const int64_t tiles = (int64_t)((n_c + kGT - 1) / kGT) * ((n_tok + kGT - 1) / kGT);
+    static thread_local int grid_cap = 0;
+    if (grid_cap == 0) grid_cap = filter_gemm_grid();
+    const dim3 grid((unsigned)(tiles < grid_cap ? tiles : grid_cap));
+    if (tiles == 0) return;
     if (out_bins)
         hipLaunchKernelGGL(k_filter_gemm<true>, grid, dim3(256), 0, s, q, n_tok, c, n_c, (void*)out_bins);
     else
