@@ -27,10 +27,12 @@
 // Each wave takes 16-embedding tiles of the chunk, decodes their codes into
 // weight digits in registers (v_perm_b32 lookups in 16-byte digit tables, or a
 // 256-entry LDS table at b = 8) and runs the 18 MFMAs of every 16-token tile of
-// the group, so that each 16-lane row of the result holds four tokens against the
-// tile's 16 embeddings. Every score goes into an LDS table of (token, run) maxima
-// by an LDS atomic max; at the end of the item the table is flushed with one
-// device atomicMax per (token, run) into the token-max table.
+// the group with the weight digits as rows and the query digits as columns, so that
+// each lane holds one token against four consecutive embeddings. Every score goes
+// into an LDS table of (token, run) maxima by an LDS atomic max: the 16 lanes of a
+// row write 16 different tokens, so lanes meet on one cell only where a run covers
+// embeddings four apart. At the end of the item the table is flushed with one device
+// atomicMax per (token, run) into the token-max table.
 #include "engine.h"
 
 namespace warp {
@@ -152,8 +154,8 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
     constexpr int BYTES = kDim * NBITS / 8;  // code bytes per embedding
     constexpr int CW = NBITS;                // code words per lane: 32 dimensions of b bits
     constexpr int NSLOT = 24;                // (plane, slice, lane group) slots of 16 bytes
-    // row of the run table: the four token rows a lane group writes together start 16 banks
-    // apart; column kMxChunk takes the scores of tile rows past the chunk's end and is never read
+    // row of the run table: the 16 token rows one atomic writes start 4 banks apart; column
+    // kMxChunk takes the scores of embeddings past the chunk's end and is never read
     constexpr int TPAD = kMxChunk + 4;
     constexpr int NW = kMxBlock / 64;
     constexpr int QPT = NSLOT * kMxGroup / kMxBlock;  // query slots staged per thread
@@ -164,13 +166,13 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
     static_assert(NSLOT * kMxGroup % kMxBlock == 0, "query staging");
     static_assert(kMxChunk % (16 * NW) == 0, "tiles per wave");
     __shared__ v4i s_q[NSLOT][kMxGroup];     // query digit planes of the item's tokens
-    // accumulator seeds of each token: R(S64) + 2^31 = 2^14 h + 2^6 m + l
+    // accumulator seeds of each token: R(S64) + its cell bias = 2^14 h + 2^6 m + l
     __shared__ __attribute__((aligned(16))) int s_seed_h[kMxGroup];  // h
     __shared__ __attribute__((aligned(16))) int s_seed_m[kMxGroup];  // m
     __shared__ __attribute__((aligned(16))) int s_seed_l[kMxGroup];  // 4 l
     __shared__ __attribute__((aligned(16))) int64_t s_row[kMxGroup];  // its token-max row offset
     __shared__ unsigned s_tab[kMxGroup * TPAD];  // max score of (token, document run of the chunk)
-    __shared__ int s_run[kMxChunk];          // run of each chunk embedding
+    __shared__ __attribute__((aligned(16))) int s_run[kMxChunk];  // run of each chunk embedding (kMxChunk past its end)
     __shared__ int s_rdoc[kMxChunk];         // document of each run
     __shared__ int s_rstart[kMxChunk];       // its first embedding in the chunk
     __shared__ int s_wruns[NW];              // runs starting in each wave's quarter of the chunk
@@ -370,12 +372,10 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
                 run += w8 < wave ? s_wruns[w8] : 0;
                 n_runs += s_wruns[w8];
             }
-            if (e_in) {
-                s_run[tid] = run;
-                if (start) {
-                    s_rdoc[run] = doc;
-                    s_rstart[run] = tid;
-                }
+            s_run[tid] = e_in ? run : kMxChunk;
+            if (start) {
+                s_rdoc[run] = doc;
+                s_rstart[run] = tid;
             }
         }
         // prefetch: the next item's query digits, bases and documents, then (once a claim
@@ -400,8 +400,7 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
         for (int j = 0; j < TPW; ++j) {
             const int et = wave + NW * j;
             if (et >= n_et) break;  // wave-uniform
-            const bool row_in = it.e0 + 16 * et + li < it.e1;
-            // weight digits of the tile (MFMA B operand: column li = embedding e0 + 16 et + li)
+            // weight digits of the tile (MFMA A operand: row li = embedding e0 + 16 et + li)
             v4i A[3][2];
             if (NBITS == 4) {
 #pragma unroll
@@ -454,19 +453,21 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
                     }
                 }
             }
-            const int my_run = row_in ? s_run[16 * et + li] : kMxChunk;
 
             for (int tt = 0; tt < n_tt; ++tt) {
                 // class accumulators, seeded with the rounding half and the tokens' centroid terms
                 v4i acc[5];
                 acc[0] = (v4i){1 << 17, 1 << 17, 1 << 17, 1 << 17};
                 acc[1] = (v4i){0, 0, 0, 0};
-                acc[2] = *reinterpret_cast<const v4i*>(&s_seed_l[16 * tt + 4 * lg]);
-                acc[3] = *reinterpret_cast<const v4i*>(&s_seed_m[16 * tt + 4 * lg]);
-                acc[4] = *reinterpret_cast<const v4i*>(&s_seed_h[16 * tt + 4 * lg]);
+                {
+                    const int sl = s_seed_l[16 * tt + li], sm = s_seed_m[16 * tt + li], sh = s_seed_h[16 * tt + li];
+                    acc[2] = (v4i){sl, sl, sl, sl};
+                    acc[3] = (v4i){sm, sm, sm, sm};
+                    acc[4] = (v4i){sh, sh, sh, sh};
+                }
 #pragma unroll
                 for (int s = 0; s < 2; ++s) {
-                    // query digits of slice s (MFMA A operand: row li = token 16 tt + li)
+                    // query digits of slice s (MFMA B operand: column li = token 16 tt + li)
                     v4i B[3];
 #pragma unroll
                     for (int p = 0; p < 3; ++p) B[p] = s_q[(p * 2 + s) * 4 + lg][16 * tt + li];
@@ -474,13 +475,15 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
                     for (int i = 0; i < 3; ++i)
 #pragma unroll
                         for (int jj = 0; jj < 3; ++jj)
-                            acc[i + jj] = __builtin_amdgcn_mfma_i32_16x16x64_i8(B[i], A[jj][s], acc[i + jj], 0, 0, 0);
+                            acc[i + jj] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[jj][s], B[i], acc[i + jj], 0, 0, 0);
                 }
-                // acc[k][r] of lane (li, lg): token 16 tt + 4 lg + r against embedding e0 + 16 et + li;
-                // merge into the (token, run) table
+                // acc[k][r] of lane (li, lg): token 16 tt + li against embedding e0 + 16 et + 4 lg + r;
+                // merge into the (token, run) table. The runs of the four embeddings come in one
+                // read; embeddings past the chunk's end have the padding column.
+                const v4i my_run = *reinterpret_cast<const v4i*>(&s_run[16 * et + 4 * lg]);
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
-                    atomicMax(&s_tab[(16 * tt + 4 * lg + r) * TPAD + my_run],
+                    atomicMax(&s_tab[(16 * tt + li) * TPAD + my_run[r]],
                               mx_fold(acc[0][r], acc[1][r], acc[2][r], acc[3][r], acc[4][r]));
             }
         }
