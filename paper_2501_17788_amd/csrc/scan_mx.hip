@@ -165,7 +165,9 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
     static_assert(kMxChunk <= kMxBlock, "one thread per chunk embedding");
     static_assert(NSLOT * kMxGroup % kMxBlock == 0, "query staging");
     static_assert(kMxChunk % (16 * NW) == 0, "tiles per wave");
-    __shared__ v4i s_q[NSLOT][kMxGroup];     // query digit planes of the item's tokens
+    // query digit planes of the item's tokens, one padded row per token: the staging writes
+    // of consecutive threads are contiguous, and the 16 tokens of an operand read lie 400 bytes apart
+    __shared__ v4i s_q[kMxGroup][NSLOT + 1];
     // accumulator seeds of each token: R(S64) + its cell bias = 2^14 h + 2^6 m + l
     __shared__ __attribute__((aligned(16))) int s_seed_h[kMxGroup];  // h
     __shared__ __attribute__((aligned(16))) int s_seed_m[kMxGroup];  // m
@@ -353,7 +355,7 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
 #pragma unroll
         for (int i = 0; i < QPT; ++i) {
             const int k = tid + kMxBlock * i;
-            s_q[k % NSLOT][k / NSLOT] = st.q[i];
+            s_q[k / NSLOT][k % NSLOT] = st.q[i];
         }
         if (tid == 0 && claimed) s_claim = claim;  // after the wait for the staged data
         // runs of equal documents along a new chunk (ids ascend inside a cluster)
@@ -470,7 +472,7 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
                     // query digits of slice s (MFMA B operand: column li = token 16 tt + li)
                     v4i B[3];
 #pragma unroll
-                    for (int p = 0; p < 3; ++p) B[p] = s_q[(p * 2 + s) * 4 + lg][16 * tt + li];
+                    for (int p = 0; p < 3; ++p) B[p] = s_q[16 * tt + li][(p * 2 + s) * 4 + lg];
 #pragma unroll
                     for (int i = 0; i < 3; ++i)
 #pragma unroll
