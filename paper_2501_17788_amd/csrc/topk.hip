@@ -11,13 +11,14 @@
 // K largest keys then lies in a block whose maximum is within D0, and the keys of any
 // other block are smaller than all of these. The passes below visit only those blocks,
 // listed in LDS (all blocks when more than kTopkListCap pass, or no D0 is found). The
-// K largest keys are found in one or two histogram passes over the keys: bins of the distance below the largest score
-// (4096 bins of 2^-6, then, inside the bin holding the K-th key, 4096 bins of
-// 2^-18), after which every key at or above the bin holding the K-th key is
-// gathered (at most kMaxK), sorted in LDS, and the first K decoded. When the
-// K-th key lies more than 64 below the best, or its fine bin alone would overflow
-// the gather buffer, an MSB-first radix select over the whole key (8 bits per
-// pass) finds the K-th key exactly instead.
+// K largest keys are found in one or two histogram passes over the keys: bins of the
+// distance below the largest score (4096 bins of 2^-6, then, inside the bin holding the
+// K-th key, 4096 bins of 2^-18), after which every key at or above the bin holding the
+// K-th key is gathered (at most kMaxK); each takes its rank among them as its position
+// (up to kRankMax keys), or they are sorted in LDS, and the first K are decoded. When
+// the K-th key lies more than 64 below the best, or its fine bin alone would overflow
+// the gather buffer, an MSB-first radix select over the whole key (8 bits per pass)
+// finds the K-th key exactly instead.
 #include "engine.h"
 
 namespace warp {
@@ -26,26 +27,31 @@ constexpr int kTopkThreads = 1024;
 constexpr int kTopkBins = 4096;
 constexpr int kCoarseShift = 20;  // coarse bin width: 2^20 units of 2^-26
 constexpr int kFineShift = 8;     // fine bin width inside one coarse bin: 2^8 units
+constexpr int kRankMax = 512;     // up to this many gathered keys are placed by rank, more are sorted
 
 // Smallest bin b with hist[0] + ... + hist[b] >= need, and the count of bins
-// before it; b = -1 if the total is below need. Every thread calls it.
+// before it; b = -1 if the total is below need. Every thread calls it. The prefix over
+// the threads' bin counts is a shuffle scan inside each wave, then over the wave totals.
 __device__ void find_crossing(const uint32_t* hist, uint32_t need, uint32_t* scan, int* s_bin,
                               uint32_t* s_before) {
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     constexpr int PER = kTopkBins / kTopkThreads;
+    constexpr int NWV = kTopkThreads / 64;
     uint32_t mine = 0;
 #pragma unroll
     for (int i = 0; i < PER; ++i) mine += hist[PER * tid + i];
-    scan[tid] = mine;
+    uint32_t incl = mine;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t t = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += t;
+    }
+    if (lane == 63) scan[wave] = incl;  // wave totals
     if (tid == 0) *s_bin = -1;
     __syncthreads();
-    for (int off = 1; off < kTopkThreads; off <<= 1) {
-        const uint32_t v = tid >= off ? scan[tid - off] : 0;
-        __syncthreads();
-        scan[tid] += v;
-        __syncthreads();
-    }
-    const uint32_t incl = scan[tid], excl = incl - mine;
+#pragma unroll
+    for (int w = 0; w < NWV; ++w) incl += w < wave ? scan[w] : 0;
+    const uint32_t excl = incl - mine;
     if (excl < need && incl >= need) {
         uint32_t cum = excl;
         for (int i = 0; i < PER; ++i) {
@@ -63,7 +69,7 @@ __device__ void find_crossing(const uint32_t* hist, uint32_t need, uint32_t* sca
 
 __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
     __shared__ uint32_t hist[kTopkBins];
-    __shared__ uint32_t scan[kTopkThreads];
+    __shared__ uint32_t scan[kTopkThreads / 64];
     __shared__ unsigned long long buf[kMaxK];
     __shared__ int32_t blist[kTopkListCap];
     __shared__ unsigned long long s_prefix, s_mask, s_max, s_lim;
@@ -250,14 +256,30 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
         });
         __syncthreads();
     }
-    // bitonic sort, descending, of the gathered keys padded with zeros; the first K are the result
     const int cnt = K == 0 ? 0 : (int)(s_count < (uint32_t)kMaxK ? s_count : (uint32_t)kMaxK);
-    int np = 2;
-    while (np < cnt) np <<= 1;
-    for (int i = tid; i < np; i += kTopkThreads)
-        if (i >= cnt) buf[i] = 0;
-    __syncthreads();
-    if (cnt > 1) {
+    auto emit = [&](int r, unsigned long long key) {  // output position r < K
+        const int64_t o = (int64_t)q * a.k + r;
+        const int32_t doc = (int32_t)(kMaxDocs - 1 - (int32_t)(key & (kMaxDocs - 1)));
+        const int64_t score = (int64_t)(key >> 24) - (1ll << 39);
+        a.out_ids[o] = doc;
+        a.out_scores[o] = (float)((double)score * (1.0 / (double)(1 << kFrac)));
+        if (a.out_fixed) a.out_fixed[o] = score;
+    };
+    if (cnt <= kRankMax) {
+        // few gathered keys: each key's position is the number of larger ones (keys are distinct)
+        for (int t = tid; t < cnt; t += kTopkThreads) {
+            const unsigned long long key = buf[t];
+            int r = 0;
+            for (int j = 0; j < cnt; ++j) r += buf[j] > key ? 1 : 0;
+            if (r < K) emit(r, key);
+        }
+    } else {
+        // bitonic sort, descending, of the gathered keys padded with zeros; the first K are the result
+        int np = 2;
+        while (np < cnt) np <<= 1;
+        for (int i = tid; i < np; i += kTopkThreads)
+            if (i >= cnt) buf[i] = 0;
+        __syncthreads();
         for (int kk = 2; kk <= np; kk <<= 1) {
             for (int j = kk >> 1; j > 0; j >>= 1) {
                 for (int i = tid; i < np; i += kTopkThreads) {
@@ -274,21 +296,13 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
                 __syncthreads();
             }
         }
+        for (int r = tid; r < K; r += kTopkThreads) emit(r, buf[r]);
     }
-    for (int r = tid; r < a.k; r += kTopkThreads) {
+    for (int r = K + tid; r < a.k; r += kTopkThreads) {
         const int64_t o = (int64_t)q * a.k + r;
-        if (r < K) {
-            const unsigned long long key = buf[r];
-            const int32_t doc = (int32_t)(kMaxDocs - 1 - (int32_t)(key & (kMaxDocs - 1)));
-            const int64_t score = (int64_t)(key >> 24) - (1ll << 39);
-            a.out_ids[o] = doc;
-            a.out_scores[o] = (float)((double)score * (1.0 / (double)(1 << kFrac)));
-            if (a.out_fixed) a.out_fixed[o] = score;
-        } else {
-            a.out_ids[o] = -1;
-            a.out_scores[o] = -__builtin_inff();
-            if (a.out_fixed) a.out_fixed[o] = INT64_MIN;
-        }
+        a.out_ids[o] = -1;
+        a.out_scores[o] = -__builtin_inff();
+        if (a.out_fixed) a.out_fixed[o] = INT64_MIN;
     }
     if (tid == 0 && a.out_counts) a.out_counts[q] = K;
 }
