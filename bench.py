@@ -211,6 +211,8 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="small")
+    ap.add_argument("--nprobe", type=int, default=0, help="override the workload's nprobe (the full workload "
+                                                            "is also measured at 16 and 64)")
     ap.add_argument("--latency-runs", type=int, default=200)
     ap.add_argument("--cpu-queries", type=int, default=128)
     ap.add_argument("--no-cpu", action="store_true")
@@ -242,6 +244,8 @@ def main() -> int:
     from paper_2501_17788_amd import Index
 
     wl = synth.WORKLOADS[args.workload]
+    if args.nprobe:
+        wl = synth.with_overrides(wl, nprobe=args.nprobe)
     log(f"bench: generating {describe(wl)}")
     t0 = time.time()
     data = synth.make_index(wl, workers=min(16, host_threads()))
