@@ -11,13 +11,13 @@
 // digits x = x2 2^16 + x1 2^8 + x0 with x_j in [-128, 127], and
 //     V = sum_s 2^(8 s) A_s,   A_s = sum_{i + j = s} sum_d qdig_i[d] * wdig_j[d]
 // for s = 0..4. Every A_s is an int8 matrix product over d, computed by
-// v_mfma_i32_16x16x64_i8 with query digits as rows and embedding digits as
-// columns (|A_s| <= 3 * 128 * 2^14 < 2^23: no overflow). The accumulators start
-// from the rounding half and the token's centroid term plus its query's cell bias
-// (added by the pairing), and mx_fold turns the five class sums into the biased
-// token score (below 2^32) without loss. No result
-// depends on the order of a summation, so the scan equals the CPU definition bit
-// for bit.
+// v_mfma_i32_16x16x64_i8 with embedding digits as rows and query digits as
+// columns (|A_s| <= 3 * 128 * 2^14 < 2^23: no overflow). The class-0 accumulator
+// starts from the rounding half, mx_fold turns the five class sums into the rounded
+// residual term, and adding the token's centroid term plus its query's cell bias
+// (added by the pairing) gives the biased token score (below 2^32) without loss. No
+// result depends on the order of a summation, so the scan equals the CPU definition
+// bit for bit.
 //
 // Work. A work item is (cluster, chunk of kMxChunk embeddings, group of up to
 // kMxGroup probing tokens); a persistent workgroup of four waves walks a
@@ -53,11 +53,10 @@ __device__ __forceinline__ void digits3(int x, int& d0, int& d1, int& d2) {
 // floor((a0 + 2^8 a1 + 2^16 a2 + 2^24 a3 + 2^32 a4) / 2^18) modulo 2^32. Writing
 // a2 = 4 alpha + rho (0 <= rho < 4) and n = a0 + 2^8 a1 + 2^16 rho, the quotient is
 // 2^14 a4 + 2^6 a3 + alpha + floor(n / 2^18); n fits in int32 for |a0| <= 2^22 and
-// |a1| <= 2^22, and the other terms are exact modulo 2^32. The scan seeds the class
-// accumulators so that this one expression is the rounded token score plus its bias:
-// a0 = A0 + 2^17 (round half up), and with the centroid term plus the cell bias split as
-// 2^14 h + 2^6 m + l (0 <= m < 2^8, 0 <= l < 2^6), a2 = A2 + 4 l, a3 = A3 + m, a4 = A4 + h.
-// The result is below 2^32, hence exact.
+// |a1| <= 2^22, and the other terms are exact modulo 2^32. With a0 = A0 + 2^17 (the
+// class-0 accumulator starts at the rounding half: round half up) this is the rounded
+// residual term floor(V / 2^18 + 1/2) modulo 2^32; the scan adds the token's centroid term
+// plus its cell bias, and the sum, the biased token score, lies below 2^32, hence is exact.
 __device__ __forceinline__ unsigned mx_fold(int a0, int a1, int a2, int a3, int a4) {
     const int n = (int)((unsigned)a0 + ((unsigned)a1 << 8) + (((unsigned)a2 & 3u) << 16));
     return ((unsigned)a4 << 14) + ((unsigned)a3 << 6) + (unsigned)(a2 >> 2) + (unsigned)(n >> 18);
@@ -168,10 +167,7 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
     // query digit planes of the item's tokens, one padded row per token: the staging writes
     // of consecutive threads are contiguous, and the 16 tokens of an operand read lie 400 bytes apart
     __shared__ v4i s_q[kMxGroup][NSLOT + 1];
-    // accumulator seeds of each token: R(S64) + its cell bias = 2^14 h + 2^6 m + l
-    __shared__ __attribute__((aligned(16))) int s_seed_h[kMxGroup];  // h
-    __shared__ __attribute__((aligned(16))) int s_seed_m[kMxGroup];  // m
-    __shared__ __attribute__((aligned(16))) int s_seed_l[kMxGroup];  // 4 l
+    __shared__ unsigned s_cterm[kMxGroup];   // R(S64) + the cell bias of each token (0 past the group)
     __shared__ __attribute__((aligned(16))) int64_t s_row[kMxGroup];  // its token-max row offset
     __shared__ unsigned s_tab[kMxGroup * TPAD];  // max score of (token, document run of the chunk)
     __shared__ __attribute__((aligned(16))) int s_run[kMxChunk];  // run of each chunk embedding (kMxChunk past its end)
@@ -345,11 +341,9 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
     for (;;) {
         __syncthreads();  // the previous item's table is flushed and its tokens are no longer read
         // stage the item from registers
-        if (tid < kMxGroup) {  // tokens past the group's end have zero digits and seeds: score 0 = absent
+        if (tid < kMxGroup) {  // tokens past the group's end have zero digits and centroid terms: score 0 = absent
             const unsigned b = tid < it.np ? (unsigned)st.base : 0u;  // R(S64) + the cell bias
-            s_seed_h[tid] = (int)(b >> 14);
-            s_seed_m[tid] = (int)((b >> 6) & 255u);
-            s_seed_l[tid] = (int)((b & 63u) << 2);
+            s_cterm[tid] = b;
             s_row[tid] = (int64_t)st.tok * a.n_docs;
         }
 #pragma unroll
@@ -457,16 +451,11 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
             }
 
             for (int tt = 0; tt < n_tt; ++tt) {
-                // class accumulators, seeded with the rounding half and the tokens' centroid terms
+                // class accumulators; class 0 starts at the rounding half
                 v4i acc[5];
                 acc[0] = (v4i){1 << 17, 1 << 17, 1 << 17, 1 << 17};
-                acc[1] = (v4i){0, 0, 0, 0};
-                {
-                    const int sl = s_seed_l[16 * tt + li], sm = s_seed_m[16 * tt + li], sh = s_seed_h[16 * tt + li];
-                    acc[2] = (v4i){sl, sl, sl, sl};
-                    acc[3] = (v4i){sm, sm, sm, sm};
-                    acc[4] = (v4i){sh, sh, sh, sh};
-                }
+#pragma unroll
+                for (int c = 1; c < 5; ++c) acc[c] = (v4i){0, 0, 0, 0};
 #pragma unroll
                 for (int s = 0; s < 2; ++s) {
                     // query digits of slice s (MFMA B operand: column li = token 16 tt + li)
@@ -483,10 +472,11 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
                 // merge into the (token, run) table. The runs of the four embeddings come in one
                 // read; embeddings past the chunk's end have the padding column.
                 const v4i my_run = *reinterpret_cast<const v4i*>(&s_run[16 * et + 4 * lg]);
+                const unsigned cterm = s_cterm[16 * tt + li];
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
                     atomicMax(&s_tab[(16 * tt + li) * TPAD + my_run[r]],
-                              mx_fold(acc[0][r], acc[1][r], acc[2][r], acc[3][r], acc[4][r]));
+                              mx_fold(acc[0][r], acc[1][r], acc[2][r], acc[3][r], acc[4][r]) + cterm);
             }
         }
         // the next item's codes, in flight during the flush (the same codes for the same chunk)
