@@ -28,6 +28,7 @@ constexpr int kTopkBins = 4096;
 constexpr int kCoarseShift = 20;  // coarse bin width: 2^20 units of 2^-26
 constexpr int kFineShift = 8;     // fine bin width inside one coarse bin: 2^8 units
 constexpr int kRankMax = 512;     // up to this many gathered keys are placed by rank, more are sorted
+constexpr int kKeysInFlight = 8;  // key loads per thread in flight in every pass over the keys
 
 // Smallest bin b with hist[0] + ... + hist[b] >= need, and the count of bins
 // before it; b = -1 if the total is below need. Every thread calls it. The prefix over
@@ -83,6 +84,24 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
     const unsigned long long* keys = reinterpret_cast<const unsigned long long*>(a.keys) + (int64_t)q * n;
     const uint64_t* part = a.qpart + 2 * (int64_t)q * nb;
 
+    // every block's (candidate count, largest key), kKeysInFlight 16-byte loads in flight per thread
+    typedef unsigned long long u64x2 __attribute__((ext_vector_type(2)));
+    auto for_each_part = [&](auto&& f) {
+        for (int64_t b0 = tid; b0 < nb; b0 += kKeysInFlight * kTopkThreads) {
+            u64x2 pv[kKeysInFlight];
+#pragma unroll
+            for (int u = 0; u < kKeysInFlight; ++u) {
+                const int64_t b = b0 + (int64_t)u * kTopkThreads;
+                pv[u] = b < nb ? *reinterpret_cast<const u64x2*>(part + 2 * b) : (u64x2){0ull, 0ull};
+            }
+#pragma unroll
+            for (int u = 0; u < kKeysInFlight; ++u) {
+                const int64_t b = b0 + (int64_t)u * kTopkThreads;
+                if (b < nb) f(b, pv[u].x, pv[u].y);
+            }
+        }
+    };
+
     // candidates and the largest key, from the fold's per-block partials
     if (tid == 0) {
         s_ncand = 0;
@@ -93,10 +112,10 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
     __syncthreads();
     {
         unsigned long long cnt = 0, mx = 0;
-        for (int64_t b = tid; b < nb; b += kTopkThreads) {
-            cnt += part[2 * b];
-            mx = part[2 * b + 1] > mx ? part[2 * b + 1] : mx;
-        }
+        for_each_part([&](int64_t, unsigned long long c, unsigned long long m) {
+            cnt += c;
+            mx = m > mx ? m : mx;
+        });
         atomicAdd(&s_ncand, (uint32_t)cnt);
         atomicMax(&s_max, mx);
     }
@@ -111,12 +130,10 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
     if (!done) {
         for (int i = tid; i < kTopkBins; i += kTopkThreads) hist[i] = 0;
         __syncthreads();
-        for (int64_t b = tid; b < nb; b += kTopkThreads) {
-            const unsigned long long mx = part[2 * b + 1];
-            if (mx == 0) continue;
+        for_each_part([&](int64_t, unsigned long long, unsigned long long mx) {
             const unsigned long long d = smax - (mx >> 24);
-            if (d < ((unsigned long long)kTopkBins << kCoarseShift)) atomicAdd(&hist[d >> kCoarseShift], 1u);
-        }
+            if (mx != 0 && d < ((unsigned long long)kTopkBins << kCoarseShift)) atomicAdd(&hist[d >> kCoarseShift], 1u);
+        });
         __syncthreads();
         find_crossing(hist, (uint32_t)K, scan, &s_bin, &s_before);
         const int b1 = s_bin;
@@ -126,44 +143,42 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
             for (int i = tid; i < kTopkBins; i += kTopkThreads) hist[i] = 0;
             __syncthreads();
             const unsigned long long base = (unsigned long long)b1 << kCoarseShift;
-            for (int64_t b = tid; b < nb; b += kTopkThreads) {
-                const unsigned long long mx = part[2 * b + 1];
-                if (mx == 0) continue;
+            for_each_part([&](int64_t, unsigned long long, unsigned long long mx) {
                 const unsigned long long d = smax - (mx >> 24);
-                if (d >= base && d - base < (1ull << kCoarseShift)) atomicAdd(&hist[(d - base) >> kFineShift], 1u);
-            }
+                if (mx != 0 && d >= base && d - base < (1ull << kCoarseShift))
+                    atomicAdd(&hist[(d - base) >> kFineShift], 1u);
+            });
             __syncthreads();
             find_crossing(hist, need, scan, &s_bin, &s_before);
             d0 = base + ((unsigned long long)(s_bin + 1) << kFineShift);  // the crossing exists
         }
         if (d0 != 0) {
-            for (int64_t b = tid; b < nb; b += kTopkThreads) {
-                const unsigned long long mx = part[2 * b + 1];
+            for_each_part([&](int64_t b, unsigned long long, unsigned long long mx) {
                 if (mx != 0 && smax - (mx >> 24) < d0) {
                     const uint32_t p = atomicAdd(&s_nlist, 1u);
                     if (p < (uint32_t)kTopkListCap) blist[p] = (int32_t)b;
                 }
-            }
+            });
         }
         __syncthreads();
     }
     const uint32_t nlist = s_nlist;
     const bool pruned = d0 != 0 && nlist <= (uint32_t)a.topk_list_cap;
     // every key of the listed blocks, or of all blocks
+    // (kKeysInFlight loads per thread are issued before any of their keys is used)
     auto for_each_key = [&](auto&& f) {
-        if (pruned) {
-            for (int64_t j = tid; j < (int64_t)nlist * 256; j += kTopkThreads) {
-                const int64_t x = (int64_t)blist[j >> 8] * 256 + (j & 255);
-                if (x < n) {
-                    const unsigned long long key = keys[x];
-                    if (key != 0) f(key);
-                }
+        const int64_t total = pruned ? (int64_t)nlist * 256 : n;
+        for (int64_t j0 = tid; j0 < total; j0 += kKeysInFlight * kTopkThreads) {
+            unsigned long long kv[kKeysInFlight];
+#pragma unroll
+            for (int u = 0; u < kKeysInFlight; ++u) {
+                const int64_t j = j0 + (int64_t)u * kTopkThreads;
+                const int64_t x = pruned ? (int64_t)blist[j < total ? j >> 8 : 0] * 256 + (j & 255) : j;
+                kv[u] = j < total && x < n ? keys[x] : 0ull;
             }
-        } else {
-            for (int64_t x = tid; x < n; x += kTopkThreads) {
-                const unsigned long long key = keys[x];
-                if (key != 0) f(key);
-            }
+#pragma unroll
+            for (int u = 0; u < kKeysInFlight; ++u)
+                if (kv[u] != 0) f(kv[u]);
         }
     };
     // level 1: coarse bins of the distance below the best score
