@@ -139,14 +139,13 @@ void launch_filter_gemm(const float* q, int32_t n_tok, const float* c, int32_t n
 void launch_select(const WaveArgs& a, hipStream_t s);
 void launch_scored(const WaveArgs& a, hipStream_t s);
 void launch_pairing(const WaveArgs& a, hipStream_t s);
-void launch_qdigits(const WaveArgs& a, hipStream_t s);
+void launch_wave_prep(const WaveArgs& a, uint32_t* ep, uint32_t last, hipStream_t s);
 void launch_scan_mx(const WaveArgs& a, hipStream_t s);
 int scan_mx_blocks_per_cu(int nbits);
 void launch_fold(const WaveArgs& a, hipStream_t s);
 void launch_topk(const WaveArgs& a, hipStream_t s);
 void launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
 void launch_zero_cells(uint32_t* p, int64_t n, hipStream_t s);  // streaming stores
-void launch_epoch_step(uint32_t* ep, int32_t n, uint32_t last, hipStream_t s);
 void launch_check_docs(const int32_t* ids, int64_t n, int32_t n_docs, int32_t* err, hipStream_t s);
 void launch_check_queries(const float* q, int64_t n_tok, int32_t* err, hipStream_t s);
 void launch_doc_len(const int32_t* doc_ids, int64_t n, int32_t* doc_len, int32_t n_docs, hipStream_t s);

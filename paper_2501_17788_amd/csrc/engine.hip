@@ -518,7 +518,6 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
     const int32_t qw = wave_queries(idx, n_queries, T);
     int rc = reserve(idx, qw, T, P, s);
     if (rc) return rc;
-    launch_check_queries(dq, (int64_t)n_queries * T, idx->err, s);
     const int64_t words = ((int64_t)idx->n_docs + 31) / 32;
     for (int32_t q0 = 0; q0 < n_queries; q0 += qw) {
         const int32_t nq = n_queries - q0 < qw ? n_queries - q0 : qw;
@@ -589,15 +588,15 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         mark(1);
         launch_select(a, s);
         mark(2);
-        if (epochs) {  // the slots' next epochs, after zeroing those past the last one
+        if (epochs) {  // the slots' next epochs (the preparation applies the same rule on the device),
+                       // after zeroing those past the last one
             zero_slots(idx, nq, true, s);
             for (int32_t q = 0; q < nq; ++q)
                 idx->slot_ep[q] = idx->slot_ep[q] >= (uint32_t)idx->tab_epochs ? 1u : idx->slot_ep[q] + 1u;
-            launch_epoch_step((uint32_t*)idx->q_epoch.p, nq, (uint32_t)idx->tab_epochs, s);
         }
+        launch_wave_prep(a, epochs ? (uint32_t*)idx->q_epoch.p : nullptr, (uint32_t)idx->tab_epochs, s);
         launch_scored(a, s);
         launch_pairing(a, s);
-        launch_qdigits(a, s);
         mark(3);
         launch_scan_mx(a, s);
         mark(4);

@@ -195,7 +195,7 @@ void launch_pairing(const WaveArgs& a, hipStream_t s) {
     const int64_t n = (int64_t)a.n_q * a.n_qtok * a.nprobe;
     const unsigned pb = (unsigned)((n + 255) / 256);
     const unsigned nblk = (unsigned)((a.n_c + kPlanBlock - 1) / kPlanBlock);
-    launch_fill_i32(a.ccount, a.n_c, 0, s);
+    // (the token counters were zeroed by the wave's preparation)
     hipLaunchKernelGGL(k_pair_count, dim3(pb), dim3(256), 0, s, a);
     hipLaunchKernelGGL(k_cplan_local, dim3(nblk), dim3(kPlanBlock), 0, s, a);
     hipLaunchKernelGGL(k_cplan_add, dim3(nblk), dim3(kPlanBlock), 0, s, a);

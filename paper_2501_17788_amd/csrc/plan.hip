@@ -56,17 +56,7 @@ void launch_zero_cells(uint32_t* p, int64_t n, hipStream_t s) {
     launch_fill_i32(reinterpret_cast<int32_t*>(p + head + 4 * units), n - head - 4 * units, 0, s);
 }
 
-// The next epoch of every query slot of a wave: 1 after the last one (whose rows the host
-// has just zeroed), else one more.
-__global__ void k_epoch_step(uint32_t* ep, int32_t n, uint32_t last) {
-    const int32_t i = blockIdx.x * 256 + threadIdx.x;
-    if (i < n) ep[i] = ep[i] >= last ? 1u : ep[i] + 1u;
-}
 
-void launch_epoch_step(uint32_t* ep, int32_t n, uint32_t last, hipStream_t s) {
-    if (n <= 0) return;
-    hipLaunchKernelGGL(k_epoch_step, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, ep, n, last);
-}
 
 }  // namespace warp
 

@@ -94,18 +94,44 @@ __device__ __forceinline__ void slot_of_dim(int d, int& s, int& g, int& j) {
     }
 }
 
-// Query digit planes of every wave token: qdig[t][(p * 2 + s) * 4 + g][16] bytes.
+// Per-wave preparation in one launch, ordered after the previous wave's scan and fold and
+// before this wave's planning and scan. Blocks [0, nb0): the clusters' token counters zeroed,
+// the query slots' next epochs (1 after the last one, else one more; ep may be null) and the
+// scan's batch counter set to the grid size. The next nb1 blocks: the norm check of the wave's
+// query tokens (one wave per token; a failure sets kErrQueryNorm). The rest: the query digit
+// planes of every wave token, qdig[t][(p * 2 + s) * 4 + g][16] bytes.
 template <int NBITS>
-__global__ __launch_bounds__(256) void k_qdigits(const float* __restrict__ q, int64_t n_tok,
-                                                 int8_t* __restrict__ qdig) {
-    const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
+__global__ __launch_bounds__(256) void k_wave_prep(WaveArgs a, uint32_t* ep, uint32_t last, int32_t nb0,
+                                                   int32_t nb1) {
+    const int64_t n_tok = (int64_t)a.n_q * a.n_qtok;
+    const int b = blockIdx.x;
+    if (b < nb0) {
+        const int64_t i = (int64_t)b * 256 + threadIdx.x;
+        if (i < a.n_c) a.ccount[i] = 0;
+        if (ep && i < a.n_q) ep[i] = ep[i] >= last ? 1u : ep[i] + 1u;
+        if (i == 0) *a.scan_queue = (uint32_t)a.scan_grid;
+        return;
+    }
+    if (b < nb0 + nb1) {
+        const int64_t t = (int64_t)(b - nb0) * 4 + (threadIdx.x >> 6);
+        const int lane = threadIdx.x & 63;
+        if (t >= n_tok) return;  // wave-uniform
+        const float x0 = a.queries[t * kDim + lane], x1 = a.queries[t * kDim + 64 + lane];
+        double ss = (double)x0 * x0 + (double)x1 * x1;
+        bool bad = !(__builtin_isfinite(x0) && __builtin_isfinite(x1));
+        for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
+        bad = __any(bad);
+        if (lane == 0 && (bad || !(ss <= (1.0 + 1e-3) * (1.0 + 1e-3)))) atomicOr(a.err, kErrQueryNorm);
+        return;
+    }
+    const int64_t x = (int64_t)(b - nb0 - nb1) * 256 + threadIdx.x;
     if (x >= n_tok * kDim) return;
     const int64_t t = x / kDim;
     const int d = (int)(x % kDim);
     int s, g, j, d0, d1, d2;
     slot_of_dim<NBITS>(d, s, g, j);
-    digits3(quant22(q[x]), d0, d1, d2);
-    int8_t* row = qdig + t * kQdigBytes;
+    digits3(quant22(a.queries[x]), d0, d1, d2);
+    int8_t* row = a.qdig + t * kQdigBytes;
     row[((0 * 2 + s) * 4 + g) * 16 + j] = (int8_t)d0;
     row[((1 * 2 + s) * 4 + g) * 16 + j] = (int8_t)d1;
     row[((2 * 2 + s) * 4 + g) * 16 + j] = (int8_t)d2;
@@ -510,21 +536,23 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
     }
 }
 
-void launch_qdigits(const WaveArgs& a, hipStream_t s) {
+void launch_wave_prep(const WaveArgs& a, uint32_t* ep, uint32_t last, hipStream_t s) {
     const int64_t n_tok = (int64_t)a.n_q * a.n_qtok;
-    const dim3 grid((unsigned)((n_tok * kDim + 255) / 256));
+    const int64_t n0 = a.n_c > a.n_q ? a.n_c : a.n_q;
+    const int32_t nb0 = (int32_t)((n0 + 255) / 256), nb1 = (int32_t)((n_tok + 3) / 4);
+    const dim3 grid((unsigned)(nb0 + nb1 + (n_tok * kDim + 255) / 256));
     switch (a.nbits) {
-        case 1: hipLaunchKernelGGL(k_qdigits<1>, grid, dim3(256), 0, s, a.queries, n_tok, a.qdig); break;
-        case 2: hipLaunchKernelGGL(k_qdigits<2>, grid, dim3(256), 0, s, a.queries, n_tok, a.qdig); break;
-        case 4: hipLaunchKernelGGL(k_qdigits<4>, grid, dim3(256), 0, s, a.queries, n_tok, a.qdig); break;
-        default: hipLaunchKernelGGL(k_qdigits<8>, grid, dim3(256), 0, s, a.queries, n_tok, a.qdig); break;
+        case 1: hipLaunchKernelGGL(k_wave_prep<1>, grid, dim3(256), 0, s, a, ep, last, nb0, nb1); break;
+        case 2: hipLaunchKernelGGL(k_wave_prep<2>, grid, dim3(256), 0, s, a, ep, last, nb0, nb1); break;
+        case 4: hipLaunchKernelGGL(k_wave_prep<4>, grid, dim3(256), 0, s, a, ep, last, nb0, nb1); break;
+        default: hipLaunchKernelGGL(k_wave_prep<8>, grid, dim3(256), 0, s, a, ep, last, nb0, nb1); break;
     }
 }
 
 void launch_scan_mx(const WaveArgs& a, hipStream_t s) {
     const dim3 grid(a.scan_grid), block(kMxBlock);
-    // the first batch of every workgroup is fixed; the counter hands out the rest
-    launch_fill_i32(reinterpret_cast<int32_t*>(a.scan_queue), 1, a.scan_grid, s);
+    // the first batch of every workgroup is fixed; the counter (set to the grid size by the
+    // wave's preparation) hands out the rest
     switch (a.nbits) {
         case 1: hipLaunchKernelGGL(k_scan_mx<1>, grid, block, 0, s, a); break;
         case 2: hipLaunchKernelGGL(k_scan_mx<2>, grid, block, 0, s, a); break;
