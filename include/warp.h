@@ -252,8 +252,9 @@ int warp_set_scoring(warp_index* index, int32_t mode);
  * warp_stage_timings returns, per stage, the summed milliseconds and the number
  * of launches since then, counting the searches completed by a synchronising
  * call (warp_search, warp_search_debug, warp_index_sync). Stages: [0] centroid
- * filter GEMM, [1] selection, [2] plan, [3] residual scan, [4] document fold,
- * [5] top-k.
+ * filter GEMM, [1] selection (with the wave's preparation before it: query
+ * checks and digit planes, counters, and the zeroing of token-max rows whose
+ * epochs ran out), [2] plan, [3] residual scan, [4] document fold, [5] top-k.
  */
 int warp_set_timing(warp_index* idx, int32_t enable);
 int warp_stage_timings(const warp_index* idx, double* total_ms, int64_t* launches, int32_t n);

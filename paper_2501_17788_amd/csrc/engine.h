@@ -88,11 +88,9 @@ struct WaveArgs {
     // cluster-major pairing
     int32_t* ccount;            // [n_c] probing tokens per cluster
     int32_t* cursor;            // [n_c] scatter cursors
-    int64_t* item_start;        // [n_c + 1] exclusive prefix of work items
     int32_t* pair_start;        // [n_c + 1] exclusive prefix of pairs
     int32_t* plist;             // [n_tok * nprobe][2]: (wave token, R(S64) + cell bias) grouped by cluster
     int8_t* qdig;               // [n_tok][kQdigBytes] query digit planes in operand order
-    int64_t* blk;               // [2 * ceil(n_c / kPlanBlock)] block sums of items and pairs
     // The scan's items run over the probed chunks in the index's fixed pseudo-random chunk
     // order, the token groups of one chunk consecutively, so that the equal shares of the
     // persistent grid hold similar mixes of dense and sparse chunks of all clusters.

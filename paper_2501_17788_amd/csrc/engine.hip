@@ -84,7 +84,7 @@ struct warp_index {
     bool tab_force_zero = false;   // zero every slot first (after a query-norm error)
     std::vector<uint32_t> slot_ep; // epoch of each query slot's rows; 0: all zero
     DevBuf q_epoch;                // device copy of slot_ep
-    DevBuf ccount, cursor, item_start, pair_start, plist, qdig, blk;
+    DevBuf ccount, cursor, pair_start, plist, qdig;
     DevBuf list_rec, list_item, cblk;  // the wave's probed chunks (see WaveArgs)
     DevBuf scan_queue;
     int32_t scoring = WARP_SCORING_PAPER;
@@ -381,14 +381,11 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, hipStream_t s) {
     if (!rc) rc = grow(idx->m_fixed, (size_t)n_tok * 8);
     if (!rc) rc = grow(idx->keys, (size_t)qw * idx->n_docs * 8);
     if (!rc) rc = grow(idx->qpart, (size_t)qw * (((size_t)idx->n_docs + 255) / 256) * 16);
-    const int64_t nblk = ((int64_t)idx->n_c + kPlanBlock - 1) / kPlanBlock;
     if (!rc) rc = grow(idx->ccount, (size_t)idx->n_c * 4);
     if (!rc) rc = grow(idx->cursor, (size_t)idx->n_c * 4);
-    if (!rc) rc = grow(idx->item_start, ((size_t)idx->n_c + 1) * 8);
     if (!rc) rc = grow(idx->pair_start, ((size_t)idx->n_c + 1) * 4);
     if (!rc) rc = grow(idx->plist, (size_t)n_tok * P * 8);
     if (!rc) rc = grow(idx->qdig, (size_t)n_tok * kQdigBytes);
-    if (!rc) rc = grow(idx->blk, (size_t)nblk * 16);
     const int64_t cblocks = (idx->n_chunks + kPlanBlock - 1) / kPlanBlock;
     if (!rc) rc = grow(idx->list_rec, (size_t)idx->n_chunks * 16);
     if (!rc) rc = grow(idx->list_item, ((size_t)idx->n_chunks + 2) * 8);  // + the count
@@ -561,10 +558,8 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         a.dbg_scored = o.scored ? o.scored + q0 : nullptr;
         a.ccount = (int32_t*)idx->ccount.p;
         a.cursor = (int32_t*)idx->cursor.p;
-        a.item_start = (int64_t*)idx->item_start.p;
         a.pair_start = (int32_t*)idx->pair_start.p;
         a.plist = (int32_t*)idx->plist.p;
-        a.blk = (int64_t*)idx->blk.p;
         a.chunk_c = idx->chunk_c;
         a.chunk_k = idx->chunk_k;
         a.n_chunks = idx->n_chunks;
@@ -586,15 +581,16 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
         mark(0);
         launch_filter_gemm(a.queries, nq * T, idx->centroids, idx->n_c, a.filter_bins, nullptr, s);
         mark(1);
-        launch_select(a, s);
-        mark(2);
         if (epochs) {  // the slots' next epochs (the preparation applies the same rule on the device),
                        // after zeroing those past the last one
             zero_slots(idx, nq, true, s);
             for (int32_t q = 0; q < nq; ++q)
                 idx->slot_ep[q] = idx->slot_ep[q] >= (uint32_t)idx->tab_epochs ? 1u : idx->slot_ep[q] + 1u;
         }
+        // the preparation zeroes the cluster token counters that the selection counts into
         launch_wave_prep(a, epochs ? (uint32_t*)idx->q_epoch.p : nullptr, (uint32_t)idx->tab_epochs, s);
+        launch_select(a, s);
+        mark(2);
         launch_scored(a, s);
         launch_pairing(a, s);
         mark(3);
@@ -714,8 +710,8 @@ void warp_index_free(warp_index* idx) {
                         (void*)idx->codes, (void*)idx->weights, (void*)idx->err})
             if (p) (void)hipFree(p);
         for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_pref, &idx->m_fixed,
-                          &idx->tokmax, &idx->q_epoch, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount, &idx->cursor, &idx->item_start,
-                          &idx->pair_start, &idx->plist, &idx->qdig, &idx->blk, &idx->list_rec, &idx->list_item, &idx->cblk, &idx->scan_queue, &idx->st_q, &idx->st_ids, &idx->st_scores,
+                          &idx->tokmax, &idx->q_epoch, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount, &idx->cursor,
+                          &idx->pair_start, &idx->plist, &idx->qdig, &idx->list_rec, &idx->list_item, &idx->cblk, &idx->scan_queue, &idx->st_q, &idx->st_ids, &idx->st_scores,
                           &idx->st_fixed, &idx->st_counts, &idx->st_sel, &idx->st_m, &idx->st_bitmap,
                           &idx->st_scored})
             release(*b);

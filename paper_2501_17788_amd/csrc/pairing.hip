@@ -1,105 +1,83 @@
 // Cluster-major work plan of one wave of queries: every (query token, probed
-// cluster) pair is bucketed by cluster (a counting sort), and each probed
-// cluster is cut into work items of (kMxChunk embeddings) x (kMxGroup tokens),
-// so that the residual scan reads a cluster chunk once for all the tokens that
-// probe it. Pair order inside a bucket follows atomic arrival and does not
-// affect results: the token-level max is exact and commutative.
+// cluster) pair is bucketed by cluster (a counting sort whose counts the selection
+// takes), and each probed cluster is cut into work items of (kMxChunk embeddings) x
+// (kMxGroup tokens), so that the residual scan reads a cluster chunk once for all the
+// tokens that probe it. Pair order inside a bucket follows atomic arrival and does not
+// affect results: the token-level max is exact and commutative. Two launches: the
+// counts' prefix sums, then the buckets and the list of probed chunks.
 #include "engine.h"
 
 namespace warp {
 
-// pairs of tokens whose selection overflowed carry cluster -1 and are skipped
-__global__ __launch_bounds__(256) void k_pair_count(WaveArgs a) {
-    const int64_t n = (int64_t)a.n_q * a.n_qtok * a.nprobe;
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (i >= n) return;
-    const int c = a.sel[i];
-    if (c >= 0) atomicAdd(&a.ccount[c], 1);
-}
+constexpr int kPairPer = 32;  // clusters per thread and pass of the pair offsets
 
-__device__ __forceinline__ int64_t cluster_items(int32_t n_tok, int32_t size) {
-    if (n_tok <= 0 || size <= 0) return 0;
-    return (int64_t)((size + kMxChunk - 1) / kMxChunk) * ((n_tok + kMxGroup - 1) / kMxGroup);
-}
-
-// exclusive scans of items and pairs inside each block of kPlanBlock clusters
-__global__ __launch_bounds__(kPlanBlock) void k_cplan_local(WaveArgs a) {
-    __shared__ int64_t si[kPlanBlock];
-    __shared__ int64_t sp[kPlanBlock];
-    const int tid = threadIdx.x;
-    const int64_t c = (int64_t)blockIdx.x * kPlanBlock + tid;
-    const bool in = c < a.n_c;
-    const int32_t nt = in ? a.ccount[c] : 0;
-    const int64_t items = in ? cluster_items(nt, a.sizes[c]) : 0;
-    si[tid] = items;
-    sp[tid] = nt;
-    __syncthreads();
-    for (int off = 1; off < kPlanBlock; off <<= 1) {
-        const int64_t vi = tid >= off ? si[tid - off] : 0;
-        const int64_t vp = tid >= off ? sp[tid - off] : 0;
-        __syncthreads();
-        si[tid] += vi;
-        sp[tid] += vp;
-        __syncthreads();
-    }
-    if (in) {
-        a.item_start[c] = si[tid] - items;
-        a.pair_start[c] = (int32_t)(sp[tid] - nt);
-        a.cursor[c] = 0;
-    }
-    if (tid == kPlanBlock - 1) {
-        a.blk[2 * blockIdx.x] = si[tid];
-        a.blk[2 * blockIdx.x + 1] = sp[tid];
-    }
-}
-
-// add the sums of all earlier blocks; the last block also writes the totals
-__global__ __launch_bounds__(kPlanBlock) void k_cplan_add(WaveArgs a) {
-    __shared__ int64_t ri[kPlanBlock];
-    __shared__ int64_t rp[kPlanBlock];
-    const int tid = threadIdx.x;
-    const int b = blockIdx.x;
-    const int nblk = gridDim.x;
-    int64_t vi = 0, vp = 0;
-    for (int j = tid; j < b; j += kPlanBlock) {
-        vi += a.blk[2 * j];
-        vp += a.blk[2 * j + 1];
-    }
-    ri[tid] = vi;
-    rp[tid] = vp;
-    __syncthreads();
-    for (int off = kPlanBlock / 2; off > 0; off >>= 1) {
-        if (tid < off) {
-            ri[tid] += ri[tid + off];
-            rp[tid] += rp[tid + off];
+// The exclusive prefix of the clusters' probing-token counts (each cluster's first pair in
+// the bucketed list), by one workgroup of kPlanBlock threads: per pass, thread tid takes
+// kPairPer consecutive clusters, and the pass's running total carries to the next.
+__device__ void pair_offsets(const WaveArgs& a, int64_t* ws) {
+    constexpr int NW = kPlanBlock / 64;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int64_t n_c = a.n_c;
+    int64_t carry = 0;
+    for (int64_t c0 = 0; c0 < n_c; c0 += (int64_t)kPlanBlock * kPairPer) {  // uniform
+        const int64_t cb = c0 + (int64_t)tid * kPairPer;
+        int32_t v[kPairPer];
+        const bool whole = cb + kPairPer <= n_c;  // 16-byte aligned: cb is a multiple of 32
+        if (whole) {
+            const int4* src = reinterpret_cast<const int4*>(a.ccount + cb);
+#pragma unroll
+            for (int j = 0; j < kPairPer / 4; ++j) {
+                const int4 x = src[j];
+                v[4 * j] = x.x;
+                v[4 * j + 1] = x.y;
+                v[4 * j + 2] = x.z;
+                v[4 * j + 3] = x.w;
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < kPairPer; ++j) v[j] = cb + j < n_c ? a.ccount[cb + j] : 0;
         }
+        int64_t sum = 0;
+#pragma unroll
+        for (int j = 0; j < kPairPer; ++j) sum += v[j];
+        int64_t x = sum;  // inclusive scan of the threads' sums
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int64_t t = __shfl_up(x, off, 64);
+            if (lane >= off) x += t;
+        }
+        if (lane == 63) ws[w] = x;
         __syncthreads();
+        int64_t before = 0, total = 0;
+#pragma unroll
+        for (int i = 0; i < NW; ++i) {
+            before += i < w ? ws[i] : 0;
+            total += ws[i];
+        }
+        __syncthreads();  // ws is free for the next pass
+        int32_t run = (int32_t)(carry + before + x - sum);
+        if (whole) {
+            int4* dst = reinterpret_cast<int4*>(a.pair_start + cb);
+#pragma unroll
+            for (int j = 0; j < kPairPer / 4; ++j) {
+                int4 o;
+                o.x = run;
+                o.y = o.x + v[4 * j];
+                o.z = o.y + v[4 * j + 1];
+                o.w = o.z + v[4 * j + 2];
+                run = o.w + v[4 * j + 3];
+                dst[j] = o;
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < kPairPer; ++j) {
+                if (cb + j < n_c) a.pair_start[cb + j] = run;
+                run += v[j];
+            }
+        }
+        carry += total;
     }
-    const int64_t oi = ri[0], op = rp[0];
-    const int64_t c = (int64_t)b * kPlanBlock + tid;
-    if (c < a.n_c) {
-        a.item_start[c] += oi;
-        a.pair_start[c] += (int32_t)op;
-    }
-    if (b == nblk - 1 && tid == 0) {
-        a.item_start[a.n_c] = oi + a.blk[2 * b];
-        a.pair_start[a.n_c] = (int32_t)(op + a.blk[2 * b + 1]);
-    }
-}
-
-__global__ __launch_bounds__(256) void k_pair_scatter(WaveArgs a) {
-    const int64_t n = (int64_t)a.n_q * a.n_qtok * a.nprobe;
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (i >= n) return;
-    const int c = a.sel[i];
-    if (c < 0) return;
-    const int slot = atomicAdd(&a.cursor[c], 1);
-    const int64_t p = (int64_t)a.pair_start[c] + slot;
-    const int32_t tok = (int32_t)(i / a.nprobe);
-    uint32_t bias, vmin;
-    cell_code(a, tok / a.n_qtok, bias, vmin);
-    a.plist[2 * p] = tok;                                   // wave token
-    a.plist[2 * p + 1] = (int32_t)((uint32_t)a.base[i] + bias);  // R(S64) of (token, cluster) + the cell bias
+    if (tid == 0) a.pair_start[n_c] = (int32_t)carry;
 }
 
 // Probed chunks and their items (token groups of their cluster) in the index's chunk order.
@@ -138,24 +116,52 @@ __device__ __forceinline__ void block_scan2(int64_t& f, int64_t& it, int64_t* wf
     it += bi;
 }
 
-// per block of kPlanBlock chunks: the number of probed chunks and their items
-__global__ __launch_bounds__(kPlanBlock) void k_chunk_count(WaveArgs a) {
+// Block 0: the clusters' pair offsets. Blocks 1 ..: per block of kPlanBlock chunks, the
+// number of probed chunks and their items.
+__global__ __launch_bounds__(kPlanBlock) void k_plan_count(WaveArgs a) {
     __shared__ int64_t wf[kPlanBlock / 64], wi[kPlanBlock / 64];
+    if (blockIdx.x == 0) {
+        pair_offsets(a, wf);
+        return;
+    }
+    const int64_t b = (int64_t)blockIdx.x - 1;
     int64_t f, it;
-    chunk_items(a, (int64_t)blockIdx.x * kPlanBlock + threadIdx.x, f, it);
+    chunk_items(a, b * kPlanBlock + threadIdx.x, f, it);
     block_scan2(f, it, wf, wi);
     if (threadIdx.x == kPlanBlock - 1) {
-        a.cblk[2 * blockIdx.x] = f;
-        a.cblk[2 * blockIdx.x + 1] = it;
+        a.cblk[2 * b] = f;
+        a.cblk[2 * b + 1] = it;
     }
 }
 
-// the compacted list of probed chunks with the exclusive prefix of their items
-__global__ __launch_bounds__(kPlanBlock) void k_chunk_list(WaveArgs a) {
+// Every (token, probed cluster) pair placed in its cluster's bucket: the wave token and the
+// token's centroid term R(S64) plus its query's cell bias. Pairs of tokens whose selection
+// overflowed carry cluster -1 and are skipped.
+__device__ __forceinline__ void pair_scatter(const WaveArgs& a, int64_t i) {
+    const int64_t n = (int64_t)a.n_q * a.n_qtok * a.nprobe;
+    if (i >= n) return;
+    const int c = a.sel[i];
+    if (c < 0) return;
+    const int slot = atomicAdd(&a.cursor[c], 1);
+    const int64_t p = (int64_t)a.pair_start[c] + slot;
+    const int32_t tok = (int32_t)(i / a.nprobe);
+    uint32_t bias, vmin;
+    cell_code(a, tok / a.n_qtok, bias, vmin);
+    a.plist[2 * p] = tok;
+    a.plist[2 * p + 1] = (int32_t)((uint32_t)a.base[i] + bias);
+}
+
+// Blocks [0, cb): the compacted list of probed chunks with the exclusive prefix of their
+// items. Blocks [cb, ...): the pairs, kPlanBlock per block, scattered into their buckets.
+__global__ __launch_bounds__(kPlanBlock) void k_plan_emit(WaveArgs a, int32_t cb) {
     __shared__ int64_t wf[kPlanBlock / 64], wi[kPlanBlock / 64];
     __shared__ unsigned long long s_of, s_oi;
     const int tid = threadIdx.x;
     const int b = blockIdx.x;
+    if (b >= cb) {  // uniform over the block
+        pair_scatter(a, (int64_t)(b - cb) * kPlanBlock + tid);
+        return;
+    }
     if (tid == 0) {
         s_of = 0;
         s_oi = 0;
@@ -185,29 +191,24 @@ __global__ __launch_bounds__(kPlanBlock) void k_chunk_list(WaveArgs a) {
         a.list_rec[pos] = make_int4((int)(uint32_t)ew, (int)(uint32_t)(ew >> 32), a.pair_start[c], a.ccount[c]);
         a.list_item[pos] = item;
     }
-    if (b == (int)gridDim.x - 1 && tid == kPlanBlock - 1) {
+    if (b == cb - 1 && tid == kPlanBlock - 1) {
         *a.list_n = (int64_t)s_of + f;
         a.list_item[(int64_t)s_of + f] = (int64_t)s_oi + it;
     }
 }
 
 void launch_pairing(const WaveArgs& a, hipStream_t s) {
-    const int64_t n = (int64_t)a.n_q * a.n_qtok * a.nprobe;
-    const unsigned pb = (unsigned)((n + 255) / 256);
-    const unsigned nblk = (unsigned)((a.n_c + kPlanBlock - 1) / kPlanBlock);
-    // (the token counters were zeroed by the wave's preparation)
-    hipLaunchKernelGGL(k_pair_count, dim3(pb), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_cplan_local, dim3(nblk), dim3(kPlanBlock), 0, s, a);
-    hipLaunchKernelGGL(k_cplan_add, dim3(nblk), dim3(kPlanBlock), 0, s, a);
-    hipLaunchKernelGGL(k_pair_scatter, dim3(pb), dim3(256), 0, s, a);
+    // (the wave's preparation zeroed the token counters and cursors; the selection counted)
     const unsigned cb = (unsigned)((a.n_chunks + kPlanBlock - 1) / kPlanBlock);
-    if (cb == 0) {  // an index without embeddings: no chunk, no item
+    if (cb == 0) {  // an index without embeddings: no chunk, no item, no pair is read
         launch_fill_i32(reinterpret_cast<int32_t*>(a.list_n), 2, 0, s);
         launch_fill_i32(reinterpret_cast<int32_t*>(a.list_item), 2, 0, s);
         return;
     }
-    hipLaunchKernelGGL(k_chunk_count, dim3(cb), dim3(kPlanBlock), 0, s, a);
-    hipLaunchKernelGGL(k_chunk_list, dim3(cb), dim3(kPlanBlock), 0, s, a);
+    const int64_t n = (int64_t)a.n_q * a.n_qtok * a.nprobe;
+    const unsigned pb = (unsigned)((n + kPlanBlock - 1) / kPlanBlock);
+    hipLaunchKernelGGL(k_plan_count, dim3(1 + cb), dim3(kPlanBlock), 0, s, a);
+    hipLaunchKernelGGL(k_plan_emit, dim3(cb + pb), dim3(kPlanBlock), 0, s, a, (int32_t)cb);
 }
 
 }  // namespace warp

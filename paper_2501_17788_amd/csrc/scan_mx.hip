@@ -95,9 +95,9 @@ __device__ __forceinline__ void slot_of_dim(int d, int& s, int& g, int& j) {
 }
 
 // Per-wave preparation in one launch, ordered after the previous wave's scan and fold and
-// before this wave's planning and scan. Blocks [0, nb0): the clusters' token counters zeroed,
-// the query slots' next epochs (1 after the last one, else one more; ep may be null) and the
-// scan's batch counter set to the grid size. The next nb1 blocks: the norm check of the wave's
+// before this wave's selection. Blocks [0, nb0): the clusters' token counters and scatter
+// cursors zeroed, the query slots' next epochs (1 after the last one, else one more; ep may
+// be null) and the scan's batch counter set to the grid size. The next nb1 blocks: the norm check of the wave's
 // query tokens (one wave per token; a failure sets kErrQueryNorm). The rest: the query digit
 // planes of every wave token, qdig[t][(p * 2 + s) * 4 + g][16] bytes.
 template <int NBITS>
@@ -107,7 +107,10 @@ __global__ __launch_bounds__(256) void k_wave_prep(WaveArgs a, uint32_t* ep, uin
     const int b = blockIdx.x;
     if (b < nb0) {
         const int64_t i = (int64_t)b * 256 + threadIdx.x;
-        if (i < a.n_c) a.ccount[i] = 0;
+        if (i < a.n_c) {
+            a.ccount[i] = 0;
+            a.cursor[i] = 0;
+        }
         if (ep && i < a.n_q) ep[i] = ep[i] >= last ? 1u : ep[i] + 1u;
         if (i == 0) *a.scan_queue = (uint32_t)a.scan_grid;
         return;

@@ -285,12 +285,14 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
     __syncthreads();
 
     // 5. the n_probe best in exact order (an entry's position is its rank among the rescored
-    //    entries), their fixed-point scores and the prefix of their sizes
+    //    entries), their fixed-point scores and the prefix of their sizes; each selected
+    //    cluster counts the token among its probing tokens (the work plan's bucket sizes)
     for (int p = tid; p < nA; p += NT) {
         const int r = rank_of(sA, idA, nA, sA[p], idA[p]);
         if (r < P) {
             const int c = idA[p];
             sel[r] = c;
+            atomicAdd(&a.ccount[c], 1);
             base[r] = (int32_t)to_fixed(sA[p]);
             cum[r] = szA[p];
             if (a.dbg_sel) a.dbg_sel[(int64_t)t * P + r] = c;
