@@ -32,24 +32,40 @@ __device__ __forceinline__ bool before(double xs, int xi, double ys, int yi) {
     return xs > ys || (xs == ys && xi < yi);
 }
 
-// Number of the n LDS entries that come before entry (xs, xi) in (score desc, id asc)
-// order: its position in that order, since ids are distinct.
-__device__ __forceinline__ int rank_of(const double* s, const int* id, int n, double xs, int xi) {
-    int r = 0;
-    for (int j = 0; j < n; ++j) r += before(s[j], id[j], xs, xi) ? 1 : 0;
-    return r;
+constexpr int kSelThreads = 512;
+
+// Calls place(p, r) for each of the n LDS entries p, with r the number of entries that come
+// before it in (score desc, id asc) order: its position in that order, since ids are
+// distinct. Each entry is ranked by a group of L lanes of one wave (the largest power of two
+// up to 64 with n L <= kSelThreads, at least 1), which split the comparisons and add their
+// counts; place runs on the group's first lane. Every thread calls it.
+template <typename F>
+__device__ __forceinline__ void rank_all(const double* s, const int* id, int n, F place) {
+    int L = 64;
+    while (L > 1 && n * L > kSelThreads) L >>= 1;
+    const int sub = threadIdx.x & (L - 1);
+    for (int p = threadIdx.x / L; p < n; p += kSelThreads / L) {  // uniform over each group
+        const double xs = s[p];
+        const int xi = id[p];
+        int r = 0;
+        for (int j = sub; j < n; j += L) r += before(s[j], id[j], xs, xi) ? 1 : 0;
+        for (int off = L >> 1; off > 0; off >>= 1) r += __shfl_xor(r, off, 64);
+        if (sub == 0) place(p, r);
+    }
 }
 
 // fp64 centroid score, accumulated in dimension order (each product is exact), by the
 // four lanes 4 m .. 4 m + 3 of a wave that share centroid c: lane part loads dimensions
 // 32 part .. 32 part + 31 (one round trip for the whole row), and the running sum passes
-// from lane to lane in that order. Every lane of the four returns the score.
-__device__ __noinline__ double score64_quad(const float* __restrict__ cen, int c, const float* qs,
-                                               int part) {
+// from lane to lane in that order. Every lane of the four returns the score; the cluster's
+// size is loaded with the row.
+__device__ __noinline__ double score64_quad(const float* __restrict__ cen, const int32_t* __restrict__ sizes,
+                                               int c, const float* qs, int part, int& size) {
     const float4* row = reinterpret_cast<const float4*>(cen + (int64_t)c * kDim) + 8 * part;
     float4 v[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) v[k] = row[k];
+    size = sizes[c];
     const int lead = (threadIdx.x & 63) & ~3;
     const float* qp = qs + 32 * part;
     double s = 0.0;
@@ -72,7 +88,7 @@ __device__ __noinline__ double score64_quad(const float* __restrict__ cen, int c
     return s;
 }
 
-constexpr int kSelThreads = 512;
+constexpr int kBinLoads = 8;  // 16-byte bin loads in flight per thread: 2^15 bins in one round
 
 // Inclusive prefix sum over the block of one value per thread: shuffle scans inside
 // each wave, then the wave totals through LDS (wtot: one entry per wave). Also returns
@@ -115,7 +131,7 @@ constexpr unsigned long long kCntOne = 1ull << 40;  // histogram word: (count <<
 constexpr unsigned long long kSizeMask = kCntOne - 1;
 
 // Calls f(c, bin) for every centroid of the token's row of bins: 16-byte loads of
-// eight bins when the row is 16-byte aligned, four loads in flight per thread.
+// eight bins when the row is 16-byte aligned, kBinLoads loads in flight per thread.
 template <typename F>
 __device__ __forceinline__ void for_each_bin(const uint16_t* bins, int n_c, F f) {
     constexpr int NT = kSelThreads;
@@ -123,15 +139,15 @@ __device__ __forceinline__ void for_each_bin(const uint16_t* bins, int n_c, F f)
     if ((n_c & 7) == 0 && ((uintptr_t)bins & 15) == 0) {
         const uint4* b4 = reinterpret_cast<const uint4*>(bins);
         const int n8 = n_c >> 3;
-        for (int j0 = 0; j0 < n8; j0 += 4 * NT) {
-            uint4 v[4];
+        for (int j0 = 0; j0 < n8; j0 += kBinLoads * NT) {
+            uint4 v[kBinLoads];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < kBinLoads; ++u) {
                 const int j = j0 + u * NT + tid;
                 v[u] = j < n8 ? b4[j] : make_uint4(0, 0, 0, 0);
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < kBinLoads; ++u) {
                 const int j = j0 + u * NT + tid;
                 if (j >= n8) continue;
                 const unsigned w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
@@ -220,12 +236,15 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
             run += w;
         }
     }
-    for (int j = 0; j < PER; ++j) {
-        if (hist[PER * tid + j] >> 40) {
-            atomicMin(&s_blo, PER * tid + j);
-            break;
-        }
+    int lo = kSelBins;  // the lowest occupied bin: one LDS atomic per wave
+    for (int j = PER - 1; j >= 0; --j)
+        if (hist[PER * tid + j] >> 40) lo = PER * tid + j;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const int o = __shfl_xor(lo, off, 64);
+        lo = o < lo ? o : lo;
     }
+    if ((tid & 63) == 0 && lo < kSelBins) atomicMin(&s_blo, lo);
     __syncthreads();
 
     // 3. collect the centroids near the boundaries
@@ -271,14 +290,15 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
     // 4. fp64 rescoring of both lists, four lanes per centroid; the sizes come in beside
     for (int p = tid >> 2; p < nA + nB; p += NT / 4) {  // uniform over each four lanes
         const int c = p < nA ? idA[p] : idB[p - nA];
-        const double v = score64_quad(a.centroids, c, qs, tid & 3);
+        int sz;
+        const double v = score64_quad(a.centroids, sizes, c, qs, tid & 3, sz);
         if ((tid & 3) == 0) {
             if (p < nA) {
                 sA[p] = v;
-                szA[p] = sizes[c];
+                szA[p] = sz;
             } else {
                 sB[p - nA] = v;
-                szB[p - nA] = sizes[c];
+                szB[p - nA] = sz;
             }
         }
     }
@@ -287,8 +307,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
     // 5. the n_probe best in exact order (an entry's position is its rank among the rescored
     //    entries), their fixed-point scores and the prefix of their sizes; each selected
     //    cluster counts the token among its probing tokens (the work plan's bucket sizes)
-    for (int p = tid; p < nA; p += NT) {
-        const int r = rank_of(sA, idA, nA, sA[p], idA[p]);
+    rank_all(sA, idA, nA, [&](int p, int r) {
         if (r < P) {
             const int c = idA[p];
             sel[r] = c;
@@ -297,7 +316,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
             cum[r] = szA[p];
             if (a.dbg_sel) a.dbg_sel[(int64_t)t * P + r] = c;
         }
-    }
+    });
     __syncthreads();
     block_inclusive_scan(cum, P, wtot);
     for (int j = tid; j <= P; j += NT) seg_pref[j] = j == 0 ? 0 : cum[j - 1];
@@ -306,11 +325,10 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
     // 6. m_i: the band in exact order (its scores placed by rank into sA, free now), and the
     //    first entry whose cumulative size (from the size of everything above the band)
     //    exceeds t'
-    for (int p = tid; p < nB; p += NT) {
-        const int r = rank_of(sB, idB, nB, sB[p], idB[p]);
+    rank_all(sB, idB, nB, [&](int p, int r) {
         sA[r] = sB[p];
         cum[r] = szB[p];
-    }
+    });
     __syncthreads();
     block_inclusive_scan(cum, nB, wtot);
     if (!clamp) {

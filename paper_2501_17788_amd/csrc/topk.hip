@@ -116,8 +116,16 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
             cnt += c;
             mx = m > mx ? m : mx;
         });
-        atomicAdd(&s_ncand, (uint32_t)cnt);
-        atomicMax(&s_max, mx);
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {  // one LDS atomic of each kind per wave
+            cnt += __shfl_xor(cnt, off, 64);
+            const unsigned long long o = __shfl_xor(mx, off, 64);
+            mx = o > mx ? o : mx;
+        }
+        if ((tid & 63) == 0) {
+            atomicAdd(&s_ncand, (uint32_t)cnt);
+            atomicMax(&s_max, mx);
+        }
     }
     __syncthreads();
     const uint32_t ncand = s_ncand;
