@@ -68,6 +68,23 @@ __device__ void find_crossing(const uint32_t* hist, uint32_t need, uint32_t* sca
     __syncthreads();
 }
 
+// Appends key to buf[*count] where pred holds, with one LDS atomic per wave for the lanes
+// that call it together; positions past kMaxK are counted but not written.
+__device__ __forceinline__ void append_key(bool pred, unsigned long long key, uint32_t* count,
+                                           unsigned long long* buf) {
+    const unsigned long long m = __ballot(pred);
+    if (m == 0) return;
+    const int lane = threadIdx.x & 63;
+    const int leader = __builtin_ctzll(m);
+    uint32_t base = 0;
+    if (lane == leader) base = atomicAdd(count, (uint32_t)__popcll(m));
+    base = __shfl(base, leader, 64);
+    if (pred) {
+        const uint32_t p = base + (uint32_t)__popcll(m & ((1ull << lane) - 1));
+        if (p < (uint32_t)kMaxK) buf[p] = key;
+    }
+}
+
 __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
     __shared__ uint32_t hist[kTopkBins];
     __shared__ uint32_t scan[kTopkThreads / 64];
@@ -189,15 +206,26 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
                 if (kv[u] != 0) f(kv[u]);
         }
     };
-    // level 1: coarse bins of the distance below the best score
+    // level 1: coarse bins of the distance below the best score. For K <= kRankMax the same
+    // pass gathers every key within D0, a set that holds the K best: when it has at most
+    // kRankMax keys, they are ranked directly and the passes below are skipped.
     if (!done) {
         for (int i = tid; i < kTopkBins; i += kTopkThreads) hist[i] = 0;
         __syncthreads();
+        const bool spec = d0 != 0 && K <= kRankMax;  // uniform
         for_each_key([&](unsigned long long key) {
             const unsigned long long d = smax - (key >> 24);
             if (d < ((unsigned long long)kTopkBins << kCoarseShift)) atomicAdd(&hist[d >> kCoarseShift], 1u);
+            if (spec) append_key(d < d0, key, &s_count, buf);
         });
         __syncthreads();
+        if (spec && s_count <= (uint32_t)kRankMax) done = true;  // uniform
+        else if (spec) {
+            __syncthreads();  // every thread has read s_count
+            if (tid == 0) s_count = 0;
+        }
+    }
+    if (!done) {
         find_crossing(hist, (uint32_t)K, scan, &s_bin, &s_before);
         const int b1 = s_bin;
         if (b1 >= 0) {
@@ -226,12 +254,7 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
             __syncthreads();
             lim = s_lim;
             if (lim != 0) {
-                for_each_key([&](unsigned long long key) {
-                    if (smax - (key >> 24) < lim) {
-                        const uint32_t p = atomicAdd(&s_count, 1u);
-                        if (p < (uint32_t)kMaxK) buf[p] = key;
-                    }
-                });
+                for_each_key([&](unsigned long long key) { append_key(smax - (key >> 24) < lim, key, &s_count, buf); });
                 done = true;
             }
         }
@@ -271,12 +294,7 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
             __syncthreads();
         }
         const unsigned long long kth = s_prefix;  // the K-th largest key
-        for_each_key([&](unsigned long long key) {
-            if (key >= kth) {
-                const uint32_t p = atomicAdd(&s_count, 1u);
-                if (p < (uint32_t)kMaxK) buf[p] = key;
-            }
-        });
+        for_each_key([&](unsigned long long key) { append_key(key >= kth, key, &s_count, buf); });
         __syncthreads();
     }
     const int cnt = K == 0 ? 0 : (int)(s_count < (uint32_t)kMaxK ? s_count : (uint32_t)kMaxK);
