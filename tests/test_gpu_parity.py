@@ -143,6 +143,16 @@ def test_empty_clusters_and_ragged_tiles():
     run_both(data, label="empty clusters")
 
 
+def test_cluster_offsets_over_several_passes():
+    # 70,001 clusters: the work plan's pair offsets (one workgroup, 32,768 clusters per pass)
+    # carry a running total over three passes and end in a ragged tail; most clusters are empty
+    wl = synth.random_small_workload(11, n_centroids=70001, n_docs=3000, max_len=24, nbits=2, n_queries=4,
+                                     n_qtok=32, nprobe=64, t_prime=50, k=20)
+    data = synth.make_index(wl, workers=1)
+    assert len(data.offsets) - 1 == 70001 and (np.diff(data.offsets) == 0).sum() > 50000
+    run_both(data, label="70001 clusters")
+
+
 # ----------------------------------------------------------------------------- workloads
 
 def test_tiny_workload_exact_and_real_valued():
