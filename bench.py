@@ -2,7 +2,9 @@
 
 A step is one batched search (centroid filter GEMM, selection, plan, residual
 scan, document fold, top-k) of the workload's whole query batch, with the
-index and the queries already resident in HBM. Prints one JSON line.
+index and the queries already resident in HBM. Prints one JSON line. The
+default workload is the full-scale one (8.8M passages, about 600M embeddings,
+b = 2, 4,096 queries of 32 tokens, nprobe 32, k = 1000).
 """
 from __future__ import annotations
 
@@ -73,10 +75,13 @@ def cpu_model() -> str:
 
 
 def host_threads() -> int:
+    """Host threads for the generator and the oracle: the CPUs this process may run on, at
+    most 16 (a one-GPU share of the host)."""
     try:
-        return len(os.sched_getaffinity(0))
+        n = len(os.sched_getaffinity(0))
     except AttributeError:
-        return os.cpu_count() or 1
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
 
 
 def describe(wl) -> str:
@@ -210,11 +215,16 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="small")
+    ap.add_argument("--workload", default=None,
+                    help="tiny, small, mid, long or full (default: full, the largest, at nprobe 32; "
+                         "small for --recall-study and --build)")
     ap.add_argument("--nprobe", type=int, default=0, help="override the workload's nprobe (the full workload "
                                                             "is also measured at 16 and 64)")
     ap.add_argument("--latency-runs", type=int, default=200)
-    ap.add_argument("--cpu-queries", type=int, default=128)
+    ap.add_argument("--cpu-queries", type=int, default=2, help="queries the oracle runs on all host threads")
+    ap.add_argument("--cpu1-tokens", type=int, default=4,
+                    help="tokens of query 0 the oracle runs on one thread (scaled to a query)")
+    ap.add_argument("--host-steps", type=int, default=2, help="batches through the blocking host-pointer call")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the run, copy a buffer of this size 3 times on the device (a kernel of "
@@ -233,6 +243,8 @@ def main() -> int:
               f"requested). Run with --gpus 1.", file=sys.stderr)
         return 2
 
+    if args.workload is None:
+        args.workload = "small" if (args.recall_study or args.build) else "full"
     if args.recall_study:
         return recall_study(args)
     if args.build:
@@ -252,16 +264,18 @@ def main() -> int:
     log(f"bench: {data.n_embeddings} embeddings in {time.time() - t0:.1f} s")
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
+    t0 = time.time()
     ix = Index.from_synthetic(data)
+    log(f"bench: index loaded in {time.time() - t0:.1f} s")
     q = torch.from_numpy(data.queries).to(dev)
     nq = wl.n_queries
 
-    # scored embeddings per query (exact, from the engine's own counters)
-    dbg = ix.search_debug(data.queries, wl.nprobe, wl.t_prime, wl.k)
+    # scored embeddings per query (exact, from the engine's own counters) and the probed
+    # clusters, from a debug search of the same batch
+    dbg = ix.search_debug(data.queries, wl.nprobe, wl.t_prime, wl.k, bitmap=False)
     scored = dbg["n_scored"].astype(np.int64)
     row_bytes = 128 * wl.nbits // 8 + 4
 
-    stream = torch.cuda.current_stream(dev)
     out = None
     for _ in range(args.warmup):
         out = ix.search_async(q, wl.nprobe, wl.t_prime, wl.k, out=out)
@@ -286,15 +300,15 @@ def main() -> int:
     ids = out[0].cpu().numpy()
     same_as_debug = bool(np.array_equal(ids, dbg["ids"]))
 
-    # the same batches through the blocking host-pointer call: the host's query check and the
-    # host <-> device copies of queries and results included
-    for _ in range(2):
-        ix.search(data.queries, wl.nprobe, wl.t_prime, wl.k)
+    # the blocking host-pointer call: the host's query check and the host <-> device copies
+    # of queries and results included (a few batches: not the headline figure)
+    host_steps = max(1, min(args.steps, args.host_steps))
+    ix.search(data.queries, wl.nprobe, wl.t_prime, wl.k)
     a = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(host_steps):
         ix.search(data.queries, wl.nprobe, wl.t_prime, wl.k)
-    host_qps = nq * args.steps / (time.perf_counter() - a)
-    log(f"bench: blocking host-pointer searches {host_qps:.1f} queries/s")
+    host_qps = nq * host_steps / (time.perf_counter() - a)
+    log(f"bench: blocking host-pointer searches {host_qps:.1f} queries/s ({host_steps} batches)")
 
     # batch-1 latency
     lat = []
@@ -310,6 +324,7 @@ def main() -> int:
         lat.append((time.perf_counter() - a) * 1e3)
     p50, p99 = float(np.percentile(lat, 50)), float(np.percentile(lat, 99))
     log(f"bench: batch-1 latency p50 {p50:.3f} ms p99 {p99:.3f} ms")
+    ix.close()
 
     # roofline of the dominant kernel: the residual scan
     scan_ms, scan_n = stages["scan"]
@@ -317,28 +332,46 @@ def main() -> int:
     launches_per_step = max(scan_n, 1) / args.steps
     pairs_per_launch = float(scored.sum()) / launches_per_step  # scored (token, embedding) pairs
     hbm_equiv = pairs_per_launch * row_bytes / scan_avg_s / 1e9  # 16b + 4 bytes per scored pair
-    # int8 matrix-core work of the scan: 9 digit products x 128 dimensions per pair
-    mac = pairs_per_launch * 9 * 128
-    roofline = {"bound": "mfma", "kernel": "k_scan_mx", "resource": "int8 MFMA (exact 3 x 3 digit products)",
-                "achieved": 2 * mac / scan_avg_s / 1e12, "peak": INT8_MFMA_PEAK_TOPS, "unit": "TOP/s",
-                "frac": 2 * mac / scan_avg_s / 1e12 / INT8_MFMA_PEAK_TOPS,
-                "traffic": measured_traffic("k_scan_mx", wl.name),
-                "algorithmic_ops_per_launch": 2 * mac, "avg_launch_ms": scan_avg_s * 1e3}
-    # the same bytes from the rocprofv3 counters of these sources, if recorded: HBM bytes moved per second
-    traffic = roofline["traffic"]
-    scan_achieved = None if traffic is None else {
-        "GBps": traffic / scan_avg_s / 1e9, "frac_of_hbm_peak": traffic / scan_avg_s / 1e9 / HBM_PEAK_GBS,
-        "source": "rocprofv3 FETCH_SIZE and WRITE_SIZE of k_scan_mx, calibrated against a device copy"}
+    # distinct probed embeddings per launch: each probed cluster is read once per wave
+    sizes = np.diff(data.offsets)
+    waves = max(1, int(round(launches_per_step)))
+    per_wave = -(-nq // waves)
+    distinct = sum(int(sizes[np.unique(dbg["sel"][w0:w0 + per_wave])].sum()) for w0 in range(0, nq, per_wave))
+    distinct_per_launch = distinct / waves  # waves taken as equal slices of the batch (an estimate)
+    traffic = measured_traffic("k_scan_mx", wl.name)
+    counted_gbs = None if traffic is None else traffic / scan_avg_s / 1e9
+    roofline = {
+        "bound": "hbm", "kernel": "k_scan_mx", "unit": "GB/s", "peak": HBM_PEAK_GBS,
+        "achieved": counted_gbs, "frac": None if counted_gbs is None else counted_gbs / HBM_PEAK_GBS,
+        "traffic": traffic, "avg_launch_ms": scan_avg_s * 1e3, "launches_per_step": launches_per_step,
+        "basis": "HBM bytes per launch counted by rocprofv3 (FETCH_SIZE x 2 + WRITE_SIZE, calibrated on a "
+                 "device copy; profiles/traffic.md, valid for these sources only) / average launch time "
+                 "from HIP events on the search stream",
+        "min_read": {"bytes_per_launch": distinct_per_launch * row_bytes,
+                     "GBps": distinct_per_launch * row_bytes / scan_avg_s / 1e9,
+                     "frac": distinct_per_launch * row_bytes / scan_avg_s / 1e9 / HBM_PEAK_GBS,
+                     "what": "codes and document ids of every distinct probed embedding, read once per "
+                             "launch (the least a cluster-major scan reads)"},
+    }
+    # matrix-core work of the scan: the method's 128 multiply-adds per scored pair, and the 9 int8
+    # digit products per dimension that the exact kernel issues
+    method_tops = pairs_per_launch * 2 * 128 / scan_avg_s / 1e12
+    issued_tops = pairs_per_launch * 2 * 9 * 128 / scan_avg_s / 1e12
+    scan_mfma = {"method_TOPs": method_tops, "method_frac_of_int8_peak": method_tops / INT8_MFMA_PEAK_TOPS,
+                 "issued_TOPs": issued_tops, "issued_frac_of_int8_peak": issued_tops / INT8_MFMA_PEAK_TOPS,
+                 "pairs_per_launch": pairs_per_launch, "peak": INT8_MFMA_PEAK_TOPS, "unit": "TOP/s"}
     gemm_ms, gemm_n = stages["filter_gemm"]
     gemm_flops = 2.0 * nq * wl.n_qtok * wl.n_centroids * 128 / (max(gemm_n, 1) / args.steps)
     gemm_tflops = gemm_flops / (gemm_ms / 1e3 / max(gemm_n, 1)) / 1e12 if gemm_n else None
 
-    cpu = None
+    cpu, cpu1 = None, None
     if not args.no_cpu:
         import oracle
 
-        nc = min(args.cpu_queries, nq)
         threads = host_threads()
+        # all host threads: whole queries (the tokens of a query in parallel when there are
+        # fewer queries than threads), checked against the engine's results
+        nc = min(args.cpu_queries, nq)
         log(f"bench: oracle on {nc} queries with {threads} threads")
         a = time.perf_counter()
         ref = oracle.search_index(data, queries=data.queries[:nc], threads=threads, debug=False)
@@ -346,9 +379,25 @@ def main() -> int:
         cpu = {"value": nc / cpu_s, "unit": "queries/s", "cores": threads, "kind": "oracle",
                "sample": f"first {nc} of the {nq} queries of the same workload "
                          f"({int(scored[:nc].sum())} scored embeddings), {cpu_s:.1f} s wall",
-               "cpu_model": cpu_model()}
-        cpu["parity_ids"] = bool(np.array_equal(ref["ids"], dbg["ids"][:nc]))
-        cpu["parity_fixed_scores"] = bool(np.array_equal(ref["fixed"], dbg["fixed"][:nc]))
+               "cpu_model": cpu_model(),
+               "parity_ids": bool(np.array_equal(ref["ids"], dbg["ids"][:nc])),
+               "parity_fixed_scores": bool(np.array_equal(ref["fixed"], dbg["fixed"][:nc]))}
+        # one thread (the paper's setting): the first tokens of one query, scaled to a whole
+        # query by embeddings scored
+        nt1 = max(1, min(wl.n_qtok, args.cpu1_tokens))
+        log(f"bench: oracle on 1 thread, query 0 restricted to its first {nt1} tokens")
+        a = time.perf_counter()
+        r1 = oracle.search_index(data, queries=data.queries[:1, :nt1], threads=1, debug=True)
+        t1 = time.perf_counter() - a
+        rate1 = float(r1["n_scored"][0]) / t1
+        cpu1 = {"value": rate1 / float(scored.mean()), "unit": "queries/s", "cores": 1, "kind": "oracle",
+                "scored_emb_per_s": rate1, "ms_per_query": float(scored.mean()) / rate1 * 1e3,
+                "sample": f"query 0, first {nt1} of {wl.n_qtok} tokens ({int(r1['n_scored'][0])} scored "
+                          f"embeddings, {t1:.1f} s); per-query figures scaled by the batch's mean "
+                          f"{float(scored.mean()):.4g} scored embeddings per query",
+                "paper_context": "the paper's WARP engine: 171.3 ms end to end per query on LoTTE Pooled "
+                                 "(660M tokens, nprobe 32), one thread of a Xeon Gold 6132 at 2.6 GHz, "
+                                 "query encoding included (Section 5)"}
 
     rec = {
         "metric": METRIC,
@@ -371,21 +420,25 @@ def main() -> int:
         "hbm_frac_effective": float(scored.sum()) * args.steps * row_bytes / elapsed / (HBM_PEAK_GBS * 1e9),
         "stage_ms_per_step": {k: v[0] / args.steps for k, v in stages.items()},
         "roofline": roofline,
+        "scan_mfma": scan_mfma,
         "scan_hbm_equivalent": {"bytes_per_scored_embedding": row_bytes, "GBps": hbm_equiv,
-                                "frac_of_hbm_peak": hbm_equiv / HBM_PEAK_GBS},
-        "scan_hbm_achieved": scan_achieved,
-        "filter_gemm": {"tflops_fp32_equivalent": gemm_tflops,
-                        "fp16_mfma_tflops": 3 * gemm_tflops if gemm_tflops else None,
+                                "frac_of_hbm_peak": hbm_equiv / HBM_PEAK_GBS,
+                                "what": "scored pairs x (16b + 4) bytes: what a token-major scan would "
+                                        "stream (not a roofline fraction for the cluster-major scan)"},
+        "filter_gemm": {"TFLOPs": gemm_tflops, "flops_per_launch": gemm_flops,
+                        "frac_of_fp16_peak": (gemm_tflops / FP16_MFMA_PEAK_TFLOPS) if gemm_tflops else None,
+                        "issued_fp16_TFLOPs": 3 * gemm_tflops if gemm_tflops else None,
                         "peak": FP16_MFMA_PEAK_TFLOPS,
-                        "frac": (3 * gemm_tflops / FP16_MFMA_PEAK_TFLOPS) if gemm_tflops else None},
-        "host_api": {"value": host_qps, "unit": "queries/s",
+                        "what": "2 x M x N x 128 per launch; the kernel issues three fp16 products per "
+                                "multiply-add (split operands)"},
+        "host_api": {"value": host_qps, "unit": "queries/s", "batches": host_steps,
                      "what": "warp_search with host buffers: query check on the host, queries copied in, "
                              "ids, scores and counts copied out"},
         "cpu_baseline": cpu,
+        "cpu_baseline_1thread": cpu1,
         "timed_batch_matches_debug_run": same_as_debug,
     }
     print(json.dumps(rec), flush=True)
-    ix.close()
     if args.copy_calibration_mib:
         n = args.copy_calibration_mib << 18  # float32 elements
         src = torch.ones(n, dtype=torch.float32, device=dev)

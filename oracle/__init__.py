@@ -31,26 +31,43 @@ def build() -> str:
     return LIB
 
 
+def build_variant(src_text: str, out_dir: str) -> str:
+    """Compile oracle source text (for example a copy with a planted mistake) into
+    out_dir/liboracle_variant.so with the same flags; returns its path."""
+    c = os.path.join(out_dir, "warp_oracle.c")
+    with open(c, "w") as f:
+        f.write(src_text)
+    so = os.path.join(out_dir, "liboracle_variant.so")
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-fno-fast-math",
+                           "-I", _HERE, c, "-o", so, "-lm"])
+    return so
+
+
+def load_library(path: str) -> ctypes.CDLL:
+    """A compiled oracle library with its function signatures set."""
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+    lib.oracle_centroid_scores.argtypes = [P, i32, i32, P, P]
+    lib.oracle_centroid_scores.restype = None
+    lib.oracle_select.argtypes = [P, P, i32, i32, i64, P, P]
+    lib.oracle_select.restype = None
+    lib.oracle_token_scores.argtypes = [P, i32, f64, P, i32, P, i64, i64, P]
+    lib.oracle_token_scores.restype = None
+    lib.oracle_search.argtypes = [P, i32, i32, P, P, P, i32, P, i32, P, i32, i32, i32, i64, i32,
+                                  i32, P, P, P, P, P, P, P, P, P, i32]
+    lib.oracle_search.restype = ctypes.c_int
+    lib.oracle_build_index.argtypes = [P, P, i64, P, i32, P, i64, i32, i32, i64, P, P, P, P, P, P, P, i32]
+    lib.oracle_build_index.restype = ctypes.c_int
+    return lib
+
+
 def _load():
     global _lib
     if _lib is None:
         if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
             build()
-        lib = ctypes.CDLL(LIB)
-        P = ctypes.c_void_p
-        i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
-        lib.oracle_centroid_scores.argtypes = [P, i32, i32, P, P]
-        lib.oracle_centroid_scores.restype = None
-        lib.oracle_select.argtypes = [P, P, i32, i32, i64, P, P]
-        lib.oracle_select.restype = None
-        lib.oracle_token_scores.argtypes = [P, i32, f64, P, i32, P, i64, i64, P]
-        lib.oracle_token_scores.restype = None
-        lib.oracle_search.argtypes = [P, i32, i32, P, P, P, i32, P, i32, P, i32, i32, i32, i64, i32,
-                                      i32, P, P, P, P, P, P, P, P, P, i32]
-        lib.oracle_search.restype = ctypes.c_int
-        lib.oracle_build_index.argtypes = [P, P, i64, P, i32, P, i64, i32, i32, i64, P, P, P, P, P, P, P, i32]
-        lib.oracle_build_index.restype = ctypes.c_int
-        _lib = lib
+        _lib = load_library(LIB)
     return _lib
 
 
@@ -91,8 +108,9 @@ def token_scores(q, centroid_score: float, codes, nbits: int, bucket_weights, e0
 
 def search(centroids, offsets, doc_ids, codes, nbits, bucket_weights, n_docs, queries, nprobe,
            t_prime, k, flags: int = 0, debug: bool = True, doc_scores: bool = False,
-           threads: int = 0) -> dict:
-    """Run the oracle on a batch of queries [n_queries, n_qtok, dim]."""
+           threads: int = 0, lib: ctypes.CDLL | None = None) -> dict:
+    """Run the oracle on a batch of queries [n_queries, n_qtok, dim] (with `lib`, a
+    library from load_library instead of the built oracle)."""
     C = _c(centroids, np.float32)
     off = _c(offsets, np.int64)
     ids = _c(doc_ids, np.int32)
@@ -117,7 +135,7 @@ def search(centroids, offsets, doc_ids, codes, nbits, bucket_weights, n_docs, qu
         r["n_scored"] = np.empty(nq, np.int64)
     if doc_scores:
         r["doc_fixed"] = np.empty((nq, n_docs), np.int64)
-    rc = _load().oracle_search(
+    rc = (lib or _load()).oracle_search(
         _ptr(C), n_c, dim, _ptr(off), _ptr(ids), _ptr(cd), nbits, _ptr(w), int(n_docs), _ptr(Q), nq, nt,
         nprobe, int(t_prime), k, flags, _ptr(r["ids"]), _ptr(r["fixed"]), _ptr(r["scores"]),
         _ptr(r["counts"]), _ptr(r.get("sel")), _ptr(r.get("m_fixed")), _ptr(r.get("cand_bitmap")),

@@ -13,7 +13,8 @@
  *                           top-k; scores follow Eq. 1 without the 1/Z factor.
  *
  * Written to be read, not to be fast: full sorts, dense per-query arrays, one
- * embedding at a time. Parallel over queries only.
+ * embedding at a time. Parallel over queries, or over the tokens of one query
+ * when there are fewer queries than threads (each token owns its rows).
  */
 #include "warp_oracle.h"
 
@@ -144,6 +145,7 @@ typedef struct {
     int32_t n_qtok, nprobe, k, flags;
     int64_t t_prime;
     const int32_t* doc_len; /* only with ORACLE_EQ1_LITERAL */
+    int32_t token_threads;  /* > 1: the tokens of one query are processed in parallel */
 } search_args;
 
 static void search_one(const search_args* a, const float* query, int32_t* out_ids, int64_t* out_fixed,
@@ -151,10 +153,8 @@ static void search_one(const search_args* a, const float* query, int32_t* out_id
                        uint32_t* cand_bitmap, int64_t* n_scored, int64_t* doc_fixed) {
     const int32_t T = a->n_qtok, D = a->dim, P = a->nprobe, n_docs = a->n_docs;
     const int64_t row_bytes = (int64_t)D * a->nbits / 8;
-    double* S = (double*)malloc(sizeof(double) * (size_t)a->n_c);
     int32_t* my_sel = (int32_t*)malloc(sizeof(int32_t) * (size_t)T * P);
     int64_t* M = (int64_t*)malloc(sizeof(int64_t) * (size_t)T);
-    int64_t* lut = (int64_t*)malloc(sizeof(int64_t) * (size_t)D << a->nbits);
     /* best[i][doc]: token-level max over every retrieved embedding of doc for token i */
     int64_t* best = (int64_t*)malloc(sizeof(int64_t) * (size_t)T * n_docs);
     int32_t* seen = NULL; /* retrieved embeddings per (token, doc), Eq.-1-literal reading only */
@@ -162,8 +162,12 @@ static void search_one(const search_args* a, const float* query, int32_t* out_id
     for (int64_t x = 0; x < (int64_t)T * n_docs; ++x) best[x] = ABSENT;
     int64_t scored = 0;
 
+#pragma omp parallel for schedule(dynamic, 1) reduction(+ : scored) if (a->token_threads > 1) \
+    num_threads(a->token_threads > 1 ? a->token_threads : 1)
     for (int32_t i = 0; i < T; ++i) {
         const float* q = query + (int64_t)i * D;
+        double* S = (double*)malloc(sizeof(double) * (size_t)a->n_c);
+        int64_t* lut = (int64_t*)malloc(sizeof(int64_t) * (size_t)D << a->nbits);
         /* candidate generation: centroid scores, n_probe best, missing similarity */
         double m;
         oracle_centroid_scores(a->centroids, a->n_c, D, q, S);
@@ -186,6 +190,8 @@ static void search_one(const search_args* a, const float* query, int32_t* out_id
             }
         }
         if (a->flags & ORACLE_M_MIN_RETRIEVED) M[i] = (min_retrieved == INT64_MAX) ? 0 : min_retrieved;
+        free(lut);
+        free(S);
     }
 
     /* document-level reduction over the candidate set (docs with any retrieved token) */
@@ -233,10 +239,8 @@ static void search_one(const search_args* a, const float* query, int32_t* out_id
     free(cand);
     free(seen);
     free(best);
-    free(lut);
     free(M);
     free(my_sel);
-    free(S);
 }
 
 int oracle_search(const float* centroids, int32_t n_c, int32_t dim, const int64_t* offsets,
@@ -255,12 +259,14 @@ int oracle_search(const float* centroids, int32_t n_c, int32_t dim, const int64_
         doc_len = (int32_t*)calloc((size_t)(n_docs > 0 ? n_docs : 1), sizeof(int32_t));
         for (int64_t e = 0; e < offsets[n_c]; ++e) doc_len[doc_ids[e]] += 1;
     }
-    search_args a = {centroids, n_c,   dim,     offsets, doc_ids, codes, nbits, bucket_weights,
-                     n_docs,    n_qtok, nprobe, k,       flags,   t_prime, doc_len};
+    if (n_threads <= 0) n_threads = omp_get_num_procs();
+    /* fewer queries than threads: one query at a time, its tokens in parallel */
+    const int32_t token_threads = n_queries < n_threads ? n_threads : 1;
+    search_args a = {centroids, n_c,   dim,     offsets, doc_ids, codes,   nbits,   bucket_weights,
+                     n_docs,    n_qtok, nprobe, k,       flags,   t_prime, doc_len, token_threads};
     int64_t words = ((int64_t)n_docs + 31) / 32;
     if (cand_bitmap) memset(cand_bitmap, 0, sizeof(uint32_t) * (size_t)(words * n_queries));
-    if (n_threads <= 0) n_threads = omp_get_num_procs();
-#pragma omp parallel for schedule(dynamic, 1) num_threads(n_threads)
+#pragma omp parallel for schedule(dynamic, 1) num_threads(token_threads > 1 ? 1 : n_threads)
     for (int32_t qi = 0; qi < n_queries; ++qi) {
         search_one(&a, queries + (int64_t)qi * n_qtok * dim, out_ids + (int64_t)qi * k,
                    out_fixed + (int64_t)qi * k, out_scores + (int64_t)qi * k, out_counts + qi,

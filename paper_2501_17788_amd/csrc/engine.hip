@@ -13,6 +13,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <unordered_set>
 #include <utility>
 #include <vector>
 
@@ -41,7 +42,6 @@ int fail(int code, const char* fmt, ...) {
         if (e_ != hipSuccess) return fail(WARP_EDEVICE, "%s failed: %s", #expr, hipGetErrorString(e_)); \
     } while (0)
 
-constexpr uint64_t kMagic = 0x5741525049445831ull;  // "WARPIDX1"
 constexpr int kStages = 6;
 
 struct DevBuf {
@@ -52,7 +52,6 @@ struct DevBuf {
 }  // namespace
 
 struct warp_index {
-    uint64_t magic = kMagic;
     int device = 0;
     int32_t n_c = 0, n_docs = 0, nbits = 0;
     int64_t n_emb = 0;
@@ -91,6 +90,7 @@ struct warp_index {
     DevBuf tokcnt, doc_len;    // Eq.-1-literal scoring only
     int64_t tokcnt_ready = 0;  // leading elements of tokcnt holding 0
     bool doc_len_ready = false;
+    size_t scratch_held = 0;  // bytes of per-search scratch (all DevBufs above and below)
     // staging of the host-pointer calls
     DevBuf st_q, st_ids, st_scores, st_fixed, st_counts, st_sel, st_m, st_bitmap, st_scored;
     std::mutex lock;
@@ -124,6 +124,38 @@ void release(DevBuf& b) {
     b.bytes = 0;
 }
 
+// Cap on an index's per-search scratch: WARP_MAX_SCRATCH_BYTES if set (bytes), else none.
+// A search whose scratch would exceed it fails with WARP_ENOMEM, as if the device memory
+// had run out; the waves of a search are sized to stay below it.
+size_t scratch_cap() {
+    const char* s = std::getenv("WARP_MAX_SCRATCH_BYTES");
+    if (!s || !*s) return SIZE_MAX;
+    const long long v = std::atoll(s);
+    return v < 0 ? 0 : (size_t)v;
+}
+
+// grow() for the index's per-search scratch, counted against scratch_cap().
+int grow_scratch(warp_index* idx, DevBuf& b, size_t bytes) {
+    if (bytes == 0) bytes = 16;
+    if (b.bytes >= bytes) return WARP_OK;
+    const size_t cap = scratch_cap();
+    const size_t after = idx->scratch_held - b.bytes + bytes;
+    if (after > cap)
+        return fail(WARP_ENOMEM, "search scratch of %zu bytes exceeds WARP_MAX_SCRATCH_BYTES = %zu", after, cap);
+    idx->scratch_held -= b.bytes;
+    const int rc = grow(b, bytes);
+    idx->scratch_held += b.bytes;
+    return rc;
+}
+
+// Live index handles: a call on a handle that was never returned by a load, or was freed,
+// fails with WARP_EINVAL instead of touching freed memory.
+std::mutex g_live_lock;
+std::unordered_set<const warp_index*>& live_handles() {
+    static std::unordered_set<const warp_index*>* s = new std::unordered_set<const warp_index*>();
+    return *s;
+}
+
 int check_device() {
     int n = 0;
     if (hipGetDeviceCount(&n) != hipSuccess || n < 1) {
@@ -140,7 +172,35 @@ int check_device() {
     return WARP_OK;
 }
 
-bool is_index(const warp_index* idx) { return idx && idx->magic == kMagic; }
+bool is_index(const warp_index* idx) {
+    if (!idx) return false;
+    std::lock_guard<std::mutex> g(g_live_lock);
+    return live_handles().count(idx) != 0;
+}
+
+// Free everything an index owns (registered or not).
+void destroy_index(warp_index* idx) {
+    {
+        std::lock_guard<std::mutex> g(idx->lock);
+        (void)hipSetDevice(idx->device);
+        if (idx->stream) (void)hipStreamSynchronize(idx->stream);
+        for (void* p : {(void*)idx->centroids, (void*)idx->offsets, (void*)idx->sizes, (void*)idx->chunk_c,
+                        (void*)idx->chunk_k, (void*)idx->doc_ids, (void*)idx->codes, (void*)idx->weights,
+                        (void*)idx->err})
+            if (p) (void)hipFree(p);
+        for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_pref, &idx->m_fixed, &idx->tokmax,
+                          &idx->q_epoch, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount,
+                          &idx->cursor, &idx->pair_start, &idx->plist, &idx->qdig, &idx->list_rec,
+                          &idx->list_item, &idx->cblk, &idx->scan_queue, &idx->st_q, &idx->st_ids,
+                          &idx->st_scores, &idx->st_fixed, &idx->st_counts, &idx->st_sel, &idx->st_m,
+                          &idx->st_bitmap, &idx->st_scored})
+            release(*b);
+        for (hipEvent_t e : idx->ev_pool) (void)hipEventDestroy(e);
+        for (hipEvent_t e : idx->ev_pending) (void)hipEventDestroy(e);
+        if (idx->stream) (void)hipStreamDestroy(idx->stream);
+    }
+    delete idx;
+}
 
 // Host-side checks of the small index arrays.
 int validate_index_host(const float* C, int32_t n_c, int32_t dim, const int64_t* off, int32_t nbits,
@@ -280,7 +340,10 @@ int load_common(const float* C, int32_t n_c, int32_t dim, const int64_t* off, co
     const int64_t* voff = off;
     const float* vw = w;
     if (device_ptrs) {
-        if (nbits != 2 && nbits != 4) return validate_index_host(C, n_c, dim, off, nbits, w, n_docs);
+        // the small arrays are read on the host: copy them first, whatever nbits is (an
+        // invalid nbits is rejected below before the weights are used)
+        if (nbits != 1 && nbits != 2 && nbits != 4 && nbits != 8)
+            return fail(WARP_EINVAL, "nbits must be 1, 2, 4 or 8 (got %d)", nbits);
         hC.resize((size_t)n_c * kDim);
         hoff.resize((size_t)n_c + 1);
         hw.resize((size_t)1 << nbits);
@@ -332,9 +395,13 @@ int load_common(const float* C, int32_t n_c, int32_t dim, const int64_t* off, co
     if (!rc) rc = finish_load(idx, voff);
     if (rc) {
         std::string msg = g_err;
-        warp_index_free(idx);
+        destroy_index(idx);
         g_err = msg;
         return rc;
+    }
+    {
+        std::lock_guard<std::mutex> g(g_live_lock);
+        live_handles().insert(idx);
     }
     *out = idx;
     return WARP_OK;
@@ -374,23 +441,23 @@ void clear_slots(warp_index* idx, hipStream_t s) {
 int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, hipStream_t s) {
     const int64_t n_tok = (int64_t)qw * T;
     int rc = WARP_OK;
-    if (!rc) rc = grow(idx->filter, (size_t)n_tok * idx->n_c * 2);
-    if (!rc) rc = grow(idx->sel, (size_t)n_tok * P * 4);
-    if (!rc) rc = grow(idx->base, (size_t)n_tok * P * 4);
-    if (!rc) rc = grow(idx->seg_pref, (size_t)n_tok * (P + 1) * 8);
-    if (!rc) rc = grow(idx->m_fixed, (size_t)n_tok * 8);
-    if (!rc) rc = grow(idx->keys, (size_t)qw * idx->n_docs * 8);
-    if (!rc) rc = grow(idx->qpart, (size_t)qw * (((size_t)idx->n_docs + 255) / 256) * 16);
-    if (!rc) rc = grow(idx->ccount, (size_t)idx->n_c * 4);
-    if (!rc) rc = grow(idx->cursor, (size_t)idx->n_c * 4);
-    if (!rc) rc = grow(idx->pair_start, ((size_t)idx->n_c + 1) * 4);
-    if (!rc) rc = grow(idx->plist, (size_t)n_tok * P * 8);
-    if (!rc) rc = grow(idx->qdig, (size_t)n_tok * kQdigBytes);
+    if (!rc) rc = grow_scratch(idx, idx->filter, (size_t)n_tok * idx->n_c * 2);
+    if (!rc) rc = grow_scratch(idx, idx->sel, (size_t)n_tok * P * 4);
+    if (!rc) rc = grow_scratch(idx, idx->base, (size_t)n_tok * P * 4);
+    if (!rc) rc = grow_scratch(idx, idx->seg_pref, (size_t)n_tok * (P + 1) * 8);
+    if (!rc) rc = grow_scratch(idx, idx->m_fixed, (size_t)n_tok * 8);
+    if (!rc) rc = grow_scratch(idx, idx->keys, (size_t)qw * idx->n_docs * 8);
+    if (!rc) rc = grow_scratch(idx, idx->qpart, (size_t)qw * (((size_t)idx->n_docs + 255) / 256) * 16);
+    if (!rc) rc = grow_scratch(idx, idx->ccount, (size_t)idx->n_c * 4);
+    if (!rc) rc = grow_scratch(idx, idx->cursor, (size_t)idx->n_c * 4);
+    if (!rc) rc = grow_scratch(idx, idx->pair_start, ((size_t)idx->n_c + 1) * 4);
+    if (!rc) rc = grow_scratch(idx, idx->plist, (size_t)n_tok * P * 8);
+    if (!rc) rc = grow_scratch(idx, idx->qdig, (size_t)n_tok * kQdigBytes);
     const int64_t cblocks = (idx->n_chunks + kPlanBlock - 1) / kPlanBlock;
-    if (!rc) rc = grow(idx->list_rec, (size_t)idx->n_chunks * 16);
-    if (!rc) rc = grow(idx->list_item, ((size_t)idx->n_chunks + 2) * 8);  // + the count
-    if (!rc) rc = grow(idx->cblk, (size_t)cblocks * 16);
-    if (!rc) rc = grow(idx->scan_queue, 256);
+    if (!rc) rc = grow_scratch(idx, idx->list_rec, (size_t)idx->n_chunks * 16);
+    if (!rc) rc = grow_scratch(idx, idx->list_item, ((size_t)idx->n_chunks + 2) * 8);  // + the count
+    if (!rc) rc = grow_scratch(idx, idx->cblk, (size_t)cblocks * 16);
+    if (!rc) rc = grow_scratch(idx, idx->scan_queue, 256);
     if (rc) return rc;
     // the token-max table and its query slots' epochs. All slots are zeroed before a search
     // that resets cells or lays the table out with another token count, and after a search
@@ -398,7 +465,7 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, hipStream_t s) {
     const int64_t need = n_tok * idx->n_docs;
     if (idx->tab_cells < need) {
         idx->tab_cells = 0;
-        rc = grow(idx->tokmax, (size_t)need * 4);
+        rc = grow_scratch(idx, idx->tokmax, (size_t)need * 4);
         if (rc) return rc;
         launch_zero_cells((uint32_t*)idx->tokmax.p, need, s);
         idx->tab_cells = need;
@@ -412,19 +479,19 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, hipStream_t s) {
         idx->tab_T = T;
     }
     if ((int64_t)idx->slot_ep.size() < qw) {
-        rc = grow(idx->q_epoch, (size_t)qw * 4);
+        rc = grow_scratch(idx, idx->q_epoch, (size_t)qw * 4);
         if (rc) return rc;
         idx->slot_ep.assign((size_t)qw, 0u);
         launch_fill_i32((int32_t*)idx->q_epoch.p, qw, 0, s);
     }
     if (idx->scoring == WARP_SCORING_EQ1_LITERAL) {
         if ((int64_t)(idx->tokcnt.bytes / 4) < need) {
-            rc = grow(idx->tokcnt, (size_t)need * 4);
+            rc = grow_scratch(idx, idx->tokcnt, (size_t)need * 4);
             if (rc) return rc;
             idx->tokcnt_ready = 0;
         }
         if (!idx->doc_len_ready) {
-            rc = grow(idx->doc_len, (size_t)idx->n_docs * 4);
+            rc = grow_scratch(idx, idx->doc_len, (size_t)idx->n_docs * 4);
             if (rc) return rc;
             launch_doc_len(idx->doc_ids, idx->n_emb, (int32_t*)idx->doc_len.p, idx->n_docs, s);
         }
@@ -453,6 +520,7 @@ int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T) {
         }
         budget = (size_t)(0.6 * (double)(free_b + held));
     }
+    budget = std::min(budget, scratch_cap());
     const size_t per = (size_t)T * idx->n_docs * (idx->scoring == WARP_SCORING_EQ1_LITERAL ? 8 : 4) +
                        (size_t)idx->n_docs * 8 + (size_t)T * idx->n_c * 2 + (size_t)T * kMaxProbe * 32 +
                        (size_t)T * 1024;
@@ -637,15 +705,15 @@ int search_host(warp_index* idx, const float* queries, int32_t n_queries, int32_
     if (rc) return rc;
     const int64_t words = ((int64_t)idx->n_docs + 31) / 32;
     const size_t nk = (size_t)n_queries * k;
-    if (!rc) rc = grow(idx->st_q, (size_t)n_tok * kDim * 4);
-    if (!rc) rc = grow(idx->st_ids, nk * 4);
-    if (!rc) rc = grow(idx->st_scores, nk * 4);
-    if (!rc) rc = grow(idx->st_fixed, nk * 8);
-    if (!rc) rc = grow(idx->st_counts, (size_t)n_queries * 4);
-    if (!rc && sel) rc = grow(idx->st_sel, (size_t)n_tok * nprobe * 4);
-    if (!rc && m) rc = grow(idx->st_m, (size_t)n_tok * 8);
-    if (!rc && bitmap) rc = grow(idx->st_bitmap, (size_t)n_queries * words * 4);
-    if (!rc && scored) rc = grow(idx->st_scored, (size_t)n_queries * 8);
+    if (!rc) rc = grow_scratch(idx, idx->st_q, (size_t)n_tok * kDim * 4);
+    if (!rc) rc = grow_scratch(idx, idx->st_ids, nk * 4);
+    if (!rc) rc = grow_scratch(idx, idx->st_scores, nk * 4);
+    if (!rc) rc = grow_scratch(idx, idx->st_fixed, nk * 8);
+    if (!rc) rc = grow_scratch(idx, idx->st_counts, (size_t)n_queries * 4);
+    if (!rc && sel) rc = grow_scratch(idx, idx->st_sel, (size_t)n_tok * nprobe * 4);
+    if (!rc && m) rc = grow_scratch(idx, idx->st_m, (size_t)n_tok * 8);
+    if (!rc && bitmap) rc = grow_scratch(idx, idx->st_bitmap, (size_t)n_queries * words * 4);
+    if (!rc && scored) rc = grow_scratch(idx, idx->st_scored, (size_t)n_queries * 8);
     if (rc) return rc;
     hipStream_t s = idx->stream;
     HIP_TRY(hipMemcpyAsync(idx->st_q.p, queries, (size_t)n_tok * kDim * 4, hipMemcpyHostToDevice, s));
@@ -700,27 +768,15 @@ int warp_index_load_device(const float* centroids, int32_t n_centroids, int32_t 
 }
 
 void warp_index_free(warp_index* idx) {
-    if (!is_index(idx)) return;
+    if (!idx) return;
     {
-        std::lock_guard<std::mutex> g(idx->lock);
-        (void)hipSetDevice(idx->device);
-        if (idx->stream) (void)hipStreamSynchronize(idx->stream);
-        for (void* p : {(void*)idx->centroids, (void*)idx->offsets, (void*)idx->sizes, (void*)idx->chunk_c,
-                        (void*)idx->chunk_k, (void*)idx->doc_ids,
-                        (void*)idx->codes, (void*)idx->weights, (void*)idx->err})
-            if (p) (void)hipFree(p);
-        for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_pref, &idx->m_fixed,
-                          &idx->tokmax, &idx->q_epoch, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount, &idx->cursor,
-                          &idx->pair_start, &idx->plist, &idx->qdig, &idx->list_rec, &idx->list_item, &idx->cblk, &idx->scan_queue, &idx->st_q, &idx->st_ids, &idx->st_scores,
-                          &idx->st_fixed, &idx->st_counts, &idx->st_sel, &idx->st_m, &idx->st_bitmap,
-                          &idx->st_scored})
-            release(*b);
-        for (hipEvent_t e : idx->ev_pool) (void)hipEventDestroy(e);
-        for (hipEvent_t e : idx->ev_pending) (void)hipEventDestroy(e);
-        if (idx->stream) (void)hipStreamDestroy(idx->stream);
-        idx->magic = 0;
+        std::lock_guard<std::mutex> g(g_live_lock);
+        if (live_handles().erase(idx) == 0) {  // never loaded, or already freed: nothing to do
+            g_err = "warp_index_free: invalid or already freed index handle";
+            return;
+        }
     }
-    delete idx;
+    destroy_index(idx);
 }
 
 int warp_index_info(const warp_index* idx, int32_t* n_centroids, int64_t* n_embeddings, int32_t* n_docs,

@@ -204,8 +204,9 @@ class Index:
                                _ptr(counts)))
         return ids, scores, counts
 
-    def search_debug(self, queries, nprobe: int, t_prime: int, k: int) -> dict:
-        """Blocking search returning every intermediate the C ABI exposes."""
+    def search_debug(self, queries, nprobe: int, t_prime: int, k: int, bitmap: bool = True) -> dict:
+        """Blocking search returning every intermediate the C ABI exposes (the candidate
+        bitmap, n_queries x n_docs / 8 bytes, only with `bitmap`)."""
         Q = self._queries(queries)
         nq, nt, _ = Q.shape
         words = (self.n_docs + 31) // 32
@@ -216,7 +217,7 @@ class Index:
             "fixed": np.empty((nq, k), np.int64),
             "sel": np.empty((nq, nt, nprobe), np.int32),
             "m_fixed": np.empty((nq, nt), np.int64),
-            "cand_bitmap": np.empty((nq, words), np.uint32),
+            "cand_bitmap": np.empty((nq, words), np.uint32) if bitmap else None,
             "n_scored": np.empty(nq, np.int64),
         }
         _check(lib.warp_search_debug(self._h, _ptr(Q), nq, nt, nprobe, int(t_prime), k, _ptr(r["ids"]),

@@ -46,6 +46,26 @@ def test_null_handles():
     assert lib.warp_set_timing(None, 1) == w.EINVAL
 
 
+def test_unknown_handle_is_rejected():
+    """A pointer that no load returned is not a live handle: every call rejects it without
+    reading through it, and freeing it is a no-op."""
+    lib = w.lib
+    junk = ctypes.create_string_buffer(4096)  # readable memory that is not an index
+    h = ctypes.cast(junk, ctypes.c_void_p)
+    lib.warp_index_free(h)
+    assert "invalid" in w.last_error()
+    assert lib.warp_index_info(h, None, None, None, None) == w.EINVAL
+    assert lib.warp_index_sync(h, None) == w.EINVAL
+    assert lib.warp_set_scoring(h, 0) == w.EINVAL
+    assert lib.warp_set_timing(h, 1) == w.EINVAL
+    Q = np.zeros((1, 4, 128), np.float32)
+    ids = np.empty((1, 2), np.int32)
+    sc = np.empty((1, 2), np.float32)
+    P = ctypes.c_void_p
+    rc = lib.warp_search(h, Q.ctypes.data_as(P), 1, 4, 1, 0, 2, ids.ctypes.data_as(P), sc.ctypes.data_as(P), None)
+    assert rc == w.EINVAL and "handle" in w.last_error()
+
+
 def _arrays(**over):
     idx = synth.make_index(synth.random_small_workload(3, n_centroids=6, n_docs=20), workers=1)
     a = dict(centroids=idx.centroids, offsets=idx.offsets, doc_ids=idx.doc_ids, codes=idx.codes,

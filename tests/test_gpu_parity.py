@@ -3,7 +3,8 @@
 Bit-exact: probed centroids and their order, the missing-similarity estimates,
 candidate sets, embeddings scored, top-k ids and fixed-point document scores.
 Float scores: the float of the same fixed-point value (identical), and within
-1e-4 relative of the fp64 real-valued score.
+1e-4 relative of the fp64 real-valued score from explicit decompression
+(helpers.realvalued_doc_scores, which recomputes selection and m_i itself).
 """
 from __future__ import annotations
 
@@ -14,7 +15,7 @@ import pytest
 
 import oracle
 import synth
-from helpers import FRAC, explicit_decompress, load_dyadic, unpack_msb_first
+from helpers import FRAC, check_real_valued, index_arrays, load_dyadic, unpack_msb_first
 
 pytestmark = pytest.mark.gpu
 
@@ -57,26 +58,6 @@ def run_both(data, queries=None, nprobe=None, t_prime=None, k=None, label="", li
                                flags=oracle.EQ1_LITERAL if literal else 0)
     compare(got, want, label=label)
     return got
-
-
-def real_valued_scores(data, Q, sel, m_fixed, docs):
-    """fp64 scores of `docs` for one query: explicit decompression of every probed
-    embedding (Eq. decompress), token max per doc, missing entries take m_i."""
-    X = explicit_decompress(data.centroids, data.offsets, data.codes, data.nbits, data.bucket_weights)
-    out = np.zeros(len(docs))
-    pos = {d: j for j, d in enumerate(docs)}
-    for i, q in enumerate(Q):
-        best = {}
-        for c in sel[i]:
-            e0, e1 = int(data.offsets[c]), int(data.offsets[c + 1])
-            s = X[e0:e1] @ q.astype(np.float64)
-            for d, v in zip(data.doc_ids[e0:e1].tolist(), s.tolist()):
-                if d in pos:
-                    best[d] = max(best.get(d, -np.inf), v)
-        # m_i as a real value: the estimate is an fp64 centroid score, R() of it is stored
-        for d, j in pos.items():
-            out[j] += best[d] if d in best else m_fixed[i] / FRAC
-    return out
 
 
 # ----------------------------------------------------------------------------- hand-built
@@ -157,14 +138,41 @@ def test_cluster_offsets_over_several_passes():
 
 def test_tiny_workload_exact_and_real_valued():
     data = synth.make_index(synth.with_overrides(synth.WORKLOADS["tiny"], n_queries=4), workers=1)
+    wl = data.workload
     got = run_both(data, label="tiny")
     for qi in range(len(data.queries)):
-        n = int(got["counts"][qi])
-        docs = got["ids"][qi, :n]
-        ref = real_valued_scores(data, data.queries[qi], got["sel"][qi], got["m_fixed"][qi], docs)
-        rel = np.abs(got["scores"][qi, :n].astype(np.float64) - ref) / np.maximum(1.0, np.abs(ref))
-        assert rel.max() <= 1e-4, rel.max()
+        gap = check_real_valued(got["scores"][qi], got["counts"][qi], got["ids"][qi], index_arrays(data),
+                                data.queries[qi], wl.nprobe, wl.t_prime)
+        say(f"[tiny] query {qi}: largest relative gap to the fp64 scores {gap:.2e}")
     assert got["ids"][0, 0] == data.query_targets[0]
+
+
+@pytest.mark.parametrize("case", range(4))
+@pytest.mark.parametrize("mode", ["paper", "eq1_literal"])
+def test_eq1_literal_hand_worked(case, mode):
+    """The hand-worked example that separates Section 4.5's imputation from Eq. 1 read
+    literally (a fully retrieved document whose best score is below m_i, a partly
+    retrieved one): the engine gives the hand-worked results in both modes."""
+    w = _engine()
+    g, ix_arrays, Q = load_dyadic("eq1_literal_example.json")
+    c = g["cases"][case]
+    say(f"[eq1 hand-worked {c['name']} {mode}] nprobe={c['nprobe']} t'={c['t_prime']} k={c['k']}")
+    with w.Index(**ix_arrays) as ix:
+        if mode == "eq1_literal":
+            ix.set_scoring(w.SCORING_EQ1_LITERAL)
+        got = ix.search_debug(Q, c["nprobe"], c["t_prime"], c["k"])
+    want = c[mode]
+    assert got["ids"].tolist() == want["ids"]
+    assert got["counts"].tolist() == want["counts"]
+    for qi in range(len(want["ids"])):
+        for v, f in zip(want["scores"][qi], got["fixed"][qi].tolist()):
+            assert f == (np.iinfo(np.int64).min if v is None else int(v * FRAC))
+    assert got["sel"].tolist() == c["sel"]
+    assert (got["m_fixed"] / FRAC).tolist() == c["m"]
+    assert got["n_scored"].tolist() == c["n_scored"]
+    flags = oracle.EQ1_LITERAL if mode == "eq1_literal" else 0
+    compare(got, oracle.search(queries=Q, nprobe=c["nprobe"], t_prime=c["t_prime"], k=c["k"], flags=flags,
+                               **ix_arrays), label=f"eq1 hand-worked {c['name']} {mode}")
 
 
 @pytest.mark.parametrize("nbits", [1, 2, 4, 8])
@@ -209,19 +217,72 @@ def test_deterministic_and_async_matches_sync():
         np.testing.assert_array_equal(fixed.cpu().numpy(), a["fixed"])
 
 
-def test_index_from_device_tensors():
+@pytest.mark.parametrize("nbits", [1, 2, 4, 8])
+def test_index_from_device_tensors(nbits):
+    """warp_index_load_device copies the small arrays to the host for validation at every
+    code width, then searches like a host-loaded index."""
     import torch
 
     w = _engine()
-    data = synth.make_index(synth.with_overrides(synth.WORKLOADS["tiny"], n_queries=2), workers=1)
+    data = synth.make_index(synth.with_overrides(synth.WORKLOADS["tiny"], n_queries=2, nbits=nbits), workers=1)
     wl = data.workload
     t = {k: torch.from_numpy(np.ascontiguousarray(getattr(data, k))).cuda()
          for k in ("centroids", "offsets", "doc_ids", "codes", "bucket_weights")}
-    say("[device load]")
+    say(f"[device load] nbits={nbits}")
     with w.Index.from_device(t["centroids"], t["offsets"], t["doc_ids"], t["codes"], data.nbits,
                              t["bucket_weights"], data.n_docs) as ix:
         got = ix.search_debug(data.queries, wl.nprobe, wl.t_prime, wl.k)
-    compare(got, oracle.search_index(data), label="device load")
+    compare(got, oracle.search_index(data), label=f"device load nbits={nbits}")
+    # validation still runs on device arrays: a non-unit centroid is rejected
+    bad = t["centroids"].clone()
+    bad[3] *= 1.01
+    with pytest.raises(w.WarpError) as e:
+        w.Index.from_device(bad, t["offsets"], t["doc_ids"], t["codes"], data.nbits, t["bucket_weights"],
+                            data.n_docs)
+    assert e.value.code == w.EINVAL and "unit norm" in e.value.msg
+
+
+def test_scratch_cap_gives_enomem_then_recovers(monkeypatch):
+    """WARP_MAX_SCRATCH_BYTES caps an index's search scratch: below what one query needs the
+    search fails with WARP_ENOMEM; a cap that holds a few queries splits the batch into
+    waves; without it the same index searches normally."""
+    w = _engine()
+    data = synth.make_index(synth.with_overrides(synth.WORKLOADS["tiny"], n_queries=6), workers=1)
+    wl = data.workload
+    want = oracle.search_index(data)
+    with w.Index.from_synthetic(data) as ix:
+        monkeypatch.setenv("WARP_MAX_SCRATCH_BYTES", "4096")
+        say("[scratch cap] 4 KiB")
+        with pytest.raises(w.WarpError) as e:
+            ix.search_debug(data.queries, wl.nprobe, wl.t_prime, wl.k)
+        assert e.value.code == w.ENOMEM and "WARP_MAX_SCRATCH_BYTES" in e.value.msg
+        monkeypatch.setenv("WARP_MAX_SCRATCH_BYTES", str(3 << 20))
+        say("[scratch cap] 3 MiB")
+        compare(ix.search_debug(data.queries, wl.nprobe, wl.t_prime, wl.k), want, label="3 MiB cap")
+        monkeypatch.delenv("WARP_MAX_SCRATCH_BYTES")
+        say("[scratch cap] none")
+        compare(ix.search_debug(data.queries, wl.nprobe, wl.t_prime, wl.k), want, label="no cap")
+
+
+def test_freed_handle_is_rejected():
+    """A freed handle is no longer live: a second free is a no-op and a search on it fails
+    with WARP_EINVAL instead of touching freed memory."""
+    import ctypes
+
+    w = _engine()
+    data = synth.make_index(synth.random_small_workload(4), workers=1)
+    ix = w.Index.from_synthetic(data)
+    h = ctypes.c_void_p(ix.handle.value)
+    ix.close()
+    w.lib.warp_index_free(h)  # second free: ignored
+    assert "invalid" in w.last_error()
+    Q = np.ascontiguousarray(data.queries, np.float32)
+    ids = np.empty((len(Q), 3), np.int32)
+    sc = np.empty((len(Q), 3), np.float32)
+    rc = w.lib.warp_search(h, Q.ctypes.data_as(ctypes.c_void_p), len(Q), Q.shape[1], 2, 0, 3,
+                           ids.ctypes.data_as(ctypes.c_void_p), sc.ctypes.data_as(ctypes.c_void_p), None)
+    assert rc == w.EINVAL and "handle" in w.last_error()
+    assert w.lib.warp_index_info(h, None, None, None, None) == w.EINVAL
 
 
 def test_filter_scores_within_selection_margin():
@@ -296,6 +357,10 @@ def test_small_workload_sampled_queries(small_data):
     say(f"[small] oracle on queries {rows.tolist()}")
     want = oracle.search_index(data, queries=data.queries[rows])
     compare(got, want, rows=rows, label="small")
+    for qi in rows:
+        gap = check_real_valued(got["scores"][qi], got["counts"][qi], got["ids"][qi], index_arrays(data),
+                                data.queries[qi], wl.nprobe, wl.t_prime)
+        say(f"[small] query {qi}: largest relative gap to the fp64 scores {gap:.2e}")
     hit = (got["ids"][:, 0] == data.query_targets).mean()
     say(f"[small] target doc ranked first for {hit:.1%} of queries; mean scored/query "
         f"{got['n_scored'].mean():.3g}")

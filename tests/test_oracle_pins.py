@@ -9,7 +9,11 @@ O3  WARP_SELECT's estimate (Section 4.3) equals the size-weighted order
 O4  the recursive stride merge of Section 4.5 (Eq. merge_strides with
     Eq. doc_level_reduce, any split point) equals the oracle's document sums;
 O5  the two readings of imputation coincide when m_i is the smallest retrieved
-    score (XTR's estimate), and the literal Eq. 1 reading never scores lower;
+    score (XTR's estimate), and the literal Eq. 1 reading never scores lower; a
+    hand-worked example (tests/golden/eq1_literal_example.json) fixes both
+    readings exactly, including a fully retrieved document whose best score is
+    below m_i and a partly retrieved one, and oracle copies with the literal
+    reading's count test changed are caught by it;
 O6  results do not depend on the order of embeddings inside a cluster nor on
     centroid labels;
 O7  a hand-built dyadic example whose outputs were worked out by hand.
@@ -24,8 +28,9 @@ import pytest
 
 import oracle
 import synth
-from helpers import (FRAC, bruteforce_maxsim, cluster_of_embeddings, explicit_decompress,
-                     load_dyadic, topp_by_score, unpack_msb_first, weighted_order_statistic)
+from helpers import (FRAC, bruteforce_maxsim, check_real_valued, cluster_of_embeddings, explicit_decompress,
+                     load_dyadic, realvalued_doc_scores, topp_by_score, unpack_msb_first,
+                     weighted_order_statistic)
 
 
 
@@ -163,6 +168,28 @@ def test_o2_planted_mistake_is_caught():
         _check_against_bruteforce(idx, r, 10)
 
 
+def test_o2_realvalued_reference_agrees_with_oracle():
+    """The fp64 explicit-decompression reference that the GPU tests apply to returned
+    documents (helpers.realvalued_doc_scores, which recomputes selection and m_i in numpy)
+    agrees with the oracle's fixed-point scores within the rounding bound, in both scoring
+    readings, at nprobe below the number of clusters (so imputation takes part)."""
+    for seed, literal in ((40, False), (41, True), (42, False)):
+        idx = _index(seed, n_centroids=24, n_docs=120, n_queries=3, n_qtok=8, nprobe=5, t_prime=40, k=25)
+        w = idx.workload
+        r = oracle.search_index(idx, flags=oracle.EQ1_LITERAL if literal else 0)
+        arrays = dict(centroids=idx.centroids, offsets=idx.offsets, doc_ids=idx.doc_ids, codes=idx.codes,
+                      nbits=idx.nbits, bucket_weights=idx.bucket_weights, n_docs=idx.n_docs)
+        for qi, Q in enumerate(idx.queries):
+            n = int(r["counts"][qi])
+            ref = realvalued_doc_scores(Q=Q, docs=r["ids"][qi, :n], nprobe=w.nprobe, t_prime=w.t_prime,
+                                        literal=literal, **arrays)
+            # the estimate m_i enters as R(m_i) in the oracle: one more 2^-27 per token
+            bound = doc_tol(Q, idx.bucket_weights) + len(Q) * 2.0 ** -27
+            assert np.all(np.abs(r["fixed"][qi, :n] / FRAC - ref) <= bound)
+            assert check_real_valued(r["scores"][qi], n, r["ids"][qi], arrays, Q, w.nprobe, w.t_prime,
+                                     literal=literal) <= 1e-4
+
+
 # ----------------------------------------------------------------------------- O3
 
 def _random_scores(rng, n, ties):
@@ -279,6 +306,69 @@ def test_o5_readings_coincide_with_min_retrieved_estimate(seed):
     a = oracle.search_index(idx, doc_scores=True)
     b = oracle.search_index(idx, flags=oracle.EQ1_LITERAL, doc_scores=True)
     assert np.all(b["doc_fixed"] >= a["doc_fixed"])
+
+
+EQ1_CASES = range(4)
+
+
+def _eq1_expected_check(r, c, mode, n_docs):
+    want = c[mode]
+    assert r["ids"].tolist() == want["ids"], (c["name"], mode)
+    assert r["counts"].tolist() == want["counts"]
+    for qi in range(len(want["ids"])):
+        for w, f, s in zip(want["scores"][qi], r["fixed"][qi].tolist(), r["scores"][qi].tolist()):
+            if w is None:
+                assert f == np.iinfo(np.int64).min and s == -math.inf
+            else:
+                assert f == int(w * FRAC) and s == w, (c["name"], mode, w, f)
+    assert r["sel"].tolist() == c["sel"]
+    assert (r["m_fixed"] / FRAC).tolist() == c["m"]
+    assert r["n_scored"].tolist() == c["n_scored"]
+    for qi, bm in enumerate(r["cand_bitmap"]):
+        assert [d for d in range(n_docs) if (bm[d >> 5] >> (d & 31)) & 1] == c["candidates"][qi]
+
+
+@pytest.mark.parametrize("case", EQ1_CASES)
+@pytest.mark.parametrize("mode", ["paper", "eq1_literal"])
+def test_o5_eq1_literal_hand_worked(case, mode):
+    g, ix, Q = load_dyadic("eq1_literal_example.json")
+    assert np.bincount(ix["doc_ids"], minlength=g["n_docs"]).tolist() == g["doc_lengths"]
+    c = g["cases"][case]
+    flags = oracle.EQ1_LITERAL if mode == "eq1_literal" else 0
+    r = oracle.search(queries=Q, nprobe=c["nprobe"], t_prime=c["t_prime"], k=c["k"], flags=flags, **ix)
+    _eq1_expected_check(r, c, mode, g["n_docs"])
+
+
+# The literal reading's test "some embedding of the document was not retrieved for this
+# token" (retrieved count below the document's embedding count), and two plausible slips.
+_COUNT_TEST = "seen && seen[(int64_t)i * n_docs + doc] < a->doc_len[doc]"
+_MUTANTS = {
+    "unchanged (control)": _COUNT_TEST,
+    "count test <=": _COUNT_TEST.replace(" < a->", " <= a->"),
+    "count test dropped": "seen",
+}
+
+
+@pytest.mark.parametrize("mutant", sorted(_MUTANTS))
+def test_o5_eq1_literal_mutants_are_caught(mutant, tmp_path):
+    """A copy of the oracle with the count test changed fails the hand-worked literal cases;
+    the unchanged copy, built the same way, passes them."""
+    src = open(oracle.SRC).read()
+    assert src.count(_COUNT_TEST) == 1, "the oracle's count test moved; update the mutants"
+    lib = oracle.load_library(oracle.build_variant(src.replace(_COUNT_TEST, _MUTANTS[mutant]), str(tmp_path)))
+    g, ix, Q = load_dyadic("eq1_literal_example.json")
+    caught = False
+    for c in g["cases"]:
+        r = oracle.search(queries=Q, nprobe=c["nprobe"], t_prime=c["t_prime"], k=c["k"],
+                          flags=oracle.EQ1_LITERAL, lib=lib, **ix)
+        try:
+            _eq1_expected_check(r, c, "eq1_literal", g["n_docs"])
+        except AssertionError:
+            caught = True
+    if mutant.startswith("unchanged"):
+        assert not caught
+    else:
+        assert caught, f"mutant '{mutant}' passes the hand-worked literal cases"
 
 
 # ----------------------------------------------------------------------------- O6
