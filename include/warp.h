@@ -172,6 +172,28 @@ int warp_search_async(warp_index* idx, const float* queries, int32_t n_queries, 
                       float* out_scores, int32_t* out_counts, int64_t* out_fixed_scores,
                       void* hip_stream);
 
+/*
+ * warp_search_async without any allocation, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc). Same arguments, results and errors as
+ * warp_search_async; every pointer is device memory and the work is enqueued on
+ * `hip_stream`. It calls no hipMalloc or hipFree: all of its scratch lives in
+ * one static device array of 256 MiB per GPU, held from the first index load on
+ * that GPU until the process ends. A search takes waves of as many queries as
+ * the array holds; if one query does not fit (roughly 4 * n_qtok * n_docs +
+ * 2 * n_qtok * n_centroids + 8 * n_docs bytes, e.g. about 17 MB for 100k
+ * documents, 1.1 GB for 8.8M) it fails with WARP_ENOMEM before enqueuing
+ * anything. Every call on a GPU shares that GPU's array, whichever index it
+ * searches, and finds what the last call left there (the call clears what must
+ * start at zero): calls that overlap on one GPU race, so enqueue them on one
+ * stream or wait for each before the next. The index's own scratch is not
+ * used, so this call and warp_search_async may alternate on an index.
+ */
+int warp_search_noalloc(warp_index* idx, const float* queries, int32_t n_queries, int32_t n_qtok,
+                        int32_t nprobe, int64_t t_prime, int32_t k, int32_t* out_doc_ids,
+                        float* out_scores, int32_t* out_counts, int64_t* out_fixed_scores,
+                        void* hip_stream);
+
 /* Wait for the index's outstanding work on `hip_stream` and report any deferred
  * device-side error. */
 int warp_index_sync(warp_index* idx, void* hip_stream);

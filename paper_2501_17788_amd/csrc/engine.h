@@ -44,6 +44,11 @@ constexpr int kMxBlock = 256;
 // The persistent scan grid takes its items in batches of kScanBatch consecutive items:
 // workgroup b starts with batch b, and every later batch comes from a device counter.
 constexpr int kScanBatch = 4;
+// Chunks probed by at most kNarrowMax tokens of a wave take the narrow scan (k_scan_narrow):
+// one wave per chunk, with groups of kNrGroup tokens whose five digit classes are the rows
+// of one matrix-core tile, so a 16-embedding tile of a group costs 6 int8 MFMAs instead of 18.
+constexpr int kNarrowMax = 6;
+constexpr int kNrGroup = 3;
 constexpr int kQdigBytes = 3 * kDim;  // three base-256 digit planes of a query token
 // Largest bucket weight magnitude: Q(omega) = round(omega * 2^22) must have three
 // signed base-256 digits, i.e. lie in [-8421504, 8355711].
@@ -101,8 +106,12 @@ struct WaveArgs {
                                 // embedding (x, y: low and high words; the chunk's length in the
                                 // top bits of y), first pair of the cluster (z), probing tokens (w)
     int64_t* list_item;         // [n_chunks + 1] exclusive prefix of their items; list_item[*list_n] = total
-    int64_t* list_n;            // [1] number of probed chunks
-    int64_t* cblk;              // [2 * ceil(n_chunks / kPlanBlock)] block sums of probed chunks and items
+    int64_t* list_n;            // [1] number of probed chunks of the wide scan (more than kNarrowMax tokens)
+    int4* list_rec2;            // [n_chunks] the probed chunks of the narrow scan (1..kNarrowMax tokens),
+                                // in the same order, with records like list_rec
+    int64_t* list_n2;           // [1] their number
+    int64_t* cblk;              // [3 * ceil(n_chunks / kPlanBlock)] block sums: wide chunks, their items,
+                                // narrow chunks
     uint32_t* scan_queue;       // [1] next unclaimed batch of the scan's items
     // outputs (device; the debug ones may be null)
     int32_t* out_ids;           // [n_q][k]
@@ -140,6 +149,8 @@ void launch_pairing(const WaveArgs& a, hipStream_t s);
 void launch_wave_prep(const WaveArgs& a, uint32_t* ep, uint32_t last, hipStream_t s);
 void launch_scan_mx(const WaveArgs& a, hipStream_t s);
 int scan_mx_blocks_per_cu(int nbits);
+void launch_scan_narrow(const WaveArgs& a, int32_t grid, hipStream_t s);
+int scan_narrow_blocks_per_cu(int nbits);
 void launch_fold(const WaveArgs& a, hipStream_t s);
 void launch_topk(const WaveArgs& a, hipStream_t s);
 void launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);

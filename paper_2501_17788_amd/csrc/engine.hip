@@ -22,6 +22,12 @@
 
 using namespace warp;
 
+// Scratch of warp_search_noalloc: one array per GPU (each device holds its own copy), kept
+// until the process ends. Host code never uses this name as an address: the device address
+// comes from hipGetSymbolAddress, once per device, when the first index is loaded on it.
+constexpr size_t kNoAllocBytes = (size_t)256 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
 namespace {
 
 thread_local std::string g_err;
@@ -67,6 +73,7 @@ struct warp_index {
     int32_t* err = nullptr;
     hipStream_t stream = nullptr;
     int scan_grid = 0;     // persistent workgroups of the residual scan
+    int narrow_grid = 0;   // workgroups of the narrow scan (four waves, one chunk per wave at a time)
     // per-search scratch, grown on demand
     DevBuf filter, sel, base, seg_pref, m_fixed, tokmax, keys, qpart;
     // Token-max table [wave query slot][token][document]. The rows of query slot q carry an
@@ -85,6 +92,7 @@ struct warp_index {
     DevBuf q_epoch;                // device copy of slot_ep
     DevBuf ccount, cursor, pair_start, plist, qdig;
     DevBuf list_rec, list_item, cblk;  // the wave's probed chunks (see WaveArgs)
+    DevBuf list_rec2;                  // the wave's probed chunks of the narrow scan
     DevBuf scan_queue;
     int32_t scoring = WARP_SCORING_PAPER;
     DevBuf tokcnt, doc_len;    // Eq.-1-literal scoring only
@@ -172,6 +180,33 @@ int check_device() {
     return WARP_OK;
 }
 
+// Per-device address of `scratch`, set by bind_noalloc_scratch.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_lock;
+unsigned char* g_scratch_ptr[kMaxDevices] = {};
+
+// Look up this device's copy of `scratch` (device `dev` must be current); once per device.
+int bind_noalloc_scratch(int dev) {
+    if (dev < 0 || dev >= kMaxDevices) return fail(WARP_EDEVICE, "device %d is out of range", dev);
+    std::lock_guard<std::mutex> g(g_scratch_lock);
+    if (g_scratch_ptr[dev]) return WARP_OK;
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+        (void)hipGetLastError();
+        return fail(WARP_EDEVICE, "hipGetSymbolAddress of the no-allocation scratch failed: %s",
+                    hipGetErrorString(e));
+    }
+    g_scratch_ptr[dev] = (unsigned char*)p;
+    return WARP_OK;
+}
+
+unsigned char* noalloc_scratch(int dev) {
+    if (dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> g(g_scratch_lock);
+    return g_scratch_ptr[dev];
+}
+
 bool is_index(const warp_index* idx) {
     if (!idx) return false;
     std::lock_guard<std::mutex> g(g_live_lock);
@@ -191,7 +226,8 @@ void destroy_index(warp_index* idx) {
         for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_pref, &idx->m_fixed, &idx->tokmax,
                           &idx->q_epoch, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount,
                           &idx->cursor, &idx->pair_start, &idx->plist, &idx->qdig, &idx->list_rec,
-                          &idx->list_item, &idx->cblk, &idx->scan_queue, &idx->st_q, &idx->st_ids,
+                          &idx->list_item, &idx->cblk, &idx->list_rec2, &idx->scan_queue, &idx->st_q,
+                          &idx->st_ids,
                           &idx->st_scores, &idx->st_fixed, &idx->st_counts, &idx->st_sel, &idx->st_m,
                           &idx->st_bitmap, &idx->st_scored})
             release(*b);
@@ -316,6 +352,7 @@ int finish_load(warp_index* idx, const int64_t* off_host) {
     int cus = 0;
     HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, idx->device));
     idx->scan_grid = cus * scan_mx_blocks_per_cu(idx->nbits);
+    idx->narrow_grid = cus * scan_narrow_blocks_per_cu(idx->nbits);
     return WARP_OK;
 }
 
@@ -359,8 +396,12 @@ int load_common(const float* C, int32_t n_c, int32_t dim, const int64_t* off, co
         if (rc) return rc;
     }
 
+    int device = 0;
+    HIP_TRY(hipGetDevice(&device));
+    rc = bind_noalloc_scratch(device);
+    if (rc) return rc;
     warp_index* idx = new warp_index();
-    HIP_TRY(hipGetDevice(&idx->device));
+    idx->device = device;
     idx->n_c = n_c;
     idx->n_docs = n_docs;
     idx->nbits = nbits;
@@ -455,8 +496,9 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, hipStream_t s) {
     if (!rc) rc = grow_scratch(idx, idx->qdig, (size_t)n_tok * kQdigBytes);
     const int64_t cblocks = (idx->n_chunks + kPlanBlock - 1) / kPlanBlock;
     if (!rc) rc = grow_scratch(idx, idx->list_rec, (size_t)idx->n_chunks * 16);
-    if (!rc) rc = grow_scratch(idx, idx->list_item, ((size_t)idx->n_chunks + 2) * 8);  // + the count
-    if (!rc) rc = grow_scratch(idx, idx->cblk, (size_t)cblocks * 16);
+    if (!rc) rc = grow_scratch(idx, idx->list_rec2, (size_t)idx->n_chunks * 16);
+    if (!rc) rc = grow_scratch(idx, idx->list_item, ((size_t)idx->n_chunks + 3) * 8);  // + the two counts
+    if (!rc) rc = grow_scratch(idx, idx->cblk, (size_t)cblocks * 24);
     if (!rc) rc = grow_scratch(idx, idx->scan_queue, 256);
     if (rc) return rc;
     // the token-max table and its query slots' epochs. All slots are zeroed before a search
@@ -577,99 +619,154 @@ struct SearchOut {
     int64_t* scored;
 };
 
+// Scratch of one wave: the device memory its kernels use besides the index and the outputs.
+struct WaveScratch {
+    uint16_t* filter;
+    int32_t *sel, *base;
+    int64_t *seg_pref, *m_fixed;
+    uint32_t *tokmax, *tokcnt;
+    const uint32_t* q_epoch;  // null: cells hold t + 2^31 and the fold resets what it reads
+    int32_t* doc_len;
+    uint64_t *keys, *qpart;
+    int32_t *ccount, *cursor, *pair_start, *plist;
+    int8_t* qdig;
+    int4 *list_rec, *list_rec2;
+    int64_t *list_item, *cblk;
+    uint32_t* scan_queue;
+};
+
+// The index's own scratch (grown by reserve()).
+WaveScratch index_scratch(warp_index* idx) {
+    WaveScratch w{};
+    w.filter = (uint16_t*)idx->filter.p;
+    w.sel = (int32_t*)idx->sel.p;
+    w.base = (int32_t*)idx->base.p;
+    w.seg_pref = (int64_t*)idx->seg_pref.p;
+    w.m_fixed = (int64_t*)idx->m_fixed.p;
+    w.tokmax = (uint32_t*)idx->tokmax.p;
+    const bool epochs = idx->scoring == WARP_SCORING_PAPER && idx->tab_epochs != 0;
+    w.q_epoch = epochs ? (const uint32_t*)idx->q_epoch.p : nullptr;
+    w.tokcnt = idx->scoring == WARP_SCORING_EQ1_LITERAL ? (uint32_t*)idx->tokcnt.p : nullptr;
+    w.doc_len = (int32_t*)idx->doc_len.p;
+    w.keys = (uint64_t*)idx->keys.p;
+    w.qpart = (uint64_t*)idx->qpart.p;
+    w.ccount = (int32_t*)idx->ccount.p;
+    w.cursor = (int32_t*)idx->cursor.p;
+    w.pair_start = (int32_t*)idx->pair_start.p;
+    w.plist = (int32_t*)idx->plist.p;
+    w.qdig = (int8_t*)idx->qdig.p;
+    w.list_rec = (int4*)idx->list_rec.p;
+    w.list_item = (int64_t*)idx->list_item.p;
+    w.list_rec2 = (int4*)idx->list_rec2.p;
+    w.cblk = (int64_t*)idx->cblk.p;
+    w.scan_queue = (uint32_t*)idx->scan_queue.p;
+    return w;
+}
+
+// Enqueue the kernels of one wave (queries [q0, q0 + nq) of the search) on `s`. With epochs,
+// the host's copy of the query slots' epochs advances (after zeroing the slots that ran out).
+void launch_wave(warp_index* idx, const WaveScratch& w, const float* dq, int32_t q0, int32_t nq, int32_t T,
+                 int32_t P, int64_t t_prime, int32_t k, const SearchOut& o, hipStream_t s, bool timed) {
+    const int64_t words = ((int64_t)idx->n_docs + 31) / 32;
+    WaveArgs a{};
+    a.centroids = idx->centroids;
+    a.offsets = idx->offsets;
+    a.sizes = idx->sizes;
+    a.doc_ids = idx->doc_ids;
+    a.codes = idx->codes;
+    a.weights = idx->weights;
+    a.n_c = idx->n_c;
+    a.n_docs = idx->n_docs;
+    a.nbits = idx->nbits;
+    a.queries = dq + (int64_t)q0 * T * kDim;
+    a.n_q = nq;
+    a.n_qtok = T;
+    a.nprobe = P;
+    a.k = k;
+    a.t_prime = t_prime;
+    a.filter_bins = w.filter;
+    a.sel = w.sel;
+    a.base = w.base;
+    a.seg_pref = w.seg_pref;
+    a.m_fixed = w.m_fixed;
+    a.tokmax = w.tokmax;
+    a.q_epoch = w.q_epoch;
+    a.tok_w = idx->tab_w;
+    a.tokcnt = w.tokcnt;
+    a.doc_len = w.doc_len;
+    a.keys = w.keys;
+    a.qpart = w.qpart;
+    a.err = idx->err;
+    a.out_ids = o.ids + (int64_t)q0 * k;
+    a.out_scores = o.scores + (int64_t)q0 * k;
+    a.out_fixed = o.fixed ? o.fixed + (int64_t)q0 * k : nullptr;
+    a.out_counts = o.counts ? o.counts + q0 : nullptr;
+    a.dbg_sel = o.sel ? o.sel + (int64_t)q0 * T * P : nullptr;
+    a.dbg_m = o.m ? o.m + (int64_t)q0 * T : nullptr;
+    a.dbg_bitmap = o.bitmap ? o.bitmap + (int64_t)q0 * words : nullptr;
+    a.dbg_scored = o.scored ? o.scored + q0 : nullptr;
+    a.ccount = w.ccount;
+    a.cursor = w.cursor;
+    a.pair_start = w.pair_start;
+    a.plist = w.plist;
+    a.chunk_c = idx->chunk_c;
+    a.chunk_k = idx->chunk_k;
+    a.n_chunks = idx->n_chunks;
+    a.list_rec = w.list_rec;
+    a.list_item = w.list_item;
+    a.list_n = w.list_item + idx->n_chunks + 1;
+    a.list_rec2 = w.list_rec2;
+    a.list_n2 = w.list_item + idx->n_chunks + 2;
+    a.cblk = w.cblk;
+    a.scan_queue = w.scan_queue;
+    a.qdig = w.qdig;
+    a.scan_grid = idx->scan_grid;
+    a.topk_list_cap = topk_list_cap();
+
+    const bool epochs = w.q_epoch != nullptr;
+    hipEvent_t ev[kStages + 1] = {};
+    if (timed)
+        for (int e = 0; e <= kStages; ++e) ev[e] = take_event(idx);
+    auto mark = [&](int e) {
+        if (timed) (void)hipEventRecord(ev[e], s);
+    };
+    mark(0);
+    launch_filter_gemm(a.queries, nq * T, idx->centroids, idx->n_c, a.filter_bins, nullptr, s);
+    mark(1);
+    if (epochs) {  // the slots' next epochs (the preparation applies the same rule on the device),
+                   // after zeroing those past the last one
+        zero_slots(idx, nq, true, s);
+        for (int32_t q = 0; q < nq; ++q)
+            idx->slot_ep[q] = idx->slot_ep[q] >= (uint32_t)idx->tab_epochs ? 1u : idx->slot_ep[q] + 1u;
+    }
+    // the preparation zeroes the cluster token counters that the selection counts into
+    launch_wave_prep(a, epochs ? (uint32_t*)idx->q_epoch.p : nullptr, (uint32_t)idx->tab_epochs, s);
+    launch_select(a, s);
+    mark(2);
+    launch_scored(a, s);
+    launch_pairing(a, s);
+    mark(3);
+    launch_scan_mx(a, s);
+    launch_scan_narrow(a, idx->narrow_grid, s);
+    mark(4);
+    launch_fold(a, s);
+    mark(5);
+    launch_topk(a, s);
+    mark(6);
+    if (timed)
+        for (int e = 0; e <= kStages; ++e) idx->ev_pending.push_back(ev[e]);
+}
+
 // Enqueue a whole search on `s`; every pointer is device memory.
 int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t T, int32_t P,
                    int64_t t_prime, int32_t k, const SearchOut& o, hipStream_t s) {
     const int32_t qw = wave_queries(idx, n_queries, T);
     int rc = reserve(idx, qw, T, P, s);
     if (rc) return rc;
-    const int64_t words = ((int64_t)idx->n_docs + 31) / 32;
+    const WaveScratch w = index_scratch(idx);
     for (int32_t q0 = 0; q0 < n_queries; q0 += qw) {
         const int32_t nq = n_queries - q0 < qw ? n_queries - q0 : qw;
-        WaveArgs a{};
-        a.centroids = idx->centroids;
-        a.offsets = idx->offsets;
-        a.sizes = idx->sizes;
-        a.doc_ids = idx->doc_ids;
-        a.codes = idx->codes;
-        a.weights = idx->weights;
-        a.n_c = idx->n_c;
-        a.n_docs = idx->n_docs;
-        a.nbits = idx->nbits;
-        a.queries = dq + (int64_t)q0 * T * kDim;
-        a.n_q = nq;
-        a.n_qtok = T;
-        a.nprobe = P;
-        a.k = k;
-        a.t_prime = t_prime;
-        a.filter_bins = (uint16_t*)idx->filter.p;
-        a.sel = (int32_t*)idx->sel.p;
-        a.base = (int32_t*)idx->base.p;
-        a.seg_pref = (int64_t*)idx->seg_pref.p;
-        a.m_fixed = (int64_t*)idx->m_fixed.p;
-        a.tokmax = (uint32_t*)idx->tokmax.p;
-        const bool epochs = idx->scoring == WARP_SCORING_PAPER && idx->tab_epochs != 0;
-        a.q_epoch = epochs ? (const uint32_t*)idx->q_epoch.p : nullptr;
-        a.tok_w = idx->tab_w;
-        a.tokcnt = idx->scoring == WARP_SCORING_EQ1_LITERAL ? (uint32_t*)idx->tokcnt.p : nullptr;
-        a.doc_len = (const int32_t*)idx->doc_len.p;
-        a.keys = (uint64_t*)idx->keys.p;
-        a.qpart = (uint64_t*)idx->qpart.p;
-        a.err = idx->err;
-        a.out_ids = o.ids + (int64_t)q0 * k;
-        a.out_scores = o.scores + (int64_t)q0 * k;
-        a.out_fixed = o.fixed ? o.fixed + (int64_t)q0 * k : nullptr;
-        a.out_counts = o.counts ? o.counts + q0 : nullptr;
-        a.dbg_sel = o.sel ? o.sel + (int64_t)q0 * T * P : nullptr;
-        a.dbg_m = o.m ? o.m + (int64_t)q0 * T : nullptr;
-        a.dbg_bitmap = o.bitmap ? o.bitmap + (int64_t)q0 * words : nullptr;
-        a.dbg_scored = o.scored ? o.scored + q0 : nullptr;
-        a.ccount = (int32_t*)idx->ccount.p;
-        a.cursor = (int32_t*)idx->cursor.p;
-        a.pair_start = (int32_t*)idx->pair_start.p;
-        a.plist = (int32_t*)idx->plist.p;
-        a.chunk_c = idx->chunk_c;
-        a.chunk_k = idx->chunk_k;
-        a.n_chunks = idx->n_chunks;
-        a.list_rec = (int4*)idx->list_rec.p;
-        a.list_item = (int64_t*)idx->list_item.p;
-        a.list_n = (int64_t*)idx->list_item.p + idx->n_chunks + 1;
-        a.cblk = (int64_t*)idx->cblk.p;
-        a.scan_queue = (uint32_t*)idx->scan_queue.p;
-        a.qdig = (int8_t*)idx->qdig.p;
-        a.scan_grid = idx->scan_grid;
-        a.topk_list_cap = topk_list_cap();
-
-        hipEvent_t ev[kStages + 1] = {};
-        if (idx->timing)
-            for (int e = 0; e <= kStages; ++e) ev[e] = take_event(idx);
-        auto mark = [&](int e) {
-            if (idx->timing) (void)hipEventRecord(ev[e], s);
-        };
-        mark(0);
-        launch_filter_gemm(a.queries, nq * T, idx->centroids, idx->n_c, a.filter_bins, nullptr, s);
-        mark(1);
-        if (epochs) {  // the slots' next epochs (the preparation applies the same rule on the device),
-                       // after zeroing those past the last one
-            zero_slots(idx, nq, true, s);
-            for (int32_t q = 0; q < nq; ++q)
-                idx->slot_ep[q] = idx->slot_ep[q] >= (uint32_t)idx->tab_epochs ? 1u : idx->slot_ep[q] + 1u;
-        }
-        // the preparation zeroes the cluster token counters that the selection counts into
-        launch_wave_prep(a, epochs ? (uint32_t*)idx->q_epoch.p : nullptr, (uint32_t)idx->tab_epochs, s);
-        launch_select(a, s);
-        mark(2);
-        launch_scored(a, s);
-        launch_pairing(a, s);
-        mark(3);
-        launch_scan_mx(a, s);
-        mark(4);
-        launch_fold(a, s);
-        mark(5);
-        launch_topk(a, s);
-        mark(6);
-        if (idx->timing)
-            for (int e = 0; e <= kStages; ++e) idx->ev_pending.push_back(ev[e]);
+        launch_wave(idx, w, dq, q0, nq, T, P, t_prime, k, o, s, idx->timing);
         hipError_t le = hipGetLastError();
         if (le != hipSuccess) return fail(WARP_EDEVICE, "kernel launch failed: %s", hipGetErrorString(le));
     }
@@ -735,9 +832,90 @@ int search_host(warp_index* idx, const float* queries, int32_t n_queries, int32_
     return read_device_errors(idx, s);
 }
 
+// The no-allocation scratch laid out for waves of qw queries of T tokens (nprobe P), in
+// 256-byte aligned pieces from `base` (null: sizes only); returns the bytes it takes.
+size_t noalloc_layout(const warp_index* idx, int32_t qw, int32_t T, int32_t P, bool literal, unsigned char* base,
+                      WaveScratch* out) {
+    size_t at = 0;
+    auto take = [&](size_t bytes) -> void* {
+        void* p = base ? (void*)(base + at) : nullptr;
+        at += (std::max<size_t>(bytes, 256) + 255) & ~(size_t)255;
+        return p;
+    };
+    const size_t n_tok = (size_t)qw * T, nd = (size_t)idx->n_docs, nc = (size_t)idx->n_c;
+    const size_t chunks = (size_t)idx->n_chunks, cblocks = (chunks + kPlanBlock - 1) / kPlanBlock;
+    WaveScratch w{};
+    w.ccount = (int32_t*)take(nc * 4);
+    w.cursor = (int32_t*)take(nc * 4);
+    w.pair_start = (int32_t*)take((nc + 1) * 4);
+    w.list_rec = (int4*)take(chunks * 16);
+    w.list_rec2 = (int4*)take(chunks * 16);
+    w.list_item = (int64_t*)take((chunks + 3) * 8);
+    w.cblk = (int64_t*)take(cblocks * 24);
+    w.scan_queue = (uint32_t*)take(256);
+    w.doc_len = literal ? (int32_t*)take(nd * 4) : nullptr;
+    w.filter = (uint16_t*)take(n_tok * nc * 2);
+    w.sel = (int32_t*)take(n_tok * P * 4);
+    w.base = (int32_t*)take(n_tok * P * 4);
+    w.seg_pref = (int64_t*)take(n_tok * (P + 1) * 8);
+    w.m_fixed = (int64_t*)take(n_tok * 8);
+    w.keys = (uint64_t*)take((size_t)qw * nd * 8);
+    w.qpart = (uint64_t*)take((size_t)qw * ((nd + 255) / 256) * 16);
+    w.plist = (int32_t*)take(n_tok * P * 8);
+    w.qdig = (int8_t*)take(n_tok * kQdigBytes);
+    w.tokmax = (uint32_t*)take(n_tok * nd * 4);
+    w.tokcnt = literal ? (uint32_t*)take(n_tok * nd * 4) : nullptr;
+    w.q_epoch = nullptr;  // cells hold t + 2^31 and the fold resets every cell it reads
+    if (out) *out = w;
+    return at;
+}
+
 }  // namespace
 
 extern "C" {
+
+int warp_search_noalloc(warp_index* idx, const float* queries, int32_t n_queries, int32_t n_qtok, int32_t nprobe,
+                        int64_t t_prime, int32_t k, int32_t* out_doc_ids, float* out_scores, int32_t* out_counts,
+                        int64_t* out_fixed_scores, void* hip_stream) {
+    int rc = validate_search(idx, queries, n_queries, n_qtok, nprobe, t_prime, k, out_doc_ids, out_scores);
+    if (rc) return rc;
+    std::lock_guard<std::mutex> g(idx->lock);
+    HIP_TRY(hipSetDevice(idx->device));
+    unsigned char* base = noalloc_scratch(idx->device);
+    if (!base) return fail(WARP_EDEVICE, "no-allocation scratch of device %d is not bound", idx->device);
+    const bool literal = idx->scoring == WARP_SCORING_EQ1_LITERAL;
+    const size_t one = noalloc_layout(idx, 1, n_qtok, nprobe, literal, nullptr, nullptr);
+    if (one > kNoAllocBytes)
+        return fail(WARP_ENOMEM,
+                    "warp_search_noalloc: one query of %d tokens on this index needs %zu bytes of scratch; "
+                    "the static scratch holds %zu (use warp_search_async)", n_qtok, one, kNoAllocBytes);
+    // the largest wave that fits (the layout grows with the wave)
+    int32_t lo = 1, hi = n_queries;
+    while (lo < hi) {
+        const int32_t mid = lo + (hi - lo + 1) / 2;
+        if (noalloc_layout(idx, mid, n_qtok, nprobe, literal, nullptr, nullptr) <= kNoAllocBytes) lo = mid;
+        else hi = mid - 1;
+    }
+    const int32_t qw = lo;
+    WaveScratch w{};
+    noalloc_layout(idx, qw, n_qtok, nprobe, literal, base, &w);
+    hipStream_t s = (hipStream_t)hip_stream;
+    // the array keeps what the last call left: the token-max cells (and counts) start at
+    // zero; each wave's fold then resets every cell it reads
+    launch_zero_cells(w.tokmax, (int64_t)qw * n_qtok * idx->n_docs, s);
+    if (literal) {
+        launch_zero_cells(w.tokcnt, (int64_t)qw * n_qtok * idx->n_docs, s);
+        launch_doc_len(idx->doc_ids, idx->n_emb, w.doc_len, idx->n_docs, s);
+    }
+    SearchOut o{out_doc_ids, out_scores, out_fixed_scores, out_counts, nullptr, nullptr, nullptr, nullptr};
+    for (int32_t q0 = 0; q0 < n_queries; q0 += qw) {
+        const int32_t nq = n_queries - q0 < qw ? n_queries - q0 : qw;
+        launch_wave(idx, w, queries, q0, nq, n_qtok, nprobe, t_prime, k, o, s, false);
+    }
+    const hipError_t le = hipGetLastError();
+    if (le != hipSuccess) return fail(WARP_EDEVICE, "kernel launch failed: %s", hipGetErrorString(le));
+    return WARP_OK;
+}
 
 int warp_fixed_point_bits(void) { return kFrac; }
 

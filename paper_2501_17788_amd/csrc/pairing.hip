@@ -80,57 +80,70 @@ __device__ void pair_offsets(const WaveArgs& a, int64_t* ws) {
     if (tid == 0) a.pair_start[n_c] = (int32_t)carry;
 }
 
-// Probed chunks and their items (token groups of their cluster) in the index's chunk order.
-__device__ __forceinline__ void chunk_items(const WaveArgs& a, int64_t j, int64_t& flag, int64_t& items) {
-    flag = items = 0;
+// Probed chunks in the index's chunk order: a chunk probed by more than kNarrowMax tokens
+// goes to the wide scan with its items (token groups of its cluster), one probed by
+// 1..kNarrowMax tokens to the narrow scan.
+__device__ __forceinline__ void chunk_items(const WaveArgs& a, int64_t j, int64_t& flag, int64_t& items,
+                                            int64_t& narrow) {
+    flag = items = narrow = 0;
     if (j < a.n_chunks) {
         const int32_t nt = a.ccount[a.chunk_c[j]];
-        items = (nt + kMxGroup - 1) / kMxGroup;
-        flag = items > 0;
+        if (nt > kNarrowMax) {
+            items = (nt + kMxGroup - 1) / kMxGroup;
+            flag = 1;
+        } else {
+            narrow = nt > 0;
+        }
     }
 }
 
-// Inclusive prefix sums of two values per thread over a block of kPlanBlock threads
+// Inclusive prefix sums of three values per thread over a block of kPlanBlock threads
 // (wave shuffles, then the wave totals through LDS).
-__device__ __forceinline__ void block_scan2(int64_t& f, int64_t& it, int64_t* wf, int64_t* wi) {
+__device__ __forceinline__ void block_scan3(int64_t& f, int64_t& it, int64_t& nr, int64_t* wf, int64_t* wi,
+                                            int64_t* wn) {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
-        const int64_t tf = __shfl_up(f, off, 64), ti = __shfl_up(it, off, 64);
+        const int64_t tf = __shfl_up(f, off, 64), ti = __shfl_up(it, off, 64), tn = __shfl_up(nr, off, 64);
         if (lane >= off) {
             f += tf;
             it += ti;
+            nr += tn;
         }
     }
     if (lane == 63) {
         wf[w] = f;
         wi[w] = it;
+        wn[w] = nr;
     }
     __syncthreads();
-    int64_t bf = 0, bi = 0;
+    int64_t bf = 0, bi = 0, bn = 0;
     for (int i = 0; i < w; ++i) {
         bf += wf[i];
         bi += wi[i];
+        bn += wn[i];
     }
     f += bf;
     it += bi;
+    nr += bn;
 }
 
 // Block 0: the clusters' pair offsets. Blocks 1 ..: per block of kPlanBlock chunks, the
 // number of probed chunks and their items.
 __global__ __launch_bounds__(kPlanBlock) void k_plan_count(WaveArgs a) {
-    __shared__ int64_t wf[kPlanBlock / 64], wi[kPlanBlock / 64];
+    __shared__ int64_t wf[kPlanBlock / 64], wi[kPlanBlock / 64], wn[kPlanBlock / 64];
     if (blockIdx.x == 0) {
         pair_offsets(a, wf);
         return;
     }
     const int64_t b = (int64_t)blockIdx.x - 1;
-    int64_t f, it;
-    chunk_items(a, b * kPlanBlock + threadIdx.x, f, it);
-    block_scan2(f, it, wf, wi);
+    int64_t f, it, nr;
+    chunk_items(a, b * kPlanBlock + threadIdx.x, f, it, nr);
+    block_scan3(f, it, nr, wf, wi, wn);
     if (threadIdx.x == kPlanBlock - 1) {
-        a.cblk[2 * b] = f;
-        a.cblk[2 * b + 1] = it;
+        a.cblk[3 * b] = f;
+        a.cblk[3 * b + 1] = it;
+        a.cblk[3 * b + 2] = nr;
     }
 }
 
@@ -151,11 +164,12 @@ __device__ __forceinline__ void pair_scatter(const WaveArgs& a, int64_t i) {
     a.plist[2 * p + 1] = (int32_t)((uint32_t)a.base[i] + bias);
 }
 
-// Blocks [0, cb): the compacted list of probed chunks with the exclusive prefix of their
-// items. Blocks [cb, ...): the pairs, kPlanBlock per block, scattered into their buckets.
+// Blocks [0, cb): the compacted lists of probed chunks (wide, with the exclusive prefix of
+// their items, and narrow). Blocks [cb, ...): the pairs, kPlanBlock per block, scattered
+// into their buckets.
 __global__ __launch_bounds__(kPlanBlock) void k_plan_emit(WaveArgs a, int32_t cb) {
-    __shared__ int64_t wf[kPlanBlock / 64], wi[kPlanBlock / 64];
-    __shared__ unsigned long long s_of, s_oi;
+    __shared__ int64_t wf[kPlanBlock / 64], wi[kPlanBlock / 64], wn[kPlanBlock / 64];
+    __shared__ unsigned long long s_of, s_oi, s_on;
     const int tid = threadIdx.x;
     const int b = blockIdx.x;
     if (b >= cb) {  // uniform over the block
@@ -165,35 +179,44 @@ __global__ __launch_bounds__(kPlanBlock) void k_plan_emit(WaveArgs a, int32_t cb
     if (tid == 0) {
         s_of = 0;
         s_oi = 0;
+        s_on = 0;
     }
     __syncthreads();
     {  // offsets of this block: the sums of the blocks before it
-        int64_t vf = 0, vi = 0;
+        int64_t vf = 0, vi = 0, vn = 0;
         for (int j = tid; j < b; j += kPlanBlock) {
-            vf += a.cblk[2 * j];
-            vi += a.cblk[2 * j + 1];
+            vf += a.cblk[3 * j];
+            vi += a.cblk[3 * j + 1];
+            vn += a.cblk[3 * j + 2];
         }
         if (vf) atomicAdd(&s_of, (unsigned long long)vf);
         if (vi) atomicAdd(&s_oi, (unsigned long long)vi);
+        if (vn) atomicAdd(&s_on, (unsigned long long)vn);
     }
     const int64_t j = (int64_t)b * kPlanBlock + tid;
-    int64_t f0, it0;
-    chunk_items(a, j, f0, it0);
-    int64_t f = f0, it = it0;
-    block_scan2(f, it, wf, wi);  // its barrier also orders the offsets above
-    const int64_t pos = (int64_t)s_of + f - f0, item = (int64_t)s_oi + it - it0;
-    if (f0) {
+    int64_t f0, it0, n0;
+    chunk_items(a, j, f0, it0, n0);
+    int64_t f = f0, it = it0, nr = n0;
+    block_scan3(f, it, nr, wf, wi, wn);  // its barrier also orders the offsets above
+    if (f0 || n0) {
         const int c = a.chunk_c[j];
         const int64_t e0 = a.offsets[c] + (int64_t)a.chunk_k[j] * kMxChunk;
         const int64_t e1 = a.offsets[c + 1];
         const int64_t len = e1 - e0 < kMxChunk ? e1 - e0 : kMxChunk;  // 1 .. kMxChunk
         const uint64_t ew = (uint64_t)e0 | ((uint64_t)len << kRecLenShift);
-        a.list_rec[pos] = make_int4((int)(uint32_t)ew, (int)(uint32_t)(ew >> 32), a.pair_start[c], a.ccount[c]);
-        a.list_item[pos] = item;
+        const int4 rec = make_int4((int)(uint32_t)ew, (int)(uint32_t)(ew >> 32), a.pair_start[c], a.ccount[c]);
+        if (f0) {
+            const int64_t pos = (int64_t)s_of + f - f0;
+            a.list_rec[pos] = rec;
+            a.list_item[pos] = (int64_t)s_oi + it - it0;
+        } else {
+            a.list_rec2[(int64_t)s_on + nr - n0] = rec;
+        }
     }
     if (b == cb - 1 && tid == kPlanBlock - 1) {
         *a.list_n = (int64_t)s_of + f;
         a.list_item[(int64_t)s_of + f] = (int64_t)s_oi + it;
+        *a.list_n2 = (int64_t)s_on + nr;
     }
 }
 
@@ -202,6 +225,7 @@ void launch_pairing(const WaveArgs& a, hipStream_t s) {
     const unsigned cb = (unsigned)((a.n_chunks + kPlanBlock - 1) / kPlanBlock);
     if (cb == 0) {  // an index without embeddings: no chunk, no item, no pair is read
         launch_fill_i32(reinterpret_cast<int32_t*>(a.list_n), 2, 0, s);
+        launch_fill_i32(reinterpret_cast<int32_t*>(a.list_n2), 2, 0, s);
         launch_fill_i32(reinterpret_cast<int32_t*>(a.list_item), 2, 0, s);
         return;
     }

@@ -94,6 +94,109 @@ __device__ __forceinline__ void slot_of_dim(int d, int& s, int& g, int& j) {
     }
 }
 
+// Weight digit tables of a workgroup: for b <= 4, tab[p][k] holds digit p of Q(omega[v]) for
+// v = 4 k .. 4 k + 3 (in registers); for b = 8, s_wd[v] holds the three digits of Q(omega[v]) in
+// bytes 0..2 (LDS, written by threads 0..255: the caller orders it with a barrier).
+template <int NBITS>
+__device__ __forceinline__ void weight_tables(const float* weights, unsigned (&tab)[3][4], unsigned* s_wd, int tid) {
+    if (NBITS <= 4) {
+#pragma unroll
+        for (int v = 0; v < (NBITS <= 4 ? 1 << NBITS : 0); ++v) {
+            int d[3];
+            digits3(quant22(weights[v]), d[0], d[1], d[2]);
+#pragma unroll
+            for (int p = 0; p < 3; ++p) tab[p][v >> 2] |= ((unsigned)d[p] & 255u) << (8 * (v & 3));
+        }
+    } else if (tid < 256) {
+        int d[3];
+        digits3(quant22(weights[tid]), d[0], d[1], d[2]);
+        s_wd[tid] = ((unsigned)d[0] & 255u) | (((unsigned)d[1] & 255u) << 8) | (((unsigned)d[2] & 255u) << 16);
+    }
+}
+
+// The three weight-digit planes of one lane's 32 dimensions of a 16-embedding tile, in
+// operand order: W[p][s] is digit plane p of K slice s (slot_of_dim). `wj` holds the
+// lane's code words of the tile: v_perm_b32 lookups in the register tables (3 per four
+// nibbles and plane at b = 4; 1 per four fields at b = 2 and per four bits at b = 1), or at
+// b = 8 one LDS table lookup per code byte followed by 3 v_perm per plane and four dimensions.
+template <int NBITS>
+__device__ __forceinline__ void decode_weight_digits(const unsigned (&wj)[NBITS], const unsigned (&tab)[3][4],
+                                                     const unsigned* s_wd, v4i (&W)[3][2]) {
+    constexpr int CW = NBITS;
+    if (NBITS == 4) {
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const unsigned x = h == 0 ? (wj[m % CW] >> 4) & 0x0F0F0F0Fu : wj[m % CW] & 0x0F0F0F0Fu;
+                const unsigned x7 = x & 0x07070707u;
+                const unsigned pick = ((x >> 1) & 0x04040404u) | 0x03020100u;
+#pragma unroll
+                for (int p = 0; p < 3; ++p) {
+                    const unsigned lo8 = __builtin_amdgcn_perm(tab[p][1], tab[p][0], x7);
+                    const unsigned hi8 = __builtin_amdgcn_perm(tab[p][3], tab[p][2], x7);
+                    W[p][m >> 1][2 * (m & 1) + h] = (int)__builtin_amdgcn_perm(hi8, lo8, pick);
+                }
+            }
+        }
+    } else if (NBITS == 2) {
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const unsigned x = (wj[s % CW] >> (6 - 2 * u)) & 0x03030303u;
+#pragma unroll
+                for (int p = 0; p < 3; ++p) W[p][s][u] = (int)__builtin_amdgcn_perm(tab[p][0], tab[p][0], x);
+            }
+        }
+    } else if (NBITS == 1) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const unsigned x = (wj[0] >> k) & 0x01010101u;  // bit k of each byte: 0 or 1
+#pragma unroll
+            for (int p = 0; p < 3; ++p) W[p][k >> 2][k & 3] = (int)__builtin_amdgcn_perm(tab[p][0], tab[p][0], x);
+        }
+    } else {
+#pragma unroll
+        for (int m = 0; m < 8; ++m) {
+            const unsigned wm = wj[m % CW];
+            const unsigned e0 = s_wd[wm & 255u], e1 = s_wd[(wm >> 8) & 255u];
+            const unsigned e2 = s_wd[(wm >> 16) & 255u], e3 = s_wd[wm >> 24];
+#pragma unroll
+            for (int p = 0; p < 3; ++p) {
+                const unsigned sel = 0x0C0C0000u | ((unsigned)(4 + p) << 8) | (unsigned)p;
+                const unsigned lo2 = __builtin_amdgcn_perm(e1, e0, sel);  // bytes 0, 1: digit p of e0, e1
+                const unsigned hi2 = __builtin_amdgcn_perm(e3, e2, sel);
+                W[p][m >> 2][m & 3] = (int)__builtin_amdgcn_perm(hi2, lo2, 0x05040100u);
+            }
+        }
+    }
+}
+
+// A lane's code words of embedding `row` (null: zeros) in the tile layout: 4 * NBITS bytes
+// at lane group lg of the embedding's code row.
+template <int NBITS>
+__device__ __forceinline__ void load_code_words(const uint8_t* row, int lg, unsigned (&wj)[NBITS]) {
+#pragma unroll
+    for (int m = 0; m < NBITS; ++m) wj[m] = 0;
+    if (!row) return;
+    row += 4 * NBITS * lg;
+    if (NBITS == 8) {
+        const uint4 v0 = reinterpret_cast<const uint4*>(row)[0];
+        const uint4 v1 = reinterpret_cast<const uint4*>(row)[1];
+        wj[0] = v0.x; wj[1 % NBITS] = v0.y; wj[2 % NBITS] = v0.z; wj[3 % NBITS] = v0.w;
+        wj[4 % NBITS] = v1.x; wj[5 % NBITS] = v1.y; wj[6 % NBITS] = v1.z; wj[7 % NBITS] = v1.w;
+    } else if (NBITS == 4) {
+        const uint4 v = *reinterpret_cast<const uint4*>(row);
+        wj[0] = v.x; wj[1 % NBITS] = v.y; wj[2 % NBITS] = v.z; wj[3 % NBITS] = v.w;
+    } else if (NBITS == 2) {
+        const uint2 v = *reinterpret_cast<const uint2*>(row);
+        wj[0] = v.x; wj[1 % NBITS] = v.y;
+    } else {
+        wj[0] = *reinterpret_cast<const unsigned*>(row);
+    }
+}
+
 // Per-wave preparation in one launch, ordered after the previous wave's scan and fold and
 // before this wave's selection. Blocks [0, nb0): the clusters' token counters and scatter
 // cursors zeroed, the query slots' next epochs (1 after the last one, else one more; ep may
@@ -212,22 +315,9 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
     const int li = lane & 15;  // operand row / column inside a 16 x 16 tile
     const int lg = lane >> 4;  // operand lane group
 
-    // weight digit tables: tab[p][k] holds digit p of Q(omega[v]) for v = 4 k .. 4 k + 3
-    // (b <= 4); for b = 8 a 256-entry table in LDS, ordered by the first barrier below
+    // weight digit tables (for b = 8 in LDS, ordered by the first barrier below)
     unsigned tab[3][4] = {};
-    if (NBITS <= 4) {
-#pragma unroll
-        for (int v = 0; v < (NBITS <= 4 ? 1 << NBITS : 0); ++v) {
-            int d[3];
-            digits3(quant22(a.weights[v]), d[0], d[1], d[2]);
-#pragma unroll
-            for (int p = 0; p < 3; ++p) tab[p][v >> 2] |= ((unsigned)d[p] & 255u) << (8 * (v & 3));
-        }
-    } else if (tid < 256) {
-        int d[3];
-        digits3(quant22(a.weights[tid]), d[0], d[1], d[2]);
-        s_wd[tid] = ((unsigned)d[0] & 255u) | (((unsigned)d[1] & 255u) << 8) | (((unsigned)d[2] & 255u) << 16);
-    }
+    weight_tables<NBITS>(a.weights, tab, s_wd, tid);
 
     // Items of the wave's probed chunks, in the index's chunk order, in batches of R =
     // kScanBatch: workgroup b starts with batch b; every later batch is claimed from the
@@ -300,25 +390,7 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
             const int64_t er = x.e0 + 16 * (wave + NW * j) + li;
-#pragma unroll
-            for (int m = 0; m < CW; ++m) w[j][m] = 0;
-            if (er < x.e1) {
-                const uint8_t* row = codes + er * BYTES + 4 * NBITS * lg;
-                if (NBITS == 8) {
-                    const uint4 v0 = reinterpret_cast<const uint4*>(row)[0];
-                    const uint4 v1 = reinterpret_cast<const uint4*>(row)[1];
-                    w[j][0] = v0.x; w[j][1] = v0.y; w[j][2] = v0.z; w[j][3] = v0.w;
-                    w[j][4 % CW] = v1.x; w[j][5 % CW] = v1.y; w[j][6 % CW] = v1.z; w[j][7 % CW] = v1.w;
-                } else if (NBITS == 4) {
-                    const uint4 v = *reinterpret_cast<const uint4*>(row);
-                    w[j][0] = v.x; w[j][1 % CW] = v.y; w[j][2 % CW] = v.z; w[j][3 % CW] = v.w;
-                } else if (NBITS == 2) {
-                    const uint2 v = *reinterpret_cast<const uint2*>(row);
-                    w[j][0] = v.x; w[j][1 % CW] = v.y;
-                } else {
-                    w[j][0] = *reinterpret_cast<const unsigned*>(row);
-                }
-            }
+            load_code_words<NBITS>(er < x.e1 ? codes + er * BYTES : nullptr, lg, w[j]);
         }
     };
     // the list entry of item (at or after p): galloping from p, then bisection; the entry's
@@ -427,57 +499,7 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
             if (et >= n_et) break;  // wave-uniform
             // weight digits of the tile (MFMA A operand: row li = embedding e0 + 16 et + li)
             v4i A[3][2];
-            if (NBITS == 4) {
-#pragma unroll
-                for (int m = 0; m < 4; ++m) {
-#pragma unroll
-                    for (int h = 0; h < 2; ++h) {
-                        const unsigned x = h == 0 ? (w[j][m % CW] >> 4) & 0x0F0F0F0Fu : w[j][m % CW] & 0x0F0F0F0Fu;
-                        const unsigned x7 = x & 0x07070707u;
-                        const unsigned pick = ((x >> 1) & 0x04040404u) | 0x03020100u;
-#pragma unroll
-                        for (int p = 0; p < 3; ++p) {
-                            const unsigned lo8 = __builtin_amdgcn_perm(tab[p][1], tab[p][0], x7);
-                            const unsigned hi8 = __builtin_amdgcn_perm(tab[p][3], tab[p][2], x7);
-                            A[p][m >> 1][2 * (m & 1) + h] = (int)__builtin_amdgcn_perm(hi8, lo8, pick);
-                        }
-                    }
-                }
-            } else if (NBITS == 2) {
-#pragma unroll
-                for (int s = 0; s < 2; ++s) {
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        const unsigned x = (w[j][s % CW] >> (6 - 2 * u)) & 0x03030303u;
-#pragma unroll
-                        for (int p = 0; p < 3; ++p)
-                            A[p][s][u] = (int)__builtin_amdgcn_perm(tab[p][0], tab[p][0], x);
-                    }
-                }
-            } else if (NBITS == 1) {
-#pragma unroll
-                for (int k = 0; k < 8; ++k) {
-                    const unsigned x = (w[j][0] >> k) & 0x01010101u;  // bit k of each byte: 0 or 1
-#pragma unroll
-                    for (int p = 0; p < 3; ++p)
-                        A[p][k >> 2][k & 3] = (int)__builtin_amdgcn_perm(tab[p][0], tab[p][0], x);
-                }
-            } else {
-                // b = 8: one table lookup per code byte, then gather digit p of four entries
-#pragma unroll
-                for (int m = 0; m < 8; ++m) {
-                    const unsigned wm = w[j][m % CW];
-                    const unsigned e0 = s_wd[wm & 255u], e1 = s_wd[(wm >> 8) & 255u];
-                    const unsigned e2 = s_wd[(wm >> 16) & 255u], e3 = s_wd[wm >> 24];
-#pragma unroll
-                    for (int p = 0; p < 3; ++p) {
-                        const unsigned sel = 0x0C0C0000u | ((unsigned)(4 + p) << 8) | (unsigned)p;
-                        const unsigned lo2 = __builtin_amdgcn_perm(e1, e0, sel);  // bytes 0, 1: digit p of e0, e1
-                        const unsigned hi2 = __builtin_amdgcn_perm(e3, e2, sel);
-                        A[p][m >> 2][m & 3] = (int)__builtin_amdgcn_perm(hi2, lo2, 0x05040100u);
-                    }
-                }
-            }
+            decode_weight_digits<NBITS>(w[j], tab, s_wd, A);
 
             for (int tt = 0; tt < n_tt; ++tt) {
                 // class accumulators; class 0 starts at the rounding half
@@ -539,6 +561,175 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
     }
 }
 
+// Orders a wave's LDS writes before its later LDS reads by other lanes (one wave per table).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_wave_barrier();
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_wave_barrier();
+}
+
+// Narrow scan: the chunks probed by 1..kNarrowMax tokens of the wave (Sections 4.4 and 4.5,
+// the same arithmetic as k_scan_mx). One wave takes one chunk at a time, with no workgroup
+// barrier: it numbers the chunk's runs of equal documents, then scores the chunk's 16-embedding
+// tiles against groups of up to kNrGroup = 3 tokens. In a group's matrix-core tile the rows
+// are (token t, digit class s) = 5 t + s and the columns are the tile's embeddings; the K
+// dimension runs over (weight-digit plane j, dimension d), and row (t, s) takes query-digit
+// plane s - j of token t (zero outside 0..2), so six v_mfma_i32_16x16x64_i8 give all five
+// class sums A_s of up to three tokens. Lane (e, g) then holds rows 4 g .. 4 g + 3 of
+// embedding e; lane group g folds token g, taking the rows it lacks from lane group g + 1.
+// Scores go into the wave's LDS table of (token, run) maxima, flushed with one device
+// atomicMax per (token, run) after each group.
+template <int NBITS>
+__global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
+    constexpr int BYTES = kDim * NBITS / 8;
+    constexpr int NW = kMxBlock / 64;
+    constexpr int NT = kMxChunk / 16;  // tiles of a chunk
+    constexpr int NSLOT = 24;          // 16-byte query digit slots of a token
+    constexpr int TPAD = kMxChunk + 4;
+    constexpr bool PRELOAD = NBITS <= 4;  // every tile's code words in registers at once
+    static_assert(kMxChunk % 64 == 0 && kMxChunk <= 4 * 64, "four rounds of the run pass");
+    static_assert(5 * kNrGroup <= 16, "rows of a group's tile");
+    __shared__ unsigned s_tab[NW][kNrGroup * TPAD];  // (token of the group, run) maxima
+    __shared__ int s_run[NW][kMxChunk];              // run of each embedding of the chunk
+    __shared__ int s_rdoc[NW][kMxChunk];             // document of each run
+    __shared__ int s_rstart[NW][kMxChunk + 1];       // its first embedding; the chunk's length after the last
+    __shared__ unsigned s_wd[NBITS == 8 ? 256 : 1];
+
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6;
+    const int lane = tid & 63;
+    const int li = lane & 15;  // embedding of a tile (column), or row of the query operand
+    const int lg = lane >> 4;  // lane group: rows 4 lg .. 4 lg + 3 of the output; token lg of the group
+    unsigned tab[3][4] = {};
+    weight_tables<NBITS>(a.weights, tab, s_wd, tid);
+    if (NBITS == 8) __syncthreads();  // the only workgroup barrier: s_wd is written
+
+    unsigned* stab = s_tab[wave];
+    int* runs = s_run[wave];
+    int* rdoc = s_rdoc[wave];
+    int* rstart = s_rstart[wave];
+    for (int i = lane; i < kNrGroup * TPAD; i += 64) stab[i] = kTokAbsent;
+    const int64_t n_list = plan_load(a.list_n2, 0);
+    const v4i* qdig = reinterpret_cast<const v4i*>(a.qdig);
+    const int32_t* __restrict__ plist = a.plist;
+    const uint8_t* __restrict__ codes = a.codes;
+    const int32_t* __restrict__ doc_ids = a.doc_ids;
+    unsigned* __restrict__ tokmax = a.tokmax;
+    const int64_t stride = (int64_t)gridDim.x * NW;
+    // row (token, class) of this lane in the query operand, and its shifts for the fold
+    const int rt = li / 5, rs = li - 5 * (li / 5);
+
+    for (int64_t p = (int64_t)blockIdx.x * NW + wave; p < n_list; p += stride) {  // wave-uniform
+        const v4i rec = plan_load(reinterpret_cast<const v4i*>(a.list_rec2), p);
+        const uint64_t ew = (uint64_t)(uint32_t)rec[0] | ((uint64_t)(uint32_t)rec[1] << 32);
+        const int64_t e0 = (int64_t)(ew & ((1ull << kRecLenShift) - 1));
+        const int len = (int)(ew >> kRecLenShift);  // 1 .. kMxChunk
+        const int p0 = rec[2], nt = rec[3];        // 1 .. kNarrowMax tokens
+        // the chunk's documents and (b <= 4) all its code words, loads issued together
+        int d[kMxChunk / 64];
+#pragma unroll
+        for (int j = 0; j < kMxChunk / 64; ++j) d[j] = 64 * j + lane < len ? doc_ids[e0 + 64 * j + lane] : -1;
+        unsigned w[PRELOAD ? NT : 1][NBITS];
+        if (PRELOAD) {
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const int e = 16 * t + li;
+                load_code_words<NBITS>(e < len ? codes + (e0 + e) * BYTES : nullptr, lg, w[PRELOAD ? t : 0]);
+            }
+        }
+        // runs of equal documents along the chunk (ids ascend inside a cluster); the chunk's
+        // first embedding starts a run
+        int n_runs = 0;
+#pragma unroll
+        for (int j = 0; j < kMxChunk / 64; ++j) {
+            const int last = j > 0 ? __shfl(d[j > 0 ? j - 1 : 0], 63, 64) : -1;
+            int prev = __shfl_up(d[j], 1, 64);
+            if (lane == 0) prev = last;
+            const int e = 64 * j + lane;
+            const bool in = e < len;
+            const bool start = in && (e == 0 || prev != d[j]);
+            const unsigned long long m = __ballot(start);
+            const int r = n_runs + __popcll(m & ((2ull << lane) - 1)) - 1;
+            runs[e] = in ? r : kMxChunk;
+            if (start) {
+                rdoc[r] = d[j];
+                rstart[r] = e;
+            }
+            n_runs += __popcll(m);
+        }
+        if (lane == 0) rstart[n_runs] = len;
+        wave_lds_sync();
+        const int n_tiles = (len + 15) >> 4;
+        for (int g0 = 0; g0 < nt; g0 += kNrGroup) {  // wave-uniform
+            const int ng = nt - g0 < kNrGroup ? nt - g0 : kNrGroup;
+            // query operand: row (rt, rs) takes digit plane rs - j of token g0 + rt in K segment j
+            const int trow = li < 5 * ng ? plist[2 * (p0 + g0 + rt)] : -1;
+            v4i Q[3][2];
+#pragma unroll
+            for (int j = 0; j < 3; ++j) {
+#pragma unroll
+                for (int sl = 0; sl < 2; ++sl) {
+                    const int pl = rs - j;
+                    Q[j][sl] = trow >= 0 && pl >= 0 && pl <= 2 ? qdig[(unsigned)(trow * NSLOT + (pl * 2 + sl) * 4 + lg)]
+                                                               : (v4i){0, 0, 0, 0};
+                }
+            }
+            const bool mine = lg < ng;  // this lane group folds token g0 + lg
+            const unsigned cterm = mine ? (unsigned)plist[2 * (p0 + g0 + lg) + 1] : 0u;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                if (t >= n_tiles) break;  // wave-uniform
+                unsigned wt[NBITS];
+                if (PRELOAD) {
+#pragma unroll
+                    for (int m = 0; m < NBITS; ++m) wt[m] = w[PRELOAD ? t : 0][m];
+                } else {
+                    const int e = 16 * t + li;
+                    load_code_words<NBITS>(e < len ? codes + (e0 + e) * BYTES : nullptr, lg, wt);
+                }
+                v4i W[3][2];
+                decode_weight_digits<NBITS>(wt, tab, s_wd, W);
+                v4i acc = {0, 0, 0, 0};
+#pragma unroll
+                for (int j = 0; j < 3; ++j)
+#pragma unroll
+                    for (int sl = 0; sl < 2; ++sl)
+                        acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(Q[j][sl], W[j][sl], acc, 0, 0, 0);
+                // token lg's classes s = 0..4 are rows 5 lg + s: rows 4 lg + k of this lane for
+                // k = lg + s < 4, rows of lane group lg + 1 beyond; a two-step shift by lg
+                // brings them to positions 0..4
+                const int x0 = __shfl_down(acc[0], 16, 64);
+                const int x1 = __shfl_down(acc[1], 16, 64);
+                const int x2 = __shfl_down(acc[2], 16, 64);
+                const int rr[7] = {acc[0], acc[1], acc[2], acc[3], x0, x1, x2};
+                int r1[7];  // rr shifted by lg & 1 (entry 6 is only used for lg = 2)
+#pragma unroll
+                for (int k = 0; k < 7; ++k) r1[k] = (lg & 1) && k < 6 ? rr[k + 1] : rr[k];
+                int c[5];  // then by lg & 2: c[k] = rr[k + lg]
+#pragma unroll
+                for (int k = 0; k < 5; ++k) c[k] = (lg & 2) ? r1[k + 2] : r1[k];
+                const unsigned v = mx_fold(c[0] + (1 << 17), c[1], c[2], c[3], c[4]) + cterm;
+                const int e = 16 * t + li;
+                if (mine && e < len) atomicMax(&stab[lg * TPAD + runs[e]], v);
+            }
+            wave_lds_sync();
+            // flush: one device atomic per (token, run)
+            for (int tk = 0; tk < ng; ++tk) {  // wave-uniform
+                const int64_t row = (int64_t)plist[2 * (p0 + g0 + tk)] * a.n_docs;
+                for (int r = lane; r < n_runs; r += 64) {
+                    unsigned* cell = &stab[tk * TPAD + r];
+                    const unsigned v = *cell;
+                    *cell = kTokAbsent;
+                    const int64_t o = row + rdoc[r];
+                    atomicMax(&tokmax[o], v);
+                    if (a.tokcnt) atomicAdd(&a.tokcnt[o], (unsigned)(rstart[r + 1] - rstart[r]));
+                }
+            }
+            wave_lds_sync();
+        }
+    }
+}
+
 void launch_wave_prep(const WaveArgs& a, uint32_t* ep, uint32_t last, hipStream_t s) {
     const int64_t n_tok = (int64_t)a.n_q * a.n_qtok;
     const int64_t n0 = a.n_c > a.n_q ? a.n_c : a.n_q;
@@ -562,6 +753,27 @@ void launch_scan_mx(const WaveArgs& a, hipStream_t s) {
         case 4: hipLaunchKernelGGL(k_scan_mx<4>, grid, block, 0, s, a); break;
         default: hipLaunchKernelGGL(k_scan_mx<8>, grid, block, 0, s, a); break;
     }
+}
+
+void launch_scan_narrow(const WaveArgs& a, int32_t grid, hipStream_t s) {
+    if (grid <= 0) return;
+    const dim3 g((unsigned)grid), block(kMxBlock);
+    switch (a.nbits) {
+        case 1: hipLaunchKernelGGL(k_scan_narrow<1>, g, block, 0, s, a); break;
+        case 2: hipLaunchKernelGGL(k_scan_narrow<2>, g, block, 0, s, a); break;
+        case 4: hipLaunchKernelGGL(k_scan_narrow<4>, g, block, 0, s, a); break;
+        default: hipLaunchKernelGGL(k_scan_narrow<8>, g, block, 0, s, a); break;
+    }
+}
+
+int scan_narrow_blocks_per_cu(int nbits) {
+    int n = 0;
+    const void* k = nbits == 1   ? (const void*)k_scan_narrow<1>
+                    : nbits == 2 ? (const void*)k_scan_narrow<2>
+                    : nbits == 4 ? (const void*)k_scan_narrow<4>
+                                 : (const void*)k_scan_narrow<8>;
+    (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, kMxBlock, 0);
+    return n > 0 ? n : 1;
 }
 
 int scan_mx_blocks_per_cu(int nbits) {

@@ -25,7 +25,7 @@ EXPORTS = (
     "warp_fixed_point_bits", "warp_last_error", "warp_index_load", "warp_index_load_device",
     "warp_index_free", "warp_index_info", "warp_search", "warp_search_async", "warp_index_sync",
     "warp_search_debug", "warp_centroid_filter_scores", "warp_set_timing", "warp_stage_timings",
-    "warp_t_prime_policy", "warp_set_scoring", "warp_build_index",
+    "warp_t_prime_policy", "warp_set_scoring", "warp_build_index", "warp_search_noalloc",
 )
 
 
@@ -57,6 +57,7 @@ def _load() -> ctypes.CDLL:
         "warp_index_info": ([P, P, P, P, P], ctypes.c_int),
         "warp_search": ([P, P, i32, i32, i32, i64, i32, P, P, P], ctypes.c_int),
         "warp_search_async": ([P, P, i32, i32, i32, i64, i32, P, P, P, P, P], ctypes.c_int),
+        "warp_search_noalloc": ([P, P, i32, i32, i32, i64, i32, P, P, P, P, P], ctypes.c_int),
         "warp_index_sync": ([P, P], ctypes.c_int),
         "warp_search_debug": ([P, P, i32, i32, i32, i64, i32, P, P, P, P, P, P, P, P], ctypes.c_int),
         "warp_centroid_filter_scores": ([P, P, i32, P], ctypes.c_int),
@@ -245,6 +246,28 @@ class Index:
         s = stream if stream is not None else torch.cuda.current_stream(dev)
         _check(lib.warp_search_async(self._h, _ptr(queries), nq, nt, nprobe, int(t_prime), k, _ptr(ids),
                                      _ptr(scores), _ptr(counts), _ptr(fixed), ctypes.c_void_p(s.cuda_stream)))
+        return out
+
+    def search_noalloc(self, queries, nprobe: int, t_prime: int, k: int, out=None, stream=None):
+        """As search_async through warp_search_noalloc: the library allocates nothing (its
+        scratch is a static 256 MiB device array per GPU). `out` as in search_async; the
+        output tensors are allocated here by torch only when `out` is None."""
+        import torch
+
+        if not queries.is_cuda or queries.dtype != torch.float32 or queries.dim() != 3:
+            raise ValueError("queries must be a float32 device tensor [n_queries, n_qtok, 128]")
+        queries = queries.contiguous()
+        nq, nt, _ = queries.shape
+        dev = queries.device
+        if out is None:
+            out = (torch.empty((nq, k), dtype=torch.int32, device=dev),
+                   torch.empty((nq, k), dtype=torch.float32, device=dev),
+                   torch.empty(nq, dtype=torch.int32, device=dev),
+                   torch.empty((nq, k), dtype=torch.int64, device=dev))
+        ids, scores, counts, fixed = out
+        s = stream if stream is not None else torch.cuda.current_stream(dev)
+        _check(lib.warp_search_noalloc(self._h, _ptr(queries), nq, nt, nprobe, int(t_prime), k, _ptr(ids),
+                                       _ptr(scores), _ptr(counts), _ptr(fixed), ctypes.c_void_p(s.cuda_stream)))
         return out
 
     def sync(self, stream=None) -> None:
