@@ -44,7 +44,8 @@ constexpr int kMxBlock = 256;
 // The persistent scan grid takes its items in batches of kScanBatch consecutive items:
 // workgroup b starts with batch b, and every later batch comes from a device counter.
 constexpr int kScanBatch = 4;
-// Chunks probed by at most kNarrowMax tokens of a wave take the narrow scan (k_scan_narrow):
+// Chunks probed by at most kNarrowMax tokens of a wave (by default; WARP_NARROW_MAX) take the
+// narrow scan (k_scan_narrow):
 // one wave per chunk, with groups of kNrGroup tokens whose five digit classes are the rows
 // of one matrix-core tile, so a 16-embedding tile of a group costs 6 int8 MFMAs instead of 18.
 constexpr int kNarrowMax = 6;
@@ -123,6 +124,7 @@ struct WaveArgs {
     uint32_t* dbg_bitmap;       // [n_q][ceil(n_docs / 32)] or null
     int64_t* dbg_scored;        // [n_q] or null
     int32_t scan_grid;          // persistent workgroups of the residual scan
+    int32_t narrow_max;         // chunks probed by 1..narrow_max tokens take the narrow scan
     int32_t topk_list_cap;      // at most kTopkListCap; the top-k visits every block when more pass
 };
 

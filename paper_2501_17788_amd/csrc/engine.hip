@@ -582,6 +582,14 @@ int32_t topk_list_cap() {
     return (int32_t)(v < 0 ? 0 : (v > kTopkListCap ? kTopkListCap : v));
 }
 
+// Largest number of probing tokens for which a chunk takes the narrow scan: kNarrowMax, or
+// WARP_NARROW_MAX (0 sends every chunk to the wide scan; results do not depend on it).
+int32_t narrow_max() {
+    int64_t v = kNarrowMax;
+    if (const char* s = std::getenv("WARP_NARROW_MAX")) v = std::atoll(s);
+    return (int32_t)(v < 0 ? 0 : (v > 4096 ? 4096 : v));
+}
+
 hipEvent_t take_event(warp_index* idx) {
     if (!idx->ev_pool.empty()) {
         hipEvent_t e = idx->ev_pool.back();
@@ -722,6 +730,7 @@ void launch_wave(warp_index* idx, const WaveScratch& w, const float* dq, int32_t
     a.qdig = w.qdig;
     a.scan_grid = idx->scan_grid;
     a.topk_list_cap = topk_list_cap();
+    a.narrow_max = narrow_max();
 
     const bool epochs = w.q_epoch != nullptr;
     hipEvent_t ev[kStages + 1] = {};

@@ -80,15 +80,15 @@ __device__ void pair_offsets(const WaveArgs& a, int64_t* ws) {
     if (tid == 0) a.pair_start[n_c] = (int32_t)carry;
 }
 
-// Probed chunks in the index's chunk order: a chunk probed by more than kNarrowMax tokens
+// Probed chunks in the index's chunk order: a chunk probed by more than narrow_max tokens
 // goes to the wide scan with its items (token groups of its cluster), one probed by
-// 1..kNarrowMax tokens to the narrow scan.
+// 1..narrow_max tokens to the narrow scan.
 __device__ __forceinline__ void chunk_items(const WaveArgs& a, int64_t j, int64_t& flag, int64_t& items,
                                             int64_t& narrow) {
     flag = items = narrow = 0;
     if (j < a.n_chunks) {
         const int32_t nt = a.ccount[a.chunk_c[j]];
-        if (nt > kNarrowMax) {
+        if (nt > a.narrow_max) {
             items = (nt + kMxGroup - 1) / kMxGroup;
             flag = 1;
         } else {

@@ -586,7 +586,6 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
     constexpr int NT = kMxChunk / 16;  // tiles of a chunk
     constexpr int NSLOT = 24;          // 16-byte query digit slots of a token
     constexpr int TPAD = kMxChunk + 4;
-    constexpr bool PRELOAD = NBITS <= 4;  // every tile's code words in registers at once
     static_assert(kMxChunk % 64 == 0 && kMxChunk <= 4 * 64, "four rounds of the run pass");
     static_assert(5 * kNrGroup <= 16, "rows of a group's tile");
     __shared__ unsigned s_tab[NW][kNrGroup * TPAD];  // (token of the group, run) maxima
@@ -619,24 +618,47 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
     // row (token, class) of this lane in the query operand, and its shifts for the fold
     const int rt = li / 5, rs = li - 5 * (li / 5);
 
-    for (int64_t p = (int64_t)blockIdx.x * NW + wave; p < n_list; p += stride) {  // wave-uniform
-        const v4i rec = plan_load(reinterpret_cast<const v4i*>(a.list_rec2), p);
+    // The chunks of this wave: p, p + stride, ... While a chunk is scored, the next one's
+    // documents are in flight; inside a chunk, the code words of tile t + 2 are loaded while
+    // tile t is scored (a rolled loop keeps the registers few and the waves many).
+    struct NrChunk {
+        int64_t e0;
+        int len, p0, nt;  // embeddings (1 .. kMxChunk), first pair, probing tokens (1 .. narrow_max)
+    };
+    auto chunk_at = [&](int64_t q) {
+        const v4i rec = plan_load(reinterpret_cast<const v4i*>(a.list_rec2), q);
         const uint64_t ew = (uint64_t)(uint32_t)rec[0] | ((uint64_t)(uint32_t)rec[1] << 32);
-        const int64_t e0 = (int64_t)(ew & ((1ull << kRecLenShift) - 1));
-        const int len = (int)(ew >> kRecLenShift);  // 1 .. kMxChunk
-        const int p0 = rec[2], nt = rec[3];        // 1 .. kNarrowMax tokens
-        // the chunk's documents and (b <= 4) all its code words, loads issued together
-        int d[kMxChunk / 64];
+        NrChunk c;
+        c.e0 = (int64_t)(ew & ((1ull << kRecLenShift) - 1));
+        c.len = (int)(ew >> kRecLenShift);
+        c.p0 = rec[2];
+        c.nt = rec[3];
+        return c;
+    };
+    auto load_docs = [&](const NrChunk& c, int (&dd)[kMxChunk / 64]) {
 #pragma unroll
-        for (int j = 0; j < kMxChunk / 64; ++j) d[j] = 64 * j + lane < len ? doc_ids[e0 + 64 * j + lane] : -1;
-        unsigned w[PRELOAD ? NT : 1][NBITS];
-        if (PRELOAD) {
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                const int e = 16 * t + li;
-                load_code_words<NBITS>(e < len ? codes + (e0 + e) * BYTES : nullptr, lg, w[PRELOAD ? t : 0]);
-            }
+        for (int j = 0; j < kMxChunk / 64; ++j) dd[j] = 64 * j + lane < c.len ? doc_ids[c.e0 + 64 * j + lane] : -1;
+    };
+    int64_t p = (int64_t)blockIdx.x * NW + wave;
+    if (p >= n_list) return;  // wave-uniform; no barrier follows
+    NrChunk cur = chunk_at(p);
+    int d[kMxChunk / 64];
+    load_docs(cur, d);
+    for (;;) {
+        const int64_t pn = p + stride;
+        const bool has_next = pn < n_list;  // wave-uniform
+        NrChunk nx = cur;
+        int dn[kMxChunk / 64] = {};
+        if (has_next) {
+            nx = chunk_at(pn);
+            load_docs(nx, dn);
         }
+        const int64_t e0 = cur.e0;
+        const int len = cur.len, p0 = cur.p0, nt = cur.nt;
+        auto tile_row = [&](int t) -> const uint8_t* {
+            const int e = 16 * t + li;
+            return e < len ? codes + (e0 + e) * BYTES : nullptr;
+        };
         // runs of equal documents along the chunk (ids ascend inside a cluster); the chunk's
         // first embedding starts a run
         int n_runs = 0;
@@ -676,17 +698,19 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
             }
             const bool mine = lg < ng;  // this lane group folds token g0 + lg
             const unsigned cterm = mine ? (unsigned)plist[2 * (p0 + g0 + lg) + 1] : 0u;
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                if (t >= n_tiles) break;  // wave-uniform
+            const int mytok = mine ? plist[2 * (p0 + g0 + lg)] : 0;  // its wave token (the flush's row)
+            unsigned c0[NBITS], c1[NBITS];
+            load_code_words<NBITS>(tile_row(0), lg, c0);
+            load_code_words<NBITS>(tile_row(1), lg, c1);
+#pragma unroll 1
+            for (int t = 0; t < n_tiles; ++t) {  // wave-uniform
                 unsigned wt[NBITS];
-                if (PRELOAD) {
 #pragma unroll
-                    for (int m = 0; m < NBITS; ++m) wt[m] = w[PRELOAD ? t : 0][m];
-                } else {
-                    const int e = 16 * t + li;
-                    load_code_words<NBITS>(e < len ? codes + (e0 + e) * BYTES : nullptr, lg, wt);
+                for (int m = 0; m < NBITS; ++m) {
+                    wt[m] = c0[m];
+                    c0[m] = c1[m];
                 }
+                load_code_words<NBITS>(tile_row(t + 2), lg, c1);
                 v4i W[3][2];
                 decode_weight_digits<NBITS>(wt, tab, s_wd, W);
                 v4i acc = {0, 0, 0, 0};
@@ -696,26 +720,31 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
                     for (int sl = 0; sl < 2; ++sl)
                         acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(Q[j][sl], W[j][sl], acc, 0, 0, 0);
                 // token lg's classes s = 0..4 are rows 5 lg + s: rows 4 lg + k of this lane for
-                // k = lg + s < 4, rows of lane group lg + 1 beyond; a two-step shift by lg
-                // brings them to positions 0..4
+                // k = lg + s < 4, rows of lane group lg + 1 beyond
                 const int x0 = __shfl_down(acc[0], 16, 64);
-                const int x1 = __shfl_down(acc[1], 16, 64);
-                const int x2 = __shfl_down(acc[2], 16, 64);
-                const int rr[7] = {acc[0], acc[1], acc[2], acc[3], x0, x1, x2};
-                int r1[7];  // rr shifted by lg & 1 (entry 6 is only used for lg = 2)
-#pragma unroll
-                for (int k = 0; k < 7; ++k) r1[k] = (lg & 1) && k < 6 ? rr[k + 1] : rr[k];
-                int c[5];  // then by lg & 2: c[k] = rr[k + lg]
-#pragma unroll
-                for (int k = 0; k < 5; ++k) c[k] = (lg & 2) ? r1[k + 2] : r1[k];
-                const unsigned v = mx_fold(c[0] + (1 << 17), c[1], c[2], c[3], c[4]) + cterm;
+                unsigned v;
+                if (ng == 1) {  // wave-uniform: only lane group 0 folds, rows 0..3 here and row 4
+                    v = mx_fold(acc[0] + (1 << 17), acc[1], acc[2], acc[3], x0) + cterm;
+                } else {
+                    // with r = (acc[0..3], x0, x1, x2), class s of token lg is r[s + lg]: shift
+                    // by lg & 1, then by lg & 2 (named values, not an array: a select between
+                    // array elements may become an indexed load from private memory)
+                    const int x1 = __shfl_down(acc[1], 16, 64);
+                    const int x2 = __shfl_down(acc[2], 16, 64);
+                    const bool o1 = (lg & 1) != 0, o2 = (lg & 2) != 0;
+                    const int u0 = o1 ? acc[1] : acc[0], u1 = o1 ? acc[2] : acc[1], u2 = o1 ? acc[3] : acc[2];
+                    const int u3 = o1 ? x0 : acc[3], u4 = o1 ? x1 : x0, u5 = o1 ? x2 : x1, u6 = x2;
+                    const int c0s = o2 ? u2 : u0, c1s = o2 ? u3 : u1, c2s = o2 ? u4 : u2;
+                    const int c3s = o2 ? u5 : u3, c4s = o2 ? u6 : u4;
+                    v = mx_fold(c0s + (1 << 17), c1s, c2s, c3s, c4s) + cterm;
+                }
                 const int e = 16 * t + li;
                 if (mine && e < len) atomicMax(&stab[lg * TPAD + runs[e]], v);
             }
             wave_lds_sync();
             // flush: one device atomic per (token, run)
             for (int tk = 0; tk < ng; ++tk) {  // wave-uniform
-                const int64_t row = (int64_t)plist[2 * (p0 + g0 + tk)] * a.n_docs;
+                const int64_t row = (int64_t)__builtin_amdgcn_readlane(mytok, 16 * tk) * a.n_docs;
                 for (int r = lane; r < n_runs; r += 64) {
                     unsigned* cell = &stab[tk * TPAD + r];
                     const unsigned v = *cell;
@@ -727,6 +756,11 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
             }
             wave_lds_sync();
         }
+        if (!has_next) break;
+        p = pn;
+        cur = nx;
+#pragma unroll
+        for (int j = 0; j < kMxChunk / 64; ++j) d[j] = dn[j];
     }
 }
 

@@ -115,6 +115,24 @@ def test_random_small(case):
     run_both(data, label=f"random seed {seed}")
 
 
+@pytest.mark.parametrize("narrow_max", ["0", "3", "4096"], ids=["all-wide", "narrow3", "all-narrow"])
+def test_wide_and_narrow_scans_agree(narrow_max, monkeypatch):
+    """Chunks probed by few tokens take the narrow scan (one wave per chunk, groups of three
+    tokens per matrix-core tile), the others the wide one; WARP_NARROW_MAX moves the split.
+    Every split gives the oracle's results: all chunks wide, a three-token split, and every
+    chunk narrow (up to 32 tokens in eleven groups), in both scoring modes and at b = 1, 2, 4, 8."""
+    monkeypatch.setenv("WARP_NARROW_MAX", narrow_max)
+    for case in (CASES[3], CASES[6], CASES[10], CASES[11], CASES[12]):
+        seed, n_c, n_docs, max_len, nbits, nq, nt, nprobe, tp, k = case
+        wl = synth.random_small_workload(seed, n_centroids=n_c, n_docs=n_docs, max_len=max_len, nbits=nbits,
+                                         n_queries=nq, n_qtok=nt, nprobe=nprobe, t_prime=tp, k=k)
+        run_both(synth.make_index(wl, workers=1), label=f"narrow_max={narrow_max} seed {seed}")
+    wl = synth.with_overrides(synth.WORKLOADS["tiny"], n_queries=6, nbits=2, nprobe=24, k=40)
+    data = synth.make_index(wl, workers=1)
+    run_both(data, label=f"narrow_max={narrow_max} tiny b=2")
+    run_both(data, label=f"narrow_max={narrow_max} tiny b=2 literal", literal=True)
+
+
 def test_empty_clusters_and_ragged_tiles():
     # many centroids, few embeddings: most clusters are empty; tails of every tile are ragged
     wl = synth.random_small_workload(11, n_centroids=1024, n_docs=700, max_len=9, nbits=4, n_queries=6,
