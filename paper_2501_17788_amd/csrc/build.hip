@@ -18,8 +18,6 @@
 //   * codes: the number of cutoffs <= the fp32 residual component, packed with
 //     the first dimension in the most significant bits; embeddings ordered by
 //     cluster, then by input order (a stable sort).
-#include <hipcub/hipcub.hpp>
-
 #include <algorithm>
 #include <cmath>
 #include <string>
@@ -264,22 +262,6 @@ void launch_count_clusters(const int32_t* assign, int64_t n, unsigned long long*
 
 void launch_iota64(int64_t* out, int64_t n, hipStream_t s) {
     if (n > 0) hipLaunchKernelGGL(k_iota64, dim3(blocks_for(n, 256)), dim3(256), 0, s, out, n);
-}
-
-// Device-wide primitives (hipCUB). With temp == nullptr they only set *temp_bytes.
-hipError_t sort_floats(void* temp, size_t* temp_bytes, const float* in, float* out, int64_t n, hipStream_t s) {
-    return hipcub::DeviceRadixSort::SortKeys(temp, *temp_bytes, in, out, (int)n, 0, 32, s);
-}
-
-hipError_t sort_by_cluster(void* temp, size_t* temp_bytes, const int32_t* keys_in, int32_t* keys_out,
-                           const int64_t* vals_in, int64_t* vals_out, int64_t n, int end_bit, hipStream_t s) {
-    return hipcub::DeviceRadixSort::SortPairs(temp, *temp_bytes, keys_in, keys_out, vals_in, vals_out, (int)n, 0,
-                                              end_bit, s);
-}
-
-hipError_t exclusive_sum_u64(void* temp, size_t* temp_bytes, const unsigned long long* in, int64_t* out,
-                             int64_t n, hipStream_t s) {
-    return hipcub::DeviceScan::ExclusiveSum(temp, *temp_bytes, in, out, (int)n, s);
 }
 
 }  // namespace warp

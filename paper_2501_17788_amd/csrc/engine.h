@@ -44,11 +44,12 @@ constexpr int kMxBlock = 256;
 // The persistent scan grid takes its items in batches of kScanBatch consecutive items:
 // workgroup b starts with batch b, and every later batch comes from a device counter.
 constexpr int kScanBatch = 4;
-// Chunks probed by at most kNarrowMax tokens of a wave (by default; WARP_NARROW_MAX) take the
-// narrow scan (k_scan_narrow):
+// In waves of at most kNarrowWave queries, chunks probed by at most kNarrowMax tokens (by
+// default; WARP_NARROW_MAX) take the narrow scan (k_scan_narrow):
 // one wave per chunk, with groups of kNrGroup tokens whose five digit classes are the rows
 // of one matrix-core tile, so a 16-embedding tile of a group costs 6 int8 MFMAs instead of 18.
-constexpr int kNarrowMax = 6;
+constexpr int kNarrowMax = 3;
+constexpr int kNarrowWave = 16;  // waves of more queries send every chunk to the wide scan
 constexpr int kNrGroup = 3;
 constexpr int kQdigBytes = 3 * kDim;  // three base-256 digit planes of a query token
 // Largest bucket weight magnitude: Q(omega) = round(omega * 2^22) must have three
@@ -107,8 +108,8 @@ struct WaveArgs {
                                 // embedding (x, y: low and high words; the chunk's length in the
                                 // top bits of y), first pair of the cluster (z), probing tokens (w)
     int64_t* list_item;         // [n_chunks + 1] exclusive prefix of their items; list_item[*list_n] = total
-    int64_t* list_n;            // [1] number of probed chunks of the wide scan (more than kNarrowMax tokens)
-    int4* list_rec2;            // [n_chunks] the probed chunks of the narrow scan (1..kNarrowMax tokens),
+    int64_t* list_n;            // [1] number of probed chunks of the wide scan (more than narrow_max tokens)
+    int4* list_rec2;            // [n_chunks] the probed chunks of the narrow scan (1..narrow_max tokens),
                                 // in the same order, with records like list_rec
     int64_t* list_n2;           // [1] their number
     int64_t* cblk;              // [3 * ceil(n_chunks / kPlanBlock)] block sums: wide chunks, their items,

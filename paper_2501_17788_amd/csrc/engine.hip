@@ -582,10 +582,14 @@ int32_t topk_list_cap() {
     return (int32_t)(v < 0 ? 0 : (v > kTopkListCap ? kTopkListCap : v));
 }
 
-// Largest number of probing tokens for which a chunk takes the narrow scan: kNarrowMax, or
-// WARP_NARROW_MAX (0 sends every chunk to the wide scan; results do not depend on it).
-int32_t narrow_max() {
-    int64_t v = kNarrowMax;
+// Largest number of probing tokens for which a chunk of a wave of nq queries takes the narrow
+// scan: kNarrowMax for waves of at most kNarrowWave queries, where most probed chunks have few
+// probing tokens and the wide scan's 16-token tiles would be mostly padding; 0 (every chunk
+// wide) for larger waves, where the narrow scan measured slower on the same chunks.
+// WARP_NARROW_MAX sets it for every wave (0 sends every chunk to the wide scan); results do
+// not depend on it.
+int32_t narrow_max(int32_t nq) {
+    int64_t v = nq <= kNarrowWave ? kNarrowMax : 0;
     if (const char* s = std::getenv("WARP_NARROW_MAX")) v = std::atoll(s);
     return (int32_t)(v < 0 ? 0 : (v > 4096 ? 4096 : v));
 }
@@ -730,7 +734,7 @@ void launch_wave(warp_index* idx, const WaveScratch& w, const float* dq, int32_t
     a.qdig = w.qdig;
     a.scan_grid = idx->scan_grid;
     a.topk_list_cap = topk_list_cap();
-    a.narrow_max = narrow_max();
+    a.narrow_max = narrow_max(nq);
 
     const bool epochs = w.q_epoch != nullptr;
     hipEvent_t ev[kStages + 1] = {};

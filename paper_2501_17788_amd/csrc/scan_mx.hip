@@ -568,7 +568,7 @@ __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_wave_barrier();
 }
 
-// Narrow scan: the chunks probed by 1..kNarrowMax tokens of the wave (Sections 4.4 and 4.5,
+// Narrow scan: the chunks probed by 1..narrow_max tokens of the wave (Sections 4.4 and 4.5,
 // the same arithmetic as k_scan_mx). One wave takes one chunk at a time, with no workgroup
 // barrier: it numbers the chunk's runs of equal documents, then scores the chunk's 16-embedding
 // tiles against groups of up to kNrGroup = 3 tokens. In a group's matrix-core tile the rows

@@ -50,6 +50,19 @@ def test_build_matches_oracle(nbits):
     _build_both(X, docs, len(lens), C0, sample, 4, nbits, 1500, label=f"b={nbits}")
 
 
+def test_build_many_tiles_and_radix_passes():
+    """600 centroids (two 8-bit passes of the stable sort by cluster) over about 60k tokens
+    (15 tiles of 4,096 keys), quantiles over 20,000 tokens (2.56M residual components: four
+    passes over 625 tiles): the hand-written sorts and prefix sums at several tiles."""
+    import paper_2501_17788_amd as w
+
+    data, X, docs, lens = _inputs(44, n_docs=3000, max_len=40, n_c=600)
+    sample = w.sample_passages(lens, c=20.0, seed=5)
+    C0 = w.initial_centroids(X, sample, 600, seed=6)
+    assert len(X) > 8 * 4096
+    _build_both(X, docs, len(lens), C0, sample, 2, 2, 20000, label="600 centroids, 20k quantile tokens")
+
+
 def test_build_edge_cases():
     import paper_2501_17788_amd as w
 
