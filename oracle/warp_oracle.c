@@ -309,7 +309,14 @@ int oracle_build_index(const float* tokens, const int32_t* token_docs, int64_t n
     if (n < 1 || n_c < 1 || n_sample < 1 || iterations < 0 || n_quant < 1 || n_quant > n) return -1;
     if (nbits != 1 && nbits != 2 && nbits != 4 && nbits != 8) return -1;
     if (n_threads > 0) omp_set_num_threads(n_threads);
-    memcpy(centroids, init, sizeof(float) * (size_t)n_c * D);
+    /* the starting centroids: the caller's starting vectors, normalised */
+    for (int32_t c = 0; c < n_c; ++c) {
+        double ss = 0.0;
+        for (int d = 0; d < D; ++d) ss += (double)init[(int64_t)c * D + d] * (double)init[(int64_t)c * D + d];
+        if (!(ss > 0.0) || !isfinite(ss)) return -1;
+        double norm = sqrt(ss);
+        for (int d = 0; d < D; ++d) centroids[(int64_t)c * D + d] = (float)((double)init[(int64_t)c * D + d] / norm);
+    }
 
     /* k-means on the sample */
     int32_t* sa = (int32_t*)malloc(sizeof(int32_t) * (size_t)n_sample);

@@ -71,6 +71,9 @@ int oracle_search(const float* centroids, int32_t n_c, int32_t dim,
                   int64_t* doc_fixed, int32_t n_threads);
 
 /* Section 4.1 (index construction), written out plainly:
+ *   start       = every starting vector init[c] normalised: (float)(init[c][d] / ||init[c]||), the
+ *                 norm in fp64 (sum of squares in dimension order, IEEE sqrt); rows must be
+ *                 finite and nonzero;
  *   assign(x)   = argmax_c sum_d (double)C[c][d] * (double)x[d] (dimension order), lowest c on ties;
  *   k-means     = `iterations` times: assign the sample tokens, then replace every centroid that
  *                 has tokens by normalise(sum over them of round(x * 2^30)) (int64 sums, fp64

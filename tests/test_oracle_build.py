@@ -1,5 +1,7 @@
 """Pins of the oracle's index construction (Section 4.1) against numpy and closed forms.
 
+B0  the starting centroids are the starting vectors normalised (numpy fp64, sequential sum of
+    squares), and a zero vector is rejected;
 B1  assignment is the fp64 argmax over centroids (numpy matrix product);
 B2  one k-means step gives the normalised mean direction of each centroid's tokens
     (numpy, float64), and keeps centroids without tokens;
@@ -37,6 +39,21 @@ def _init(X, sample, n_c, seed=1):
 
 def _objective(X, C):
     return float((X.astype(np.float64) @ C.astype(np.float64).T).max(axis=1).sum())
+
+
+def test_b0_starting_centroids_are_normalised_inputs():
+    X, docs, _ = _inputs(3)
+    sample = np.arange(0, len(X), 4)
+    rng = np.random.default_rng(9)
+    V = (rng.standard_normal((20, 128)) * rng.uniform(0.1, 3.0, (20, 1))).astype(np.float32)
+    r = oracle.build_index(X, docs, V, sample, iterations=0, nbits=2, n_quant=100)
+    V64 = V.astype(np.float64)
+    norm = np.sqrt(np.cumsum(V64 * V64, axis=1)[:, -1])  # sum of squares in dimension order
+    np.testing.assert_array_equal(r["centroids"], (V64 / norm[:, None]).astype(np.float32))
+    assert np.all(np.abs(np.linalg.norm(r["centroids"].astype(np.float64), axis=1) - 1) < 1e-6)
+    V[3] = 0
+    with pytest.raises(ValueError):
+        oracle.build_index(X, docs, V, sample, iterations=0, nbits=2, n_quant=100)
 
 
 def test_b1_assignment_is_argmax():
