@@ -143,9 +143,13 @@ int warp_index_info(const warp_index* idx, int32_t* n_centroids, int64_t* n_embe
  *   queries      [n_queries][n_qtok][dim] fp32 host, each token of norm <= 1 + 1e-3
  *   n_queries    >= 1
  *   n_qtok       1..32 (query_maxlen = 32); every token takes part in the sum
- *   nprobe       1..n_centroids; above 256: WARP_ENOTSUP
+ *   nprobe       1..n_centroids. Up to 256 the selection rescores only the
+ *                centroids near its boundaries; above, it sorts every
+ *                (token, centroid) score of a wave (same results, slower;
+ *                WARP_ENOTSUP if n_qtok * n_centroids > 2^31)
  *   t_prime      >= 0, in embeddings
- *   k            1..4096
+ *   k            >= 1. Up to 4096 the top-k gathers the best keys in LDS;
+ *                above, it sorts every document key of a query (same results)
  *   out_doc_ids  [n_queries][k] caller-owned host; -1 past the result count
  *   out_scores   [n_queries][k] caller-owned host; -inf past the result count
  *   out_counts   [n_queries] host or NULL: min(k, number of candidate documents)
@@ -182,8 +186,9 @@ int warp_search_async(warp_index* idx, const float* queries, int32_t n_queries, 
  * that GPU until the process ends. A search takes waves of as many queries as
  * the array holds; if one query does not fit (roughly 4 * n_qtok * n_docs +
  * 2 * n_qtok * n_centroids + 8 * n_docs bytes, e.g. about 17 MB for 100k
- * documents, 1.1 GB for 8.8M) it fails with WARP_ENOMEM before enqueuing
- * anything. Every call on a GPU shares that GPU's array, whichever index it
+ * documents, 1.1 GB for 8.8M; nprobe above 256 adds about 57 * n_qtok *
+ * n_centroids bytes, k above 4096 about 25 * n_docs) it fails with WARP_ENOMEM
+ * before enqueuing anything. Every call on a GPU shares that GPU's array, whichever index it
  * searches, and finds what the last call left there (the call clears what must
  * start at zero): calls that overlap on one GPU race, so enqueue them on one
  * stream or wait for each before the next. The index's own scratch is not
@@ -226,7 +231,9 @@ int warp_centroid_filter_scores(warp_index* idx, const float* queries, int32_t n
  *
  *   tokens           [n_tokens][128] fp32, finite, norm <= 1 + 1e-3
  *   token_docs       [n_tokens] document id of each token, in [0, n_docs)
- *   init_centroids   [n_centroids][128] fp32 starting centroids, unit norm
+ *   init_centroids   [n_centroids][128] fp32 starting vectors, finite and nonzero; each is
+ *                    normalised (fp64 norm, sum of squares in dimension order) into a
+ *                    starting centroid
  *   sample_ids       [n_sample] token ids (in [0, n_tokens)) used by k-means; Section
  *                    4.1 samples passages in proportion to the square root of the
  *                    collection size (the caller's choice)

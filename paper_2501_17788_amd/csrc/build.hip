@@ -142,6 +142,18 @@ __global__ void k_kmeans_normalize(const unsigned long long* __restrict__ sums,
     for (int d = 0; d < kDim; ++d) cen[(int64_t)c * kDim + d] = (float)((double)(long long)s[d] / norm);
 }
 
+// rows of 128 fp32 values scaled to unit norm: (float)(x_d / ||x||), the norm in fp64 (sum
+// of squares in dimension order, IEEE sqrt); the rows were checked to be finite and nonzero
+__global__ void k_normalize_rows(float* __restrict__ rows, int32_t n) {
+    const int c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= n) return;
+    float* r = rows + (int64_t)c * kDim;
+    double ss = 0.0;
+    for (int d = 0; d < kDim; ++d) ss += (double)r[d] * (double)r[d];
+    const double norm = __builtin_sqrt(ss);
+    for (int d = 0; d < kDim; ++d) r[d] = (float)((double)r[d] / norm);
+}
+
 // residual components of tokens [0, n): x - C[assign]
 __global__ void k_residuals(const float* __restrict__ x, const int32_t* __restrict__ assign, int64_t n,
                             const float* __restrict__ cen, float* __restrict__ out) {
@@ -230,6 +242,10 @@ void launch_kmeans_accum(const float* xs, const int32_t* assign, int64_t n, unsi
 void launch_kmeans_normalize(const unsigned long long* sums, const unsigned long long* counts, int32_t n_c,
                              float* cen, hipStream_t s) {
     hipLaunchKernelGGL(k_kmeans_normalize, dim3(blocks_for(n_c, 64)), dim3(64), 0, s, sums, counts, n_c, cen);
+}
+
+void launch_normalize_rows(float* rows, int32_t n, hipStream_t s) {
+    if (n > 0) hipLaunchKernelGGL(k_normalize_rows, dim3(blocks_for(n, 64)), dim3(64), 0, s, rows, n);
 }
 
 void launch_residuals(const float* x, const int32_t* assign, int64_t n, const float* cen, float* out,

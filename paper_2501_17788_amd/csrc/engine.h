@@ -156,6 +156,12 @@ void launch_scan_narrow(const WaveArgs& a, int32_t grid, hipStream_t s);
 int scan_narrow_blocks_per_cu(int nbits);
 void launch_fold(const WaveArgs& a, hipStream_t s);
 void launch_topk(const WaveArgs& a, hipStream_t s);
+// exact whole-list paths for n_probe > kMaxProbe and k > kMaxK (device radix sorts); the
+// scratch holds the bytes the *_bytes functions give
+size_t select_full_bytes(int64_t n_tok, int32_t n_c);
+hipError_t launch_select_full(const WaveArgs& a, void* scratch, hipStream_t s);
+size_t topk_full_bytes(int32_t n_docs);
+hipError_t launch_topk_full(const WaveArgs& a, void* scratch, hipStream_t s);
 void launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
 void launch_zero_cells(uint32_t* p, int64_t n, hipStream_t s);  // streaming stores
 void launch_check_docs(const int32_t* ids, int64_t n, int32_t n_docs, int32_t* err, hipStream_t s);
@@ -171,6 +177,7 @@ void launch_kmeans_accum(const float* xs, const int32_t* assign, int64_t n, unsi
                          unsigned long long* counts, hipStream_t s);
 void launch_kmeans_normalize(const unsigned long long* sums, const unsigned long long* counts, int32_t n_c,
                              float* cen, hipStream_t s);
+void launch_normalize_rows(float* rows, int32_t n, hipStream_t s);
 void launch_residuals(const float* x, const int32_t* assign, int64_t n, const float* cen, float* out,
                       hipStream_t s);
 void launch_pick_quantiles(const float* sorted, int64_t n, int32_t nbits, float* cutoffs, float* weights,

@@ -94,6 +94,7 @@ struct warp_index {
     DevBuf list_rec, list_item, cblk;  // the wave's probed chunks (see WaveArgs)
     DevBuf list_rec2;                  // the wave's probed chunks of the narrow scan
     DevBuf scan_queue;
+    DevBuf full_sel, full_topk;  // sort scratch of n_probe > kMaxProbe and of k > kMaxK
     int32_t scoring = WARP_SCORING_PAPER;
     DevBuf tokcnt, doc_len;    // Eq.-1-literal scoring only
     int64_t tokcnt_ready = 0;  // leading elements of tokcnt holding 0
@@ -226,7 +227,8 @@ void destroy_index(warp_index* idx) {
         for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_pref, &idx->m_fixed, &idx->tokmax,
                           &idx->q_epoch, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount,
                           &idx->cursor, &idx->pair_start, &idx->plist, &idx->qdig, &idx->list_rec,
-                          &idx->list_item, &idx->cblk, &idx->list_rec2, &idx->scan_queue, &idx->st_q,
+                          &idx->list_item, &idx->cblk, &idx->list_rec2, &idx->scan_queue, &idx->full_sel,
+                          &idx->full_topk, &idx->st_q,
                           &idx->st_ids,
                           &idx->st_scores, &idx->st_fixed, &idx->st_counts, &idx->st_sel, &idx->st_m,
                           &idx->st_bitmap, &idx->st_scored})
@@ -307,10 +309,8 @@ int validate_search(const warp_index* idx, const void* queries, int32_t n_querie
     if (n_qtok < 1 || n_qtok > kMaxQtok) return fail(WARP_EINVAL, "n_qtok must be in [1, 32] (got %d)", n_qtok);
     if (nprobe < 1 || nprobe > idx->n_c)
         return fail(WARP_EINVAL, "nprobe must be in [1, n_centroids] (got %d)", nprobe);
-    if (nprobe > kMaxProbe) return fail(WARP_ENOTSUP, "nprobe above %d is not implemented", kMaxProbe);
     if (t_prime < 0) return fail(WARP_EINVAL, "t_prime must be >= 0");
     if (k < 1) return fail(WARP_EINVAL, "k must be >= 1 (got %d)", k);
-    if (k > kMaxK) return fail(WARP_ENOTSUP, "k above %d is not implemented", kMaxK);
     return WARP_OK;
 }
 
@@ -479,7 +479,7 @@ void clear_slots(warp_index* idx, hipStream_t s) {
 
 // Device scratch for a wave of `qw` queries of `T` tokens; the fills are enqueued on the
 // search stream `s`, after the searches before it.
-int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, hipStream_t s) {
+int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, int32_t k, hipStream_t s) {
     const int64_t n_tok = (int64_t)qw * T;
     int rc = WARP_OK;
     if (!rc) rc = grow_scratch(idx, idx->filter, (size_t)n_tok * idx->n_c * 2);
@@ -500,6 +500,8 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, hipStream_t s) {
     if (!rc) rc = grow_scratch(idx, idx->list_item, ((size_t)idx->n_chunks + 3) * 8);  // + the two counts
     if (!rc) rc = grow_scratch(idx, idx->cblk, (size_t)cblocks * 24);
     if (!rc) rc = grow_scratch(idx, idx->scan_queue, 256);
+    if (!rc && P > kMaxProbe) rc = grow_scratch(idx, idx->full_sel, select_full_bytes(n_tok, idx->n_c));
+    if (!rc && k > kMaxK) rc = grow_scratch(idx, idx->full_topk, topk_full_bytes(idx->n_docs));
     if (rc) return rc;
     // the token-max table and its query slots' epochs. All slots are zeroed before a search
     // that resets cells or lays the table out with another token count, and after a search
@@ -547,8 +549,9 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, hipStream_t s) {
 // Queries per wave: as many as the scratch budget holds. The budget is
 // WARP_SCRATCH_MB if set, else 60% of the device memory that is free or already
 // held as scratch by this index. A larger wave lets the cluster-major scan read
-// each probed cluster once for more queries.
-int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T) {
+// each probed cluster once for more queries. With n_probe above kMaxProbe the exact
+// selection sorts the wave's n_tok n_c scores, at most 2^31 of them.
+int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T, int32_t P) {
     const size_t held = idx->tokmax.bytes + idx->filter.bytes + idx->keys.bytes + idx->plist.bytes +
                         idx->qdig.bytes;
     size_t budget = 0;
@@ -563,12 +566,15 @@ int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T) {
         budget = (size_t)(0.6 * (double)(free_b + held));
     }
     budget = std::min(budget, scratch_cap());
+    const bool full = P > kMaxProbe;
     const size_t per = (size_t)T * idx->n_docs * (idx->scoring == WARP_SCORING_EQ1_LITERAL ? 8 : 4) +
-                       (size_t)idx->n_docs * 8 + (size_t)T * idx->n_c * 2 + (size_t)T * kMaxProbe * 32 +
-                       (size_t)T * 1024;
+                       (size_t)idx->n_docs * 8 + (size_t)T * idx->n_c * 2 + (size_t)T * P * 32 +
+                       (size_t)T * 1024 + (full ? select_full_bytes(T, idx->n_c) : 0);
+    const int64_t sort_cap = ((int64_t)1 << 31) / ((int64_t)T * idx->n_c);
     auto clamp = [&](int64_t q) {
         if (q > n_queries) q = n_queries;
         if (q > 65535) q = 65535;
+        if (full && q > sort_cap) q = sort_cap;
         return q < 1 ? (int64_t)1 : q;
     };
     return (int32_t)clamp((int64_t)(budget / per));
@@ -645,6 +651,7 @@ struct WaveScratch {
     int4 *list_rec, *list_rec2;
     int64_t *list_item, *cblk;
     uint32_t* scan_queue;
+    void *full_sel, *full_topk;  // sort scratch of n_probe > kMaxProbe and of k > kMaxK
 };
 
 // The index's own scratch (grown by reserve()).
@@ -672,12 +679,15 @@ WaveScratch index_scratch(warp_index* idx) {
     w.list_rec2 = (int4*)idx->list_rec2.p;
     w.cblk = (int64_t*)idx->cblk.p;
     w.scan_queue = (uint32_t*)idx->scan_queue.p;
+    w.full_sel = idx->full_sel.p;
+    w.full_topk = idx->full_topk.p;
     return w;
 }
 
 // Enqueue the kernels of one wave (queries [q0, q0 + nq) of the search) on `s`. With epochs,
 // the host's copy of the query slots' epochs advances (after zeroing the slots that ran out).
-void launch_wave(warp_index* idx, const WaveScratch& w, const float* dq, int32_t q0, int32_t nq, int32_t T,
+// Returns the first launch error.
+hipError_t launch_wave(warp_index* idx, const WaveScratch& w, const float* dq, int32_t q0, int32_t nq, int32_t T,
                  int32_t P, int64_t t_prime, int32_t k, const SearchOut& o, hipStream_t s, bool timed) {
     const int64_t words = ((int64_t)idx->n_docs + 31) / 32;
     WaveArgs a{};
@@ -754,7 +764,9 @@ void launch_wave(warp_index* idx, const WaveScratch& w, const float* dq, int32_t
     }
     // the preparation zeroes the cluster token counters that the selection counts into
     launch_wave_prep(a, epochs ? (uint32_t*)idx->q_epoch.p : nullptr, (uint32_t)idx->tab_epochs, s);
-    launch_select(a, s);
+    hipError_t err = hipSuccess;
+    if (P > kMaxProbe) err = launch_select_full(a, w.full_sel, s);
+    else launch_select(a, s);
     mark(2);
     launch_scored(a, s);
     launch_pairing(a, s);
@@ -764,23 +776,31 @@ void launch_wave(warp_index* idx, const WaveScratch& w, const float* dq, int32_t
     mark(4);
     launch_fold(a, s);
     mark(5);
-    launch_topk(a, s);
+    if (k > kMaxK) {
+        const hipError_t e = launch_topk_full(a, w.full_topk, s);
+        if (err == hipSuccess) err = e;
+    } else {
+        launch_topk(a, s);
+    }
     mark(6);
     if (timed)
         for (int e = 0; e <= kStages; ++e) idx->ev_pending.push_back(ev[e]);
+    const hipError_t le = hipGetLastError();
+    return err != hipSuccess ? err : le;
 }
 
 // Enqueue a whole search on `s`; every pointer is device memory.
 int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t T, int32_t P,
                    int64_t t_prime, int32_t k, const SearchOut& o, hipStream_t s) {
-    const int32_t qw = wave_queries(idx, n_queries, T);
-    int rc = reserve(idx, qw, T, P, s);
+    if (P > kMaxProbe && (int64_t)T * idx->n_c > ((int64_t)1 << 31))
+        return fail(WARP_ENOTSUP, "nprobe above %d needs n_qtok * n_centroids <= 2^31", kMaxProbe);
+    const int32_t qw = wave_queries(idx, n_queries, T, P);
+    int rc = reserve(idx, qw, T, P, k, s);
     if (rc) return rc;
     const WaveScratch w = index_scratch(idx);
     for (int32_t q0 = 0; q0 < n_queries; q0 += qw) {
         const int32_t nq = n_queries - q0 < qw ? n_queries - q0 : qw;
-        launch_wave(idx, w, dq, q0, nq, T, P, t_prime, k, o, s, idx->timing);
-        hipError_t le = hipGetLastError();
+        const hipError_t le = launch_wave(idx, w, dq, q0, nq, T, P, t_prime, k, o, s, idx->timing);
         if (le != hipSuccess) return fail(WARP_EDEVICE, "kernel launch failed: %s", hipGetErrorString(le));
     }
     return WARP_OK;
@@ -845,10 +865,10 @@ int search_host(warp_index* idx, const float* queries, int32_t n_queries, int32_
     return read_device_errors(idx, s);
 }
 
-// The no-allocation scratch laid out for waves of qw queries of T tokens (nprobe P), in
+// The no-allocation scratch laid out for waves of qw queries of T tokens (nprobe P, k results), in
 // 256-byte aligned pieces from `base` (null: sizes only); returns the bytes it takes.
-size_t noalloc_layout(const warp_index* idx, int32_t qw, int32_t T, int32_t P, bool literal, unsigned char* base,
-                      WaveScratch* out) {
+size_t noalloc_layout(const warp_index* idx, int32_t qw, int32_t T, int32_t P, int32_t k, bool literal,
+                      unsigned char* base, WaveScratch* out) {
     size_t at = 0;
     auto take = [&](size_t bytes) -> void* {
         void* p = base ? (void*)(base + at) : nullptr;
@@ -879,6 +899,8 @@ size_t noalloc_layout(const warp_index* idx, int32_t qw, int32_t T, int32_t P, b
     w.tokmax = (uint32_t*)take(n_tok * nd * 4);
     w.tokcnt = literal ? (uint32_t*)take(n_tok * nd * 4) : nullptr;
     w.q_epoch = nullptr;  // cells hold t + 2^31 and the fold resets every cell it reads
+    w.full_sel = P > kMaxProbe ? take(select_full_bytes((int64_t)n_tok, idx->n_c)) : nullptr;
+    w.full_topk = k > kMaxK ? take(topk_full_bytes(idx->n_docs)) : nullptr;
     if (out) *out = w;
     return at;
 }
@@ -897,21 +919,25 @@ int warp_search_noalloc(warp_index* idx, const float* queries, int32_t n_queries
     unsigned char* base = noalloc_scratch(idx->device);
     if (!base) return fail(WARP_EDEVICE, "no-allocation scratch of device %d is not bound", idx->device);
     const bool literal = idx->scoring == WARP_SCORING_EQ1_LITERAL;
-    const size_t one = noalloc_layout(idx, 1, n_qtok, nprobe, literal, nullptr, nullptr);
+    const size_t one = noalloc_layout(idx, 1, n_qtok, nprobe, k, literal, nullptr, nullptr);
     if (one > kNoAllocBytes)
         return fail(WARP_ENOMEM,
                     "warp_search_noalloc: one query of %d tokens on this index needs %zu bytes of scratch; "
                     "the static scratch holds %zu (use warp_search_async)", n_qtok, one, kNoAllocBytes);
-    // the largest wave that fits (the layout grows with the wave)
+    if (nprobe > kMaxProbe && (int64_t)n_qtok * idx->n_c > ((int64_t)1 << 31))
+        return fail(WARP_ENOTSUP, "nprobe above %d needs n_qtok * n_centroids <= 2^31", kMaxProbe);
+    // the largest wave that fits (the layout grows with the wave); the exact selection
+    // sorts at most 2^31 scores per wave
     int32_t lo = 1, hi = n_queries;
+    if (nprobe > kMaxProbe) hi = (int32_t)std::min<int64_t>(hi, ((int64_t)1 << 31) / ((int64_t)n_qtok * idx->n_c));
     while (lo < hi) {
         const int32_t mid = lo + (hi - lo + 1) / 2;
-        if (noalloc_layout(idx, mid, n_qtok, nprobe, literal, nullptr, nullptr) <= kNoAllocBytes) lo = mid;
+        if (noalloc_layout(idx, mid, n_qtok, nprobe, k, literal, nullptr, nullptr) <= kNoAllocBytes) lo = mid;
         else hi = mid - 1;
     }
     const int32_t qw = lo;
     WaveScratch w{};
-    noalloc_layout(idx, qw, n_qtok, nprobe, literal, base, &w);
+    noalloc_layout(idx, qw, n_qtok, nprobe, k, literal, base, &w);
     hipStream_t s = (hipStream_t)hip_stream;
     // the array keeps what the last call left: the token-max cells (and counts) start at
     // zero; each wave's fold then resets every cell it reads
@@ -923,10 +949,9 @@ int warp_search_noalloc(warp_index* idx, const float* queries, int32_t n_queries
     SearchOut o{out_doc_ids, out_scores, out_fixed_scores, out_counts, nullptr, nullptr, nullptr, nullptr};
     for (int32_t q0 = 0; q0 < n_queries; q0 += qw) {
         const int32_t nq = n_queries - q0 < qw ? n_queries - q0 : qw;
-        launch_wave(idx, w, queries, q0, nq, n_qtok, nprobe, t_prime, k, o, s, false);
+        const hipError_t le = launch_wave(idx, w, queries, q0, nq, n_qtok, nprobe, t_prime, k, o, s, false);
+        if (le != hipSuccess) return fail(WARP_EDEVICE, "kernel launch failed: %s", hipGetErrorString(le));
     }
-    const hipError_t le = hipGetLastError();
-    if (le != hipSuccess) return fail(WARP_EDEVICE, "kernel launch failed: %s", hipGetErrorString(le));
     return WARP_OK;
 }
 
@@ -1064,11 +1089,11 @@ int warp_build_index(const float* tokens, const int32_t* token_docs, int64_t n_t
         double ss = 0;
         for (int d = 0; d < kDim; ++d) {
             const float v = hC[(size_t)c * kDim + d];
-            if (!std::isfinite(v)) return fail(WARP_EINVAL, "initial centroid %lld is not finite", (long long)c);
+            if (!std::isfinite(v)) return fail(WARP_EINVAL, "starting vector %lld is not finite", (long long)c);
             ss += (double)v * v;
         }
-        if (std::fabs(std::sqrt(ss) - 1.0) > 1e-3)
-            return fail(WARP_EINVAL, "initial centroid %lld is not of unit norm", (long long)c);
+        if (!(ss > 0.0) || !std::isfinite(ss))
+            return fail(WARP_EINVAL, "starting vector %lld is zero or too large", (long long)c);
     }
     for (int64_t i = 0; i < n_sample; ++i)
         if (hS[i] < 0 || hS[i] >= n_tokens) return fail(WARP_EINVAL, "sample id %lld is out of range", (long long)i);
@@ -1127,6 +1152,7 @@ int warp_build_index(const float* tokens, const int32_t* token_docs, int64_t n_t
     if (herr & kErrDocRange) return done(fail(WARP_EINVAL, "a token's document id is outside [0, n_docs)"));
 
     HIP_TRY(hipMemcpyAsync(centroids, hC.data(), hC.size() * 4, hipMemcpyHostToDevice, s));
+    launch_normalize_rows(centroids, n_centroids, s);  // the starting centroids
     auto assign_rows = [&](const float* x, int64_t n, int32_t* out) {
         for (int64_t t0 = 0; t0 < n; t0 += chunk) {
             const int64_t nt = std::min(chunk, n - t0);

@@ -1,5 +1,8 @@
-// Device-wide primitives of the index construction (Section 4.1): a stable LSD radix
-// sort of 32-bit keys (optionally carrying 64-bit values) and an exclusive prefix sum.
+// Device-wide primitives: a stable LSD radix sort of 32- or 64-bit keys (optionally
+// carrying 64-bit values) and an exclusive prefix sum. The index construction (Section
+// 4.1) sorts residual components and (cluster, token) pairs with them; the search sorts
+// whole score lists with them when n_probe or k exceed what its selection and top-k
+// kernels hold.
 //
 // Radix sort. Each pass sorts by one 8-bit digit, stably, in three launches:
 //   1. k_radix_hist: every tile of kSortTile keys counts its digits; the counts go to a
@@ -130,7 +133,8 @@ hipError_t exclusive_sum_u64(void* temp, size_t* temp_bytes, const unsigned long
 
 // ---------------------------------------------------------------------------- radix sort
 
-__global__ __launch_bounds__(kSortThreads) void k_radix_hist(const uint32_t* __restrict__ keys, int64_t n, int shift,
+template <typename K>
+__global__ __launch_bounds__(kSortThreads) void k_radix_hist(const K* __restrict__ keys, int64_t n, int shift,
                                                              int64_t tiles, uint32_t* __restrict__ hist) {
     __shared__ uint32_t s_h[256];
     s_h[threadIdx.x] = 0;
@@ -139,16 +143,16 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_hist(const uint32_t* __r
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
         const int64_t j = base + (int64_t)i * kSortThreads + threadIdx.x;
-        if (j < n) atomicAdd(&s_h[(keys[j] >> shift) & 255u], 1u);
+        if (j < n) atomicAdd(&s_h[(uint32_t)(keys[j] >> shift) & 255u], 1u);
     }
     __syncthreads();
     hist[(int64_t)threadIdx.x * tiles + blockIdx.x] = s_h[threadIdx.x];
 }
 
 // offs[digit * tiles + tile]: the tile's first output position for that digit
-template <bool VALS>
-__global__ __launch_bounds__(kSortThreads) void k_radix_scatter(const uint32_t* __restrict__ keys_in,
-                                                                uint32_t* __restrict__ keys_out,
+template <typename K, bool VALS>
+__global__ __launch_bounds__(kSortThreads) void k_radix_scatter(const K* __restrict__ keys_in,
+                                                                K* __restrict__ keys_out,
                                                                 const int64_t* __restrict__ vals_in,
                                                                 int64_t* __restrict__ vals_out, int64_t n, int shift,
                                                                 int64_t tiles, const uint32_t* __restrict__ offs) {
@@ -165,8 +169,8 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_scatter(const uint32_t* 
     for (int r = 0; r < kSortItems; ++r) {
         const int64_t j = base + (int64_t)r * kSortThreads + tid;
         const bool in = j < n;
-        const uint32_t key = in ? keys_in[j] : 0u;
-        const uint32_t dig = (key >> shift) & 255u;
+        const K key = in ? keys_in[j] : (K)0;
+        const uint32_t dig = (uint32_t)(key >> shift) & 255u;
         // lanes of this wave holding a key with the same digit
         unsigned long long same = __ballot(in);
 #pragma unroll
@@ -200,29 +204,30 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_scatter(const uint32_t* 
 
 static int64_t sort_tiles(int64_t n) { return (n + kSortTile - 1) / kSortTile; }
 
-// temporary storage of a radix sort of n keys (with 64-bit values if vals): the two
-// alternate buffers, the digit table, and its prefix sum's temporary storage
-static size_t sort_temp_bytes(int64_t n, bool vals) {
+// temporary storage of a radix sort of n keys of kb bytes (with 64-bit values if vals):
+// the two alternate buffers, the digit table, and its prefix sum's temporary storage
+static size_t sort_temp_bytes(int64_t n, bool vals, size_t kb = 4) {
     const auto al = [](size_t b) { return (b + 255) & ~(size_t)255; };
     const int64_t tiles = sort_tiles(n);
-    return al((size_t)n * 4) + (vals ? al((size_t)n * 8) : 0) + 2 * al((size_t)tiles * 256 * 4) +
+    return al((size_t)n * kb) + (vals ? al((size_t)n * 8) : 0) + 2 * al((size_t)tiles * 256 * 4) +
            scan_temp_bytes<uint32_t>(tiles * 256);
 }
 
 // Stable sort of keys_in by bits [0, end_bit), values carried along (vals_in may be null).
-static hipError_t radix_sort(void* temp, size_t* temp_bytes, const uint32_t* keys_in, uint32_t* keys_out,
+template <typename K>
+static hipError_t radix_sort(void* temp, size_t* temp_bytes, const K* keys_in, K* keys_out,
                              const int64_t* vals_in, int64_t* vals_out, int64_t n, int end_bit, hipStream_t s) {
     const bool vals = vals_in != nullptr;
     if (!temp) {
-        *temp_bytes = sort_temp_bytes(n, vals);
+        *temp_bytes = sort_temp_bytes(n, vals, sizeof(K));
         return hipSuccess;
     }
     if (n <= 0) return hipSuccess;
     const auto al = [](size_t b) { return (b + 255) & ~(size_t)255; };
     const int64_t tiles = sort_tiles(n);
     char* p = (char*)temp;
-    uint32_t* kt = (uint32_t*)p;
-    p += al((size_t)n * 4);
+    K* kt = (K*)p;
+    p += al((size_t)n * sizeof(K));
     int64_t* vt = vals ? (int64_t*)p : nullptr;
     p += vals ? al((size_t)n * 8) : 0;
     uint32_t* hist = (uint32_t*)p;
@@ -232,26 +237,34 @@ static hipError_t radix_sort(void* temp, size_t* temp_bytes, const uint32_t* key
     void* scan_temp = p;
     const int passes = std::max(1, (end_bit + 7) / 8);
     // pass i reads src and writes dst; the last pass writes the caller's output
-    const uint32_t* ks = keys_in;
+    const K* ks = keys_in;
     const int64_t* vs = vals_in;
     for (int i = 0; i < passes; ++i) {
-        const bool last = i == passes - 1;
         const bool to_out = ((passes - 1 - i) % 2) == 0;  // so that the last pass lands in keys_out
-        uint32_t* kd = to_out ? keys_out : kt;
+        K* kd = to_out ? keys_out : kt;
         int64_t* vd = to_out ? vals_out : vt;
-        hipLaunchKernelGGL(k_radix_hist, dim3((unsigned)tiles), dim3(kSortThreads), 0, s, ks, n, 8 * i, tiles, hist);
+        hipLaunchKernelGGL(k_radix_hist<K>, dim3((unsigned)tiles), dim3(kSortThreads), 0, s, ks, n, 8 * i, tiles, hist);
         exclusive_scan<uint32_t, uint32_t>(scan_temp, hist, offs, tiles * 256, s);
         if (vals)
-            hipLaunchKernelGGL(k_radix_scatter<true>, dim3((unsigned)tiles), dim3(kSortThreads), 0, s, ks, kd, vs, vd,
-                               n, 8 * i, tiles, (const uint32_t*)offs);
+            hipLaunchKernelGGL((k_radix_scatter<K, true>), dim3((unsigned)tiles), dim3(kSortThreads), 0, s, ks, kd, vs,
+                               vd, n, 8 * i, tiles, (const uint32_t*)offs);
         else
-            hipLaunchKernelGGL(k_radix_scatter<false>, dim3((unsigned)tiles), dim3(kSortThreads), 0, s, ks, kd,
+            hipLaunchKernelGGL((k_radix_scatter<K, false>), dim3((unsigned)tiles), dim3(kSortThreads), 0, s, ks, kd,
                                (const int64_t*)nullptr, (int64_t*)nullptr, n, 8 * i, tiles, (const uint32_t*)offs);
-        (void)last;
         ks = kd;
         vs = vd;
     }
     return hipGetLastError();
+}
+
+hipError_t sort_u64(void* temp, size_t* temp_bytes, const uint64_t* keys_in, uint64_t* keys_out,
+                    const int64_t* vals_in, int64_t* vals_out, int64_t n, int end_bit, hipStream_t s) {
+    return radix_sort<uint64_t>(temp, temp_bytes, keys_in, keys_out, vals_in, vals_out, n, end_bit, s);
+}
+
+hipError_t sort_u32(void* temp, size_t* temp_bytes, const uint32_t* keys_in, uint32_t* keys_out,
+                    const int64_t* vals_in, int64_t* vals_out, int64_t n, int end_bit, hipStream_t s) {
+    return radix_sort<uint32_t>(temp, temp_bytes, keys_in, keys_out, vals_in, vals_out, n, end_bit, s);
 }
 
 // fp32 <-> order-preserving unsigned keys
@@ -283,7 +296,7 @@ hipError_t sort_floats(void* temp, size_t* temp_bytes, const float* in, float* o
     const unsigned g = (unsigned)((n + 255) / 256);
     hipLaunchKernelGGL(k_float_keys, dim3(g), dim3(256), 0, s, in, a, n);
     size_t tb = 0;
-    hipError_t e = radix_sort(rest, &tb, a, b, nullptr, nullptr, n, 32, s);
+    hipError_t e = radix_sort<uint32_t>(rest, &tb, a, b, nullptr, nullptr, n, 32, s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_key_floats, dim3(g), dim3(256), 0, s, b, out, n);
     return hipGetLastError();
@@ -293,11 +306,11 @@ hipError_t sort_floats(void* temp, size_t* temp_bytes, const float* in, float* o
 hipError_t sort_by_cluster(void* temp, size_t* temp_bytes, const int32_t* keys_in, int32_t* keys_out,
                            const int64_t* vals_in, int64_t* vals_out, int64_t n, int end_bit, hipStream_t s) {
     if (!temp) {
-        *temp_bytes = sort_temp_bytes(n, true);
+        *temp_bytes = sort_temp_bytes(n, true, 4);
         return hipSuccess;
     }
-    return radix_sort(temp, temp_bytes, reinterpret_cast<const uint32_t*>(keys_in), reinterpret_cast<uint32_t*>(keys_out),
-                      vals_in, vals_out, n, end_bit, s);
+    return radix_sort<uint32_t>(temp, temp_bytes, reinterpret_cast<const uint32_t*>(keys_in),
+                                reinterpret_cast<uint32_t*>(keys_out), vals_in, vals_out, n, end_bit, s);
 }
 
 }  // namespace warp

@@ -313,14 +313,14 @@ def sample_passages(doc_lengths, c: float = 16.0, seed: int = 0) -> np.ndarray:
 
 
 def initial_centroids(tokens, sample_ids, n_centroids: int, seed: int = 0) -> np.ndarray:
-    """n_centroids distinct sample tokens, normalised (the k-means starting point)."""
+    """n_centroids distinct sample tokens: the k-means starting vectors (warp_build_index
+    normalises them). A choice of the caller, like the sample itself."""
     ids = np.asarray(sample_ids, np.int64)
     if n_centroids > len(ids):
         raise ValueError("more centroids than sampled tokens")
     pick = np.random.default_rng(seed).choice(len(ids), size=n_centroids, replace=False)
     X = tokens[ids[np.sort(pick)]]
-    X = np.asarray(X.cpu() if hasattr(X, "cpu") else X, np.float64)
-    return (X / np.linalg.norm(X, axis=1, keepdims=True)).astype(np.float32)
+    return np.ascontiguousarray(X.cpu() if hasattr(X, "cpu") else X, np.float32)
 
 
 def build_index(tokens, token_docs, n_docs: int, init_centroids, sample_ids, iterations: int, nbits: int,

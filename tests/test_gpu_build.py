@@ -86,9 +86,11 @@ def test_build_errors():
     sample = w.sample_passages(lens, c=5.0, seed=1)
     C0 = w.initial_centroids(X, sample, 16, seed=2)
     Xt, Dt = torch.from_numpy(X).cuda(), torch.from_numpy(docs).cuda()
+    Z = C0.copy()
+    Z[2] = 0
     with pytest.raises(w.WarpError) as e:
-        w.build_index(Xt, Dt, len(lens), C0 * 1.01, sample, 1, 4, 10)
-    assert e.value.code == w.EINVAL and "unit norm" in e.value.msg
+        w.build_index(Xt, Dt, len(lens), Z, sample, 1, 4, 10)
+    assert e.value.code == w.EINVAL and "zero" in e.value.msg
     bad = sample.copy()
     bad[0] = len(X)
     with pytest.raises(w.WarpError) as e:

@@ -99,6 +99,20 @@ CASES = [
     (13, 40, 303, 12, 4, 3, 32, 9, 100, 30),     # a document count that is not a multiple of 4
 ]
 
+# n_probe above 256 (the selection sorts every (token, centroid) score) and k above 4096 (the
+# top-k sorts every document key): the same results as the boundary-band selection and the
+# LDS top-k give below those limits
+LARGE_CASES = [
+    # seed, n_centroids, n_docs, max_len, nbits, n_queries, n_qtok, nprobe, t_prime, k
+    (20, 600, 3000, 20, 4, 3, 32, 600, 1500, 5000),    # all clusters, k above n_docs
+    (21, 1000, 20000, 20, 2, 4, 8, 300, 4000, 6000),   # 300 of 1000 clusters
+    (22, 400, 2000, 10, 4, 2, 16, 400, 10 ** 9, 50),   # t' above N: lowest score
+    (23, 300, 2000, 10, 8, 2, 32, 257, 0, 4097),       # t' = 0, one past each limit
+    (24, 700, 5000, 12, 1, 5, 32, 520, 700, 4096),     # large n_probe alone
+    (25, 60, 9000, 12, 4, 3, 32, 9, 100, 8000),        # large k alone
+    (26, 4000, 40000, 6, 4, 3, 1, 260, 100, 10000),    # fewer candidates than k, one token
+]
+
 
 @pytest.mark.parametrize("case", CASES, ids=[f"seed{c[0]}" for c in CASES])
 def test_random_small(case):
@@ -113,6 +127,17 @@ def test_random_small(case):
                                          n_queries=nq, n_qtok=nt, nprobe=nprobe, t_prime=tp, k=k)
         data = synth.make_index(wl, workers=1)
     run_both(data, label=f"random seed {seed}")
+
+
+@pytest.mark.parametrize("case", LARGE_CASES, ids=[f"seed{c[0]}" for c in LARGE_CASES])
+def test_large_nprobe_and_k(case):
+    seed, n_c, n_docs, max_len, nbits, nq, nt, nprobe, tp, k = case
+    wl = synth.random_small_workload(seed, n_centroids=n_c, n_docs=n_docs, max_len=max_len, nbits=nbits,
+                                     n_queries=nq, n_qtok=nt, nprobe=nprobe, t_prime=tp, k=k)
+    data = synth.make_index(wl, workers=1)
+    run_both(data, label=f"large seed {seed}")
+    if seed == 20:
+        run_both(data, label=f"large seed {seed} literal", literal=True)
 
 
 @pytest.mark.parametrize("narrow_max", ["0", "3", "4096"], ids=["all-wide", "narrow3", "all-narrow"])
@@ -323,7 +348,7 @@ def test_gpu_argument_errors():
         Q = data.queries
         say("[errors]")
         for args, code in [((Q, 0, 1, 1), w.EINVAL), ((Q, 17, 1, 1), w.EINVAL), ((Q, 4, -1, 1), w.EINVAL),
-                           ((Q, 4, 1, 0), w.EINVAL), ((Q, 4, 1, 4097), w.ENOTSUP),
+                           ((Q, 4, 1, 0), w.EINVAL),
                            ((Q * 1.01, 4, 1, 3), w.EINVAL), ((np.zeros((1, 33, 128)), 4, 1, 3), w.EINVAL)]:
             with pytest.raises(w.WarpError) as e:
                 ix.search(*args)

@@ -92,6 +92,19 @@ def test_noalloc_matches_async_tiny(literal):
         _both(ix, data.queries[2:4, :17], wl.nprobe, wl.t_prime, wl.k, f"tiny 2x17 literal={literal}")
 
 
+def test_noalloc_matches_async_large_nprobe_and_k():
+    """n_probe above 256 and k above 4096 take the sort-based selection and top-k, whose
+    sort buffers then also live in the static array."""
+    from paper_2501_17788_amd import Index
+
+    data = synth.make_index(synth.random_small_workload(21, n_centroids=1000, n_docs=20000, max_len=20, nbits=2,
+                                                        n_queries=4, n_qtok=8, nprobe=300, t_prime=4000,
+                                                        k=6000), workers=1)
+    with Index.from_synthetic(data) as ix:
+        _both(ix, data.queries, 300, 4000, 6000, "large 4")
+        _both(ix, data.queries[1:3, :5], 600, 900, 5000, "large 2x5")
+
+
 def test_noalloc_rejects_an_index_too_large_for_its_scratch():
     """With 3M documents one query's token-max table alone is 384 MiB: the call fails with
     WARP_ENOMEM and enqueues nothing; warp_search_async still serves the index."""
