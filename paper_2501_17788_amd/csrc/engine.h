@@ -55,7 +55,8 @@ constexpr int kQdigBytes = 3 * kDim;  // three base-256 digit planes of a query 
 // Largest bucket weight magnitude: Q(omega) = round(omega * 2^22) must have three
 // signed base-256 digits, i.e. lie in [-8421504, 8355711].
 constexpr float kMaxWeight = 1.99f;
-constexpr int kPlanBlock = 1024;  // clusters (chunks) per block of the work plan's prefix sums
+constexpr int kPlanBlock = 1024;  // threads of the work plan's kernels; chunks per block of its prefix sums
+constexpr int kPairBlock = 8192;  // clusters per block of the pair offsets (8 per thread)
 constexpr int kRecLenShift = 48;   // a chunk's length above its first embedding (< 2^40) in a list record
 
 // Error bits the device reports through the index's flag word.
@@ -95,7 +96,9 @@ struct WaveArgs {
     // cluster-major pairing
     int32_t* ccount;            // [n_c] probing tokens per cluster
     int32_t* cursor;            // [n_c] scatter cursors
-    int32_t* pair_start;        // [n_c + 1] exclusive prefix of pairs
+    int32_t* pair_start;        // [n_c] exclusive prefix of pairs within the cluster's block of
+                                // kPairBlock clusters; the cluster's first pair is this plus coff
+    int64_t* coff;              // [ceil(n_c / kPairBlock)] pairs of the blocks before each block
     int32_t* plist;             // [n_tok * nprobe][2]: (wave token, R(S64) + cell bias) grouped by cluster
     int8_t* qdig;               // [n_tok][kQdigBytes] query digit planes in operand order
     // The scan's items run over the probed chunks in the index's fixed pseudo-random chunk
@@ -112,8 +115,9 @@ struct WaveArgs {
     int4* list_rec2;            // [n_chunks] the probed chunks of the narrow scan (1..narrow_max tokens),
                                 // in the same order, with records like list_rec
     int64_t* list_n2;           // [1] their number
-    int64_t* cblk;              // [3 * ceil(n_chunks / kPlanBlock)] block sums: wide chunks, their items,
-                                // narrow chunks
+    int64_t* cblk;              // [3 * ceil(n_chunks / kPlanBlock)] per block of chunks: wide chunks,
+                                // their items and narrow chunks before it (block sums until the
+                                // prefix kernel turns them into prefixes)
     uint32_t* scan_queue;       // [1] next unclaimed batch of the scan's items
     // outputs (device; the debug ones may be null)
     int32_t* out_ids;           // [n_q][k]

@@ -90,7 +90,7 @@ struct warp_index {
     bool tab_force_zero = false;   // zero every slot first (after a query-norm error)
     std::vector<uint32_t> slot_ep; // epoch of each query slot's rows; 0: all zero
     DevBuf q_epoch;                // device copy of slot_ep
-    DevBuf ccount, cursor, pair_start, plist, qdig;
+    DevBuf ccount, cursor, pair_start, coff, plist, qdig;
     DevBuf list_rec, list_item, cblk;  // the wave's probed chunks (see WaveArgs)
     DevBuf list_rec2;                  // the wave's probed chunks of the narrow scan
     DevBuf scan_queue;
@@ -226,7 +226,7 @@ void destroy_index(warp_index* idx) {
             if (p) (void)hipFree(p);
         for (DevBuf* b : {&idx->filter, &idx->sel, &idx->base, &idx->seg_pref, &idx->m_fixed, &idx->tokmax,
                           &idx->q_epoch, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount,
-                          &idx->cursor, &idx->pair_start, &idx->plist, &idx->qdig, &idx->list_rec,
+                          &idx->cursor, &idx->pair_start, &idx->coff, &idx->plist, &idx->qdig, &idx->list_rec,
                           &idx->list_item, &idx->cblk, &idx->list_rec2, &idx->scan_queue, &idx->full_sel,
                           &idx->full_topk, &idx->st_q,
                           &idx->st_ids,
@@ -492,6 +492,7 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, int32_t k, hipStr
     if (!rc) rc = grow_scratch(idx, idx->ccount, (size_t)idx->n_c * 4);
     if (!rc) rc = grow_scratch(idx, idx->cursor, (size_t)idx->n_c * 4);
     if (!rc) rc = grow_scratch(idx, idx->pair_start, ((size_t)idx->n_c + 1) * 4);
+    if (!rc) rc = grow_scratch(idx, idx->coff, (((size_t)idx->n_c + kPairBlock - 1) / kPairBlock) * 8);
     if (!rc) rc = grow_scratch(idx, idx->plist, (size_t)n_tok * P * 8);
     if (!rc) rc = grow_scratch(idx, idx->qdig, (size_t)n_tok * kQdigBytes);
     const int64_t cblocks = (idx->n_chunks + kPlanBlock - 1) / kPlanBlock;
@@ -647,6 +648,7 @@ struct WaveScratch {
     int32_t* doc_len;
     uint64_t *keys, *qpart;
     int32_t *ccount, *cursor, *pair_start, *plist;
+    int64_t* coff;
     int8_t* qdig;
     int4 *list_rec, *list_rec2;
     int64_t *list_item, *cblk;
@@ -672,6 +674,7 @@ WaveScratch index_scratch(warp_index* idx) {
     w.ccount = (int32_t*)idx->ccount.p;
     w.cursor = (int32_t*)idx->cursor.p;
     w.pair_start = (int32_t*)idx->pair_start.p;
+    w.coff = (int64_t*)idx->coff.p;
     w.plist = (int32_t*)idx->plist.p;
     w.qdig = (int8_t*)idx->qdig.p;
     w.list_rec = (int4*)idx->list_rec.p;
@@ -730,6 +733,7 @@ hipError_t launch_wave(warp_index* idx, const WaveScratch& w, const float* dq, i
     a.ccount = w.ccount;
     a.cursor = w.cursor;
     a.pair_start = w.pair_start;
+    a.coff = w.coff;
     a.plist = w.plist;
     a.chunk_c = idx->chunk_c;
     a.chunk_k = idx->chunk_k;
@@ -881,6 +885,7 @@ size_t noalloc_layout(const warp_index* idx, int32_t qw, int32_t T, int32_t P, i
     w.ccount = (int32_t*)take(nc * 4);
     w.cursor = (int32_t*)take(nc * 4);
     w.pair_start = (int32_t*)take((nc + 1) * 4);
+    w.coff = (int64_t*)take((nc + kPairBlock - 1) / kPairBlock * 8);
     w.list_rec = (int4*)take(chunks * 16);
     w.list_rec2 = (int4*)take(chunks * 16);
     w.list_item = (int64_t*)take((chunks + 3) * 8);
