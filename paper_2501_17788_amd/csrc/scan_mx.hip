@@ -50,16 +50,18 @@ __device__ __forceinline__ void digits3(int x, int& d0, int& d1, int& d2) {
     d2 = (x - d1) >> 8;
 }
 
-// floor((a0 + 2^8 a1 + 2^16 a2 + 2^24 a3 + 2^32 a4) / 2^18) modulo 2^32. Writing
-// a2 = 4 alpha + rho (0 <= rho < 4) and n = a0 + 2^8 a1 + 2^16 rho, the quotient is
-// 2^14 a4 + 2^6 a3 + alpha + floor(n / 2^18); n fits in int32 for |a0| <= 2^22 and
-// |a1| <= 2^22, and the other terms are exact modulo 2^32. With a0 = A0 + 2^17 (the
-// class-0 accumulator starts at the rounding half: round half up) this is the rounded
-// residual term floor(V / 2^18 + 1/2) modulo 2^32; the scan adds the token's centroid term
-// plus its cell bias, and the sum, the biased token score, lies below 2^32, hence is exact.
+// floor((a0 + 2^8 a1 + 2^16 a2 + 2^24 a3 + 2^32 a4) / 2^18) modulo 2^32. The last two terms
+// divide exactly, to 2^6 a3 + 2^14 a4. For the rest, n = a0 + 2^8 a1 fits in int32 (|a0| <=
+// 2^21 + 2^17, |a1| <= 2^22) and nested floor division gives
+// floor((n + 2^16 a2) / 2^18) = floor((floor(n / 2^16) + a2) / 4), two arithmetic shifts. With
+// a0 = A0 + 2^17 (the class-0 accumulator starts at the rounding half: round half up) this is
+// the rounded residual term floor(V / 2^18 + 1/2) modulo 2^32; the scan adds the token's
+// centroid term plus its cell bias, and the sum, the biased token score, lies below 2^32,
+// hence is exact.
 __device__ __forceinline__ unsigned mx_fold(int a0, int a1, int a2, int a3, int a4) {
-    const int n = (int)((unsigned)a0 + ((unsigned)a1 << 8) + (((unsigned)a2 & 3u) << 16));
-    return ((unsigned)a4 << 14) + ((unsigned)a3 << 6) + (unsigned)(a2 >> 2) + (unsigned)(n >> 18);
+    const int n = (int)((unsigned)a0 + ((unsigned)a1 << 8));
+    const int u = (n >> 16) + a2;
+    return ((((unsigned)a4 << 8) + (unsigned)a3) << 6) + (unsigned)(u >> 2);
 }
 
 // Operand slot of dimension d: lane group g = d / 32 of the 16 x 64 operands,
