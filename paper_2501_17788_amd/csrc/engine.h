@@ -26,6 +26,8 @@ constexpr float kFilterEps = 1.0f / 8192.0f;
 constexpr int kSelBins = 2048;
 constexpr float kSelLim = 1.0625f;  // |score| <= (1 + 1e-3)^2 < kSelLim
 constexpr int kSelCap = 1024;       // centroids near one selection boundary held in LDS
+constexpr int kSplitTokens = 256;   // waves of at most this many tokens take the split selection
+constexpr int kSplitSlice = 4096;   // fewest centroids per workgroup of the split selection
 static_assert(2.0f * kSelLim / kSelBins > 2.0f * kFilterEps, "a bin must be wider than 2 eps");
 
 // Histogram bin of a filter score: floor((f + kSelLim) * kSelBins / (2 kSelLim)),
@@ -94,6 +96,11 @@ struct WaveArgs {
     uint64_t* qpart;            // [n_q][ceil(n_docs / 256)][2]: candidate count and largest key of each fold block
     int32_t* err;               // device flag word
     // cluster-major pairing
+    // split selection (sel_slices > 1 workgroups per token; see launch_select)
+    unsigned long long* sel_hist;  // [n_tok][kSelBins] packed (count, size) histogram, zeroed per wave
+    int32_t* sel_lists;         // [n_tok][2][kSelCap] centroids of the two rescoring bands
+    int32_t* sel_cnt;           // [n_tok][2] their counts (may exceed kSelCap), zeroed per wave
+    int32_t sel_slices;         // workgroups per token of the split selection; 1: one workgroup
     int32_t* ccount;            // [n_c] probing tokens per cluster
     int32_t* cursor;            // [n_c] scatter cursors
     int32_t* pair_start;        // [n_c] exclusive prefix of pairs within the cluster's block of

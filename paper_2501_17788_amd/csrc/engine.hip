@@ -74,6 +74,7 @@ struct warp_index {
     hipStream_t stream = nullptr;
     int scan_grid = 0;     // persistent workgroups of the residual scan
     int narrow_grid = 0;   // workgroups of the narrow scan (four waves, one chunk per wave at a time)
+    int n_cu = 0;          // compute units of the device
     // per-search scratch, grown on demand
     DevBuf filter, sel, base, seg_pref, m_fixed, tokmax, keys, qpart;
     // Token-max table [wave query slot][token][document]. The rows of query slot q carry an
@@ -95,6 +96,7 @@ struct warp_index {
     DevBuf list_rec2;                  // the wave's probed chunks of the narrow scan
     DevBuf scan_queue;
     DevBuf full_sel, full_topk;  // sort scratch of n_probe > kMaxProbe and of k > kMaxK
+    DevBuf sel_hist, sel_lists, sel_cnt;  // split selection of small waves
     int32_t scoring = WARP_SCORING_PAPER;
     DevBuf tokcnt, doc_len;    // Eq.-1-literal scoring only
     int64_t tokcnt_ready = 0;  // leading elements of tokcnt holding 0
@@ -228,7 +230,7 @@ void destroy_index(warp_index* idx) {
                           &idx->q_epoch, &idx->tokcnt, &idx->doc_len, &idx->keys, &idx->qpart, &idx->ccount,
                           &idx->cursor, &idx->pair_start, &idx->coff, &idx->plist, &idx->qdig, &idx->list_rec,
                           &idx->list_item, &idx->cblk, &idx->list_rec2, &idx->scan_queue, &idx->full_sel,
-                          &idx->full_topk, &idx->st_q,
+                          &idx->full_topk, &idx->sel_hist, &idx->sel_lists, &idx->sel_cnt, &idx->st_q,
                           &idx->st_ids,
                           &idx->st_scores, &idx->st_fixed, &idx->st_counts, &idx->st_sel, &idx->st_m,
                           &idx->st_bitmap, &idx->st_scored})
@@ -352,6 +354,7 @@ int finish_load(warp_index* idx, const int64_t* off_host) {
     int cus = 0;
     HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, idx->device));
     idx->scan_grid = cus * scan_mx_blocks_per_cu(idx->nbits);
+    idx->n_cu = cus;
     idx->narrow_grid = cus * scan_narrow_blocks_per_cu(idx->nbits);
     return WARP_OK;
 }
@@ -477,6 +480,29 @@ void clear_slots(warp_index* idx, hipStream_t s) {
     launch_fill_i32((int32_t*)idx->q_epoch.p, (int64_t)idx->slot_ep.size(), 0, s);
 }
 
+// Workgroups per token of the selection for a wave of n_tok tokens: one for large waves; for
+// waves of at most kSplitTokens tokens, enough to give every compute unit three workgroups, with
+// at least kSplitSlice centroids each (WARP_SELECT_SLICES sets the number for every wave).
+int select_slices(const warp_index* idx, int64_t n_tok) {
+    if (const char* e = std::getenv("WARP_SELECT_SLICES")) {
+        const long v = std::atol(e);
+        return v < 1 ? 1 : (v > 256 ? 256 : (int)v);
+    }
+    if (n_tok > kSplitTokens || n_tok < 1) return 1;
+    int64_t sl = (3 * (int64_t)idx->n_cu + n_tok - 1) / n_tok;
+    const int64_t by_size = idx->n_c / kSplitSlice;
+    if (sl > by_size) sl = by_size;
+    if (sl > 64) sl = 64;
+    return sl < 2 ? 1 : (int)sl;
+}
+
+// Tokens whose split-selection scratch waves of n_tok tokens reserve: all of them if such a wave
+// splits its selection, else none (a smaller last wave of a larger search then keeps one
+// workgroup per token).
+int64_t split_tokens(const warp_index* idx, int64_t n_tok) {
+    return select_slices(idx, n_tok) > 1 ? n_tok : 0;
+}
+
 // Device scratch for a wave of `qw` queries of `T` tokens; the fills are enqueued on the
 // search stream `s`, after the searches before it.
 int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, int32_t k, hipStream_t s) {
@@ -503,6 +529,10 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, int32_t k, hipStr
     if (!rc) rc = grow_scratch(idx, idx->scan_queue, 256);
     if (!rc && P > kMaxProbe) rc = grow_scratch(idx, idx->full_sel, select_full_bytes(n_tok, idx->n_c));
     if (!rc && k > kMaxK) rc = grow_scratch(idx, idx->full_topk, topk_full_bytes(idx->n_docs));
+    const int64_t st = split_tokens(idx, n_tok);
+    if (!rc) rc = grow_scratch(idx, idx->sel_hist, (size_t)st * kSelBins * 8);
+    if (!rc) rc = grow_scratch(idx, idx->sel_lists, (size_t)st * 2 * kSelCap * 4);
+    if (!rc) rc = grow_scratch(idx, idx->sel_cnt, (size_t)st * 2 * 4);
     if (rc) return rc;
     // the token-max table and its query slots' epochs. All slots are zeroed before a search
     // that resets cells or lays the table out with another token count, and after a search
@@ -654,6 +684,9 @@ struct WaveScratch {
     int64_t *list_item, *cblk;
     uint32_t* scan_queue;
     void *full_sel, *full_topk;  // sort scratch of n_probe > kMaxProbe and of k > kMaxK
+    unsigned long long* sel_hist;  // split selection: histograms, band lists and counts of up
+    int32_t *sel_lists, *sel_cnt;  // to split_cap tokens
+    int64_t split_cap;
 };
 
 // The index's own scratch (grown by reserve()).
@@ -684,6 +717,12 @@ WaveScratch index_scratch(warp_index* idx) {
     w.scan_queue = (uint32_t*)idx->scan_queue.p;
     w.full_sel = idx->full_sel.p;
     w.full_topk = idx->full_topk.p;
+    w.sel_hist = (unsigned long long*)idx->sel_hist.p;
+    w.sel_lists = (int32_t*)idx->sel_lists.p;
+    w.sel_cnt = (int32_t*)idx->sel_cnt.p;
+    // tokens that all three buffers hold (an unused buffer keeps a 16-byte stub)
+    w.split_cap = (int64_t)std::min({idx->sel_hist.bytes / ((size_t)kSelBins * 8),
+                                     idx->sel_lists.bytes / ((size_t)2 * kSelCap * 4), idx->sel_cnt.bytes / 8});
     return w;
 }
 
@@ -749,6 +788,11 @@ hipError_t launch_wave(warp_index* idx, const WaveScratch& w, const float* dq, i
     a.scan_grid = idx->scan_grid;
     a.topk_list_cap = topk_list_cap();
     a.narrow_max = narrow_max(nq);
+    const int64_t n_tok = (int64_t)nq * T;
+    a.sel_slices = n_tok <= w.split_cap ? select_slices(idx, n_tok) : 1;
+    a.sel_hist = w.sel_hist;
+    a.sel_lists = w.sel_lists;
+    a.sel_cnt = w.sel_cnt;
 
     const bool epochs = w.q_epoch != nullptr;
     hipEvent_t ev[kStages + 1] = {};
@@ -906,6 +950,10 @@ size_t noalloc_layout(const warp_index* idx, int32_t qw, int32_t T, int32_t P, i
     w.q_epoch = nullptr;  // cells hold t + 2^31 and the fold resets every cell it reads
     w.full_sel = P > kMaxProbe ? take(select_full_bytes((int64_t)n_tok, idx->n_c)) : nullptr;
     w.full_topk = k > kMaxK ? take(topk_full_bytes(idx->n_docs)) : nullptr;
+    w.split_cap = split_tokens(idx, (int64_t)n_tok);
+    w.sel_hist = (unsigned long long*)take((size_t)w.split_cap * kSelBins * 8);
+    w.sel_lists = (int32_t*)take((size_t)w.split_cap * 2 * kSelCap * 4);
+    w.sel_cnt = (int32_t*)take((size_t)w.split_cap * 2 * 4);
     if (out) *out = w;
     return at;
 }

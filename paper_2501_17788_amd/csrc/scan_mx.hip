@@ -202,7 +202,8 @@ __device__ __forceinline__ void load_code_words(const uint8_t* row, int lg, unsi
 // Per-wave preparation in one launch, ordered after the previous wave's scan and fold and
 // before this wave's selection. Blocks [0, nb0): the clusters' token counters and scatter
 // cursors zeroed, the query slots' next epochs (1 after the last one, else one more; ep may
-// be null) and the scan's batch counter set to the grid size. The next nb1 blocks: the norm check of the wave's
+// be null), the scan's batch counter set to the grid size, and for the split selection the
+// tokens' histograms and band counts zeroed. The next nb1 blocks: the norm check of the wave's
 // query tokens (one wave per token; a failure sets kErrQueryNorm). The rest: the query digit
 // planes of every wave token, qdig[t][(p * 2 + s) * 4 + g][16] bytes.
 template <int NBITS>
@@ -215,6 +216,10 @@ __global__ __launch_bounds__(256) void k_wave_prep(WaveArgs a, uint32_t* ep, uin
         if (i < a.n_c) {
             a.ccount[i] = 0;
             a.cursor[i] = 0;
+        }
+        if (a.sel_slices > 1) {  // the split selection's histograms and band counts
+            if (i < n_tok * kSelBins) a.sel_hist[i] = 0;
+            if (i < 2 * n_tok) a.sel_cnt[i] = 0;
         }
         if (ep && i < a.n_q) ep[i] = ep[i] >= last ? 1u : ep[i] + 1u;
         if (i == 0) *a.scan_queue = (uint32_t)a.scan_grid;
@@ -768,7 +773,8 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
 
 void launch_wave_prep(const WaveArgs& a, uint32_t* ep, uint32_t last, hipStream_t s) {
     const int64_t n_tok = (int64_t)a.n_q * a.n_qtok;
-    const int64_t n0 = a.n_c > a.n_q ? a.n_c : a.n_q;
+    int64_t n0 = a.n_c > a.n_q ? a.n_c : a.n_q;
+    if (a.sel_slices > 1 && n_tok * kSelBins > n0) n0 = n_tok * kSelBins;
     const int32_t nb0 = (int32_t)((n0 + 255) / 256), nb1 = (int32_t)((n_tok + 3) / 4);
     const dim3 grid((unsigned)(nb0 + nb1 + (n_tok * kDim + 255) / 256));
     switch (a.nbits) {

@@ -59,6 +59,9 @@ __device__ __forceinline__ void rank_all(const double* s, const int* id, int n, 
 // 32 part .. 32 part + 31 (one round trip for the whole row), and the running sum passes
 // from lane to lane in that order. Every lane of the four returns the score; the cluster's
 // size is loaded with the row.
+// (one copy per calling kernel: with one copy called from both selection kernels, each took
+// 97 VGPRs instead of 68)
+template <bool K>
 __device__ __noinline__ double score64_quad(const float* __restrict__ cen, const int32_t* __restrict__ sizes,
                                                int c, const float* qs, int part, int& size) {
     const float4* row = reinterpret_cast<const float4*>(cen + (int64_t)c * kDim) + 8 * part;
@@ -163,49 +166,29 @@ __device__ __forceinline__ void for_each_bin(const uint16_t* bins, int n_c, F f)
     }
 }
 
-__global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
+// Step 2 of the selection over the token's histogram in LDS (every thread calls it, after a
+// barrier that follows the histogram's last write): from the top bin down, the bin b_P where the
+// centroid count reaches n_probe (-1: none) and the bin b_t where the size sum first exceeds t'
+// (-1: none) with the size of every bin above it, and the lowest occupied bin.
+struct SelBounds {
+    int bP, bt, blo;
+    unsigned long long wabove;
+};
+__device__ __forceinline__ SelBounds hist_bounds(const unsigned long long* hist, unsigned long long* wtot, uint32_t P,
+                                                 unsigned long long tp) {
     constexpr int NT = kSelThreads;
     constexpr int PER = kSelBins / NT;
-    __shared__ unsigned long long hist[kSelBins];
-    __shared__ unsigned long long wtot[NT / 64];
-    __shared__ float qs[kDim];
-    __shared__ double sA[kSelCap], sB[kSelCap];
-    __shared__ int idA[kSelCap], idB[kSelCap];
-    __shared__ int64_t cum[kSelCap];
-    // from step 4 on, hist holds the sizes of the rescored centroids
-    int* const szA = reinterpret_cast<int*>(hist);
-    int* const szB = szA + kSelCap;
-    static_assert(2 * kSelCap * sizeof(int) <= sizeof(hist), "sizes must fit the histogram's LDS");
-    __shared__ int s_bP, s_bt, s_blo, s_nA, s_nB, s_cross;
-    __shared__ unsigned long long s_wabove, s_band_above;
-
-    const int t = blockIdx.x;
+    __shared__ int s_bP, s_bt, s_blo;
+    __shared__ unsigned long long s_wabove;
     const int tid = threadIdx.x;
-    const int n_c = a.n_c, P = a.nprobe;
-    const unsigned long long tp = (unsigned long long)a.t_prime;
-    for (int i = tid; i < kSelBins; i += NT) hist[i] = 0;
-    if (tid < kDim) qs[tid] = a.queries[(int64_t)t * kDim + tid];
-    if (tid == 0) {
+    if (tid == 0) {  // ordered before the writes below by the block scan's barrier
         s_bP = -1;
         s_bt = -1;
         s_blo = kSelBins;
-        s_nA = 0;
-        s_nB = 0;
         s_wabove = 0;
-        s_cross = kSelCap;
     }
-    __syncthreads();
-
-    // 1. histogram: one packed (count, size) word per bin
-    const uint16_t* bins = a.filter_bins + (int64_t)t * n_c;
-    const int32_t* sizes = a.sizes;
-    for_each_bin(bins, n_c, [&](int c, int b) {
-        atomicAdd(&hist[b], kCntOne | (unsigned long long)sizes[c]);
-    });
-    __syncthreads();
-
-    // 2. suffix sums over bins; thread tid owns bins [PER * tid, PER * tid + PER).
-    //    Packed words add field by field: sizes total < 2^40, counts < 2^24.
+    // suffix sums over bins; thread tid owns bins [PER * tid, PER * tid + PER). Packed words
+    // add field by field: sizes total < 2^40, counts < 2^24.
     unsigned long long own = 0;
     for (int j = 0; j < PER; ++j) own += hist[PER * tid + j];
     unsigned long long total;
@@ -246,26 +229,179 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
     }
     if ((tid & 63) == 0 && lo < kSelBins) atomicMin(&s_blo, lo);
     __syncthreads();
+    return SelBounds{s_bP, s_bt, s_blo, s_wabove};
+}
 
-    // 3. collect the centroids near the boundaries
-    const int bA = s_bP - 2 < 0 ? 0 : s_bP - 2;
-    const bool clamp = s_bt < 0;  // total size <= t': m is the lowest score
-    const int bt_lo = clamp ? s_blo : (s_bt - 2 < 0 ? 0 : s_bt - 2);
-    const int bt_hi = clamp ? (s_blo + 2 < kSelBins ? s_blo + 2 : kSelBins - 1)
-                            : (s_bt + 2 < kSelBins ? s_bt + 2 : kSelBins - 1);
-    for_each_bin(bins, n_c, [&](int c, int b) {
-        if (b >= bA) {
-            const int p = atomicAdd(&s_nA, 1);
-            if (p < kSelCap) idA[p] = c;
+// The bins whose centroids the selection rescores: every bin from b_P - 2 up (list A, the
+// n_probe best), and b_t - 2 .. b_t + 2 (list B, the t' crossing; around the lowest occupied
+// bin when the total size does not exceed t').
+struct SelBand {
+    int bA, lo, hi;
+    bool clamp;
+};
+__device__ __forceinline__ SelBand sel_band(int bP, int bt, int blo) {
+    SelBand r;
+    r.bA = bP - 2 < 0 ? 0 : bP - 2;
+    r.clamp = bt < 0;  // total size <= t': m is the lowest score
+    r.lo = r.clamp ? blo : (bt - 2 < 0 ? 0 : bt - 2);
+    r.hi = r.clamp ? (blo + 2 < kSelBins ? blo + 2 : kSelBins - 1) : (bt + 2 < kSelBins ? bt + 2 : kSelBins - 1);
+    return r;
+}
+
+// Centroids [c0, c1) of token t's row of bins: the slice that workgroup x of S takes (slices of
+// a multiple of 8 centroids, so that 16-byte loads stay aligned).
+__device__ __forceinline__ void sel_slice(int n_c, int S, int x, int& c0, int& c1) {
+    const int len = ((n_c + S - 1) / S + 7) & ~7;
+    c0 = x * len < n_c ? x * len : n_c;
+    c1 = c0 + len < n_c ? c0 + len : n_c;
+}
+
+// Split selection, for waves of few tokens (one workgroup per token would leave most of the
+// GPU idle while each reads its whole row of bins twice). Grid (S, n_tok): each workgroup adds
+// the histogram of its slice of the token's bins into the token's histogram in global memory
+// (zeroed by the wave's preparation).
+__global__ __launch_bounds__(kSelThreads) void k_select_hist(WaveArgs a) {
+    __shared__ unsigned long long hist[kSelBins];
+    const int t = blockIdx.y, tid = threadIdx.x;
+    const int n_c = a.n_c;
+    int c0, c1;
+    sel_slice(n_c, gridDim.x, blockIdx.x, c0, c1);
+    for (int i = tid; i < kSelBins; i += kSelThreads) hist[i] = 0;
+    __syncthreads();
+    const int32_t* sizes = a.sizes + c0;
+    for_each_bin(a.filter_bins + (int64_t)t * n_c + c0, c1 - c0, [&](int c, int b) {
+        atomicAdd(&hist[b], kCntOne | (unsigned long long)sizes[c]);
+    });
+    __syncthreads();
+    unsigned long long* g = a.sel_hist + (int64_t)t * kSelBins;
+    for (int i = tid; i < kSelBins; i += kSelThreads)
+        if (hist[i]) atomicAdd(&g[i], hist[i]);
+}
+
+// Then each workgroup reads the token's whole histogram, finds the bands, gathers the centroids
+// of its slice that fall in them in LDS and appends them to the token's two lists in global
+// memory with one atomic per list (the counts may exceed kSelCap; the final kernel treats that
+// as the overflow it is).
+__global__ __launch_bounds__(kSelThreads) void k_select_collect(WaveArgs a) {
+    __shared__ unsigned long long hist[kSelBins];
+    __shared__ unsigned long long wtot[kSelThreads / 64];
+    __shared__ int s_list[2][kSelCap];
+    __shared__ int s_n[2], s_at[2];
+    const int t = blockIdx.y, tid = threadIdx.x;
+    const int n_c = a.n_c;
+    const unsigned long long* g = a.sel_hist + (int64_t)t * kSelBins;
+    for (int i = tid; i < kSelBins; i += kSelThreads) hist[i] = g[i];
+    if (tid == 0) {
+        s_n[0] = 0;
+        s_n[1] = 0;
+    }
+    __syncthreads();
+    const SelBounds bd = hist_bounds(hist, wtot, (uint32_t)a.nprobe, (unsigned long long)a.t_prime);
+    const SelBand band = sel_band(bd.bP, bd.bt, bd.blo);
+    int c0, c1;
+    sel_slice(n_c, gridDim.x, blockIdx.x, c0, c1);
+    int32_t* cnt = a.sel_cnt + 2 * (int64_t)t;
+    int32_t* listA = a.sel_lists + 2 * (int64_t)t * kSelCap;
+    int32_t* listB = listA + kSelCap;
+    for_each_bin(a.filter_bins + (int64_t)t * n_c + c0, c1 - c0, [&](int c, int b) {
+        if (b >= band.bA) {
+            const int p = atomicAdd(&s_n[0], 1);
+            if (p < kSelCap) s_list[0][p] = c0 + c;
         }
-        if (b >= bt_lo && b <= bt_hi) {
-            const int p = atomicAdd(&s_nB, 1);
-            if (p < kSelCap) idB[p] = c;
+        if (b >= band.lo && b <= band.hi) {
+            const int p = atomicAdd(&s_n[1], 1);
+            if (p < kSelCap) s_list[1][p] = c0 + c;
         }
     });
+    __syncthreads();
+    if (tid < 2) s_at[tid] = s_n[tid] ? atomicAdd(&cnt[tid], s_n[tid]) : 0;
+    __syncthreads();
+    for (int l = 0; l < 2; ++l) {
+        const int n = s_n[l] < kSelCap ? s_n[l] : kSelCap;
+        int32_t* dst = l == 0 ? listA : listB;
+        for (int p = tid; p < n; p += kSelThreads)
+            if (s_at[l] + p < kSelCap) dst[s_at[l] + p] = s_list[l][p];
+    }
+}
+
+// SPLIT: the histogram and the band lists come from k_select_hist and k_select_collect.
+template <bool SPLIT>
+__global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
+    constexpr int NT = kSelThreads;
+    __shared__ unsigned long long hist[kSelBins];
+    __shared__ unsigned long long wtot[NT / 64];
+    __shared__ float qs[kDim];
+    __shared__ double sA[kSelCap], sB[kSelCap];
+    __shared__ int idA[kSelCap], idB[kSelCap];
+    __shared__ int64_t cum[kSelCap];
+    // from step 4 on, hist holds the sizes of the rescored centroids
+    int* const szA = reinterpret_cast<int*>(hist);
+    int* const szB = szA + kSelCap;
+    static_assert(2 * kSelCap * sizeof(int) <= sizeof(hist), "sizes must fit the histogram's LDS");
+    __shared__ int s_nA, s_nB, s_cross;
+    __shared__ unsigned long long s_band_above;
+
+    const int t = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int n_c = a.n_c, P = a.nprobe;
+    const unsigned long long tp = (unsigned long long)a.t_prime;
+    for (int i = tid; i < kSelBins; i += NT) hist[i] = 0;
+    if (tid < kDim) qs[tid] = a.queries[(int64_t)t * kDim + tid];
+    if (tid == 0) {
+        s_nA = 0;
+        s_nB = 0;
+        s_cross = kSelCap;
+    }
+    __syncthreads();
+
+    // 1. histogram: one packed (count, size) word per bin
+    const uint16_t* bins = a.filter_bins + (int64_t)t * n_c;
+    const int32_t* sizes = a.sizes;
+    if (SPLIT) {
+        const unsigned long long* g = a.sel_hist + (int64_t)t * kSelBins;
+        for (int i = tid; i < kSelBins; i += NT) hist[i] = g[i];
+    } else {
+        for_each_bin(bins, n_c, [&](int c, int b) {
+            atomicAdd(&hist[b], kCntOne | (unsigned long long)sizes[c]);
+        });
+    }
+    __syncthreads();
+
+    // 2. the bins of the n_probe-th centroid and of the t' crossing
+    const SelBounds bd = hist_bounds(hist, wtot, (uint32_t)P, tp);
+
+    // 3. collect the centroids near the boundaries
+    const SelBand band = sel_band(bd.bP, bd.bt, bd.blo);
+    const bool clamp = band.clamp;
+    const int bt_hi = band.hi;
+    if (SPLIT) {
+        // both lists are read whole, beside their counts (entries past a count are unused)
+        const int32_t* cnt = a.sel_cnt + 2 * (int64_t)t;
+        const int32_t* listA = a.sel_lists + 2 * (int64_t)t * kSelCap;
+        const int nA0 = cnt[0], nB0 = cnt[1];
+        for (int p = tid; p < kSelCap; p += NT) {
+            idA[p] = listA[p];
+            idB[p] = listA[kSelCap + p];
+        }
+        if (tid == 0) {
+            s_nA = nA0;
+            s_nB = nB0;
+        }
+    } else {
+        for_each_bin(bins, n_c, [&](int c, int b) {
+            if (b >= band.bA) {
+                const int p = atomicAdd(&s_nA, 1);
+                if (p < kSelCap) idA[p] = c;
+            }
+            if (b >= band.lo && b <= band.hi) {
+                const int p = atomicAdd(&s_nB, 1);
+                if (p < kSelCap) idB[p] = c;
+            }
+        });
+    }
     if (tid == 0 && !clamp) {  // size of every bin above the band (the histogram is reused below)
-        unsigned long long band_above = s_wabove;
-        for (int b = s_bt + 1; b <= bt_hi; ++b) band_above -= hist[b] & kSizeMask;
+        unsigned long long band_above = bd.wabove;
+        for (int b = bd.bt + 1; b <= bt_hi; ++b) band_above -= hist[b] & kSizeMask;
         s_band_above = band_above;
     }
     __syncthreads();
@@ -291,7 +427,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
     for (int p = tid >> 2; p < nA + nB; p += NT / 4) {  // uniform over each four lanes
         const int c = p < nA ? idA[p] : idB[p - nA];
         int sz;
-        const double v = score64_quad(a.centroids, sizes, c, qs, tid & 3, sz);
+        const double v = score64_quad<SPLIT>(a.centroids, sizes, c, qs, tid & 3, sz);
         if ((tid & 3) == 0) {
             if (p < nA) {
                 sA[p] = v;
@@ -350,7 +486,14 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
 
 void launch_select(const WaveArgs& a, hipStream_t s) {
     const int n_tok = a.n_q * a.n_qtok;
-    hipLaunchKernelGGL(k_select, dim3(n_tok), dim3(kSelThreads), 0, s, a);
+    if (a.sel_slices > 1) {
+        const dim3 grid((unsigned)a.sel_slices, (unsigned)n_tok);
+        hipLaunchKernelGGL(k_select_hist, grid, dim3(kSelThreads), 0, s, a);
+        hipLaunchKernelGGL(k_select_collect, grid, dim3(kSelThreads), 0, s, a);
+        hipLaunchKernelGGL(k_select<true>, dim3(n_tok), dim3(kSelThreads), 0, s, a);
+    } else {
+        hipLaunchKernelGGL(k_select<false>, dim3(n_tok), dim3(kSelThreads), 0, s, a);
+    }
 }
 
 }  // namespace warp

@@ -140,6 +140,23 @@ def test_large_nprobe_and_k(case):
         run_both(data, label=f"large seed {seed} literal", literal=True)
 
 
+@pytest.mark.parametrize("slices", ["3", "7"])
+def test_split_selection(slices, monkeypatch):
+    """Waves of few tokens split each token's selection over several workgroups (histogram and
+    band lists in global memory). WARP_SELECT_SLICES forces the split on every wave: the
+    probed centroids, m_i and the results must be the oracle's, at t' = 0, t' above N, nprobe
+    = all clusters, nprobe 256 with k 4096, one query token, and in both scoring modes."""
+    monkeypatch.setenv("WARP_SELECT_SLICES", slices)
+    for case in (CASES[2], CASES[3], CASES[4], CASES[5], CASES[7], CASES[8], CASES[12]):
+        seed, n_c, n_docs, max_len, nbits, nq, nt, nprobe, tp, k = case
+        wl = synth.random_small_workload(seed, n_centroids=n_c, n_docs=n_docs, max_len=max_len, nbits=nbits,
+                                         n_queries=nq, n_qtok=nt, nprobe=nprobe, t_prime=tp, k=k)
+        run_both(synth.make_index(wl, workers=1), label=f"slices={slices} seed {seed}")
+    data = synth.make_index(synth.with_overrides(synth.WORKLOADS["tiny"], n_queries=5, nprobe=24, k=40), workers=1)
+    run_both(data, label=f"slices={slices} tiny")
+    run_both(data, label=f"slices={slices} tiny literal", literal=True)
+
+
 @pytest.mark.parametrize("narrow_max", ["0", "3", "4096"], ids=["all-wide", "narrow3", "all-narrow"])
 def test_wide_and_narrow_scans_agree(narrow_max, monkeypatch):
     """Chunks probed by few tokens take the narrow scan (one wave per chunk, groups of three
@@ -394,12 +411,17 @@ def test_small_workload_sampled_queries(small_data):
     data = small_data
     wl = data.workload
     say(f"[small] {data.n_embeddings} embeddings, 256 queries, nprobe={wl.nprobe} t'={wl.t_prime} k={wl.k}")
+    rows = np.array([0, 1, 37, 100, 128, 200, 254, 255])
     with w.Index.from_synthetic(data) as ix:
         got = ix.search_debug(data.queries, wl.nprobe, wl.t_prime, wl.k)
-    rows = np.array([0, 1, 37, 100, 128, 200, 254, 255])
+        # the sampled queries on their own (256 tokens: the split selection) and one query
+        got_few = ix.search_debug(data.queries[rows], wl.nprobe, wl.t_prime, wl.k)
+        got_one = ix.search_debug(data.queries[rows[2:3]], wl.nprobe, wl.t_prime, wl.k)
     say(f"[small] oracle on queries {rows.tolist()}")
     want = oracle.search_index(data, queries=data.queries[rows])
     compare(got, want, rows=rows, label="small")
+    compare(got_few, want, label="small, sampled queries alone")
+    compare(got_one, {key: v[2:3] for key, v in want.items()}, label="small, one query")
     for qi in rows:
         gap = check_real_valued(got["scores"][qi], got["counts"][qi], got["ids"][qi], index_arrays(data),
                                 data.queries[qi], wl.nprobe, wl.t_prime)
