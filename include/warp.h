@@ -42,7 +42,7 @@
  *
  * Scratch. An index grows device scratch on demand and keeps it until freed. A
  * search runs in waves of as many queries as the scratch budget holds: the value
- * of the environment variable WARP_SCRATCH_MB (MiB) if set, else 60% of the free
+ * of the environment variable WARP_SCRATCH_MB (MiB) if set, else 80% of the free
  * device memory. The dominant scratch is a [tokens][documents] table of token
  * maxima per wave, one slot of rows per query of the wave. Each wave tags its
  * cells with its slots' epochs, in the bits that the score range leaves spare

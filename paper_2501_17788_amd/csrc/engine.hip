@@ -578,7 +578,7 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, int32_t k, hipStr
 }
 
 // Queries per wave: as many as the scratch budget holds. The budget is
-// WARP_SCRATCH_MB if set, else 60% of the device memory that is free or already
+// WARP_SCRATCH_MB if set, else 80% of the device memory that is free or already
 // held as scratch by this index. A larger wave lets the cluster-major scan read
 // each probed cluster once for more queries. With n_probe above kMaxProbe the exact
 // selection sorts the wave's n_tok n_c scores, at most 2^31 of them.
@@ -594,7 +594,7 @@ int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T, int32_
             (void)hipGetLastError();
             free_b = (size_t)8 << 30;
         }
-        budget = (size_t)(0.6 * (double)(free_b + held));
+        budget = (size_t)(0.8 * (double)(free_b + held));
     }
     budget = std::min(budget, scratch_cap());
     const bool full = P > kMaxProbe;
