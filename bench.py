@@ -338,7 +338,9 @@ def main() -> int:
     per_wave = -(-nq // waves)
     distinct = sum(int(sizes[np.unique(dbg["sel"][w0:w0 + per_wave])].sum()) for w0 in range(0, nq, per_wave))
     distinct_per_launch = distinct / waves  # waves taken as equal slices of the batch (an estimate)
-    traffic = measured_traffic("k_scan_mx", wl.name)
+    # a traffic row is keyed by the workload as configured (nprobe overrides get their own key)
+    traffic_key = wl.name if wl.nprobe == synth.WORKLOADS[wl.name].nprobe else f"{wl.name}:nprobe{wl.nprobe}"
+    traffic = measured_traffic("k_scan_mx", traffic_key)
     counted_gbs = None if traffic is None else traffic / scan_avg_s / 1e9
     roofline = {
         "bound": "hbm", "kernel": "k_scan_mx", "unit": "GB/s", "peak": HBM_PEAK_GBS,
