@@ -100,6 +100,18 @@ const char* warp_last_error(void);
 int warp_t_prime_policy(int64_t n_embeddings, double c, int64_t t_max, int64_t* out);
 
 /*
+ * The k-means sample size of Section 4.1 (index construction): the centroids
+ * are trained on a sample of passages whose size grows with the square root of
+ * the collection size:
+ *   *out = min(n_passages, ceil(c * sqrt(n_passages)))
+ * The paper fixes no constant; the caller passes c (ColBERTv2's recipe, which
+ * the paper follows, uses 16). Which passages form the sample is the caller's
+ * random draw. Host-only, no device call. WARP_EINVAL for a null out,
+ * n_passages < 0, or c negative or not finite.
+ */
+int warp_kmeans_sample_size(int64_t n_passages, double c, int64_t* out);
+
+/*
  * Build a device-resident index (Section 4.1's index: centroids, per-cluster
  * document ids and packed residual codes, bucket weights).
  *

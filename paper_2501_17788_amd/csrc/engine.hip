@@ -1022,6 +1022,15 @@ int warp_t_prime_policy(int64_t n_embeddings, double c, int64_t t_max, int64_t* 
     return WARP_OK;
 }
 
+int warp_kmeans_sample_size(int64_t n_passages, double c, int64_t* out) {
+    if (!out) return fail(WARP_EINVAL, "out is null");
+    if (n_passages < 0) return fail(WARP_EINVAL, "n_passages must be >= 0");
+    if (!(c >= 0.0) || !std::isfinite(c)) return fail(WARP_EINVAL, "c must be finite and >= 0");
+    const double k = std::ceil(c * std::sqrt((double)n_passages));
+    *out = k >= (double)n_passages ? n_passages : (int64_t)k;
+    return WARP_OK;
+}
+
 int warp_index_load(const float* centroids, int32_t n_centroids, int32_t dim, const int64_t* cluster_offsets,
                     const int32_t* doc_ids, const uint8_t* codes, int32_t nbits, const float* bucket_weights,
                     int32_t n_docs, warp_index** out) {

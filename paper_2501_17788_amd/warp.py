@@ -26,6 +26,7 @@ EXPORTS = (
     "warp_index_free", "warp_index_info", "warp_search", "warp_search_async", "warp_index_sync",
     "warp_search_debug", "warp_centroid_filter_scores", "warp_set_timing", "warp_stage_timings",
     "warp_t_prime_policy", "warp_set_scoring", "warp_build_index", "warp_search_noalloc",
+    "warp_kmeans_sample_size",
 )
 
 
@@ -64,6 +65,7 @@ def _load() -> ctypes.CDLL:
         "warp_set_timing": ([P, i32], ctypes.c_int),
         "warp_stage_timings": ([P, P, P, i32], ctypes.c_int),
         "warp_t_prime_policy": ([i64, ctypes.c_double, i64, P], ctypes.c_int),
+        "warp_kmeans_sample_size": ([i64, ctypes.c_double, P], ctypes.c_int),
         "warp_set_scoring": ([P, i32], ctypes.c_int),
         "warp_build_index": ([P, P, i64, i32, P, i32, P, i64, i32, i32, i64, P, P, P, P, P, P, P], ctypes.c_int),
     }
@@ -300,12 +302,13 @@ class Index:
 # ----------------------------------------------------------------------------- index construction
 
 def sample_passages(doc_lengths, c: float = 16.0, seed: int = 0) -> np.ndarray:
-    """Token ids (document-major order) of ceil(c * sqrt(n_docs)) passages drawn without
-    replacement: Section 4.1 clusters a sample of passages whose size grows with the square
-    root of the collection."""
+    """Token ids (document-major order) of warp_kmeans_sample_size(n_docs, c) passages
+    drawn without replacement (the draw is the caller's choice; the size is Section 4.1's)."""
     lens = np.asarray(doc_lengths, np.int64)
     n_docs = len(lens)
-    k = min(n_docs, int(np.ceil(c * np.sqrt(n_docs))))
+    size = ctypes.c_int64()
+    _check(lib.warp_kmeans_sample_size(n_docs, float(c), ctypes.byref(size)))
+    k = size.value
     docs = np.sort(np.random.default_rng(seed).choice(n_docs, size=k, replace=False))
     starts = np.zeros(n_docs + 1, np.int64)
     np.cumsum(lens, out=starts[1:])

@@ -169,3 +169,31 @@ def test_t_prime_policy():
         with pytest.raises(w.WarpError) as e:
             t_prime_policy(*bad)
         assert e.value.code == w.EINVAL
+
+
+def test_kmeans_sample_size():
+    """Section 4.1: the k-means sample of passages grows with the square root of the collection
+    (computed on the host), never more than the collection; sample_passages draws that many."""
+    import ctypes
+    import math
+
+    from paper_2501_17788_amd import sample_passages
+
+    def size(n, c):
+        out = ctypes.c_int64()
+        rc = w.lib.warp_kmeans_sample_size(n, c, ctypes.byref(out))
+        assert rc == 0, w.last_error()
+        return out.value
+
+    for n in (0, 1, 15, 256, 257, 100_000, 8_800_000):
+        for c in (0.0, 1.0, 16.0):
+            assert size(n, c) == min(n, math.ceil(c * math.sqrt(n))), (n, c)
+    assert size(100_000, 16.0) == 5060  # the small workload's sample (16 sqrt(100,000) = 5059.6)
+    assert size(4 * 10 ** 6, 16.0) == 2 * size(10 ** 6, 16.0)
+    for bad in ((-1, 1.0), (10, -1.0), (10, float("nan"))):
+        assert w.lib.warp_kmeans_sample_size(bad[0], bad[1], ctypes.byref(ctypes.c_int64())) == w.EINVAL
+    assert w.lib.warp_kmeans_sample_size(10, 1.0, None) == w.EINVAL
+    lens = np.full(400, 3, np.int64)
+    ids = sample_passages(lens, 4.0, seed=1)
+    assert len(ids) == 3 * 80 and len(np.unique(ids // 3)) == 80  # 4 sqrt(400) passages of 3 tokens
+
