@@ -167,7 +167,11 @@ int warp_index_info(const warp_index* idx, int32_t* n_centroids, int64_t* n_embe
  *   out_counts   [n_queries] host or NULL: min(k, number of candidate documents)
  *
  * Only candidate documents (those with at least one retrieved embedding) are
- * ranked. Blocks until the results are in host memory.
+ * ranked. Blocks until the results are in host memory. If more than 1024
+ * centroids of a token fall within about 3e-3 of a selection boundary (only
+ * possible with degenerate centroid sets), the search is run again with the
+ * selection that sorts every score, which gives the same results without that
+ * limit.
  */
 int warp_search(warp_index* idx, const float* queries, int32_t n_queries, int32_t n_qtok,
                 int32_t nprobe, int64_t t_prime, int32_t k, int32_t* out_doc_ids,
@@ -180,7 +184,8 @@ int warp_search(warp_index* idx, const float* queries, int32_t n_queries, int32_
  * out_counts may be NULL. Query norms are checked on the device: that error,
  * and a centroid-selection overflow (more than 1024 centroids whose scores fall
  * within about 3e-3 of a selection boundary, only possible with degenerate
- * centroid sets), are reported by warp_index_sync. The index's scratch memory
+ * centroid sets: WARP_ENOTSUP; warp_search and warp_search_debug retry such a
+ * search with the sorting selection), are reported by warp_index_sync. The index's scratch memory
  * is shared by its searches: enqueue the searches of one index on one stream.
  */
 int warp_search_async(warp_index* idx, const float* queries, int32_t n_queries, int32_t n_qtok,

@@ -97,6 +97,7 @@ struct warp_index {
     DevBuf scan_queue;
     DevBuf full_sel, full_topk;  // sort scratch of n_probe > kMaxProbe and of k > kMaxK
     DevBuf sel_hist, sel_lists, sel_cnt;  // split selection of small waves
+    bool force_full_select = false;       // the blocking search's retry after a selection overflow
     int32_t scoring = WARP_SCORING_PAPER;
     DevBuf tokcnt, doc_len;    // Eq.-1-literal scoring only
     int64_t tokcnt_ready = 0;  // leading elements of tokcnt holding 0
@@ -480,6 +481,10 @@ void clear_slots(warp_index* idx, hipStream_t s) {
     launch_fill_i32((int32_t*)idx->q_epoch.p, (int64_t)idx->slot_ep.size(), 0, s);
 }
 
+// The selection sorts whole score lists (instead of rescoring the boundary bands) for n_probe
+// above kMaxProbe, and in the blocking search's retry after a band overflowed.
+bool full_select(const warp_index* idx, int32_t P) { return P > kMaxProbe || idx->force_full_select; }
+
 // Workgroups per token of the selection for a wave of n_tok tokens: one for large waves; for
 // waves of at most kSplitTokens tokens, enough to give every compute unit three workgroups, with
 // at least kSplitSlice centroids each (WARP_SELECT_SLICES sets the number for every wave).
@@ -527,7 +532,7 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, int32_t k, hipStr
     if (!rc) rc = grow_scratch(idx, idx->list_item, ((size_t)idx->n_chunks + 3) * 8);  // + the two counts
     if (!rc) rc = grow_scratch(idx, idx->cblk, (size_t)cblocks * 24);
     if (!rc) rc = grow_scratch(idx, idx->scan_queue, 256);
-    if (!rc && P > kMaxProbe) rc = grow_scratch(idx, idx->full_sel, select_full_bytes(n_tok, idx->n_c));
+    if (!rc && full_select(idx, P)) rc = grow_scratch(idx, idx->full_sel, select_full_bytes(n_tok, idx->n_c));
     if (!rc && k > kMaxK) rc = grow_scratch(idx, idx->full_topk, topk_full_bytes(idx->n_docs));
     const int64_t st = split_tokens(idx, n_tok);
     if (!rc) rc = grow_scratch(idx, idx->sel_hist, (size_t)st * kSelBins * 8);
@@ -597,7 +602,7 @@ int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T, int32_
         budget = (size_t)(0.8 * (double)(free_b + held));
     }
     budget = std::min(budget, scratch_cap());
-    const bool full = P > kMaxProbe;
+    const bool full = full_select(idx, P);
     const size_t per = (size_t)T * idx->n_docs * (idx->scoring == WARP_SCORING_EQ1_LITERAL ? 8 : 4) +
                        (size_t)idx->n_docs * 8 + (size_t)T * idx->n_c * 2 + (size_t)T * P * 32 +
                        (size_t)T * 1024 + (full ? select_full_bytes(T, idx->n_c) : 0);
@@ -813,7 +818,7 @@ hipError_t launch_wave(warp_index* idx, const WaveScratch& w, const float* dq, i
     // the preparation zeroes the cluster token counters that the selection counts into
     launch_wave_prep(a, epochs ? (uint32_t*)idx->q_epoch.p : nullptr, (uint32_t)idx->tab_epochs, s);
     hipError_t err = hipSuccess;
-    if (P > kMaxProbe) err = launch_select_full(a, w.full_sel, s);
+    if (full_select(idx, P)) err = launch_select_full(a, w.full_sel, s);
     else launch_select(a, s);
     mark(2);
     launch_scored(a, s);
@@ -840,8 +845,8 @@ hipError_t launch_wave(warp_index* idx, const WaveScratch& w, const float* dq, i
 // Enqueue a whole search on `s`; every pointer is device memory.
 int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t T, int32_t P,
                    int64_t t_prime, int32_t k, const SearchOut& o, hipStream_t s) {
-    if (P > kMaxProbe && (int64_t)T * idx->n_c > ((int64_t)1 << 31))
-        return fail(WARP_ENOTSUP, "nprobe above %d needs n_qtok * n_centroids <= 2^31", kMaxProbe);
+    if (full_select(idx, P) && (int64_t)T * idx->n_c > ((int64_t)1 << 31))
+        return fail(WARP_ENOTSUP, "the sorted selection needs n_qtok * n_centroids <= 2^31");
     const int32_t qw = wave_queries(idx, n_queries, T, P);
     int rc = reserve(idx, qw, T, P, k, s);
     if (rc) return rc;
@@ -854,11 +859,13 @@ int enqueue_search(warp_index* idx, const float* dq, int32_t n_queries, int32_t 
     return WARP_OK;
 }
 
-int read_device_errors(warp_index* idx, hipStream_t s) {
+// The device's error bits since the last check (cleared here), as a status; *bits gets them.
+int read_device_errors(warp_index* idx, hipStream_t s, int32_t* bits = nullptr) {
     int32_t err = 0;
     HIP_TRY(hipMemcpyAsync(&err, idx->err, sizeof err, hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
     if (idx->timing) settle_timings(idx);
+    if (bits) *bits = err;
     if (err) launch_fill_i32(idx->err, 1, 0, s);
     if (err & kErrQueryNorm) idx->tab_force_zero = true;
     if (err & kErrQueryNorm)
@@ -899,7 +906,16 @@ int search_host(warp_index* idx, const float* queries, int32_t n_queries, int32_
                 (int32_t*)idx->st_counts.p,  sel ? (int32_t*)idx->st_sel.p : nullptr,
                 m ? (int64_t*)idx->st_m.p : nullptr, bitmap ? (uint32_t*)idx->st_bitmap.p : nullptr,
                 scored ? (int64_t*)idx->st_scored.p : nullptr};
-    rc = enqueue_search(idx, (const float*)idx->st_q.p, n_queries, n_qtok, nprobe, t_prime, k, o, s);
+    // A band of the selection that overflowed (a degenerate centroid set) is retried once with the
+    // selection that sorts every score, which has no band to overflow.
+    int32_t bits = 0;
+    for (int attempt = 0; attempt < 2; ++attempt) {
+        idx->force_full_select = attempt == 1;
+        rc = enqueue_search(idx, (const float*)idx->st_q.p, n_queries, n_qtok, nprobe, t_prime, k, o, s);
+        if (!rc) rc = read_device_errors(idx, s, &bits);
+        idx->force_full_select = false;
+        if (!(rc == WARP_ENOTSUP && (bits & kErrSelOverflow) && attempt == 0)) break;
+    }
     if (rc) return rc;
     HIP_TRY(hipMemcpyAsync(ids, o.ids, nk * 4, hipMemcpyDeviceToHost, s));
     HIP_TRY(hipMemcpyAsync(scores, o.scores, nk * 4, hipMemcpyDeviceToHost, s));
@@ -910,7 +926,8 @@ int search_host(warp_index* idx, const float* queries, int32_t n_queries, int32_
     if (bitmap)
         HIP_TRY(hipMemcpyAsync(bitmap, o.bitmap, (size_t)n_queries * words * 4, hipMemcpyDeviceToHost, s));
     if (scored) HIP_TRY(hipMemcpyAsync(scored, o.scored, (size_t)n_queries * 8, hipMemcpyDeviceToHost, s));
-    return read_device_errors(idx, s);
+    HIP_TRY(hipStreamSynchronize(s));
+    return WARP_OK;
 }
 
 // The no-allocation scratch laid out for waves of qw queries of T tokens (nprobe P, k results), in

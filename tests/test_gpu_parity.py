@@ -140,6 +140,35 @@ def test_large_nprobe_and_k(case):
         run_both(data, label=f"large seed {seed} literal", literal=True)
 
 
+def test_selection_band_overflow_falls_back_to_sorting():
+    """2,000 identical centroids and a query token equal to them: all 2,000 share the top
+    selection bin, more than the 1,024 that the band rescoring holds. The blocking search runs
+    again with the selection that sorts every score and must give the oracle's results; the
+    asynchronous one reports WARP_ENOTSUP at sync, and the index keeps working."""
+    import dataclasses
+
+    import torch
+
+    w = _engine()
+    wl = synth.random_small_workload(30, n_centroids=3000, n_docs=2000, max_len=12, nbits=4, n_queries=3,
+                                     n_qtok=8, nprobe=32, t_prime=500, k=20)
+    data = synth.make_index(wl, workers=1)
+    C = data.centroids.copy()
+    C[1:2001] = C[0]
+    Q = data.queries.copy()
+    Q[0, 0] = C[0]
+    data = dataclasses.replace(data, centroids=C, queries=Q)
+    run_both(data, label="band overflow, blocking search")
+    with w.Index.from_synthetic(data) as ix:
+        say("[band overflow] asynchronous search")
+        ix.search_async(torch.from_numpy(Q).cuda(), wl.nprobe, wl.t_prime, wl.k)
+        with pytest.raises(w.WarpError) as e:
+            ix.sync()
+        assert e.value.code == w.ENOTSUP and "overflow" in e.value.msg
+        compare(ix.search_debug(Q[1:], wl.nprobe, wl.t_prime, wl.k),
+                oracle.search_index(data, queries=Q[1:]), label="band overflow, after the error")
+
+
 @pytest.mark.parametrize("slices", ["3", "7"])
 def test_split_selection(slices, monkeypatch):
     """Waves of few tokens split each token's selection over several workgroups (histogram and
