@@ -1,8 +1,9 @@
 // Exact paths for requests beyond what the selection and top-k kernels hold in LDS
-// (n_probe above kMaxProbe, k above kMaxK): whole score lists are sorted with the device
+// (n_probe above kMaxProbe, k above kMaxK, and a selection band of more than kSelCap
+// centroids in the blocking search's retry): whole score lists are sorted with the device
 // radix sort, which gives the definitions of Sections 4.3 and 4.5 directly.
 //
-// Selection (Section 4.3) for n_probe > kMaxProbe: every (token, centroid) score S64 in
+// Selection (Section 4.3): every (token, centroid) score S64 in
 // fp64 (dimension order, as everywhere), sorted per token into (score desc, id asc) order
 // (a 64-bit key sort, then a stable sort by token); then, per token, the n_probe first
 // centroids, their fixed-point scores and size prefix, and m_i = the score of the first
@@ -21,6 +22,10 @@ hipError_t sort_u64(void* temp, size_t* temp_bytes, const uint64_t* keys_in, uin
                     const int64_t* vals_in, int64_t* vals_out, int64_t n, int end_bit, hipStream_t s);
 hipError_t sort_u32(void* temp, size_t* temp_bytes, const uint32_t* keys_in, uint32_t* keys_out,
                     const int64_t* vals_in, int64_t* vals_out, int64_t n, int end_bit, hipStream_t s);
+size_t sort_u64_temp_bytes(int64_t n, bool vals);
+size_t sort_u32_temp_bytes(int64_t n, bool vals);
+
+static size_t al256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 // ascending order of these keys is (score desc); S64 is never -0.0 (its sum starts at +0.0)
 __device__ __forceinline__ uint64_t desc_key(double x) {
@@ -128,15 +133,11 @@ __global__ __launch_bounds__(kWalkThreads) void k_select_walk(WaveArgs a, const 
 }
 
 // Sort scratch of the exact selection of n_tok tokens: keys and values twice, the token
-// keys twice, and the sorts' temporary storage; returns the bytes (layout: al-aligned pieces).
-static size_t al256(size_t b) { return (b + 255) & ~(size_t)255; }
-
+// keys twice, and the sorts' temporary storage, in 256-byte aligned pieces; returns the bytes.
 size_t select_full_bytes(int64_t n_tok, int32_t n_c) {
     const int64_t n = n_tok * n_c;
-    size_t t1 = 0, t2 = 0;
-    (void)sort_u64(nullptr, &t1, nullptr, nullptr, (const int64_t*)1, nullptr, n, 64, nullptr);
-    (void)sort_u32(nullptr, &t2, nullptr, nullptr, (const int64_t*)1, nullptr, n, 32, nullptr);
-    return 2 * al256((size_t)n * 8) + 2 * al256((size_t)n * 8) + 2 * al256((size_t)n * 4) + al256(std::max(t1, t2));
+    const size_t t = std::max(sort_u64_temp_bytes(n, true), sort_u32_temp_bytes(n, true));
+    return 2 * al256((size_t)n * 8) + 2 * al256((size_t)n * 8) + 2 * al256((size_t)n * 4) + al256(t);
 }
 
 hipError_t launch_select_full(const WaveArgs& a, void* scratch, hipStream_t s) {
@@ -193,9 +194,7 @@ __global__ void k_topk_sorted(WaveArgs a, const uint64_t* __restrict__ nk, int q
 }
 
 size_t topk_full_bytes(int32_t n_docs) {
-    size_t t = 0;
-    (void)sort_u64(nullptr, &t, nullptr, nullptr, nullptr, nullptr, n_docs, 64, nullptr);
-    return 2 * al256((size_t)n_docs * 8) + al256(t);
+    return 2 * al256((size_t)n_docs * 8) + al256(sort_u64_temp_bytes(n_docs, false));
 }
 
 hipError_t launch_topk_full(const WaveArgs& a, void* scratch, hipStream_t s) {

@@ -257,6 +257,10 @@ static hipError_t radix_sort(void* temp, size_t* temp_bytes, const K* keys_in, K
     return hipGetLastError();
 }
 
+// Temporary bytes of sort_u64 / sort_u32 of n keys, with 64-bit values if vals.
+size_t sort_u64_temp_bytes(int64_t n, bool vals) { return sort_temp_bytes(n, vals, 8); }
+size_t sort_u32_temp_bytes(int64_t n, bool vals) { return sort_temp_bytes(n, vals, 4); }
+
 hipError_t sort_u64(void* temp, size_t* temp_bytes, const uint64_t* keys_in, uint64_t* keys_out,
                     const int64_t* vals_in, int64_t* vals_out, int64_t n, int end_bit, hipStream_t s) {
     return radix_sort<uint64_t>(temp, temp_bytes, keys_in, keys_out, vals_in, vals_out, n, end_bit, s);
