@@ -55,6 +55,13 @@
  * Top-k. The final selection visits only the blocks of 256 documents whose best
  * score can reach the k-th, when at most WARP_TOPK_LIST_BLOCKS (default and
  * largest 4096; 0 turns this off) such blocks exist; results do not depend on it.
+ *
+ * Other tuning variables, none of which changes a result: WARP_MAX_SCRATCH_BYTES
+ * caps an index's search scratch (a search that needs more fails with
+ * WARP_ENOMEM); WARP_NARROW_MAX sets the most probing tokens of a cluster chunk
+ * scored by the few-token scan (default 3 for waves of at most 16 queries, else
+ * 0); WARP_SELECT_SLICES sets the workgroups per token of the centroid selection
+ * (default: several per token for waves of at most 256 tokens, else one).
  */
 #ifndef WARP_H
 #define WARP_H

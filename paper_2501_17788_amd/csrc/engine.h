@@ -11,8 +11,8 @@ namespace warp {
 constexpr int kDim = 128;          // token embedding dimension
 constexpr int kFrac = 26;          // fixed-point fraction bits of token and doc scores
 constexpr int kMaxQtok = 32;       // query_maxlen
-constexpr int kMaxProbe = 256;     // largest n_probe the selection and scan kernels hold
-constexpr int kMaxK = 4096;        // largest k the device top-k sorts
+constexpr int kMaxProbe = 256;     // largest n_probe of the band selection; above, the sorting one
+constexpr int kMaxK = 4096;        // largest k of the LDS top-k; above, every key is sorted
 constexpr int kMaxDocs = 1 << 24;  // document ids packed into the low 24 bits of a sort key
 constexpr int kTopkListCap = 4096;  // blocks of 256 documents the top-k's pruned passes can list
 // A token-max cell holds t plus the bias of its query's epoch (an order-preserving bias, see

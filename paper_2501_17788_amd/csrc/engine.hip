@@ -95,7 +95,7 @@ struct warp_index {
     DevBuf list_rec, list_item, cblk;  // the wave's probed chunks (see WaveArgs)
     DevBuf list_rec2;                  // the wave's probed chunks of the narrow scan
     DevBuf scan_queue;
-    DevBuf full_sel, full_topk;  // sort scratch of n_probe > kMaxProbe and of k > kMaxK
+    DevBuf full_sel, full_topk;  // sort scratch of the sorting selection and of k > kMaxK
     DevBuf sel_hist, sel_lists, sel_cnt;  // split selection of small waves
     bool force_full_select = false;       // the blocking search's retry after a selection overflow
     int32_t scoring = WARP_SCORING_PAPER;
@@ -585,8 +585,8 @@ int reserve(warp_index* idx, int32_t qw, int32_t T, int32_t P, int32_t k, hipStr
 // Queries per wave: as many as the scratch budget holds. The budget is
 // WARP_SCRATCH_MB if set, else 80% of the device memory that is free or already
 // held as scratch by this index. A larger wave lets the cluster-major scan read
-// each probed cluster once for more queries. With n_probe above kMaxProbe the exact
-// selection sorts the wave's n_tok n_c scores, at most 2^31 of them.
+// each probed cluster once for more queries. The sorting selection sorts the wave's
+// n_tok n_c scores, at most 2^31 of them.
 int32_t wave_queries(const warp_index* idx, int32_t n_queries, int32_t T, int32_t P) {
     const size_t held = idx->tokmax.bytes + idx->filter.bytes + idx->keys.bytes + idx->plist.bytes +
                         idx->qdig.bytes;
@@ -688,7 +688,7 @@ struct WaveScratch {
     int4 *list_rec, *list_rec2;
     int64_t *list_item, *cblk;
     uint32_t* scan_queue;
-    void *full_sel, *full_topk;  // sort scratch of n_probe > kMaxProbe and of k > kMaxK
+    void *full_sel, *full_topk;  // sort scratch of the sorting selection and of k > kMaxK
     unsigned long long* sel_hist;  // split selection: histograms, band lists and counts of up
     int32_t *sel_lists, *sel_cnt;  // to split_cap tokens
     int64_t split_cap;
