@@ -626,8 +626,9 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
     const int rt = li / 5, rs = li - 5 * (li / 5);
 
     // The chunks of this wave: p, p + stride, ... While a chunk is scored, the next one's
-    // documents are in flight; inside a chunk, the code words of tile t + 2 are loaded while
-    // tile t is scored (a rolled loop keeps the registers few and the waves many).
+    // documents and its first group's pair-list entries are in flight (so that group's query
+    // operand loads wait on nothing); inside a chunk, the code words of tile t + 2 are loaded
+    // while tile t is scored (a rolled loop keeps the registers few and the waves many).
     struct NrChunk {
         int64_t e0;
         int len, p0, nt;  // embeddings (1 .. kMxChunk), first pair, probing tokens (1 .. narrow_max)
@@ -646,19 +647,36 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
 #pragma unroll
         for (int j = 0; j < kMxChunk / 64; ++j) dd[j] = 64 * j + lane < c.len ? doc_ids[c.e0 + 64 * j + lane] : -1;
     };
+    // A group's per-lane inputs from the pair list: the query-operand row's wave token, and the
+    // token lane group lg folds with its centroid term.
+    struct NrGroup {
+        int trow, tok;
+        unsigned cterm;
+    };
+    auto load_group = [&](const NrChunk& c, int g0, NrGroup& g) {
+        const int ng = c.nt - g0 < kNrGroup ? c.nt - g0 : kNrGroup;
+        g.trow = li < 5 * ng ? plist[2 * (c.p0 + g0 + rt)] : -1;
+        const bool mine = lg < ng;
+        g.cterm = mine ? (unsigned)plist[2 * (c.p0 + g0 + lg) + 1] : 0u;
+        g.tok = mine ? plist[2 * (c.p0 + g0 + lg)] : 0;
+    };
     int64_t p = (int64_t)blockIdx.x * NW + wave;
     if (p >= n_list) return;  // wave-uniform; no barrier follows
     NrChunk cur = chunk_at(p);
     int d[kMxChunk / 64];
     load_docs(cur, d);
+    NrGroup first;  // the first group of the current chunk, loaded one chunk ahead
+    load_group(cur, 0, first);
     for (;;) {
         const int64_t pn = p + stride;
         const bool has_next = pn < n_list;  // wave-uniform
         NrChunk nx = cur;
         int dn[kMxChunk / 64] = {};
+        NrGroup first_n;
         if (has_next) {
             nx = chunk_at(pn);
             load_docs(nx, dn);
+            load_group(nx, 0, first_n);
         }
         const int64_t e0 = cur.e0;
         const int len = cur.len, p0 = cur.p0, nt = cur.nt;
@@ -691,8 +709,11 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
         const int n_tiles = (len + 15) >> 4;
         for (int g0 = 0; g0 < nt; g0 += kNrGroup) {  // wave-uniform
             const int ng = nt - g0 < kNrGroup ? nt - g0 : kNrGroup;
+            NrGroup gin;
+            if (g0 == 0) gin = first;  // wave-uniform
+            else load_group(cur, g0, gin);
             // query operand: row (rt, rs) takes digit plane rs - j of token g0 + rt in K segment j
-            const int trow = li < 5 * ng ? plist[2 * (p0 + g0 + rt)] : -1;
+            const int trow = gin.trow;
             v4i Q[3][2];
 #pragma unroll
             for (int j = 0; j < 3; ++j) {
@@ -704,8 +725,8 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
                 }
             }
             const bool mine = lg < ng;  // this lane group folds token g0 + lg
-            const unsigned cterm = mine ? (unsigned)plist[2 * (p0 + g0 + lg) + 1] : 0u;
-            const int mytok = mine ? plist[2 * (p0 + g0 + lg)] : 0;  // its wave token (the flush's row)
+            const unsigned cterm = gin.cterm;
+            const int mytok = gin.tok;  // its wave token (the flush's row)
             unsigned c0[NBITS], c1[NBITS];
             load_code_words<NBITS>(tile_row(0), lg, c0);
             load_code_words<NBITS>(tile_row(1), lg, c1);
@@ -766,6 +787,7 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
         if (!has_next) break;
         p = pn;
         cur = nx;
+        first = first_n;
 #pragma unroll
         for (int j = 0; j < kMxChunk / 64; ++j) d[j] = dn[j];
     }
