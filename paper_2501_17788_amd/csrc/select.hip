@@ -357,9 +357,21 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
     // 1. histogram: one packed (count, size) word per bin
     const uint16_t* bins = a.filter_bins + (int64_t)t * n_c;
     const int32_t* sizes = a.sizes;
+    // split: the token's histogram, and its two band lists read whole beside their counts (entries
+    // past a count are unused), all in flight together
     if (SPLIT) {
         const unsigned long long* g = a.sel_hist + (int64_t)t * kSelBins;
         for (int i = tid; i < kSelBins; i += NT) hist[i] = g[i];
+        const int32_t* cnt = a.sel_cnt + 2 * (int64_t)t;
+        const int32_t* listA = a.sel_lists + 2 * (int64_t)t * kSelCap;
+        for (int p = tid; p < kSelCap; p += NT) {
+            idA[p] = listA[p];
+            idB[p] = listA[kSelCap + p];
+        }
+        if (tid == 0) {  // after its zeroing above
+            s_nA = cnt[0];
+            s_nB = cnt[1];
+        }
     } else {
         for_each_bin(bins, n_c, [&](int c, int b) {
             atomicAdd(&hist[b], kCntOne | (unsigned long long)sizes[c]);
@@ -374,20 +386,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(WaveArgs a) {
     const SelBand band = sel_band(bd.bP, bd.bt, bd.blo);
     const bool clamp = band.clamp;
     const int bt_hi = band.hi;
-    if (SPLIT) {
-        // both lists are read whole, beside their counts (entries past a count are unused)
-        const int32_t* cnt = a.sel_cnt + 2 * (int64_t)t;
-        const int32_t* listA = a.sel_lists + 2 * (int64_t)t * kSelCap;
-        const int nA0 = cnt[0], nB0 = cnt[1];
-        for (int p = tid; p < kSelCap; p += NT) {
-            idA[p] = listA[p];
-            idB[p] = listA[kSelCap + p];
-        }
-        if (tid == 0) {
-            s_nA = nA0;
-            s_nB = nB0;
-        }
-    } else {
+    if (!SPLIT) {
         for_each_bin(bins, n_c, [&](int c, int b) {
             if (b >= band.bA) {
                 const int p = atomicAdd(&s_nA, 1);
