@@ -175,6 +175,53 @@ __device__ __forceinline__ void decode_weight_digits(const unsigned (&wj)[NBITS]
     }
 }
 
+// One operand of decode_weight_digits, W[p][s], alone (p and s are compile-time after
+// unrolling), so that a caller can decode each operand just before its MFMA.
+template <int NBITS>
+__device__ __forceinline__ v4i weight_operand(const unsigned (&wj)[NBITS], const unsigned (&tab)[3][4],
+                                              const unsigned* s_wd, int p, int s) {
+    v4i w;
+    if (NBITS == 4) {
+#pragma unroll
+        for (int mm = 0; mm < 2; ++mm) {
+            const int m = 2 * s + mm;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const unsigned x = h == 0 ? (wj[m % NBITS] >> 4) & 0x0F0F0F0Fu : wj[m % NBITS] & 0x0F0F0F0Fu;
+                const unsigned x7 = x & 0x07070707u;
+                const unsigned pick = ((x >> 1) & 0x04040404u) | 0x03020100u;
+                const unsigned lo8 = __builtin_amdgcn_perm(tab[p][1], tab[p][0], x7);
+                const unsigned hi8 = __builtin_amdgcn_perm(tab[p][3], tab[p][2], x7);
+                w[2 * mm + h] = (int)__builtin_amdgcn_perm(hi8, lo8, pick);
+            }
+        }
+    } else if (NBITS == 2) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const unsigned x = (wj[s % NBITS] >> (6 - 2 * u)) & 0x03030303u;
+            w[u] = (int)__builtin_amdgcn_perm(tab[p][0], tab[p][0], x);
+        }
+    } else if (NBITS == 1) {
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            const unsigned x = (wj[0] >> (4 * s + kk)) & 0x01010101u;
+            w[kk] = (int)__builtin_amdgcn_perm(tab[p][0], tab[p][0], x);
+        }
+    } else {
+#pragma unroll
+        for (int mm = 0; mm < 4; ++mm) {
+            const unsigned wm = wj[(4 * s + mm) % NBITS];
+            const unsigned e0 = s_wd[wm & 255u], e1 = s_wd[(wm >> 8) & 255u];
+            const unsigned e2 = s_wd[(wm >> 16) & 255u], e3 = s_wd[wm >> 24];
+            const unsigned sel = 0x0C0C0000u | ((unsigned)(4 + p) << 8) | (unsigned)p;
+            const unsigned lo2 = __builtin_amdgcn_perm(e1, e0, sel);
+            const unsigned hi2 = __builtin_amdgcn_perm(e3, e2, sel);
+            w[mm] = (int)__builtin_amdgcn_perm(hi2, lo2, 0x05040100u);
+        }
+    }
+    return w;
+}
+
 // A lane's code words of embedding `row` (null: zeros) in the tile layout: 4 * NBITS bytes
 // at lane group lg of the embedding's code row.
 template <int NBITS>
@@ -183,6 +230,25 @@ __device__ __forceinline__ void load_code_words(const uint8_t* row, int lg, unsi
     for (int m = 0; m < NBITS; ++m) wj[m] = 0;
     if (!row) return;
     row += 4 * NBITS * lg;
+    if (NBITS == 8) {
+        const uint4 v0 = reinterpret_cast<const uint4*>(row)[0];
+        const uint4 v1 = reinterpret_cast<const uint4*>(row)[1];
+        wj[0] = v0.x; wj[1 % NBITS] = v0.y; wj[2 % NBITS] = v0.z; wj[3 % NBITS] = v0.w;
+        wj[4 % NBITS] = v1.x; wj[5 % NBITS] = v1.y; wj[6 % NBITS] = v1.z; wj[7 % NBITS] = v1.w;
+    } else if (NBITS == 4) {
+        const uint4 v = *reinterpret_cast<const uint4*>(row);
+        wj[0] = v.x; wj[1 % NBITS] = v.y; wj[2 % NBITS] = v.z; wj[3 % NBITS] = v.w;
+    } else if (NBITS == 2) {
+        const uint2 v = *reinterpret_cast<const uint2*>(row);
+        wj[0] = v.x; wj[1 % NBITS] = v.y;
+    } else {
+        wj[0] = *reinterpret_cast<const unsigned*>(row);
+    }
+}
+
+// The code words at `row` (already offset to the lane group's bytes), which must exist.
+template <int NBITS>
+__device__ __forceinline__ void load_code_words_from(const uint8_t* row, unsigned (&wj)[NBITS]) {
     if (NBITS == 8) {
         const uint4 v0 = reinterpret_cast<const uint4*>(row)[0];
         const uint4 v1 = reinterpret_cast<const uint4*>(row)[1];
@@ -307,7 +373,7 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
     // of consecutive threads are contiguous, and the 16 tokens of an operand read lie 400 bytes apart
     __shared__ v4i s_q[kMxGroup][NSLOT + 1];
     __shared__ unsigned s_cterm[kMxGroup];   // R(S64) + the cell bias of each token (0 past the group)
-    __shared__ __attribute__((aligned(16))) int64_t s_row[kMxGroup];  // its token-max row offset
+    __shared__ __attribute__((aligned(16))) int64_t s_row[2][kMxGroup];  // its token-max row offset
     __shared__ unsigned s_tab[kMxGroup * TPAD];  // max score of (token, document run of the chunk)
     __shared__ __attribute__((aligned(16))) int s_run[kMxChunk];  // run of each chunk embedding (kMxChunk past its end)
     __shared__ int s_rdoc[kMxChunk];         // document of each run
@@ -441,27 +507,38 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
         nx = decode_item(nxi);
         load_tokens(nx, ptok);
     }
-
-    // The runs of the chunk in LDS (s_run, s_rdoc, s_rstart, n_runs) and the codes in w stay
-    // valid while consecutive items share a chunk (the token groups of one chunk).
-    int64_t run_e0 = -1;  // first embedding of the chunk whose runs are in LDS
-    int n_runs = 0;
-    for (;;) {
-        __syncthreads();  // the previous item's table is flushed and its tokens are no longer read
-        // stage the item from registers
-        if (tid < kMxGroup) {  // tokens past the group's end have zero digits and centroid terms: score 0 = absent
-            const unsigned b = tid < it.np ? (unsigned)st.base : 0u;  // R(S64) + the cell bias
-            s_cterm[tid] = b;
-            s_row[tid] = (int64_t)st.tok * a.n_docs;
+    // stage an item from registers: tokens past the group's end have zero digits and centroid
+    // terms (score 0 = absent); the token-max row offsets alternate between two buffers, since
+    // the previous item's flush still reads its own
+    auto stage = [&](const MxItem& x, int par) {
+        if (tid < kMxGroup) {
+            s_cterm[tid] = tid < x.np ? (unsigned)st.base : 0u;  // R(S64) + the cell bias
+            s_row[par][tid] = (int64_t)st.tok * a.n_docs;
         }
 #pragma unroll
         for (int i = 0; i < QPT; ++i) {
             const int k = tid + kMxBlock * i;
             s_q[k / NSLOT][k % NSLOT] = st.q[i];
         }
-        if (tid == 0 && claimed) s_claim = claim;  // after the wait for the staged data
+        if (tid == 0 && claimed) s_claim = claim;
+    };
+    stage(it, 0);
+
+    // The runs of the chunk in LDS (s_run, s_rdoc, s_rstart, n_runs) and the codes in w stay
+    // valid while consecutive items share a chunk (the token groups of one chunk).
+    int64_t run_e0 = -1;  // first embedding of the chunk whose runs are in LDS
+    int n_runs = 0;
+    int par = 0;  // buffer of s_row staged for the current item
+    for (;;) {
+        // the item is staged, and the previous item's flush has read and reset the table and
+        // read the runs
+        __syncthreads();
+        if (claimed) {
+            nb = (int64_t)s_claim * kScanBatch;
+            claimed = false;
+        }
         // runs of equal documents along a new chunk (ids ascend inside a cluster)
-        if (it.e0 != run_e0) {  // wave-uniform
+        if (it.e0 != run_e0) {  // uniform over the workgroup
             run_e0 = it.e0;
             const bool e_in = st.doc >= 0;
             const int doc = st.doc;
@@ -481,16 +558,12 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
                 s_rdoc[run] = doc;
                 s_rstart[run] = tid;
             }
+            __syncthreads();
         }
-        // prefetch: the next item's query digits, bases and documents, then (once a claim
-        // is published) the tokens of the item after it
+        // prefetch: the next item's query digits, bases and documents, then (with the claim
+        // published above) the tokens of the item after it
         const bool has_next = nxi >= 0;
         if (has_next) load_stage(nx, ptok, st, nx.e0 != it.e0);
-        __syncthreads();
-        if (claimed) {
-            nb = (int64_t)s_claim * kScanBatch;
-            claimed = false;
-        }
         MxItem nn = nx;
         const int64_t nni = has_next ? next_item() : -1;
         if (nni >= 0) {
@@ -498,15 +571,23 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
             load_tokens(nn, ptok);
         }
 
+        // the next item's codes replace each tile's codes once they are decoded (the same
+        // codes serve the next item of the same chunk)
+        const bool next_codes = has_next && nx.e0 != it.e0;
         const int n_et = (int)((it.e1 - it.e0 + 15) >> 4);
         const int n_tt = (it.np + 15) >> 4;
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
             const int et = wave + NW * j;
-            if (et >= n_et) break;  // wave-uniform
+            const bool tile_in = et < n_et;  // wave-uniform
             // weight digits of the tile (MFMA A operand: row li = embedding e0 + 16 et + li)
             v4i A[3][2];
-            decode_weight_digits<NBITS>(w[j], tab, s_wd, A);
+            if (tile_in) decode_weight_digits<NBITS>(w[j], tab, s_wd, A);
+            if (next_codes) {
+                const int64_t er = nx.e0 + 16 * et + li;
+                load_code_words<NBITS>(er < nx.e1 ? codes + er * BYTES : nullptr, lg, w[j]);
+            }
+            if (!tile_in) continue;
 
             for (int tt = 0; tt < n_tt; ++tt) {
                 // class accumulators; class 0 starts at the rounding half
@@ -537,9 +618,13 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
                               mx_fold(acc[0][r], acc[1][r], acc[2][r], acc[3][r], acc[4][r]) + cterm);
             }
         }
-        // the next item's codes, in flight during the flush (the same codes for the same chunk)
-        if (has_next && nx.e0 != it.e0) load_codes(nx, w);
-        __syncthreads();
+        __syncthreads();  // the table is complete, and the item's digits and terms are no longer read
+        // Every load of the next item (staged data, codes, the claim) has landed before the
+        // flush's atomics are issued. Vector memory operations complete in issue order, so a
+        // wait for a load issued after the atomics would also wait for them; none follows
+        // before the next item's flush, by which time they are long done.
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+        if (has_next) stage(nx, par ^ 1);
         // flush: one device atomic per (token, run). With R = 2^lr the power of two at or above
         // the run count, thread tid takes run tid mod R of tokens tid / R, tid / R + 256 / R, ...:
         // consecutive lanes take consecutive runs of one token (ascending documents of one
@@ -556,11 +641,12 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
                 unsigned* cell = &s_tab[tk * TPAD + rn];
                 const unsigned v = *cell;
                 *cell = kTokAbsent;
-                const int64_t o = s_row[tk] + rdoc;
+                const int64_t o = s_row[par][tk] + rdoc;
                 atomicMax(&tokmax[o], v);
                 if (a.tokcnt) atomicAdd(&a.tokcnt[o], len);
             }
         }
+        par ^= 1;
         if (!has_next) break;
         it = nx;
         nx = nn;
@@ -586,23 +672,34 @@ __device__ __forceinline__ void wave_lds_sync() {
 // embedding e; lane group g folds token g, taking the rows it lacks from lane group g + 1.
 // Scores go into the wave's LDS table of (token, run) maxima, flushed with one device
 // atomicMax per (token, run) after each group.
+//
+// Vector memory operations complete in issue order, so after a flush's atomics any wait for a
+// load also waits for them. The wave therefore waits once per group, just before its flush,
+// for everything the next group needs, and then runs a whole chunk of work before its next
+// wait: while chunk c is scored, the pair-list entries of chunk c + 2's first group, the
+// query digit rows of chunk c + 1's first group and the documents of chunk c + 1 are in
+// flight, and the code words stream through DEPTH buffers (below). The query rows go through
+// LDS into the operand registers, which are free once a group's tiles are scored.
 template <int NBITS>
 __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
     constexpr int BYTES = kDim * NBITS / 8;
     constexpr int NW = kMxBlock / 64;
-    constexpr int NT = kMxChunk / 16;  // tiles of a chunk
-    constexpr int NSLOT = 24;          // 16-byte query digit slots of a token
+    constexpr int NSLOT = 24;                   // 16-byte query digit slots of a token
+    constexpr int QSLOTS = kNrGroup * NSLOT;    // slots of a group's query rows
+    constexpr int DEPTH = NBITS <= 4 ? 4 : 2;  // code-word buffers of the tile stream
     constexpr int TPAD = kMxChunk + 4;
     static_assert(kMxChunk % 64 == 0 && kMxChunk <= 4 * 64, "four rounds of the run pass");
     static_assert(5 * kNrGroup <= 16, "rows of a group's tile");
+    static_assert(QSLOTS > 64 && QSLOTS <= 128, "two query-row slots per lane");
     __shared__ unsigned s_tab[NW][kNrGroup * TPAD];  // (token of the group, run) maxima
     __shared__ int s_run[NW][kMxChunk];              // run of each embedding of the chunk
     __shared__ int s_rdoc[NW][kMxChunk];             // document of each run
     __shared__ int s_rstart[NW][kMxChunk + 1];       // its first embedding; the chunk's length after the last
+    __shared__ v4i s_qrow[NW][QSLOTS];               // query digit rows of the next group's tokens
     __shared__ unsigned s_wd[NBITS == 8 ? 256 : 1];
 
     const int tid = threadIdx.x;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: the plan reads are scalar
     const int lane = tid & 63;
     const int li = lane & 15;  // embedding of a tile (column), or row of the query operand
     const int lg = lane >> 4;  // lane group: rows 4 lg .. 4 lg + 3 of the output; token lg of the group
@@ -614,6 +711,7 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
     int* runs = s_run[wave];
     int* rdoc = s_rdoc[wave];
     int* rstart = s_rstart[wave];
+    v4i* qrow = s_qrow[wave];
     for (int i = lane; i < kNrGroup * TPAD; i += 64) stab[i] = kTokAbsent;
     const int64_t n_list = plan_load(a.list_n2, 0);
     const v4i* qdig = reinterpret_cast<const v4i*>(a.qdig);
@@ -625,10 +723,6 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
     // row (token, class) of this lane in the query operand, and its shifts for the fold
     const int rt = li / 5, rs = li - 5 * (li / 5);
 
-    // The chunks of this wave: p, p + stride, ... While a chunk is scored, the next one's
-    // documents and its first group's pair-list entries are in flight (so that group's query
-    // operand loads wait on nothing); inside a chunk, the code words of tile t + 2 are loaded
-    // while tile t is scored (a rolled loop keeps the registers few and the waves many).
     struct NrChunk {
         int64_t e0;
         int len, p0, nt;  // embeddings (1 .. kMxChunk), first pair, probing tokens (1 .. narrow_max)
@@ -647,43 +741,94 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
 #pragma unroll
         for (int j = 0; j < kMxChunk / 64; ++j) dd[j] = 64 * j + lane < c.len ? doc_ids[c.e0 + 64 * j + lane] : -1;
     };
-    // A group's per-lane inputs from the pair list: the query-operand row's wave token, and the
-    // token lane group lg folds with its centroid term.
+    // A group's pair-list entries, per lane: the wave tokens of the query-row slots lane and
+    // 64 + lane (-1: none), and the wave token and centroid term of the token lane group lg folds.
     struct NrGroup {
-        int trow, tok;
+        int wa, wb, tok;
         unsigned cterm;
     };
     auto load_group = [&](const NrChunk& c, int g0, NrGroup& g) {
         const int ng = c.nt - g0 < kNrGroup ? c.nt - g0 : kNrGroup;
-        g.trow = li < 5 * ng ? plist[2 * (c.p0 + g0 + rt)] : -1;
+        const int64_t p0 = (int64_t)c.p0 + g0;
+        const int ta = lane / NSLOT, tb = (64 + lane) / NSLOT;
+        g.wa = ta < ng ? plist[2 * (p0 + ta)] : -1;
+        g.wb = 64 + lane < QSLOTS && tb < ng ? plist[2 * (p0 + tb)] : -1;
         const bool mine = lg < ng;
-        g.cterm = mine ? (unsigned)plist[2 * (c.p0 + g0 + lg) + 1] : 0u;
-        g.tok = mine ? plist[2 * (c.p0 + g0 + lg)] : 0;
+        g.cterm = mine ? (unsigned)plist[2 * (p0 + lg) + 1] : 0u;
+        g.tok = mine ? plist[2 * (p0 + lg)] : 0;
     };
+    // the group's query digit rows (slots of tokens past the group are zero)
+    auto load_qrows = [&](const NrGroup& g, v4i& qa, v4i& qb) {
+        const v4i z = {0, 0, 0, 0};
+        qa = g.wa >= 0 ? qdig[(unsigned)(g.wa * NSLOT + lane % NSLOT)] : z;
+        qb = g.wb >= 0 ? qdig[(unsigned)(g.wb * NSLOT + (64 + lane) % NSLOT)] : z;
+    };
+    // query operand from the rows in LDS: row (rt, rs) takes digit plane rs - j of token rt in
+    // K segment j
+    auto stage_q = [&](const v4i& qa, const v4i& qb, v4i (&Q)[3][2]) {
+        qrow[lane] = qa;
+        if (64 + lane < QSLOTS) qrow[64 + lane] = qb;
+        wave_lds_sync();
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+#pragma unroll
+            for (int sl = 0; sl < 2; ++sl) {
+                const int pl = rs - j;
+                Q[j][sl] = li < 5 * kNrGroup && pl >= 0 && pl <= 2 ? qrow[rt * NSLOT + (pl * 2 + sl) * 4 + lg]
+                                                                  : (v4i){0, 0, 0, 0};
+            }
+        }
+    };
+
     int64_t p = (int64_t)blockIdx.x * NW + wave;
     if (p >= n_list) return;  // wave-uniform; no barrier follows
+    // the prologue: chunk p's inputs and its first group's operand, chunk p + stride's
+    // first-group pair-list entries
     NrChunk cur = chunk_at(p);
     int d[kMxChunk / 64];
     load_docs(cur, d);
-    NrGroup first;  // the first group of the current chunk, loaded one chunk ahead
-    load_group(cur, 0, first);
+    NrGroup g_cur, g_nx;
+    load_group(cur, 0, g_cur);
+    v4i Q[3][2];
+    {
+        v4i qa, qb;
+        load_qrows(g_cur, qa, qb);
+        stage_q(qa, qb, Q);
+    }
+    if (p + stride < n_list) load_group(chunk_at(p + stride), 0, g_nx);
+    // The code words of a group's tiles stream through DEPTH buffers: tile u sits in buffer
+    // u % DEPTH, and once it is decoded the buffer takes the tile DEPTH places further along
+    // the wave's sequence of (chunk, group) tile runs, each run padded to a multiple of DEPTH
+    // tiles (padding tiles are not scored). The next run is the chunk's next group, else the
+    // next chunk's first group. Every buffer load is issued, so that the compiler can count the
+    // loads in flight and wait for each buffer alone: a lane with no embedding in the tile
+    // reads the first code row of the chunk instead, and the scores of its column are never
+    // merged.
+    unsigned cb[DEPTH][NBITS];
+    const unsigned lane_off = 4 * NBITS * lg;
+    auto tile_off = [&](int len, int t) -> unsigned {
+        const int e = 16 * t + li;
+        return e < len ? (unsigned)e * BYTES + lane_off : lane_off;
+    };
+    auto chunk_base = [&](const NrChunk& c) { return codes + c.e0 * BYTES; };
+#pragma unroll
+    for (int k = 0; k < DEPTH; ++k) load_code_words_from<NBITS>(chunk_base(cur) + tile_off(cur.len, k), cb[k]);
+    // the prologue's loads, waited for here so that no wait inside the loop is for them
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
     for (;;) {
-        const int64_t pn = p + stride;
+        const int64_t pn = p + stride, pnn = pn + stride;
         const bool has_next = pn < n_list;  // wave-uniform
         NrChunk nx = cur;
         int dn[kMxChunk / 64] = {};
-        NrGroup first_n;
+        NrGroup g_nn = g_nx;
+        v4i qa = {0, 0, 0, 0}, qb = {0, 0, 0, 0};  // query rows of the next chunk's first group
         if (has_next) {
             nx = chunk_at(pn);
             load_docs(nx, dn);
-            load_group(nx, 0, first_n);
+            load_qrows(g_nx, qa, qb);
+            if (pnn < n_list) load_group(chunk_at(pnn), 0, g_nn);
         }
-        const int64_t e0 = cur.e0;
-        const int len = cur.len, p0 = cur.p0, nt = cur.nt;
-        auto tile_row = [&](int t) -> const uint8_t* {
-            const int e = 16 * t + li;
-            return e < len ? codes + (e0 + e) * BYTES : nullptr;
-        };
+        const int len = cur.len, nt = cur.nt;
         // runs of equal documents along the chunk (ids ascend inside a cluster); the chunk's
         // first embedding starts a run
         int n_runs = 0;
@@ -707,69 +852,78 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
         if (lane == 0) rstart[n_runs] = len;
         wave_lds_sync();
         const int n_tiles = (len + 15) >> 4;
-        for (int g0 = 0; g0 < nt; g0 += kNrGroup) {  // wave-uniform
+        const int n_pad = (n_tiles + DEPTH - 1) / DEPTH * DEPTH;
+        // every chunk has a group (nt >= 1): a loop that runs at least once lets the compiler see
+        // that the wait before the flush covers every load of the chunk
+        int g0 = 0;
+        do {  // wave-uniform
             const int ng = nt - g0 < kNrGroup ? nt - g0 : kNrGroup;
-            NrGroup gin;
-            if (g0 == 0) gin = first;  // wave-uniform
-            else load_group(cur, g0, gin);
-            // query operand: row (rt, rs) takes digit plane rs - j of token g0 + rt in K segment j
-            const int trow = gin.trow;
-            v4i Q[3][2];
-#pragma unroll
-            for (int j = 0; j < 3; ++j) {
-#pragma unroll
-                for (int sl = 0; sl < 2; ++sl) {
-                    const int pl = rs - j;
-                    Q[j][sl] = trow >= 0 && pl >= 0 && pl <= 2 ? qdig[(unsigned)(trow * NSLOT + (pl * 2 + sl) * 4 + lg)]
-                                                               : (v4i){0, 0, 0, 0};
-                }
-            }
             const bool mine = lg < ng;  // this lane group folds token g0 + lg
-            const unsigned cterm = gin.cterm;
-            const int mytok = gin.tok;  // its wave token (the flush's row)
-            unsigned c0[NBITS], c1[NBITS];
-            load_code_words<NBITS>(tile_row(0), lg, c0);
-            load_code_words<NBITS>(tile_row(1), lg, c1);
-#pragma unroll 1
-            for (int t = 0; t < n_tiles; ++t) {  // wave-uniform
-                unsigned wt[NBITS];
+            const unsigned cterm = g_cur.cterm;
+            const int mytok = g_cur.tok;  // its wave token (the flush's row)
+            // the run after this one: the next group of this chunk, else the next chunk (if any)
+            const bool more = g0 + kNrGroup < nt;
+            const uint8_t* const cur_base = chunk_base(cur);
+            const uint8_t* const next_base = more || !has_next ? cur_base : chunk_base(nx);
+            const int next_len = more || !has_next ? len : nx.len;
+            const int next_n = more || has_next ? 1 << 30 : 0;  // tiles of the next run (0: none)
+            for (int t0 = 0; t0 < n_pad; t0 += DEPTH) {  // wave-uniform
 #pragma unroll
-                for (int m = 0; m < NBITS; ++m) {
-                    wt[m] = c0[m];
-                    c0[m] = c1[m];
+                for (int k = 0; k < DEPTH; ++k) {
+                    const int t = t0 + k;
+                    // each weight operand decoded just before its MFMA; then the buffer is refilled
+                    // (in place, since its words are no longer read)
+                    v4i acc = {0, 0, 0, 0};
+                    if (t < n_tiles) {  // wave-uniform
+#pragma unroll
+                        for (int sl = 0; sl < 2; ++sl)
+#pragma unroll
+                            for (int j = 0; j < 3; ++j)
+                                acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(
+                                    Q[j][sl], weight_operand<NBITS>(cb[k], tab, s_wd, j, sl), acc, 0, 0, 0);
+                    }
+                    const int u = t + DEPTH;  // stream position of the buffer's next tile
+                    if (u < n_pad) load_code_words_from<NBITS>(cur_base + tile_off(len, u), cb[k]);
+                    else load_code_words_from<NBITS>(next_base + tile_off(u - n_pad < next_n ? next_len : 0, u - n_pad), cb[k]);
+                    if (t >= n_tiles) continue;  // wave-uniform
+                    // token lg's classes s = 0..4 are rows 5 lg + s: rows 4 lg + k of this lane for
+                    // k = lg + s < 4, rows of lane group lg + 1 beyond
+                    const int x0 = __shfl_down(acc[0], 16, 64);
+                    unsigned v;
+                    if (ng == 1) {  // wave-uniform: only lane group 0 folds, rows 0..3 here and row 4
+                        v = mx_fold(acc[0] + (1 << 17), acc[1], acc[2], acc[3], x0) + cterm;
+                    } else {
+                        // with r = (acc[0..3], x0, x1, x2), class s of token lg is r[s + lg]: shift
+                        // by lg & 1, then by lg & 2 (named values, not an array: a select between
+                        // array elements may become an indexed load from private memory)
+                        const int x1 = __shfl_down(acc[1], 16, 64);
+                        const int x2 = __shfl_down(acc[2], 16, 64);
+                        const bool o1 = (lg & 1) != 0, o2 = (lg & 2) != 0;
+                        const int u0 = o1 ? acc[1] : acc[0], u1 = o1 ? acc[2] : acc[1], u2 = o1 ? acc[3] : acc[2];
+                        const int u3 = o1 ? x0 : acc[3], u4 = o1 ? x1 : x0, u5 = o1 ? x2 : x1, u6 = x2;
+                        const int c0s = o2 ? u2 : u0, c1s = o2 ? u3 : u1, c2s = o2 ? u4 : u2;
+                        const int c3s = o2 ? u5 : u3, c4s = o2 ? u6 : u4;
+                        v = mx_fold(c0s + (1 << 17), c1s, c2s, c3s, c4s) + cterm;
+                    }
+                    const int e = 16 * t + li;
+                    if (mine && e < len) atomicMax(&stab[lg * TPAD + runs[e]], v);
                 }
-                load_code_words<NBITS>(tile_row(t + 2), lg, c1);
-                v4i W[3][2];
-                decode_weight_digits<NBITS>(wt, tab, s_wd, W);
-                v4i acc = {0, 0, 0, 0};
-#pragma unroll
-                for (int j = 0; j < 3; ++j)
-#pragma unroll
-                    for (int sl = 0; sl < 2; ++sl)
-                        acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(Q[j][sl], W[j][sl], acc, 0, 0, 0);
-                // token lg's classes s = 0..4 are rows 5 lg + s: rows 4 lg + k of this lane for
-                // k = lg + s < 4, rows of lane group lg + 1 beyond
-                const int x0 = __shfl_down(acc[0], 16, 64);
-                unsigned v;
-                if (ng == 1) {  // wave-uniform: only lane group 0 folds, rows 0..3 here and row 4
-                    v = mx_fold(acc[0] + (1 << 17), acc[1], acc[2], acc[3], x0) + cterm;
-                } else {
-                    // with r = (acc[0..3], x0, x1, x2), class s of token lg is r[s + lg]: shift
-                    // by lg & 1, then by lg & 2 (named values, not an array: a select between
-                    // array elements may become an indexed load from private memory)
-                    const int x1 = __shfl_down(acc[1], 16, 64);
-                    const int x2 = __shfl_down(acc[2], 16, 64);
-                    const bool o1 = (lg & 1) != 0, o2 = (lg & 2) != 0;
-                    const int u0 = o1 ? acc[1] : acc[0], u1 = o1 ? acc[2] : acc[1], u2 = o1 ? acc[3] : acc[2];
-                    const int u3 = o1 ? x0 : acc[3], u4 = o1 ? x1 : x0, u5 = o1 ? x2 : x1, u6 = x2;
-                    const int c0s = o2 ? u2 : u0, c1s = o2 ? u3 : u1, c2s = o2 ? u4 : u2;
-                    const int c3s = o2 ? u5 : u3, c4s = o2 ? u6 : u4;
-                    v = mx_fold(c0s + (1 << 17), c1s, c2s, c3s, c4s) + cterm;
-                }
-                const int e = 16 * t + li;
-                if (mine && e < len) atomicMax(&stab[lg * TPAD + runs[e]], v);
             }
             wave_lds_sync();
+            // the next group's inputs, before the flush: its query operand and fold inputs (for
+            // a later group of this chunk, loaded here; for the next chunk's first group, from
+            // the prefetch), and every load in flight
+            if (more) {  // (only with narrow_max above kNrGroup)
+                load_group(cur, g0 + kNrGroup, g_cur);
+                v4i ga, gb;
+                load_qrows(g_cur, ga, gb);
+                __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+                stage_q(ga, gb, Q);
+            } else {
+                g_cur = g_nx;
+                __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+                if (has_next) stage_q(qa, qb, Q);
+            }
             // flush: one device atomic per (token, run)
             for (int tk = 0; tk < ng; ++tk) {  // wave-uniform
                 const int64_t row = (int64_t)__builtin_amdgcn_readlane(mytok, 16 * tk) * a.n_docs;
@@ -783,11 +937,12 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
                 }
             }
             wave_lds_sync();
-        }
+            g0 += kNrGroup;
+        } while (g0 < nt);
         if (!has_next) break;
         p = pn;
         cur = nx;
-        first = first_n;
+        g_nx = g_nn;
 #pragma unroll
         for (int j = 0; j < kMxChunk / 64; ++j) d[j] = dn[j];
     }
