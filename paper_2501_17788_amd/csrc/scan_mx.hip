@@ -664,12 +664,13 @@ __device__ __forceinline__ void wave_lds_sync() {
 // Narrow scan: the chunks probed by 1..narrow_max tokens of the wave (Sections 4.4 and 4.5,
 // the same arithmetic as k_scan_mx). One wave takes one chunk at a time, with no workgroup
 // barrier: it numbers the chunk's runs of equal documents, then scores the chunk's 16-embedding
-// tiles against groups of up to kNrGroup = 3 tokens. In a group's matrix-core tile the rows
-// are (token t, digit class s) = 5 t + s and the columns are the tile's embeddings; the K
-// dimension runs over (weight-digit plane j, dimension d), and row (t, s) takes query-digit
-// plane s - j of token t (zero outside 0..2), so six v_mfma_i32_16x16x64_i8 give all five
-// class sums A_s of up to three tokens. Lane (e, g) then holds rows 4 g .. 4 g + 3 of
-// embedding e; lane group g folds token g, taking the rows it lacks from lane group g + 1.
+// tiles against groups of up to kNrGroup = 3 tokens. In a group's matrix-core tile the
+// columns are the tile's embeddings and the rows are (token t, digit class s): row 4 t + s for
+// s = 0..3 and row 12 + t for s = 4; the K dimension runs over (weight-digit plane j,
+// dimension d), and row (t, s) takes query-digit plane s - j of token t (zero outside 0..2), so
+// six v_mfma_i32_16x16x64_i8 give all five class sums A_s of up to three tokens. Lane (e, g)
+// then holds rows 4 g .. 4 g + 3 of embedding e: lane group g < 3 holds classes 0..3 of token
+// g and folds it, taking class 4 from lane group 3.
 // Scores go into the wave's LDS table of (token, run) maxima, flushed with one device
 // atomicMax per (token, run) after each group.
 //
@@ -689,7 +690,7 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
     constexpr int DEPTH = NBITS <= 4 ? 4 : 2;  // code-word buffers of the tile stream
     constexpr int TPAD = kMxChunk + 4;
     static_assert(kMxChunk % 64 == 0 && kMxChunk <= 4 * 64, "four rounds of the run pass");
-    static_assert(5 * kNrGroup <= 16, "rows of a group's tile");
+    static_assert(kNrGroup == 3, "rows of a group's tile: four classes of three tokens, then their fifth");
     static_assert(QSLOTS > 64 && QSLOTS <= 128, "two query-row slots per lane");
     __shared__ unsigned s_tab[NW][kNrGroup * TPAD];  // (token of the group, run) maxima
     __shared__ int s_run[NW][kMxChunk];              // run of each embedding of the chunk
@@ -720,8 +721,9 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
     const int32_t* __restrict__ doc_ids = a.doc_ids;
     unsigned* __restrict__ tokmax = a.tokmax;
     const int64_t stride = (int64_t)gridDim.x * NW;
-    // row (token, class) of this lane in the query operand, and its shifts for the fold
-    const int rt = li / 5, rs = li - 5 * (li / 5);
+    // row (token, class) of this lane in the query operand (row 15 is zero)
+    const int rt = li < 12 ? li >> 2 : li - 12, rs = li < 12 ? li & 3 : 4;
+    const int c4_lane = 48 + li;  // the lane holding class 4 of this lane's embedding
 
     struct NrChunk {
         int64_t e0;
@@ -774,7 +776,7 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
 #pragma unroll
             for (int sl = 0; sl < 2; ++sl) {
                 const int pl = rs - j;
-                Q[j][sl] = li < 5 * kNrGroup && pl >= 0 && pl <= 2 ? qrow[rt * NSLOT + (pl * 2 + sl) * 4 + lg]
+                Q[j][sl] = li < 15 && pl >= 0 && pl <= 2 ? qrow[rt * NSLOT + (pl * 2 + sl) * 4 + lg]
                                                                   : (v4i){0, 0, 0, 0};
             }
         }
@@ -886,25 +888,18 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
                     if (u < n_pad) load_code_words_from<NBITS>(cur_base + tile_off(len, u), cb[k]);
                     else load_code_words_from<NBITS>(next_base + tile_off(u - n_pad < next_n ? next_len : 0, u - n_pad), cb[k]);
                     if (t >= n_tiles) continue;  // wave-uniform
-                    // token lg's classes s = 0..4 are rows 5 lg + s: rows 4 lg + k of this lane for
-                    // k = lg + s < 4, rows of lane group lg + 1 beyond
-                    const int x0 = __shfl_down(acc[0], 16, 64);
-                    unsigned v;
-                    if (ng == 1) {  // wave-uniform: only lane group 0 folds, rows 0..3 here and row 4
-                        v = mx_fold(acc[0] + (1 << 17), acc[1], acc[2], acc[3], x0) + cterm;
-                    } else {
-                        // with r = (acc[0..3], x0, x1, x2), class s of token lg is r[s + lg]: shift
-                        // by lg & 1, then by lg & 2 (named values, not an array: a select between
-                        // array elements may become an indexed load from private memory)
-                        const int x1 = __shfl_down(acc[1], 16, 64);
-                        const int x2 = __shfl_down(acc[2], 16, 64);
-                        const bool o1 = (lg & 1) != 0, o2 = (lg & 2) != 0;
-                        const int u0 = o1 ? acc[1] : acc[0], u1 = o1 ? acc[2] : acc[1], u2 = o1 ? acc[3] : acc[2];
-                        const int u3 = o1 ? x0 : acc[3], u4 = o1 ? x1 : x0, u5 = o1 ? x2 : x1, u6 = x2;
-                        const int c0s = o2 ? u2 : u0, c1s = o2 ? u3 : u1, c2s = o2 ? u4 : u2;
-                        const int c3s = o2 ? u5 : u3, c4s = o2 ? u6 : u4;
-                        v = mx_fold(c0s + (1 << 17), c1s, c2s, c3s, c4s) + cterm;
+                    // token lg's classes 0..3 are this lane's acc[0..3]; class 4 is element lg of
+                    // lane c4_lane (lane group 3)
+                    int a4 = __shfl(acc[0], c4_lane, 64);
+                    if (ng > 1) {  // wave-uniform
+                        const int a4b = __shfl(acc[1], c4_lane, 64);
+                        a4 = lg == 1 ? a4b : a4;
+                        if (ng > 2) {
+                            const int a4c = __shfl(acc[2], c4_lane, 64);
+                            a4 = lg == 2 ? a4c : a4;
+                        }
                     }
+                    const unsigned v = mx_fold(acc[0] + (1 << 17), acc[1], acc[2], acc[3], a4) + cterm;
                     const int e = 16 * t + li;
                     if (mine && e < len) atomicMax(&stab[lg * TPAD + runs[e]], v);
                 }
