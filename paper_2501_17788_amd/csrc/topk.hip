@@ -11,6 +11,8 @@
 // K largest keys then lies in a block whose maximum is within D0, and the keys of any
 // other block are smaller than all of these. The passes below visit only those blocks,
 // listed in LDS (all blocks when more than kTopkListCap pass, or no D0 is found). The
+// first pass over their keys gathers every key within D0; if at most kMaxK, these are
+// ranked or sorted and the first K decoded. Otherwise the
 // K largest keys are found in one or two histogram passes over the keys: bins of the
 // distance below the largest score (4096 bins of 2^-6, then, inside the bin holding the
 // K-th key, 4096 bins of 2^-18), after which every key at or above the bin holding the
@@ -206,20 +208,20 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(WaveArgs a) {
                 if (kv[u] != 0) f(kv[u]);
         }
     };
-    // level 1: coarse bins of the distance below the best score. For K <= kRankMax the same
-    // pass gathers every key within D0, a set that holds the K best: when it has at most
-    // kRankMax keys, they are ranked directly and the passes below are skipped.
+    // level 1: coarse bins of the distance below the best score. The same pass gathers every
+    // key within D0, a set that holds the K best: when it fits the buffer (kMaxK keys), they
+    // are ranked or sorted directly and the passes below are skipped.
     if (!done) {
         for (int i = tid; i < kTopkBins; i += kTopkThreads) hist[i] = 0;
         __syncthreads();
-        const bool spec = d0 != 0 && K <= kRankMax;  // uniform
+        const bool spec = d0 != 0;  // uniform
         for_each_key([&](unsigned long long key) {
             const unsigned long long d = smax - (key >> 24);
             if (d < ((unsigned long long)kTopkBins << kCoarseShift)) atomicAdd(&hist[d >> kCoarseShift], 1u);
             if (spec) append_key(d < d0, key, &s_count, buf);
         });
         __syncthreads();
-        if (spec && s_count <= (uint32_t)kRankMax) done = true;  // uniform
+        if (spec && s_count <= (uint32_t)kMaxK) done = true;  // uniform
         else if (spec) {
             __syncthreads();  // every thread has read s_count
             if (tid == 0) s_count = 0;
