@@ -631,19 +631,38 @@ __global__ __launch_bounds__(kMxBlock, 3) void k_scan_mx(WaveArgs a) {
         // token-max row), and no thread divides
         const int lr = n_runs <= 1 ? 0 : 32 - __builtin_clz((unsigned)(n_runs - 1));
         const int rn = tid & ((1 << lr) - 1);
+        // Each cell is read and reset by one LDS exchange; the loop is unrolled so that the LDS
+        // reads of several tokens are in flight together.
         if (rn < n_runs) {
             const int rdoc = s_rdoc[rn];
-            // Eq.-1-literal scoring: embeddings of the run retrieved for each token
-            const unsigned len =
-                (unsigned)((rn + 1 < n_runs ? s_rstart[rn + 1] : (int)(it.e1 - it.e0)) - s_rstart[rn]);
             const int step = kMxBlock >> lr;
-            for (int tk = tid >> lr; tk < it.np; tk += step) {
-                unsigned* cell = &s_tab[tk * TPAD + rn];
-                const unsigned v = *cell;
-                *cell = kTokAbsent;
-                const int64_t o = s_row[par][tk] + rdoc;
-                atomicMax(&tokmax[o], v);
-                if (a.tokcnt) atomicAdd(&a.tokcnt[o], len);
+            if (!a.tokcnt) {
+                int tk = tid >> lr;
+                for (; tk + 3 * step < it.np; tk += 4 * step) {  // four tokens at a time
+                    unsigned v[4];
+                    int64_t o[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        v[u] = atomicExch(&s_tab[(tk + u * step) * TPAD + rn], kTokAbsent);
+                        o[u] = s_row[par][tk + u * step] + rdoc;
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) atomicMax(&tokmax[o[u]], v[u]);
+                }
+                for (; tk < it.np; tk += step) {
+                    const unsigned v = atomicExch(&s_tab[tk * TPAD + rn], kTokAbsent);
+                    atomicMax(&tokmax[s_row[par][tk] + rdoc], v);
+                }
+            } else {
+                // Eq.-1-literal scoring: embeddings of the run retrieved for each token
+                const unsigned len =
+                    (unsigned)((rn + 1 < n_runs ? s_rstart[rn + 1] : (int)(it.e1 - it.e0)) - s_rstart[rn]);
+                for (int tk = tid >> lr; tk < it.np; tk += step) {
+                    const unsigned v = atomicExch(&s_tab[tk * TPAD + rn], kTokAbsent);
+                    const int64_t o = s_row[par][tk] + rdoc;
+                    atomicMax(&tokmax[o], v);
+                    atomicAdd(&a.tokcnt[o], len);
+                }
             }
         }
         par ^= 1;
@@ -918,17 +937,36 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
                 g_cur = g_nx;
                 __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
                 if (has_next) stage_q(qa, qb, Q);
+                // the next chunk's documents and the first-group entries of the chunk after it
+                // move into place here, before the atomics, so that no later wait is for them
+                g_nx = g_nn;
+#pragma unroll
+                for (int j = 0; j < kMxChunk / 64; ++j) d[j] = dn[j];
             }
-            // flush: one device atomic per (token, run)
+            // flush: one device atomic per (token, run). Every cell of a token's row is read and
+            // reset by one LDS exchange (the columns past the chunk's runs hold kTokAbsent), all
+            // before the atomics, so that the LDS reads are in flight together.
             for (int tk = 0; tk < ng; ++tk) {  // wave-uniform
                 const int64_t row = (int64_t)__builtin_amdgcn_readlane(mytok, 16 * tk) * a.n_docs;
-                for (int r = lane; r < n_runs; r += 64) {
-                    unsigned* cell = &stab[tk * TPAD + r];
-                    const unsigned v = *cell;
-                    *cell = kTokAbsent;
-                    const int64_t o = row + rdoc[r];
-                    atomicMax(&tokmax[o], v);
-                    if (a.tokcnt) atomicAdd(&a.tokcnt[o], (unsigned)(rstart[r + 1] - rstart[r]));
+                if (!a.tokcnt) {
+                    unsigned v[kMxChunk / 64];
+                    int dd[kMxChunk / 64];
+#pragma unroll
+                    for (int j = 0; j < kMxChunk / 64; ++j) {
+                        v[j] = atomicExch(&stab[tk * TPAD + lane + 64 * j], kTokAbsent);
+                        dd[j] = rdoc[lane + 64 * j];
+                    }
+#pragma unroll
+                    for (int j = 0; j < kMxChunk / 64; ++j)
+                        if (lane + 64 * j < n_runs) atomicMax(&tokmax[row + dd[j]], v[j]);
+                } else {
+                    // Eq.-1-literal scoring: embeddings of the run retrieved for each token
+                    for (int r = lane; r < n_runs; r += 64) {
+                        const unsigned v = atomicExch(&stab[tk * TPAD + r], kTokAbsent);
+                        const int64_t o = row + rdoc[r];
+                        atomicMax(&tokmax[o], v);
+                        atomicAdd(&a.tokcnt[o], (unsigned)(rstart[r + 1] - rstart[r]));
+                    }
                 }
             }
             wave_lds_sync();
@@ -937,9 +975,6 @@ __global__ __launch_bounds__(kMxBlock) void k_scan_narrow(WaveArgs a) {
         if (!has_next) break;
         p = pn;
         cur = nx;
-        g_nx = g_nn;
-#pragma unroll
-        for (int j = 0; j < kMxChunk / 64; ++j) d[j] = dn[j];
     }
 }
 
