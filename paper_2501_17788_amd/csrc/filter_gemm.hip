@@ -16,7 +16,9 @@
 // Tiling: a workgroup of 4 waves computes 128-token x 128-centroid tiles; K = 128 is
 // staged through LDS in quarters of 32, each fp32 row split into hi and lo fp16 rows
 // padded to 40 halves (80 bytes). Each wave computes a 64 x 64 block as 4 x 4 MFMA blocks
-// of 16 x 16; lane group g = lane / 16 supplies the 8 consecutive k = 8 g .. 8 g + 7 of
+// of 16 x 16, with the centroids as the rows of each product and the tokens as its
+// columns, so that a lane holds four consecutive centroids of one token and writes them
+// with one store; lane group g = lane / 16 supplies the 8 consecutive k = 8 g .. 8 g + 7 of
 // both operands to each 32-wide k step, so every k is summed once.
 #include "engine.h"
 
@@ -58,6 +60,7 @@ __global__ __launch_bounds__(256, 2) void k_filter_gemm(const float* __restrict_
     const int wc = (wave & 1) * 64;   // and columns
     const int64_t tiles_c = (n_c + kGT - 1) / kGT;
     const int64_t n_tiles = tiles_c * ((n_tok + kGT - 1) / kGT);
+    const bool vec4 = (n_c & 3) == 0;  // rows of the output start 4-element aligned
 
     // 128 rows x 32 floats per operand = 1024 float4, 4 per thread
     auto load = [&](int64_t tile, int quarter, float4 (&va)[4], float4 (&vb)[4]) {
@@ -105,9 +108,9 @@ __global__ __launch_bounds__(256, 2) void k_filter_gemm(const float* __restrict_
                 const half8 al = *reinterpret_cast<const half8*>(&Al[ra]);
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bh[j], acc[i][j], 0, 0, 0);
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bl[j], acc[i][j], 0, 0, 0);
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al, bh[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(bh[j], ah, acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(bl[j], ah, acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(bh[j], al, acc[i][j], 0, 0, 0);
                 }
             }
         }
@@ -132,20 +135,33 @@ __global__ __launch_bounds__(256, 2) void k_filter_gemm(const float* __restrict_
             multiply();
             if (h < 3) __syncthreads();
         }
-        // D[r][cidx] of a 16 x 16 block sits in lane cidx + 16 * (r / 4), element r % 4.
+        // D[r][col] of a 16 x 16 block sits in lane col + 16 * (r / 4), element r % 4: lane (li, g)
+        // holds centroids 4 g .. 4 g + 3 of block j against token li of block i.
         const int64_t t_base = tile / tiles_c * kGT, c_base = tile % tiles_c * kGT;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
+            const int64_t t = t_base + wr + 16 * i + li;
+            if (t >= n_tok) continue;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const int64_t c = c_base + wc + 16 * j + li;
-                if (c >= n_c) continue;
+                const int64_t c0 = c_base + wc + 16 * j + 4 * g;
+                const int64_t o = t * n_c + c0;
+                if (vec4 && c0 + 3 < n_c) {  // four consecutive outputs, aligned: one store
+                    if (BINS) {
+                        const uint32_t lo = (uint32_t)score_bin(acc[i][j][0]) | ((uint32_t)score_bin(acc[i][j][1]) << 16);
+                        const uint32_t hi = (uint32_t)score_bin(acc[i][j][2]) | ((uint32_t)score_bin(acc[i][j][3]) << 16);
+                        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(out) + o) = make_uint2(lo, hi);
+                    } else {
+                        *reinterpret_cast<float4*>(static_cast<float*>(out) + o) =
+                            make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+                    }
+                    continue;
+                }
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const int64_t t = t_base + wr + 16 * i + 4 * g + r;
-                    if (t >= n_tok) continue;
-                    if (BINS) static_cast<uint16_t*>(out)[t * n_c + c] = (uint16_t)score_bin(acc[i][j][r]);
-                    else static_cast<float*>(out)[t * n_c + c] = acc[i][j][r];
+                    if (c0 + r >= n_c) continue;
+                    if (BINS) static_cast<uint16_t*>(out)[o + r] = (uint16_t)score_bin(acc[i][j][r]);
+                    else static_cast<float*>(out)[o + r] = acc[i][j][r];
                 }
             }
         }
